@@ -1,0 +1,308 @@
+"""Pins of the CPU oracle to facts outside itself.
+
+Each ``pin_*`` raises AssertionError when the oracle disagrees with a closed form,
+a hand-worked example, a library routine (torch softmax / SDPA in fp64), an
+invariant, or brute force.  ``test_oracle.py`` runs them against the oracle;
+``test_oracle_mutants.py`` runs them against deliberately broken copies of the
+oracle and requires every copy to fail at least one pin.
+"""
+from __future__ import annotations
+
+import itertools
+import json
+import math
+import os
+
+import numpy as np
+import torch
+
+import oracle
+from oracle import BF16, F32, Shape
+from synth import bf16_bits_to_f32, to_bf16_bits
+
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
+E = math.e
+
+
+def _rand(shape, rng, dtype):
+    x = rng.standard_normal(shape).astype(np.float32)
+    return to_bf16_bits(x) if dtype == BF16 else x
+
+
+def _f64(x, dtype):
+    return (bf16_bits_to_f32(x) if dtype == BF16 else np.asarray(x, np.float32)).astype(np.float64)
+
+
+def _inputs(s: Shape, seed: int):
+    rng = np.random.default_rng(seed)
+    return {
+        "q": _rand((s.n_suffix, s.n_q_heads, s.head_dim), rng, s.dtype),
+        "kp": _rand((s.n_prefix, s.n_kv_heads, s.head_dim), rng, s.dtype),
+        "vp": _rand((s.n_prefix, s.n_kv_heads, s.head_dim), rng, s.dtype),
+        "ks": _rand((s.n_suffix, s.n_kv_heads, s.head_dim), rng, s.dtype),
+        "vs": _rand((s.n_suffix, s.n_kv_heads, s.head_dim), rng, s.dtype),
+    }
+
+
+# tiny shapes: GQA groups 1..4, partial last chunks, d not a power of two
+SHAPES = [
+    Shape(37, 3, 6, 2, 8, 5, BF16),
+    Shape(64, 4, 4, 1, 16, 16, F32),
+    Shape(50, 5, 8, 2, 12, 7, BF16, 0.37),
+    Shape(9, 2, 3, 3, 4, 4, F32),
+]
+
+
+def _scale(s: Shape) -> float:
+    return s.sm_scale if s.sm_scale > 0 else 1.0 / math.sqrt(s.head_dim)
+
+
+def pin_partition():
+    """Def. 4.1: m = ceil(n/c); the last chunk holds the remainder."""
+    for n, c, m in [(5, 2, 3), (1024, 16, 64), (8192, 16, 512), (32768, 32, 1024),
+                    (65536, 8, 8192), (131072, 32, 4096), (1, 1, 1), (0, 4, 0), (17, 32, 1)]:
+        assert oracle.num_chunks(n, c) == m, (n, c)
+    assert oracle.num_chunks(5, 0) == -1
+    s = Shape(5, 1, 1, 1, 1, 2, F32)
+    k = np.arange(5, dtype=np.float32)
+    kd, vd = oracle.gather_chunks(s, k, k + 10, np.array([2], np.int32))
+    assert kd.ravel().tolist() == [4.0, 0.0] and vd.ravel().tolist() == [14.0, 0.0]
+    kd, _ = oracle.gather_chunks(s, k, k, np.array([0, 1], np.int32))
+    assert kd.ravel().tolist() == [0.0, 1.0, 2.0, 3.0]
+
+
+def pin_num_keep():
+    """Budget: the 1024-token fp32 case states 25% of 64 chunks = 16 chunks."""
+    assert oracle.num_keep(64, 0.25) == 16
+    assert oracle.num_keep(10, 0.1) == 1 and oracle.num_keep(10, 1.0) == 10
+    assert oracle.num_keep(3, 1e-6) == 1 and oracle.num_keep(0, 0.5) == 0
+    assert oracle.num_keep(7, 0.5) == 4 and oracle.num_keep(7, 0.0) == -1
+
+
+def pin_h1_scores():
+    """Hand example: q=[1], keys [0,0,1,1], c=2: weights 1,1,e,e over 2+2e."""
+    s = Shape(4, 1, 1, 1, 1, 2, F32, 1.0)
+    a = oracle.token_importance(s, np.array([1.0], np.float32), np.array([0, 0, 1, 1], np.float32))
+    ref = [1 / (2 + 2 * E), 1 / (2 + 2 * E), E / (2 + 2 * E), E / (2 + 2 * E)]
+    assert np.allclose(a, ref, rtol=1e-15, atol=0), a
+    A = oracle.chunk_scores(s, a)
+    assert np.allclose(A, [1 / (1 + E), E / (1 + E)], rtol=1e-15, atol=0), A
+    assert oracle.select_topk(A, 1).tolist() == [1]
+
+
+def pin_h2_tie():
+    """All keys equal: every chunk scores 1/2; the lower index wins the tie."""
+    s = Shape(4, 1, 1, 1, 1, 2, F32, 1.0)
+    a = oracle.token_importance(s, np.array([1.0], np.float32), np.zeros(4, np.float32))
+    A = oracle.chunk_scores(s, a)
+    assert A.tolist() == [0.5, 0.5], A
+    assert oracle.select_topk(A, 1).tolist() == [0]
+    assert oracle.select_topk(A, 2).tolist() == [0, 1]
+
+
+def pin_importance_invariants():
+    """Each softmax row sums to 1, so sum_j A_j = S*Hq; with q = 0 every row is
+    uniform and A_j = S*Hq*|chunk j|/n."""
+    for i, s in enumerate(SHAPES):
+        x = _inputs(s, 100 + i)
+        A = oracle.chunk_scores(s, oracle.token_importance(s, x["q"], x["kp"]))
+        rows = s.n_suffix * s.n_q_heads
+        assert abs(A.sum() - rows) <= 1e-12 * rows, (s, A.sum())
+        zq = np.zeros_like(x["q"])
+        A0 = oracle.chunk_scores(s, oracle.token_importance(s, zq, x["kp"]))
+        lens = np.minimum(s.chunk_size, s.n_prefix - np.arange(s.n_chunks) * s.chunk_size)
+        assert np.allclose(A0, rows * lens / s.n_prefix, rtol=1e-12, atol=0), (s, A0)
+
+
+def pin_importance_vs_torch():
+    """Token importance equals torch's fp64 softmax over prefix keys, summed over
+    every query row of every head (GQA: head h reads KV head h // G)."""
+    for i, s in enumerate(SHAPES):
+        x = _inputs(s, 200 + i)
+        a = oracle.token_importance(s, x["q"], x["kp"], threads=3)
+        q = torch.from_numpy(_f64(x["q"], s.dtype))  # [S][Hq][d]
+        k = torch.from_numpy(_f64(x["kp"], s.dtype))  # [n][Hkv][d]
+        G = s.n_q_heads // s.n_kv_heads
+        ref = torch.zeros(s.n_prefix, dtype=torch.float64)
+        for h in range(s.n_q_heads):
+            logits = _scale(s) * (q[:, h, :] @ k[:, h // G, :].T)
+            ref += torch.softmax(logits, dim=-1).sum(0)
+        assert np.allclose(a, ref.numpy(), rtol=1e-12, atol=1e-15), (s, np.abs(a - ref.numpy()).max())
+        A = oracle.chunk_scores(s, a)
+        pooled = [ref[j * s.chunk_size:(j + 1) * s.chunk_size].sum().item() for j in range(s.n_chunks)]
+        assert np.allclose(A, pooled, rtol=1e-12, atol=1e-15)
+
+
+def _brute_topk(A, k):
+    """Exhaustive: among the k-subsets of maximal score sum, the lexicographically
+    smallest ascending tuple (scores are small integers, so sums are exact)."""
+    best = None
+    for sub in itertools.combinations(range(len(A)), k):
+        key = (-sum(A[j] for j in sub), sub)
+        if best is None or key < best:
+            best = key
+    return list(best[1])
+
+
+def pin_select_bruteforce():
+    """Top-k with lowest-index tie-break against exhaustive subset search."""
+    rng = np.random.default_rng(7)
+    for m in range(1, 11):
+        for trial in range(3):
+            A = rng.integers(0, 4, size=m).astype(np.float64)
+            for k in range(1, m + 1):
+                assert oracle.select_topk(A, k).tolist() == _brute_topk(A.tolist(), k), (A, k)
+
+
+def pin_select_special_values():
+    """NaN ranks below -inf, -0.0 ties with +0.0 (lower index wins)."""
+    A = np.array([np.nan, -0.0, 0.0, -np.inf, np.inf, 1.0, np.nan, -1.0])
+    order = [4, 5, 1, 2, 7, 3, 0, 6]
+    for k in range(1, len(A) + 1):
+        assert oracle.select_topk(A, k).tolist() == sorted(order[:k]), k
+
+
+def pin_attention_h1():
+    """Hand example extended: V=[1,2,3,4], suffix key 0 / value 10.
+    keep chunk {1}: weights e,e,1 over values 3,4,10 -> (7e+10)/(2e+1).
+    dense: weights 1,1,e,e,1 over 1,2,3,4,10 -> (13+7e)/(3+2e)."""
+    s = Shape(4, 1, 1, 1, 1, 2, F32, 1.0)
+    args = dict(q=np.array([1.0], np.float32), k_prefix=np.array([0, 0, 1, 1], np.float32),
+                v_prefix=np.array([1, 2, 3, 4], np.float32), k_suffix=np.array([0.0], np.float32),
+                v_suffix=np.array([10.0], np.float32))
+    o = oracle.sparse_attn(s, sel=np.array([1], np.int32), **args)
+    assert abs(o.item() - (7 * E + 10) / (2 * E + 1)) <= 1e-14, o
+    o = oracle.dense_attn(s, **args)
+    assert abs(o.item() - (13 + 7 * E) / (3 + 2 * E)) <= 1e-14, o
+    o = oracle.sparse_attn(s, sel=np.array([0], np.int32), **args)
+    assert abs(o.item() - 13.0 / 3.0) <= 1e-14, o
+
+
+def _sdpa(s: Shape, x, visible_prefix):
+    """torch fp64 SDPA over [prefix ; suffix] keys with an explicit boolean mask."""
+    q = torch.from_numpy(_f64(x["q"], s.dtype)).permute(1, 0, 2)  # [Hq][S][d]
+    G = s.n_q_heads // s.n_kv_heads
+    k = torch.cat([torch.from_numpy(_f64(x["kp"], s.dtype)), torch.from_numpy(_f64(x["ks"], s.dtype))])
+    v = torch.cat([torch.from_numpy(_f64(x["vp"], s.dtype)), torch.from_numpy(_f64(x["vs"], s.dtype))])
+    k = k.permute(1, 0, 2).repeat_interleave(G, dim=0).contiguous()
+    v = v.permute(1, 0, 2).repeat_interleave(G, dim=0).contiguous()
+    n, S = s.n_prefix, s.n_suffix
+    mask = torch.zeros(S, n + S, dtype=torch.bool)
+    mask[:, :n] = torch.from_numpy(visible_prefix)[None, :]
+    mask[:, n:] = torch.tril(torch.ones(S, S, dtype=torch.bool))
+    o = torch.nn.functional.scaled_dot_product_attention(q, k, v, attn_mask=mask, scale=_scale(s))
+    return o.permute(1, 0, 2).numpy()
+
+
+def pin_attention_vs_sdpa():
+    """Dense and sparse attention equal torch fp64 SDPA with the matching mask."""
+    for i, s in enumerate(SHAPES):
+        x = _inputs(s, 300 + i)
+        dense = oracle.dense_attn(s, x["q"], x["kp"], x["vp"], x["ks"], x["vs"])
+        ref = _sdpa(s, x, np.ones(s.n_prefix, bool))
+        assert np.allclose(dense, ref, rtol=0, atol=1e-12), (s, np.abs(dense - ref).max())
+        rng = np.random.default_rng(400 + i)
+        k = max(1, s.n_chunks // 2)
+        sel = np.sort(rng.choice(s.n_chunks, size=k, replace=False)).astype(np.int32)
+        if s.n_chunks - 1 not in sel:  # include the partial last chunk
+            sel[-1] = s.n_chunks - 1
+            sel = np.unique(sel).astype(np.int32)
+        vis = np.zeros(s.n_prefix, bool)
+        for j in sel:
+            vis[j * s.chunk_size:(j + 1) * s.chunk_size] = True
+        sparse = oracle.sparse_attn(s, x["q"], x["kp"], x["vp"], sel, x["ks"], x["vs"])
+        ref = _sdpa(s, x, vis)
+        assert np.allclose(sparse, ref, rtol=0, atol=1e-12), (s, np.abs(sparse - ref).max())
+        rows = np.array([0, s.n_suffix * s.n_q_heads - 1, 1], np.int64)
+        part = oracle.sparse_attn(s, x["q"], x["kp"], x["vp"], sel, x["ks"], x["vs"], row_ids=rows)
+        full = sparse.reshape(-1, s.head_dim)
+        assert np.array_equal(part, full[rows])
+
+
+def pin_keep_all_is_dense():
+    """With every chunk kept the sparse path visits the dense key sequence: equal bit for bit."""
+    for i, s in enumerate(SHAPES):
+        x = _inputs(s, 500 + i)
+        sel = np.arange(s.n_chunks, dtype=np.int32)
+        a = oracle.sparse_attn(s, x["q"], x["kp"], x["vp"], sel, x["ks"], x["vs"])
+        b = oracle.dense_attn(s, x["q"], x["kp"], x["vp"], x["ks"], x["vs"])
+        assert np.array_equal(a, b), s
+
+
+def pin_attention_constant_v():
+    """Softmax weights sum to 1: constant values come back unchanged."""
+    for i, s in enumerate(SHAPES):
+        x = _inputs(s, 600 + i)
+        const = np.full_like(x["vp"], to_bf16_bits(np.float32(1.5)) if s.dtype == BF16 else 1.5)
+        consts = np.full_like(x["vs"], to_bf16_bits(np.float32(1.5)) if s.dtype == BF16 else 1.5)
+        sel = np.arange(0, s.n_chunks, 2, dtype=np.int32)
+        o = oracle.sparse_attn(s, x["q"], x["kp"], const, sel, x["ks"], consts)
+        assert np.allclose(o, 1.5, rtol=1e-14, atol=0), s
+
+
+def pin_gather():
+    """Gather is a byte copy of whole chunk spans, zero past n."""
+    s = Shape(37, 1, 2, 2, 8, 5, BF16)
+    x = _inputs(s, 700)
+    sel = np.array([0, 3, 7], np.int32)  # chunk 7 is the partial one (35, 36)
+    kd, vd = oracle.gather_chunks(s, x["kp"], x["vp"], sel)
+    for u, j in enumerate(sel):
+        lo, hi = j * 5, min(j * 5 + 5, 37)
+        assert np.array_equal(kd[u * 5:u * 5 + hi - lo], x["kp"][lo:hi])
+        assert np.array_equal(vd[u * 5:u * 5 + hi - lo], x["vp"][lo:hi])
+        assert not kd[u * 5 + hi - lo:(u + 1) * 5].any() and not vd[u * 5 + hi - lo:(u + 1) * 5].any()
+
+
+def pin_accounting():
+    """Prefetch accounting is set algebra over chunk spans (Sec. 4.3.2)."""
+    s = Shape(37, 1, 2, 2, 8, 5, BF16)
+    per_tok = 2 * 2 * 8 * 2
+    lens = {j: min(5, 37 - 5 * j) for j in range(8)}
+    rng = np.random.default_rng(9)
+    cases = [(np.array([1, 2, 7]), np.array([], int)),      # first layer: no prediction
+             (np.array([1, 2, 7]), np.array([1, 2, 7])),    # perfect prediction
+             (np.array([1, 2, 7]), np.array([0, 3, 4, 5, 6]))]  # complement
+    for _ in range(20):
+        cases.append((np.sort(rng.choice(8, 3, replace=False)), np.sort(rng.choice(8, 4, replace=False))))
+    for sel, pred in cases:
+        st = oracle.layer_accounting(s, sel, pred)
+        S, P = set(sel.tolist()), set(pred.tolist())
+        assert st["k"] == len(S) and st["hits"] == len(S & P)
+        assert st["misses"] == len(S - P) and st["wasted"] == len(P - S)
+        assert st["bytes_prefetch"] == sum(lens[j] for j in P) * per_tok
+        assert st["bytes_demand"] == sum(lens[j] for j in S - P) * per_tok
+        assert st["bytes_used"] == sum(lens[j] for j in S) * per_tok
+
+
+def pin_paper_byte_accounting():
+    """Byte figures the paper prints for Qwen2.5-7B (Sec. 4.2, Sec. 3)."""
+    g = json.load(open(os.path.join(GOLDEN, "paper_byte_accounting.json")))
+    m = g["qwen25_7b"]
+    c = 16
+    s = Shape(c, 1, 28, m["kv_heads"], m["head_dim"], c, BF16)
+    st = oracle.layer_accounting(s, np.array([0]), np.array([], int))
+    # K and V of one chunk in one layer; the paper's per-token figure is one of K or V over all layers
+    per_token_one_tensor_all_layers = st["bytes_used"] // 2 // c * m["layers"]
+    assert round(per_token_one_tensor_all_layers / 1024) == g["per_token_kb_approx"]
+    block = per_token_one_tensor_all_layers * g["block_tokens"]
+    assert abs(block / 1000 - g["block_kb_approx"]) / g["block_kb_approx"] < 0.02
+    assert g["block_tokens"] // g["useful_tokens_per_block"] == g["read_amplification_block"]
+    amp = g["example_blocks"] * g["block_tokens"] / g["example_needed_tokens"]
+    assert int(amp) == g["example_read_amplification"]
+
+
+def pin_planted_chunks_found():
+    """The 1024-token fp32 workload plants 3 chunks along the query direction;
+    the full layer keeps all of them among its 16 chunks."""
+    import synth
+    w = synth.WORKLOADS["c1_f32_1k"]
+    t = synth.layer_tensors(w, 0)
+    s = Shape(w.n_prefix, w.n_suffix, w.n_q_heads, w.n_kv_heads, w.head_dim, w.chunk_size, F32)
+    A, sel, out = oracle.reprefill_layer(s, w.keep_ratio, t["q"], t["k_prefix"], t["v_prefix"],
+                                         t["k_suffix"], t["v_suffix"])
+    assert len(sel) == 16
+    assert set(synth.heavy_sets(w)[0].tolist()) <= set(sel.tolist())
+    assert abs(A.sum() - w.n_suffix * w.n_q_heads) < 1e-9
+
+
+ALL_PINS = [v for k, v in sorted(globals().items()) if k.startswith("pin_")]
