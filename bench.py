@@ -1,0 +1,170 @@
+#!/usr/bin/env python3
+"""Benchmark: prefix tokens/s per Re-Prefill layer step on one MI355X.
+
+A step is one Re-Prefill layer of the hot path (chunk scoring, fp64 fold, top-k
+selection, contiguous-span attention over the kept chunks plus the causal
+suffix) through ``ckv_reprefill_layer``.  Steps cycle over the workload's layers,
+each with its own seeded synthetic Q/K/V resident in HBM before timing starts.
+
+Prints one JSON line.  ``roofline`` describes the scoring kernel (the dominant
+kernel): its algorithmic flops per launch (2*S*Hq*n*d) over its average
+duration, taken from HIP events recorded on the layer's stream around that
+kernel inside the timed region.  ``cpu_baseline`` times the oracle (plain C,
+fp64) on a bounded sample of the same workload on this host's cores.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "prefix tokens/sec per Re-Prefill layer step"
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+
+
+def log(msg: str) -> None:
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=560)
+    ap.add_argument("--warmup", type=int, default=56)
+    ap.add_argument("--workload", default="c3_qwen7b_32k")
+    ap.add_argument("--materialize", action="store_true",
+                    help="gather the kept chunks into compact buffers before attention")
+    ap.add_argument("--cpu-layers", type=int, default=3, help="oracle layers in the CPU baseline")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py runs on exactly one GPU: this build has no multi-GPU path "
+              "(the method's per-layer path is measured on one MI355X)", file=sys.stderr)
+        return 2
+
+    import numpy as np
+    import torch
+
+    import paper_2601_13631_amd as ckv
+    import synth
+
+    w = synth.WORKLOADS[args.workload]
+    if w.host_resident:
+        print("host-resident workloads are measured by tests/bench_host.py", file=sys.stderr)
+        return 2
+    torch.cuda.set_device(0)
+    dev = torch.device("cuda:0")
+    L = w.n_layers
+    log(f"generating {L} layers of {w.name}")
+    t0 = time.time()
+    host = synth.all_layers(w, threads=min(16, os.cpu_count() or 1))
+    log(f"generated in {time.time() - t0:.1f}s; uploading")
+
+    def up(a):
+        t = torch.from_numpy(a)
+        if a.dtype == np.uint16:
+            t = t.view(torch.bfloat16)
+        return t.to(dev)
+
+    layers = [{k: up(v) for k, v in h.items()} for h in host]
+    dims = ckv.make_dims(w.n_prefix, w.n_suffix, w.n_q_heads, w.n_kv_heads, w.head_dim,
+                         w.chunk_size, ckv.DTYPE_F32 if w.dtype == "f32" else ckv.DTYPE_BF16)
+    flags = ckv.CTX_STAGE_TIMING | (ckv.CTX_MATERIALIZE if args.materialize else 0)
+    ctx = ckv.Context(dims, w.keep_ratio, flags)
+    k = ctx.k
+    outs = [torch.empty_like(l["q"]) for l in layers]
+    stream = torch.cuda.current_stream()
+
+    def step(i: int) -> None:
+        l = layers[i % L]
+        ctx.reprefill_layer(i % L, l["q"], l["k_suffix"], l["v_suffix"], l["k_prefix"], outs[i % L],
+                            k_prefix=l["k_prefix"], v_prefix=l["v_prefix"], stream=stream)
+
+    log(f"warmup {args.warmup} steps")
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    ctx.reset()  # stage times restart with the timed region
+    log(f"timing {args.steps} steps")
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(i)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    stage_ms, n_timed = ctx.stage_times()
+    ctx.close()
+    ms_per_step = elapsed * 1e3 / args.steps
+    value = w.n_prefix * args.steps / elapsed
+    per_layer = {s: stage_ms[s] / n_timed for s in stage_ms}
+    log(f"{ms_per_step * 1e3:.1f} us/step; stages (us): " +
+        ", ".join(f"{s} {v * 1e3:.1f}" for s, v in per_layer.items()))
+
+    # scoring: algorithmic flops per launch / average launch duration
+    score_flops = 2.0 * w.n_suffix * w.n_q_heads * w.n_prefix * w.head_dim
+    score_s = per_layer["score"] * 1e-3
+    achieved = score_flops / score_s / 1e12
+    roofline = {"kernel": "score_bf16_kernel", "bound": "mfma", "achieved": round(achieved, 2),
+                "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+                "traffic": None,
+                "flops_per_launch": score_flops, "avg_launch_us": round(score_s * 1e6, 2)}
+    # attention and kept-chunk bytes, as context
+    T = k * w.chunk_size
+    attn_flops = 4.0 * w.head_dim * w.n_q_heads * (w.n_suffix * T + w.n_suffix * (w.n_suffix + 1) / 2)
+    kept_bytes = 2 * T * w.n_kv_heads * w.head_dim * w.elem_bytes
+    attn_s = per_layer["attn"] * 1e-3
+    others = {
+        "attn_tflops": round(attn_flops / attn_s / 1e12, 2),
+        "attn_frac_mfma": round(attn_flops / attn_s / 1e12 / PEAK_BF16_TFLOPS, 4),
+        "attn_kept_kv_gbs": round(kept_bytes / attn_s / 1e9, 1),
+        "stage_us_per_layer": {s: round(v * 1e3, 2) for s, v in per_layer.items()},
+    }
+    if args.materialize and per_layer["move"] > 0:
+        others["gather_gbs"] = round(2 * kept_bytes / (per_layer["move"] * 1e-3) / 1e9, 1)
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        import oracle
+        s = oracle.Shape(w.n_prefix, w.n_suffix, w.n_q_heads, w.n_kv_heads, w.head_dim,
+                         w.chunk_size, oracle.F32 if w.dtype == "f32" else oracle.BF16)
+        threads = os.cpu_count() or 1
+        n_cpu = min(args.cpu_layers, L)
+        log(f"oracle on {n_cpu} layer(s), {threads} threads")
+        t0 = time.perf_counter()
+        for l in range(n_cpu):
+            h = host[l]
+            oracle.reprefill_layer(s, w.keep_ratio, h["q"], h["k_prefix"], h["v_prefix"],
+                                   h["k_suffix"], h["v_suffix"], threads=threads)
+        cpu_s = time.perf_counter() - t0
+        cpu = {"value": round(w.n_prefix * n_cpu / cpu_s, 1), "unit": "tokens/s", "cores": threads,
+               "kind": "oracle",
+               "sample": f"{n_cpu} full layer(s) of {w.name} (token importance, Eq. 1 pooling, "
+                         f"top-k, sparse attention), fp64, {cpu_s:.1f}s"}
+        log(f"oracle {cpu_s:.1f}s")
+
+    line = {
+        "metric": METRIC, "value": round(value, 1), "unit": "tokens/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 5),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16" if w.dtype == "bf16" else "f32",
+        "data": "synthetic: seeded Q/K/V with planted heavy chunks, HBM-resident",
+        "config": {"workload": w.name, "layers": L, "n_prefix": w.n_prefix, "n_suffix": w.n_suffix,
+                   "q_heads": w.n_q_heads, "kv_heads": w.n_kv_heads, "head_dim": w.head_dim,
+                   "chunk_size": w.chunk_size, "keep_ratio": w.keep_ratio, "kept_chunks": k,
+                   "gather": "materialized" if args.materialize else "in-place spans"},
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+        "detail": others,
+    }
+    print(json.dumps(line), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

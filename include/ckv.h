@@ -1,0 +1,256 @@
+/*
+ * ckv.h -- C ABI of libckv, the MI355X (gfx950) implementation of the
+ * data-parallel hot path of ContiguousKV's Re-Prefill phase.
+ *
+ * Paper: "ContiguousKV: Accelerating LLM Prefill with Granularity-Aligned KV
+ * Cache Management", arXiv 2601.13631.  For one transformer layer the path
+ *   1. scores every prefix key against the new suffix's queries and sums the
+ *      softmax probabilities per ContiguousChunk           (Sec. 4.4, Eq. 1)
+ *   2. keeps the k highest-scoring chunks                   (Sec. 4.4; Sec. 5.1 budgets)
+ *   3. moves only those chunks' contiguous K/V spans        (Sec. 4.2)
+ *      -- from HBM, or from pinned host memory with the next layer's chunks
+ *         prefetched from this layer's set                   (Sec. 4.3.2)
+ *   4. runs the suffix's attention over the kept prefix KV plus the causal
+ *      suffix KV                                            (Def. 2.1)
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * - Return value: a ckv_status.  Arguments are validated before anything is
+ *   launched; on an error nothing has been enqueued and no output is touched.
+ *   No entry point aborts, exits or throws.  ckv_last_error() returns a
+ *   thread-local text describing the most recent failure on this thread.
+ * - Ownership: the caller owns every buffer passed in.  The library never
+ *   frees, retains or reallocates caller memory.
+ * - Device pointers must point to memory of the current HIP device; tensor base
+ *   pointers must be 16-byte aligned.
+ * - Asynchrony: work is enqueued on the caller's stream (a hipStream_t passed
+ *   as void*; NULL is the null stream).  Outputs are valid once that stream has
+ *   been synchronized.  Inputs must stay valid and unchanged until then.
+ * - Scratch memory comes from a caller-provided workspace (device memory of at
+ *   least the size the matching *_workspace_bytes() call returns, 256-byte
+ *   aligned), or from a ckv_ctx.
+ * - Thread safety: entry points without a ckv_ctx are reentrant; a ckv_ctx
+ *   must be used by one host thread at a time.
+ *
+ * Tensor layouts (row-major, contiguous; element type from ckv_dims.dtype)
+ * ------------------------------------------------------------------------
+ *   q            [S][Hq][d]    suffix queries (post-RoPE)
+ *   k_prefix     [n][Hkv][d]   stored prefix keys;   chunk j = rows [j*c, min(j*c+c, n))
+ *   v_prefix     [n][Hkv][d]   stored prefix values
+ *   k_suffix     [S][Hkv][d]   suffix keys
+ *   v_suffix     [S][Hkv][d]   suffix values
+ *   k_sel, v_sel [k*c][Hkv][d] gathered chunks, chunk u at rows [u*c, u*c+c)
+ *   out          [S][Hq][d]    attention output, same element type as q
+ * With this layout one ContiguousChunk of one tensor is a single contiguous
+ * span of c*Hkv*d elements (Sec. 4.2: the chunk is the unit of storage and I/O).
+ * Query head h reads KV head h / (Hq/Hkv) (grouped-query attention, Sec. 2.1).
+ */
+#ifndef CKV_H
+#define CKV_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t ckv_status;
+#define CKV_OK 0
+#define CKV_EINVAL 1         /* bad shape, pointer, alignment or size */
+#define CKV_EUNSUPPORTED 2   /* valid but not built: dtype/head_dim/chunk_size combination */
+#define CKV_EHIP 3           /* a HIP runtime call failed; see ckv_last_error() */
+#define CKV_ENOMEM 4         /* device or pinned host allocation failed */
+#define CKV_ESTATE 5         /* ckv_ctx used out of order */
+
+#define CKV_DTYPE_F32 0
+#define CKV_DTYPE_BF16 1
+
+/* Problem shape.  Supported: dtype BF16 with head_dim 64 or 128, dtype F32
+ * with head_dim 64; chunk_size 4, 8, 16 or a multiple of 32; n_prefix >= 1;
+ * n_suffix >= 1; n_q_heads a multiple of n_kv_heads. */
+typedef struct ckv_dims {
+  int64_t n_prefix;   /* n: prefix tokens                             */
+  int32_t n_suffix;   /* S: suffix tokens (queries)                    */
+  int32_t n_q_heads;  /* Hq                                            */
+  int32_t n_kv_heads; /* Hkv                                           */
+  int32_t head_dim;   /* d                                             */
+  int32_t chunk_size; /* c: tokens per ContiguousChunk (Def. 4.1)       */
+  int32_t dtype;      /* CKV_DTYPE_F32 or CKV_DTYPE_BF16               */
+  float sm_scale;     /* logit scale; 0 selects 1/sqrt(head_dim)       */
+} ckv_dims;
+
+/* Thread-local text of the last failure on this thread ("" if none). */
+const char* ckv_last_error(void);
+
+/* Library version string. */
+const char* ckv_version(void);
+
+/* Def. 4.1: number of ContiguousChunks m = ceil(n / c).  -1 if n < 0 or c < 1.
+ * Host-only, pure. */
+int64_t ckv_num_chunks(int64_t n, int32_t c);
+
+/* Chunks kept at budget ratio r in (0, 1] (the evaluation's KV budget ratios,
+ * Sec. 5.1; the paper does not fix the rounding):
+ * k = clamp(ceil(r*m - 1e-9), 1, m), 0 when m == 0, -1 when r is outside
+ * (0, 1] or m < 0.  Host-only, pure, so a caller knows k without a device sync. */
+int64_t ckv_num_keep(int64_t m, double r);
+
+/* ---------------------------------------------------------------------------
+ * Chunk scoring -- Sec. 4.4 and Eq. 1.
+ * For every query head h and suffix query t, the probabilities
+ * softmax_i(sm_scale * q[t,h] . k_prefix[i, h/G]) over the n prefix keys are
+ * summed per chunk and over all (t, h):
+ *   chunk_scores[j] = sum_{t,h} sum_{i in chunk j} p_{t,h,i}.
+ * The softmax runs over the prefix keys only, so sum_j chunk_scores[j] = S*Hq.
+ *   q             device, [S][Hq][d]
+ *   k_prefix      device, [n][Hkv][d]
+ *   chunk_scores  device, double[m] (written)
+ *   ws            device workspace of ckv_score_workspace_bytes(dims) bytes
+ * Arithmetic: logits and exponentials in fp32 (bf16 products are exact in
+ * fp32), per-chunk partial sums in fp32 over at most one chunk, every sum
+ * across rows, ranges and heads in fp64, in a fixed order (run-to-run
+ * deterministic).
+ * ------------------------------------------------------------------------- */
+size_t ckv_score_workspace_bytes(const ckv_dims* dims);
+ckv_status ckv_score_chunks(const ckv_dims* dims, const void* q, const void* k_prefix,
+                            double* chunk_scores, void* ws, size_t ws_bytes, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * Top-k chunk selection -- Sec. 4.4 (chunks ranked by A_j, the k highest
+ * kept), budgets of Sec. 5.1.
+ * Keeps the k largest scores under the total order (score descending, index
+ * ascending): among equal scores the lower chunk index wins.  -0.0 equals
+ * +0.0; NaN ranks below every number.  Writes the k chosen indices in
+ * ascending order.  Bit-exact: the result depends only on the score bits.
+ *   chunk_scores  device, double[m]
+ *   sel_idx       device, int32[k] (written)
+ *   1 <= k <= m <= 2^31-1
+ * ------------------------------------------------------------------------- */
+size_t ckv_select_workspace_bytes(int64_t m);
+ckv_status ckv_select_topk_chunks(const double* chunk_scores, int64_t m, int64_t k,
+                                  int32_t* sel_idx, void* ws, size_t ws_bytes, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * Contiguous chunk gather -- Sec. 4.2 (only the selected chunks move, each as
+ * whole contiguous spans: no block read amplification).
+ * Copies the K and V spans of chunks sel_idx[0..k) into k_sel / v_sel,
+ * chunk u to rows [u*c, u*c+c); rows past n of a short last chunk are zeroed.
+ *   k_src, v_src  [n][Hkv][d], device memory or pinned host memory mapped
+ *                 into the device address space (hipHostMalloc)
+ *   sel_idx       device, int32[k], each in [0, m) (indices are not checked on
+ *                 the host; an index outside [0, m) is clamped by the kernel
+ *                 and its span is zero-filled)
+ *   k_sel, v_sel  device, [k*c][Hkv][d] (written)
+ * ------------------------------------------------------------------------- */
+ckv_status ckv_gather_chunks(const ckv_dims* dims, const void* k_src, const void* v_src,
+                             const int32_t* sel_idx, int64_t k, void* k_sel, void* v_sel,
+                             void* stream);
+
+/* ---------------------------------------------------------------------------
+ * Re-Prefill sparse attention -- Def. 2.1 (the suffix attends over the loaded
+ * prefix KV and its own KV), GQA of Sec. 2.1.
+ * For query t of head h the keys are the tokens of the k gathered chunks (in
+ * order; rows past n of a short last chunk skipped) followed by suffix tokens
+ * 0..t (causal).  out[t][h] = sum softmax(sm_scale * q.k) * v; softmax in
+ * fp32 with bf16 MFMA products for bf16 inputs.
+ *   q             device, [S][Hq][d]
+ *   k_sel, v_sel  device, [k*c][Hkv][d] (as written by ckv_gather_chunks)
+ *   sel_idx       device, int32[k]: the chunks' indices, used only to find the
+ *                 length of a short last chunk
+ *   k_suffix, v_suffix  device, [S][Hkv][d]
+ *   out           device, [S][Hq][d] (written)
+ *   ws            device workspace of ckv_attn_workspace_bytes(dims, k) bytes
+ * 0 <= k <= m.
+ * ------------------------------------------------------------------------- */
+size_t ckv_attn_workspace_bytes(const ckv_dims* dims, int64_t k);
+ckv_status ckv_sparse_prefill_attn(const ckv_dims* dims, const void* q, const void* k_sel,
+                                   const void* v_sel, const int32_t* sel_idx, int64_t k,
+                                   const void* k_suffix, const void* v_suffix, void* out,
+                                   void* ws, size_t ws_bytes, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * Layer step -- one Re-Prefill layer: score -> select -> move chunks ->
+ * attention, with the context owning streams, events, workspace and (for a
+ * host-resident prefix) HBM chunk slots.
+ * ------------------------------------------------------------------------- */
+typedef struct ckv_ctx ckv_ctx;
+
+/* ctx flags */
+#define CKV_CTX_HOST_PREFIX 0x1     /* prefix K/V live in pinned host memory (Sec. 4.3.2) */
+#define CKV_CTX_MATERIALIZE 0x2     /* HBM prefix: gather into compact buffers before
+                                       attention instead of reading spans in place */
+#define CKV_CTX_STAGE_TIMING 0x4    /* record HIP events between the stages of every
+                                       layer (see ckv_ctx_stage_times) */
+
+/* Stages timed with CKV_CTX_STAGE_TIMING. */
+#define CKV_STAGE_SCORE 0     /* chunk-scoring main kernel                         */
+#define CKV_STAGE_FINALIZE 1  /* fp64 fold of the partial sums into chunk scores   */
+#define CKV_STAGE_SELECT 2    /* top-k selection                                   */
+#define CKV_STAGE_MOVE 3      /* gather, or the wait for demand copies (host prefix) */
+#define CKV_STAGE_ATTN 4      /* attention (and split combine)                     */
+#define CKV_N_STAGES 5
+
+/* Creates a context for layers of shape *dims at keep ratio keep_ratio.
+ * Allocates the workspace (and, with CKV_CTX_HOST_PREFIX, two HBM slot
+ * buffers of 2k chunks each plus pinned index staging) on the current
+ * device.  *out receives the context. */
+ckv_status ckv_ctx_create(const ckv_dims* dims, double keep_ratio, int32_t flags, ckv_ctx** out);
+/* Waits for the context's streams, then frees everything the context owns. */
+ckv_status ckv_ctx_destroy(ckv_ctx* ctx);
+/* Forgets the previous layer's selection: the next layer runs without a
+ * prediction (as the first layer of a request); also clears stage times. */
+ckv_status ckv_ctx_reset(ckv_ctx* ctx);
+
+typedef struct ckv_layer_io {
+  const void* q;         /* device [S][Hq][d]                                        */
+  const void* k_suffix;  /* device [S][Hkv][d]                                       */
+  const void* v_suffix;  /* device [S][Hkv][d]                                       */
+  const void* k_probe;   /* device [n][Hkv][d]: the layer's prefix keys for scoring  */
+  const void* k_prefix;  /* device [n][Hkv][d] (HBM-resident prefix), else NULL      */
+  const void* v_prefix;  /* device [n][Hkv][d] (HBM-resident prefix), else NULL      */
+  const void* kv_host;   /* pinned host, chunk-major: chunk j of this layer at byte
+                            offset j * 2*c*Hkv*d*elem, K span then V span; rows past
+                            n of the last chunk are padding (host-resident prefix)  */
+  const void* kv_host_next; /* the next layer's kv_host, prefetched during this layer
+                               with this layer's selection as the prediction; NULL
+                               for the last layer                                    */
+  void* out;             /* device [S][Hq][d] (written)                              */
+  double* chunk_scores;  /* device double[m] (written), or NULL                      */
+  int32_t* sel_idx;      /* device int32[k] (written), or NULL                       */
+  void* stream;          /* hipStream_t for the layer's compute                      */
+} ckv_layer_io;
+
+typedef struct ckv_layer_stats {
+  int64_t k;               /* chunks selected                                         */
+  int64_t hits;            /* selected chunks that were prefetched                     */
+  int64_t misses;          /* selected chunks fetched on demand                        */
+  int64_t wasted;          /* prefetched chunks not selected                           */
+  int64_t bytes_prefetch;  /* host->HBM bytes issued for the next layer's prediction   */
+  int64_t bytes_demand;    /* host->HBM bytes fetched on demand for this layer         */
+  int64_t bytes_gathered;  /* K+V bytes of the selected chunks (= bytes attended); with
+                              an HBM-resident prefix the set stays on the device and a
+                              kept short last chunk is counted at full length          */
+} ckv_layer_stats;
+
+/* Sum of the GPU time of each stage (ms[CKV_N_STAGES], milliseconds) over
+ * every layer run since the context was created or last reset, and that
+ * number of layers in *n_layers.  Requires CKV_CTX_STAGE_TIMING; waits for the
+ * events of the layers not yet accounted.  Stage times come from events
+ * recorded on each layer's compute stream between its kernel launches. */
+ckv_status ckv_ctx_stage_times(ckv_ctx* ctx, double* ms, int64_t* n_layers);
+
+/* Runs layer `layer` (0-based; layer 0, or the first layer after
+ * ckv_ctx_reset, has no prediction).  HBM-resident prefix: returns without a
+ * host synchronization.  Host-resident prefix: synchronizes once on the
+ * selection (the only device->host dependency of the step), enqueues the
+ * demand copies of the missed chunks, the attention over the HBM slots and
+ * the prefetch of the next layer's chunks; counts in *stats (may be NULL) are
+ * exact.  With a host-resident prefix, layers must be run in order. */
+ckv_status ckv_reprefill_layer(ckv_ctx* ctx, int32_t layer, const ckv_layer_io* io,
+                               ckv_layer_stats* stats);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* CKV_H */

@@ -1,0 +1,225 @@
+"""Python binding of libckv, the MI355X (gfx950) Re-Prefill hot path of ContiguousKV.
+
+Argument marshalling only: every function forwards to the C ABI declared in
+``include/ckv.h`` (same names without the ``ckv_`` prefix).  Every step of the
+path runs in the library's HIP kernels; torch supplies device memory and
+streams.  There is no fallback: if ``libckv.so`` is missing or fails to load,
+importing this package raises.
+
+Tensor arguments are torch tensors on the current HIP device (or, where the C
+ABI allows host memory, pinned host tensors); they are passed by data pointer.
+``stream`` defaults to torch's current stream.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libckv.so")
+
+OK, EINVAL, EUNSUPPORTED, EHIP, ENOMEM, ESTATE = range(6)
+DTYPE_F32, DTYPE_BF16 = 0, 1
+CTX_HOST_PREFIX, CTX_MATERIALIZE, CTX_STAGE_TIMING = 0x1, 0x2, 0x4
+STAGES = ("score", "finalize", "select", "move", "attn")
+
+if not os.path.exists(LIB_PATH):
+    raise ImportError(f"libckv.so not built at {LIB_PATH}; run `python -m paper_2601_13631_amd.build`")
+_lib = ctypes.CDLL(LIB_PATH)
+
+
+class Dims(ctypes.Structure):
+    """``ckv_dims``: the problem shape."""
+    _fields_ = [
+        ("n_prefix", ctypes.c_int64),
+        ("n_suffix", ctypes.c_int32),
+        ("n_q_heads", ctypes.c_int32),
+        ("n_kv_heads", ctypes.c_int32),
+        ("head_dim", ctypes.c_int32),
+        ("chunk_size", ctypes.c_int32),
+        ("dtype", ctypes.c_int32),
+        ("sm_scale", ctypes.c_float),
+    ]
+
+    @property
+    def n_chunks(self) -> int:
+        return num_chunks(self.n_prefix, self.chunk_size)
+
+
+class LayerIO(ctypes.Structure):
+    """``ckv_layer_io``."""
+    _fields_ = [(f, ctypes.c_void_p) for f in (
+        "q", "k_suffix", "v_suffix", "k_probe", "k_prefix", "v_prefix", "kv_host", "kv_host_next",
+        "out", "chunk_scores", "sel_idx", "stream")]
+
+
+class LayerStats(ctypes.Structure):
+    """``ckv_layer_stats``."""
+    _fields_ = [(f, ctypes.c_int64) for f in (
+        "k", "hits", "misses", "wasted", "bytes_prefetch", "bytes_demand", "bytes_gathered")]
+
+    def as_dict(self) -> dict:
+        return {f: int(getattr(self, f)) for f, _ in self._fields_}
+
+
+_P = ctypes.c_void_p
+_DP = ctypes.POINTER(Dims)
+_SIG = {
+    "ckv_last_error": ([], ctypes.c_char_p),
+    "ckv_version": ([], ctypes.c_char_p),
+    "ckv_num_chunks": ([ctypes.c_int64, ctypes.c_int32], ctypes.c_int64),
+    "ckv_num_keep": ([ctypes.c_int64, ctypes.c_double], ctypes.c_int64),
+    "ckv_score_workspace_bytes": ([_DP], ctypes.c_size_t),
+    "ckv_score_chunks": ([_DP, _P, _P, _P, _P, ctypes.c_size_t, _P], ctypes.c_int32),
+    "ckv_select_workspace_bytes": ([ctypes.c_int64], ctypes.c_size_t),
+    "ckv_select_topk_chunks": ([_P, ctypes.c_int64, ctypes.c_int64, _P, _P, ctypes.c_size_t, _P],
+                               ctypes.c_int32),
+    "ckv_gather_chunks": ([_DP, _P, _P, _P, ctypes.c_int64, _P, _P, _P], ctypes.c_int32),
+    "ckv_attn_workspace_bytes": ([_DP, ctypes.c_int64], ctypes.c_size_t),
+    "ckv_sparse_prefill_attn": ([_DP, _P, _P, _P, _P, ctypes.c_int64, _P, _P, _P, _P,
+                                 ctypes.c_size_t, _P], ctypes.c_int32),
+    "ckv_ctx_create": ([_DP, ctypes.c_double, ctypes.c_int32, ctypes.POINTER(_P)], ctypes.c_int32),
+    "ckv_ctx_destroy": ([_P], ctypes.c_int32),
+    "ckv_ctx_reset": ([_P], ctypes.c_int32),
+    "ckv_ctx_stage_times": ([_P, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64)],
+                            ctypes.c_int32),
+    "ckv_reprefill_layer": ([_P, ctypes.c_int32, ctypes.POINTER(LayerIO),
+                             ctypes.POINTER(LayerStats)], ctypes.c_int32),
+}
+for _name, (_args, _res) in _SIG.items():
+    _f = getattr(_lib, _name)
+    _f.argtypes = _args
+    _f.restype = _res
+
+EXPORTED = tuple(_SIG)
+
+
+class CkvError(RuntimeError):
+    def __init__(self, status: int, what: str):
+        msg = _lib.ckv_last_error().decode(errors="replace")
+        super().__init__(f"{what} returned {status}: {msg}")
+        self.status = status
+
+
+def _check(status: int, what: str) -> None:
+    if status != OK:
+        raise CkvError(status, what)
+
+
+def _ptr(t) -> int | None:
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    return t.data_ptr()
+
+
+def _stream(stream) -> int | None:
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def version() -> str:
+    return _lib.ckv_version().decode()
+
+
+def last_error() -> str:
+    return _lib.ckv_last_error().decode(errors="replace")
+
+
+def num_chunks(n: int, c: int) -> int:
+    return int(_lib.ckv_num_chunks(n, c))
+
+
+def num_keep(m: int, r: float) -> int:
+    return int(_lib.ckv_num_keep(m, r))
+
+
+def make_dims(n_prefix, n_suffix, n_q_heads, n_kv_heads, head_dim, chunk_size, dtype=DTYPE_BF16,
+              sm_scale=0.0) -> Dims:
+    return Dims(n_prefix, n_suffix, n_q_heads, n_kv_heads, head_dim, chunk_size, dtype, sm_scale)
+
+
+def score_workspace_bytes(dims: Dims) -> int:
+    return int(_lib.ckv_score_workspace_bytes(ctypes.byref(dims)))
+
+
+def score_chunks(dims: Dims, q, k_prefix, chunk_scores, ws, stream=None) -> None:
+    _check(_lib.ckv_score_chunks(ctypes.byref(dims), _ptr(q), _ptr(k_prefix), _ptr(chunk_scores),
+                                 _ptr(ws), ws.numel() * ws.element_size() if ws is not None else 0,
+                                 _stream(stream)), "ckv_score_chunks")
+
+
+def select_workspace_bytes(m: int) -> int:
+    return int(_lib.ckv_select_workspace_bytes(m))
+
+
+def select_topk_chunks(chunk_scores, m: int, k: int, sel_idx, ws=None, stream=None) -> None:
+    nbytes = ws.numel() * ws.element_size() if ws is not None else 0
+    _check(_lib.ckv_select_topk_chunks(_ptr(chunk_scores), m, k, _ptr(sel_idx), _ptr(ws), nbytes,
+                                       _stream(stream)), "ckv_select_topk_chunks")
+
+
+def gather_chunks(dims: Dims, k_src, v_src, sel_idx, k: int, k_sel, v_sel, stream=None) -> None:
+    _check(_lib.ckv_gather_chunks(ctypes.byref(dims), _ptr(k_src), _ptr(v_src), _ptr(sel_idx), k,
+                                  _ptr(k_sel), _ptr(v_sel), _stream(stream)), "ckv_gather_chunks")
+
+
+def attn_workspace_bytes(dims: Dims, k: int) -> int:
+    return int(_lib.ckv_attn_workspace_bytes(ctypes.byref(dims), k))
+
+
+def sparse_prefill_attn(dims: Dims, q, k_sel, v_sel, sel_idx, k: int, k_suffix, v_suffix, out,
+                        ws=None, stream=None) -> None:
+    nbytes = ws.numel() * ws.element_size() if ws is not None else 0
+    _check(_lib.ckv_sparse_prefill_attn(ctypes.byref(dims), _ptr(q), _ptr(k_sel), _ptr(v_sel),
+                                        _ptr(sel_idx), k, _ptr(k_suffix), _ptr(v_suffix), _ptr(out),
+                                        _ptr(ws), nbytes, _stream(stream)),
+           "ckv_sparse_prefill_attn")
+
+
+class Context:
+    """``ckv_ctx``: owns workspace, streams, events and (host-resident prefix) HBM slots."""
+
+    def __init__(self, dims: Dims, keep_ratio: float, flags: int = 0):
+        self.dims = dims
+        self._h = ctypes.c_void_p()
+        _check(_lib.ckv_ctx_create(ctypes.byref(dims), keep_ratio, flags, ctypes.byref(self._h)),
+               "ckv_ctx_create")
+        self.k = num_keep(dims.n_chunks, keep_ratio)
+
+    def reprefill_layer(self, layer: int, q, k_suffix, v_suffix, k_probe, out, k_prefix=None,
+                        v_prefix=None, kv_host=None, kv_host_next=None, chunk_scores=None,
+                        sel_idx=None, stream=None) -> dict:
+        io = LayerIO(_ptr(q), _ptr(k_suffix), _ptr(v_suffix), _ptr(k_probe), _ptr(k_prefix),
+                     _ptr(v_prefix), _ptr(kv_host), _ptr(kv_host_next), _ptr(out),
+                     _ptr(chunk_scores), _ptr(sel_idx), _stream(stream))
+        st = LayerStats()
+        _check(_lib.ckv_reprefill_layer(self._h, layer, ctypes.byref(io), ctypes.byref(st)),
+               "ckv_reprefill_layer")
+        return st.as_dict()
+
+    def stage_times(self) -> tuple:
+        """(per-stage total ms dict, number of layers) since creation or reset."""
+        ms = (ctypes.c_double * len(STAGES))()
+        n = ctypes.c_int64()
+        _check(_lib.ckv_ctx_stage_times(self._h, ms, ctypes.byref(n)), "ckv_ctx_stage_times")
+        return dict(zip(STAGES, list(ms))), int(n.value)
+
+    def reset(self) -> None:
+        _check(_lib.ckv_ctx_reset(self._h), "ckv_ctx_reset")
+
+    def close(self) -> None:
+        if self._h:
+            _check(_lib.ckv_ctx_destroy(self._h), "ckv_ctx_destroy")
+            self._h = ctypes.c_void_p()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

@@ -1,0 +1,500 @@
+// attn.hip -- Re-Prefill sparse attention (Def. 2.1) for gfx950, bf16.
+//
+// For query t of head h (KV head g = h / G) the keys are the tokens of the k
+// kept chunks (compact positions 0 .. k*c-1; rows past n of a short last chunk
+// are masked) followed by the suffix tokens 0..t (causal).
+//
+// Rows of one KV head are r = t*G + i (query t, head g*G + i), so the G query
+// heads that share a KV head share every K/V tile.  A workgroup owns 128 rows
+// (4 waves x 32) and one contiguous slice ("split") of the key positions.  Per
+// 32-key tile:
+//   S^T = K Q^T   bf16 MFMA 32x32x16, A = K rows from LDS, B = Q^T in
+//                 registers: every lane owns one query row and 16 keys;
+//   online softmax in fp32 (exp2 with sm_scale*log2 e folded in);
+//   O^T += V^T P^T  A = V^T read from LDS with the transposing
+//                 ds_read_tr16_b64, B = P^T straight from the softmax registers.
+// The K operand rows are loaded in a permuted order so that the registers a
+// lane holds after the first product are exactly the 8 consecutive keys the
+// second product needs from it -- no register shuffles between the two.
+// Splits write unnormalised fp32 partials and (max, sum); a combine kernel
+// merges them in split order (deterministic).
+
+#include "ckv_internal.h"
+
+namespace ckv {
+namespace {
+
+constexpr int kWaves = 4;
+constexpr int kWaveRows = 32;
+constexpr int kBlockRows = kWaves * kWaveRows;  // 128
+constexpr int kTile = 32;
+constexpr int kNoKey = 0x7fffffff;  // visibility limit of a masked key
+
+// MFMA row p of the K operand holds key kappa(p); afterwards register v of a
+// lane in half h holds key 16*(v/8) + 8*h + v%8.
+__device__ __forceinline__ int kappa(int p) {
+  const int i = p >> 3, h = (p >> 2) & 1, j = p & 3;
+  return 16 * (i >> 1) + 8 * h + 4 * (i & 1) + j;
+}
+
+// LDS swizzles (XOR of 16-byte segment index), conflict-free for the access
+// patterns of the two operand reads.
+template <int D>
+__device__ __forceinline__ int k_swz(int row) {
+  if constexpr (D == 128)
+    return ((row & 1) ? 1 : 0) ^ ((row & 2) ? 2 : 0) ^ ((row & 4) ? 8 : 0) ^ ((row & 8) ? 4 : 0);
+  else
+    return ((row & 1) ? 1 : 0) ^ ((row & 2) ? 2 : 0) ^ ((row & 4) ? 1 : 0) ^ ((row & 8) ? 4 : 0);
+}
+template <int D>
+__device__ __forceinline__ int v_swz(int row) {
+  if constexpr (D == 128)
+    return ((row & 1) ? 4 : 0) ^ ((row & 2) ? 10 : 0);
+  else
+    return ((row & 1) ? 2 : 0) ^ ((row & 2) ? 4 : 0);
+}
+template <int D>
+__device__ __forceinline__ int k_off(int row, int seg) { return row * D + ((seg ^ k_swz<D>(row)) << 3); }
+template <int D>
+__device__ __forceinline__ int v_off(int row, int seg) { return row * D + ((seg ^ v_swz<D>(row)) << 3); }
+
+__device__ __forceinline__ float partner_f(float x) {
+  int v = __float_as_int(x);
+  auto r = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+  return __int_as_float(threadIdx.x & 32 ? r[0] : r[1]);
+}
+
+struct AttnArgs {
+  const uint16_t* q;       // [S][Hq][D]
+  const uint16_t* kbase;   // prefix chunks (see ChunkSource)
+  const uint16_t* vbase;
+  int64_t chunk_stride;    // elements
+  const int32_t* chunk_off;
+  int32_t direct;
+  const int32_t* sel;      // [k]
+  int64_t kc;              // k * c prefix positions
+  int64_t n;
+  int c;
+  const uint16_t* ks;      // [S][Hkv][D]
+  const uint16_t* vs;
+  uint16_t* out;           // [S][Hq][D]
+  float* o_part;           // [splits][Hkv][R][D]
+  float2* ml_part;         // [splits][Hkv][R]
+  int S, Hq, Hkv, G, R, n_splits, tiles_per_split, n_row_blocks;
+  float c1;
+  uint32_t nblocks, nblocks_padded;
+};
+
+// Loads tile `tile` of positions into LDS and writes each key's visibility
+// limit (a row with query t sees the key iff t >= lim).  Returns true if every
+// key of the tile is visible to every row.
+template <int D>
+__device__ __forceinline__ bool load_tile(const AttnArgs& a, int g, int64_t tile, uint16_t* lk,
+                                          uint16_t* lv, int* lim) {
+  constexpr int kSegs = D / 8;
+  constexpr int kPer = kTile * kSegs / (kWaves * 64);
+  bool all_vis = true;
+#pragma unroll
+  for (int p = 0; p < kPer; ++p) {
+    const int idx = threadIdx.x + p * kWaves * 64;
+    const int key = idx / kSegs, seg = idx % kSegs;
+    const int64_t pos = tile * kTile + key;
+    const uint16_t* ksrc = nullptr;
+    const uint16_t* vsrc = nullptr;
+    int limit = kNoKey;
+    if (pos < a.kc) {
+      const int64_t u = pos / a.c;
+      const int off = (int)(pos - u * a.c);
+      const int64_t j = a.sel[u];
+      const int64_t len = j >= 0 ? min<int64_t>(a.c, a.n - j * a.c) : 0;  // index outside [0, m): empty
+      if (off < len) {
+        const int64_t slot = a.chunk_off ? (int64_t)a.chunk_off[u] : (a.direct ? j : u);
+        const int64_t e = slot * a.chunk_stride + ((int64_t)off * a.Hkv + g) * D + seg * 8;
+        ksrc = a.kbase + e;
+        vsrc = a.vbase + e;
+        limit = -1;
+      }
+    } else if (pos < a.kc + a.S) {
+      const int64_t tok = pos - a.kc;
+      const int64_t e = (tok * a.Hkv + g) * D + seg * 8;
+      ksrc = a.ks + e;
+      vsrc = a.vs + e;
+      limit = (int)tok;
+    }
+    u32x4 kv = {0u, 0u, 0u, 0u}, vv = {0u, 0u, 0u, 0u};
+    if (ksrc) {
+      kv = *reinterpret_cast<const u32x4*>(ksrc);
+      vv = *reinterpret_cast<const u32x4*>(vsrc);
+    }
+    *reinterpret_cast<u32x4*>(lk + k_off<D>(key, seg)) = kv;
+    *reinterpret_cast<u32x4*>(lv + v_off<D>(key, seg)) = vv;
+    if (seg == 0) lim[key] = limit;
+    all_vis = all_vis && (limit == -1);
+  }
+  return all_vis;
+}
+
+template <int D>
+__global__ __launch_bounds__(kWaves * 64, 2) void attn_kernel(AttnArgs a) {
+  __shared__ __attribute__((aligned(16))) uint16_t lk[kTile * D];
+  __shared__ __attribute__((aligned(16))) uint16_t lv[kTile * D];
+  __shared__ int lim[kTile];
+
+  // logical order (g, split, row block): blocks reading the same K/V tiles are
+  // adjacent, hence on the same XCD and its L2
+  const uint32_t L = xcd_remap(blockIdx.x, a.nblocks_padded);
+  if (L >= a.nblocks) return;
+  const int rb = (int)(L % a.n_row_blocks);
+  const int split = (int)((L / a.n_row_blocks) % a.n_splits);
+  const int g = (int)(L / ((uint32_t)a.n_splits * a.n_row_blocks));
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, half = lane >> 5;
+
+  const int row = rb * kBlockRows + wave * kWaveRows + (lane & 31);
+  const bool row_ok = row < a.R;
+  const int t = row_ok ? row / a.G : -1;
+  const int hi = row_ok ? row % a.G : 0;
+
+  // last query of the block bounds the suffix keys anyone here can see
+  const int last_row = min(a.R - 1, rb * kBlockRows + kBlockRows - 1);
+  const int64_t np_block = a.kc + last_row / a.G + 1;
+  const int64_t ntiles = (np_block + kTile - 1) / kTile;
+  const int64_t tile0 = (int64_t)split * a.tiles_per_split;
+  const int64_t tile1 = min<int64_t>(ntiles, tile0 + a.tiles_per_split);
+
+  bf16x8 qf[D / 16];
+  {
+    const uint16_t* src = a.q + ((int64_t)(row_ok ? t : 0) * a.Hq + (int64_t)g * a.G + hi) * D + 8 * half;
+#pragma unroll
+    for (int ks = 0; ks < D / 16; ++ks) {
+      u32x4 v = {0u, 0u, 0u, 0u};
+      if (row_ok) v = *reinterpret_cast<const u32x4*>(src + 16 * ks);
+      qf[ks] = *reinterpret_cast<bf16x8*>(&v);
+    }
+  }
+
+  f32x16 o[D / 32];
+#pragma unroll
+  for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) o[db][v] = 0.f;
+  float m_run = -INFINITY, l_run = 0.f;
+
+  const int krow = kappa(lane & 31);
+  for (int64_t tile = tile0; tile < tile1; ++tile) {
+    __syncthreads();
+    const bool my_vis = load_tile<D>(a, g, tile, lk, lv, lim);
+    const bool all_vis = __syncthreads_and(my_vis ? 1 : 0);
+
+    f32x16 s;
+#pragma unroll
+    for (int v = 0; v < 16; ++v) s[v] = 0.f;
+#pragma unroll
+    for (int ks = 0; ks < D / 16; ++ks) {
+      bf16x8 kf = *reinterpret_cast<const bf16x8*>(lk + k_off<D>(krow, 2 * ks + half));
+      s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[ks], s, 0, 0, 0);
+    }
+    // register v holds key 16*(v/8) + 8*half + v%8
+    if (!all_vis) {
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int key = 16 * (v >> 3) + 8 * half + (v & 7);
+        if (t < lim[key]) s[v] = -INFINITY;
+      }
+    }
+    float mx = s[0];
+#pragma unroll
+    for (int v = 1; v < 16; ++v) mx = fmaxf(mx, s[v]);
+    mx = fmaxf(mx, partner_f(mx));
+    const float m_new = fmaxf(m_run, mx * a.c1);
+    const float m_use = m_new == -INFINITY ? 0.f : m_new;
+    const float alpha = __builtin_amdgcn_exp2f(m_run - m_use);
+    float rs = 0.f;
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      s[v] = __builtin_amdgcn_exp2f(fmaf(s[v], a.c1, -m_use));
+      rs += s[v];
+    }
+    rs += partner_f(rs);
+    l_run = l_run * alpha + rs;
+    m_run = m_new;
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) o[db][v] *= alpha;
+
+    bf16x8 pb[2];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) pb[kb][e] = (__bf16)s[8 * kb + e];
+
+    // V^T fragments: lane (group G4 = lane/16, s = lane%16) supplies the address of
+    // row 16*kb + 8*half + 4*rd + s/4, columns 32*db + 16*(G4%2) + 4*(s%4) .. +3
+    const int s16 = lane & 15, g4 = (lane >> 4) & 1;
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db) {
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb) {
+        s16x4 part[2];
+#pragma unroll
+        for (int rd = 0; rd < 2; ++rd) {
+          const int vrow = 16 * kb + 8 * half + 4 * rd + (s16 >> 2);
+          const int col = 32 * db + 16 * g4 + 4 * (s16 & 3);
+          const int off = v_off<D>(vrow, col >> 3) + (col & 7);
+          part[rd] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+              (__attribute__((address_space(3))) s16x4*)(lv + off));
+        }
+        bf16x8 vf;
+        *reinterpret_cast<s16x4*>(&vf) = part[0];
+        *(reinterpret_cast<s16x4*>(&vf) + 1) = part[1];
+        o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pb[kb], o[db], 0, 0, 0);
+      }
+    }
+  }
+
+  // o[db][v] holds d = 32*db + 8*(v/4) + 4*half + v%4 of this lane's row
+  if (!row_ok) return;
+  if (a.n_splits == 1) {
+    const float inv = 1.f / l_run;
+    uint16_t* dst = a.out + ((int64_t)t * a.Hq + (int64_t)g * a.G + hi) * D + 4 * half;
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+      for (int q4 = 0; q4 < 4; ++q4) {
+        __bf16 b[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) b[j] = (__bf16)(o[db][4 * q4 + j] * inv);
+        *reinterpret_cast<uint2*>(dst + 32 * db + 8 * q4) = *reinterpret_cast<uint2*>(b);
+      }
+  } else {
+    const int64_t prow = ((int64_t)split * a.Hkv + g) * a.R + row;
+    float* dst = a.o_part + prow * D + 4 * half;
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+      for (int q4 = 0; q4 < 4; ++q4)
+        *reinterpret_cast<f32x4*>(dst + 32 * db + 8 * q4) =
+            f32x4{o[db][4 * q4], o[db][4 * q4 + 1], o[db][4 * q4 + 2], o[db][4 * q4 + 3]};
+    if (half == 0) a.ml_part[prow] = make_float2(m_run, l_run);
+  }
+}
+
+// Merges the splits of each row in split order: out = sum_s e_s O_s / sum_s e_s l_s
+// with e_s = exp2(m_s - max m).  One thread per (row, 8 columns).
+template <int D>
+__global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ o_part,
+                                                      const float2* __restrict__ ml_part,
+                                                      uint16_t* __restrict__ out, int n_splits,
+                                                      int Hkv, int R, int G, int Hq) {
+  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int64_t rows = (int64_t)Hkv * R;
+  if (idx >= rows * (D / 8)) return;
+  const int64_t grow = idx / (D / 8);
+  const int c8 = (int)(idx % (D / 8)) * 8;
+  float M = -INFINITY;
+  for (int s = 0; s < n_splits; ++s) M = fmaxf(M, ml_part[s * rows + grow].x);
+  float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  float Lsum = 0.f;
+  for (int s = 0; s < n_splits; ++s) {
+    const float2 ml = ml_part[s * rows + grow];
+    const float e = ml.x == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(ml.x - M);
+    Lsum += e * ml.y;
+    const float* src = o_part + (s * rows + grow) * D + c8;
+    const f32x4 x0 = *reinterpret_cast<const f32x4*>(src);
+    const f32x4 x1 = *reinterpret_cast<const f32x4*>(src + 4);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) { acc[j] += e * x0[j]; acc[4 + j] += e * x1[j]; }
+  }
+  const int g = (int)(grow / R), row = (int)(grow % R);
+  const int t = row / G, i = row % G;
+  const float inv = 1.f / Lsum;
+  __bf16 b[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) b[j] = (__bf16)(acc[j] * inv);
+  *reinterpret_cast<uint4*>(out + ((int64_t)t * Hq + (int64_t)g * G + i) * D + c8) =
+      *reinterpret_cast<uint4*>(b);
+}
+
+// ---------------------------------------------------------------------------
+// fp32 path: one wave per (query t, head h).  Lane l visits keys l, l+64, ...
+// of the row's key sequence with its own online softmax (fp32, exp2 with the
+// scale folded in), then the 64 lane states are merged by a butterfly.
+// ---------------------------------------------------------------------------
+struct AttnArgsF32 {
+  const float* q;
+  const float* kbase;
+  const float* vbase;
+  int64_t chunk_stride;
+  const int32_t* chunk_off;
+  int32_t direct;
+  const int32_t* sel;
+  int64_t kc, n;
+  int c;
+  const float* ks;
+  const float* vs;
+  float* out;
+  int S, Hq, Hkv, G;
+  float c1;
+};
+
+template <int D>
+__global__ __launch_bounds__(64) void attn_f32_kernel(AttnArgsF32 a) {
+  const int64_t rid = blockIdx.x;  // t * Hq + h
+  const int t = (int)(rid / a.Hq), h = (int)(rid % a.Hq), g = h / a.G;
+  const int lane = threadIdx.x;
+  const float* qr = a.q + rid * D;
+  float o[D];
+#pragma unroll
+  for (int e = 0; e < D; ++e) o[e] = 0.f;
+  float m = -INFINITY, l = 0.f;
+  const int64_t np = a.kc + t + 1;
+  for (int64_t pos = lane; pos < np; pos += 64) {
+    const float* kr;
+    const float* vr;
+    if (pos < a.kc) {
+      const int64_t u = pos / a.c;
+      const int off = (int)(pos - u * a.c);
+      const int64_t j = a.sel[u];
+      if (j < 0 || off >= min<int64_t>(a.c, a.n - j * a.c)) continue;
+      const int64_t slot = a.chunk_off ? (int64_t)a.chunk_off[u] : (a.direct ? j : u);
+      const int64_t e = slot * a.chunk_stride + ((int64_t)off * a.Hkv + g) * D;
+      kr = a.kbase + e;
+      vr = a.vbase + e;
+    } else {
+      const int64_t e = ((pos - a.kc) * a.Hkv + g) * D;
+      kr = a.ks + e;
+      vr = a.vs + e;
+    }
+    float dot = 0.f;
+#pragma unroll
+    for (int e = 0; e < D; ++e) dot = fmaf(qr[e], kr[e], dot);
+    const float s = dot * a.c1;
+    const float mn = fmaxf(m, s);
+    const float alpha = __builtin_amdgcn_exp2f(m - mn);
+    const float p = __builtin_amdgcn_exp2f(s - mn);
+    l = l * alpha + p;
+#pragma unroll
+    for (int e = 0; e < D; ++e) o[e] = fmaf(p, vr[e], o[e] * alpha);
+    m = mn;
+  }
+  // butterfly merge of (m, l, o) across the wave
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const float m2 = __shfl_xor(m, off), l2 = __shfl_xor(l, off);
+    const float mn = fmaxf(m, m2);
+    const float a1 = m == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m - mn);
+    const float a2 = m2 == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m2 - mn);
+    l = l * a1 + l2 * a2;
+#pragma unroll
+    for (int e = 0; e < D; ++e) o[e] = o[e] * a1 + __shfl_xor(o[e], off) * a2;
+    m = mn;
+  }
+  const float inv = 1.f / l;
+  float* dst = a.out + rid * D;
+  // every lane holds the merged row; lane e writes element e
+#pragma unroll
+  for (int e = 0; e < D; ++e)
+    if (e % 64 == lane) dst[e] = o[e] * inv;
+}
+
+}  // namespace
+
+AttnPlan make_attn_plan(const ckv_dims* d, int64_t k) {
+  AttnPlan p{};
+  const int G = d->n_q_heads / d->n_kv_heads;
+  p.rows = G * d->n_suffix;
+  if (d->dtype == CKV_DTYPE_F32) {  // one wave per row, no splits
+    p.n_splits = 1;
+    return p;
+  }
+  const int64_t np = k * d->chunk_size + d->n_suffix;
+  const int64_t ntiles = ceil_div(np, kTile);
+  const int64_t base = (int64_t)d->n_kv_heads * ceil_div(p.rows, kBlockRows);
+  // enough workgroups for ~2 per CU, keeping >= 8 tiles per split
+  int64_t splits = ceil_div(512, base);
+  splits = std::min<int64_t>(splits, std::max<int64_t>(1, ntiles / 8));
+  splits = std::max<int64_t>(1, std::min<int64_t>(splits, 64));
+  p.n_splits = (int32_t)splits;
+  size_t off = 0;
+  if (splits > 1) {
+    const size_t rows = (size_t)d->n_kv_heads * p.rows;
+    p.off_o = off;
+    off = align_up(off + (size_t)splits * rows * d->head_dim * sizeof(float), 256);
+    p.off_ml = off;
+    off = align_up(off + (size_t)splits * rows * sizeof(float2), 256);
+  }
+  p.bytes = off;
+  return p;
+}
+
+ckv_status launch_attn(const ckv_dims* d, const void* q, const ChunkSource& src, const int32_t* sel,
+                       int64_t k, const void* k_suffix, const void* v_suffix, void* out, void* ws,
+                       size_t ws_bytes, hipStream_t st) {
+  if (d->dtype == CKV_DTYPE_F32) {
+    AttnArgsF32 a;
+    a.q = static_cast<const float*>(q);
+    a.kbase = static_cast<const float*>(src.k_base);
+    a.vbase = static_cast<const float*>(src.v_base);
+    a.chunk_stride = src.chunk_stride;
+    a.chunk_off = src.chunk_off;
+    a.direct = src.direct;
+    a.sel = sel;
+    a.kc = k * d->chunk_size;
+    a.n = d->n_prefix;
+    a.c = d->chunk_size;
+    a.ks = static_cast<const float*>(k_suffix);
+    a.vs = static_cast<const float*>(v_suffix);
+    a.out = static_cast<float*>(out);
+    a.S = d->n_suffix; a.Hq = d->n_q_heads; a.Hkv = d->n_kv_heads;
+    a.G = d->n_q_heads / d->n_kv_heads;
+    a.c1 = resolve_scale(d) * 1.4426950408889634f;
+    hipLaunchKernelGGL(attn_f32_kernel<64>, dim3((unsigned)((int64_t)a.S * a.Hq)), dim3(64), 0, st, a);
+    CKV_HIP(hipGetLastError());
+    return CKV_OK;
+  }
+  const AttnPlan p = make_attn_plan(d, k);
+  if (ws_bytes < p.bytes) CKV_FAIL(CKV_EINVAL, "attention workspace too small: %zu < %zu", ws_bytes, p.bytes);
+  AttnArgs a;
+  a.q = static_cast<const uint16_t*>(q);
+  a.kbase = static_cast<const uint16_t*>(src.k_base);
+  a.vbase = static_cast<const uint16_t*>(src.v_base);
+  a.chunk_stride = src.chunk_stride;
+  a.chunk_off = src.chunk_off;
+  a.direct = src.direct;
+  a.sel = sel;
+  a.kc = k * d->chunk_size;
+  a.n = d->n_prefix;
+  a.c = d->chunk_size;
+  a.ks = static_cast<const uint16_t*>(k_suffix);
+  a.vs = static_cast<const uint16_t*>(v_suffix);
+  a.out = static_cast<uint16_t*>(out);
+  a.o_part = p.n_splits > 1 ? reinterpret_cast<float*>(static_cast<char*>(ws) + p.off_o) : nullptr;
+  a.ml_part = p.n_splits > 1 ? reinterpret_cast<float2*>(static_cast<char*>(ws) + p.off_ml) : nullptr;
+  a.S = d->n_suffix; a.Hq = d->n_q_heads; a.Hkv = d->n_kv_heads;
+  a.G = d->n_q_heads / d->n_kv_heads; a.R = p.rows;
+  a.n_splits = p.n_splits;
+  const int64_t ntiles = ceil_div(a.kc + a.S, kTile);
+  a.tiles_per_split = (int)ceil_div(ntiles, p.n_splits);
+  a.n_row_blocks = (int)ceil_div(p.rows, kBlockRows);
+  a.c1 = resolve_scale(d) * 1.4426950408889634f;
+  a.nblocks = (uint32_t)((int64_t)a.Hkv * a.n_row_blocks * a.n_splits);
+  a.nblocks_padded = (uint32_t)align_up(a.nblocks, 8);
+  if (d->head_dim == 128)
+    hipLaunchKernelGGL(attn_kernel<128>, dim3(a.nblocks_padded), dim3(kWaves * 64), 0, st, a);
+  else
+    hipLaunchKernelGGL(attn_kernel<64>, dim3(a.nblocks_padded), dim3(kWaves * 64), 0, st, a);
+  CKV_HIP(hipGetLastError());
+  if (p.n_splits > 1) {
+    const int64_t work = (int64_t)a.Hkv * a.R * (d->head_dim / 8);
+    if (d->head_dim == 128)
+      hipLaunchKernelGGL(combine_kernel<128>, dim3((unsigned)ceil_div(work, 256)), dim3(256), 0, st,
+                         a.o_part, a.ml_part, a.out, a.n_splits, a.Hkv, a.R, a.G, a.Hq);
+    else
+      hipLaunchKernelGGL(combine_kernel<64>, dim3((unsigned)ceil_div(work, 256)), dim3(256), 0, st,
+                         a.o_part, a.ml_part, a.out, a.n_splits, a.Hkv, a.R, a.G, a.Hq);
+    CKV_HIP(hipGetLastError());
+  }
+  return CKV_OK;
+}
+
+}  // namespace ckv

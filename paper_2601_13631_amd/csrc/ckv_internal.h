@@ -1,0 +1,109 @@
+// ckv_internal.h -- internals shared by the libckv translation units (gfx950 only).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdint>
+#include <cstdio>
+#include <string>
+
+#include "../../include/ckv.h"
+
+namespace ckv {
+
+// ---- error reporting -------------------------------------------------------
+void set_error(const char* fmt, ...);
+void clear_error();
+
+#define CKV_FAIL(code, ...)   \
+  do {                        \
+    ::ckv::set_error(__VA_ARGS__); \
+    return (code);            \
+  } while (0)
+
+#define CKV_HIP(call)                                                                   \
+  do {                                                                                  \
+    hipError_t e_ = (call);                                                             \
+    if (e_ != hipSuccess)                                                               \
+      CKV_FAIL(CKV_EHIP, "%s failed: %s (%d) at %s:%d", #call, hipGetErrorString(e_),   \
+               (int)e_, __FILE__, __LINE__);                                            \
+  } while (0)
+
+// ---- vector types ----------------------------------------------------------
+typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
+typedef __attribute__((ext_vector_type(16))) float f32x16;
+typedef __attribute__((ext_vector_type(4))) float f32x4;
+typedef __attribute__((ext_vector_type(4))) short s16x4;
+typedef __attribute__((ext_vector_type(4))) uint32_t u32x4;
+
+// ---- shape checks ------------------------------------------------------------
+inline int elem_bytes(int dtype) { return dtype == CKV_DTYPE_F32 ? 4 : 2; }
+
+// Validates the shape fields; returns CKV_OK, CKV_EINVAL or CKV_EUNSUPPORTED
+// and records the reason.
+ckv_status check_dims(const ckv_dims* d);
+
+inline bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+inline float resolve_scale(const ckv_dims* d) {
+  return d->sm_scale > 0.f ? d->sm_scale : 1.0f / sqrtf((float)d->head_dim);
+}
+
+inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+// ---- launch helpers ------------------------------------------------------------
+// Workgroups are dispatched round-robin over the 8 XCDs (blockIdx % 8).  This
+// maps a hardware block id to a logical id so that consecutive logical ids run
+// on the same XCD and share its L2.  nblocks_padded is a multiple of 8.
+__device__ __forceinline__ uint32_t xcd_remap(uint32_t bid, uint32_t nblocks_padded) {
+  return (bid & 7u) * (nblocks_padded >> 3) + (bid >> 3);
+}
+
+// ---- kernels' host-side launchers (each file owns its kernels) ----------------
+struct ScorePlan {
+  int64_t m;          // chunks
+  int32_t rows;       // G*S rows per KV head
+  int32_t key_range;  // keys per range (multiple of 32 and of c)
+  int32_t n_ranges;   // ceil(n / key_range)
+  int32_t cpr;        // chunks per range
+  size_t off_part, off_mc, off_z, off_wpart, bytes;  // workspace layout
+};
+ScorePlan make_score_plan(const ckv_dims* d);
+// after_main (optional) is recorded between the main kernel and the finalize kernels.
+ckv_status launch_score(const ckv_dims* d, const void* q, const void* k, double* scores,
+                        void* ws, size_t ws_bytes, hipStream_t st,
+                        hipEvent_t after_main = nullptr);
+
+size_t select_ws_bytes(int64_t m);
+ckv_status launch_select(const double* scores, int64_t m, int64_t k, int32_t* sel, void* ws,
+                         size_t ws_bytes, hipStream_t st);
+
+// Chunk addressing for gather/attention: chunk u's K rows start at
+// k_base + off(u) * chunk_stride elements (V likewise from v_base), where
+// off(u) = chunk_off ? chunk_off[u] : (direct ? sel[u] : u).  Row stride inside a
+// chunk is Hkv*d elements.
+struct ChunkSource {
+  const void* k_base;
+  const void* v_base;
+  int64_t chunk_stride;     // elements between consecutive chunk slots
+  const int32_t* chunk_off; // optional per-chunk slot table (device)
+  int32_t direct;           // 1: off(u) = sel[u]; 0: off(u) = u (unless chunk_off)
+};
+
+ckv_status launch_gather(const ckv_dims* d, const void* k_src, const void* v_src,
+                         const int32_t* sel, int64_t k, void* k_dst, void* v_dst, hipStream_t st);
+
+struct AttnPlan {
+  int32_t rows;      // G*S rows per KV head
+  int32_t n_splits;  // key splits (1: no combine)
+  size_t off_o, off_ml, bytes;
+};
+AttnPlan make_attn_plan(const ckv_dims* d, int64_t k);
+ckv_status launch_attn(const ckv_dims* d, const void* q, const ChunkSource& src,
+                       const int32_t* sel, int64_t k, const void* k_suffix, const void* v_suffix,
+                       void* out, void* ws, size_t ws_bytes, hipStream_t st);
+
+}  // namespace ckv

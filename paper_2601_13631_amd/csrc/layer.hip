@@ -1,0 +1,373 @@
+// layer.hip -- the Re-Prefill layer step and its context (ckv_ctx).
+//
+// HBM-resident prefix: score -> select -> attention reading the kept chunks'
+// spans in place (or, with CKV_CTX_MATERIALIZE, gather -> attention over the
+// compact copy), all on the caller's stream with no host synchronisation.
+//
+// Host-resident prefix (Sec. 4.3.2, with one layer per Period): the K/V store
+// of every layer lives in pinned host memory, chunk-major (chunk j of a layer
+// is one span: K rows then V rows).  Two HBM slot buffers alternate between
+// layers.  While layer l computes, the chunks that layer l selected are copied
+// for layer l+1 into the other buffer on a prefetch stream (the prediction
+// P_{l+1} = S_l).  When layer l+1 has selected S_{l+1}, only the difference
+// S_{l+1} \ P_{l+1} is fetched on a demand stream into the free slots behind
+// the prefetched ones, and the attention reads every kept chunk through a
+// chunk -> slot table.  Copies move whole chunk spans; runs of consecutive
+// chunks are merged into one copy.  The selection is the step's only
+// device -> host dependency.
+
+#include <cstring>
+#include <new>
+#include <vector>
+
+#include "ckv_internal.h"
+
+using namespace ckv;
+
+struct ckv_ctx {
+  ckv_dims dims;
+  double keep_ratio;
+  int32_t flags;
+  int64_t m, k;
+  int device;
+  // workspace (device)
+  void* ws = nullptr;
+  size_t ws_score = 0, ws_attn = 0, off_attn = 0, off_scores = 0, off_sel = 0, off_ksel = 0,
+         off_vsel = 0, ws_bytes = 0;
+  // host-resident prefix
+  int64_t slot_bytes = 0;  // one chunk: K span + V span
+  int64_t slots_per_buf = 0;
+  void* slots[2] = {nullptr, nullptr};
+  int32_t* slot_tab_dev[2] = {nullptr, nullptr};
+  int32_t* sel_host = nullptr;      // pinned [k]
+  int32_t* slot_tab_host[2] = {nullptr, nullptr};  // pinned [k]
+  hipStream_t demand = nullptr, prefetch = nullptr;
+  hipEvent_t ev_sel = nullptr, ev_dem = nullptr, ev_pref[2] = {nullptr, nullptr},
+             ev_attn[2] = {nullptr, nullptr};
+  bool pref_pending[2] = {false, false}, attn_recorded[2] = {false, false};
+  std::vector<int32_t> pred;  // prediction for the next layer (ascending), in slots 0..|pred|-1
+  int32_t next_layer = 0;
+  // stage timing: a ring of event sets, harvested when a set is reused or on query
+  static constexpr int kRing = 64;
+  hipEvent_t tev[kRing][CKV_N_STAGES + 1] = {};
+  int64_t t_issued = 0, t_done = 0;
+  double t_ms[CKV_N_STAGES] = {};
+};
+
+namespace {
+
+ckv_status free_ctx(ckv_ctx* c) {
+  if (!c) return CKV_OK;
+  if (c->demand) (void)hipStreamSynchronize(c->demand);
+  if (c->prefetch) (void)hipStreamSynchronize(c->prefetch);
+  (void)hipFree(c->ws);
+  for (int i = 0; i < 2; ++i) {
+    (void)hipFree(c->slots[i]);
+    (void)hipFree(c->slot_tab_dev[i]);
+    (void)hipHostFree(c->slot_tab_host[i]);
+    if (c->ev_pref[i]) (void)hipEventDestroy(c->ev_pref[i]);
+    if (c->ev_attn[i]) (void)hipEventDestroy(c->ev_attn[i]);
+  }
+  (void)hipHostFree(c->sel_host);
+  for (auto& set : c->tev)
+    for (auto& e : set)
+      if (e) (void)hipEventDestroy(e);
+  if (c->ev_sel) (void)hipEventDestroy(c->ev_sel);
+  if (c->ev_dem) (void)hipEventDestroy(c->ev_dem);
+  if (c->demand) (void)hipStreamDestroy(c->demand);
+  if (c->prefetch) (void)hipStreamDestroy(c->prefetch);
+  delete c;
+  return CKV_OK;
+}
+
+#define CKV_HIP_ALLOC(call)                                                              \
+  do {                                                                                   \
+    hipError_t e_ = (call);                                                              \
+    if (e_ != hipSuccess) {                                                              \
+      set_error("%s failed: %s", #call, hipGetErrorString(e_));                          \
+      free_ctx(c);                                                                       \
+      return e_ == hipErrorOutOfMemory ? CKV_ENOMEM : CKV_EHIP;                          \
+    }                                                                                    \
+  } while (0)
+
+// Copies chunks[0..cnt) (ascending chunk indices) into consecutive slots
+// starting at slot0, one hipMemcpyAsync per run of consecutive chunk indices.
+ckv_status copy_runs(ckv_ctx* c, const int32_t* chunks, int64_t cnt, int64_t slot0,
+                     const void* host, void* buf, hipStream_t st) {
+  int64_t i = 0;
+  while (i < cnt) {
+    int64_t j = i + 1;
+    while (j < cnt && chunks[j] == chunks[j - 1] + 1) ++j;
+    const char* src = static_cast<const char*>(host) + (int64_t)chunks[i] * c->slot_bytes;
+    char* dst = static_cast<char*>(buf) + (slot0 + i) * c->slot_bytes;
+    CKV_HIP(hipMemcpyAsync(dst, src, (size_t)((j - i) * c->slot_bytes), hipMemcpyHostToDevice, st));
+    i = j;
+  }
+  return CKV_OK;
+}
+
+// Adds the stage times of the oldest unaccounted layer to the totals.
+ckv_status harvest_one(ckv_ctx* c) {
+  hipEvent_t* e = c->tev[c->t_done % ckv_ctx::kRing];
+  CKV_HIP(hipEventSynchronize(e[CKV_N_STAGES]));
+  for (int s = 0; s < CKV_N_STAGES; ++s) {
+    float ms = 0.f;
+    CKV_HIP(hipEventElapsedTime(&ms, e[s], e[s + 1]));
+    c->t_ms[s] += ms;
+  }
+  ++c->t_done;
+  return CKV_OK;
+}
+
+int64_t chunk_len(const ckv_dims* d, int64_t j) {
+  return std::min<int64_t>(d->chunk_size, d->n_prefix - j * d->chunk_size);
+}
+
+}  // namespace
+
+extern "C" {
+
+ckv_status ckv_ctx_create(const ckv_dims* dims, double keep_ratio, int32_t flags, ckv_ctx** out) {
+  clear_error();
+  if (!out) CKV_FAIL(CKV_EINVAL, "out is NULL");
+  *out = nullptr;
+  {
+    ckv_status s = check_dims(dims);
+    if (s != CKV_OK) return s;
+  }
+  if (!(keep_ratio > 0.0 && keep_ratio <= 1.0)) CKV_FAIL(CKV_EINVAL, "keep_ratio must be in (0, 1]");
+  if (flags & ~(CKV_CTX_HOST_PREFIX | CKV_CTX_MATERIALIZE | CKV_CTX_STAGE_TIMING))
+    CKV_FAIL(CKV_EINVAL, "unknown flags");
+  ckv_ctx* c = new (std::nothrow) ckv_ctx();
+  if (!c) CKV_FAIL(CKV_ENOMEM, "host allocation failed");
+  c->dims = *dims;
+  c->keep_ratio = keep_ratio;
+  c->flags = flags;
+  c->m = ckv_num_chunks(dims->n_prefix, dims->chunk_size);
+  c->k = ckv_num_keep(c->m, keep_ratio);
+  CKV_HIP_ALLOC(hipGetDevice(&c->device));
+
+  const int eb = elem_bytes(dims->dtype);
+  const int64_t span = (int64_t)dims->chunk_size * dims->n_kv_heads * dims->head_dim * eb;
+  c->ws_score = make_score_plan(dims).bytes;
+  c->ws_attn = make_attn_plan(dims, c->k).bytes;
+  // scoring and attention scratch are used one after the other on one stream,
+  // so both start at the front of the workspace
+  c->off_attn = 0;
+  size_t off = align_up(std::max(c->ws_score, c->ws_attn), 256);
+  c->off_scores = off;
+  off = align_up(off + (size_t)c->m * sizeof(double), 256);
+  c->off_sel = off;
+  off = align_up(off + (size_t)c->k * sizeof(int32_t), 256);
+  if (flags & CKV_CTX_MATERIALIZE) {
+    c->off_ksel = off;
+    off = align_up(off + (size_t)(c->k * span), 256);
+    c->off_vsel = off;
+    off = align_up(off + (size_t)(c->k * span), 256);
+  }
+  c->ws_bytes = off;
+  CKV_HIP_ALLOC(hipMalloc(&c->ws, c->ws_bytes));
+
+  if (flags & CKV_CTX_HOST_PREFIX) {
+    c->slot_bytes = 2 * span;
+    c->slots_per_buf = 2 * c->k;  // prefetched chunks plus room for a full miss set
+    for (int i = 0; i < 2; ++i) {
+      CKV_HIP_ALLOC(hipMalloc(&c->slots[i], (size_t)(c->slots_per_buf * c->slot_bytes)));
+      CKV_HIP_ALLOC(hipMalloc((void**)&c->slot_tab_dev[i], (size_t)c->k * sizeof(int32_t)));
+      CKV_HIP_ALLOC(hipHostMalloc((void**)&c->slot_tab_host[i], (size_t)c->k * sizeof(int32_t),
+                                  hipHostMallocDefault));
+      CKV_HIP_ALLOC(hipEventCreateWithFlags(&c->ev_pref[i], hipEventDisableTiming));
+      CKV_HIP_ALLOC(hipEventCreateWithFlags(&c->ev_attn[i], hipEventDisableTiming));
+    }
+    CKV_HIP_ALLOC(hipHostMalloc((void**)&c->sel_host, (size_t)c->k * sizeof(int32_t),
+                                hipHostMallocDefault));
+    CKV_HIP_ALLOC(hipStreamCreateWithFlags(&c->demand, hipStreamNonBlocking));
+    CKV_HIP_ALLOC(hipStreamCreateWithFlags(&c->prefetch, hipStreamNonBlocking));
+    CKV_HIP_ALLOC(hipEventCreateWithFlags(&c->ev_sel, hipEventDisableTiming));
+    CKV_HIP_ALLOC(hipEventCreateWithFlags(&c->ev_dem, hipEventDisableTiming));
+  }
+  if (flags & CKV_CTX_STAGE_TIMING)
+    for (auto& set : c->tev)
+      for (auto& e : set) CKV_HIP_ALLOC(hipEventCreate(&e));
+  *out = c;
+  return CKV_OK;
+}
+
+ckv_status ckv_ctx_stage_times(ckv_ctx* ctx, double* ms, int64_t* n_layers) {
+  clear_error();
+  if (!ctx || !ms || !n_layers) CKV_FAIL(CKV_EINVAL, "NULL argument");
+  if (!(ctx->flags & CKV_CTX_STAGE_TIMING)) CKV_FAIL(CKV_ESTATE, "context created without CKV_CTX_STAGE_TIMING");
+  while (ctx->t_done < ctx->t_issued) {
+    ckv_status s = harvest_one(ctx);
+    if (s != CKV_OK) return s;
+  }
+  for (int s = 0; s < CKV_N_STAGES; ++s) ms[s] = ctx->t_ms[s];
+  *n_layers = ctx->t_done;
+  return CKV_OK;
+}
+
+ckv_status ckv_ctx_destroy(ckv_ctx* ctx) { return free_ctx(ctx); }
+
+ckv_status ckv_ctx_reset(ckv_ctx* ctx) {
+  clear_error();
+  if (!ctx) CKV_FAIL(CKV_EINVAL, "ctx is NULL");
+  if (ctx->prefetch) CKV_HIP(hipStreamSynchronize(ctx->prefetch));
+  ctx->pred.clear();
+  ctx->pref_pending[0] = ctx->pref_pending[1] = false;
+  ctx->next_layer = 0;
+  while (ctx->t_done < ctx->t_issued) {
+    ckv_status s = harvest_one(ctx);
+    if (s != CKV_OK) return s;
+  }
+  for (double& x : ctx->t_ms) x = 0.0;
+  ctx->t_done = ctx->t_issued = 0;
+  return CKV_OK;
+}
+
+ckv_status ckv_reprefill_layer(ckv_ctx* c, int32_t layer, const ckv_layer_io* io,
+                               ckv_layer_stats* stats) {
+  clear_error();
+  if (!c || !io) CKV_FAIL(CKV_EINVAL, "NULL ctx or io");
+  const ckv_dims* d = &c->dims;
+  const bool host = c->flags & CKV_CTX_HOST_PREFIX;
+  if (!io->q || !io->k_suffix || !io->v_suffix || !io->k_probe || !io->out)
+    CKV_FAIL(CKV_EINVAL, "NULL tensor in io");
+  if (!aligned16(io->q) || !aligned16(io->k_suffix) || !aligned16(io->v_suffix) ||
+      !aligned16(io->k_probe) || !aligned16(io->out))
+    CKV_FAIL(CKV_EINVAL, "tensors must be 16-byte aligned");
+  if (host) {
+    if (!io->kv_host) CKV_FAIL(CKV_EINVAL, "host-resident prefix needs kv_host");
+    if (layer != c->next_layer)
+      CKV_FAIL(CKV_ESTATE, "host-resident layers must run in order (expected %d, got %d)",
+               c->next_layer, layer);
+  } else {
+    if (!io->k_prefix || !io->v_prefix) CKV_FAIL(CKV_EINVAL, "HBM-resident prefix needs k/v_prefix");
+    if (!aligned16(io->k_prefix) || !aligned16(io->v_prefix))
+      CKV_FAIL(CKV_EINVAL, "tensors must be 16-byte aligned");
+  }
+  hipStream_t st = (hipStream_t)io->stream;
+  char* ws = static_cast<char*>(c->ws);
+  double* scores = io->chunk_scores ? io->chunk_scores : reinterpret_cast<double*>(ws + c->off_scores);
+  int32_t* sel = io->sel_idx ? io->sel_idx : reinterpret_cast<int32_t*>(ws + c->off_sel);
+  const int64_t k = c->k;
+  const int eb = elem_bytes(d->dtype);
+  const int64_t span_elems = (int64_t)d->chunk_size * d->n_kv_heads * d->head_dim;
+
+  hipEvent_t* tev = nullptr;
+  if (c->flags & CKV_CTX_STAGE_TIMING) {
+    if (c->t_issued - c->t_done >= ckv_ctx::kRing) {  // reuse the oldest set: account it first
+      ckv_status s = harvest_one(c);
+      if (s != CKV_OK) return s;
+    }
+    tev = c->tev[c->t_issued % ckv_ctx::kRing];
+    CKV_HIP(hipEventRecord(tev[0], st));
+  }
+  auto mark = [&](int i) -> ckv_status {
+    if (tev) CKV_HIP(hipEventRecord(tev[i], st));
+    return CKV_OK;
+  };
+
+  ckv_status s = launch_score(d, io->q, io->k_probe, scores, ws, c->ws_score, st,
+                              tev ? tev[1] : nullptr);
+  if (s != CKV_OK) return s;
+  if ((s = mark(2)) != CKV_OK) return s;
+  s = launch_select(scores, c->m, k, sel, nullptr, 0, st);
+  if (s != CKV_OK) return s;
+  if ((s = mark(3)) != CKV_OK) return s;
+
+  ckv_layer_stats stv{};
+  stv.k = k;
+  if (!host) {
+    ChunkSource src{io->k_prefix, io->v_prefix, span_elems, nullptr, 1};
+    if (c->flags & CKV_CTX_MATERIALIZE) {
+      void* ksel = ws + c->off_ksel;
+      void* vsel = ws + c->off_vsel;
+      s = launch_gather(d, io->k_prefix, io->v_prefix, sel, k, ksel, vsel, st);
+      if (s != CKV_OK) return s;
+      src = ChunkSource{ksel, vsel, span_elems, nullptr, 0};
+    }
+    if ((s = mark(4)) != CKV_OK) return s;
+    s = launch_attn(d, io->q, src, sel, k, io->k_suffix, io->v_suffix, io->out, ws + c->off_attn,
+                    c->ws_attn, st);
+    if (s != CKV_OK) return s;
+    if ((s = mark(5)) != CKV_OK) return s;
+    if (tev) ++c->t_issued;
+    // K+V bytes of k full chunks (the set stays on the device, so a short last
+    // chunk, if kept, is counted at full length)
+    stv.bytes_gathered = 2 * k * span_elems * eb;
+    if (stats) *stats = stv;
+    return CKV_OK;
+  }
+
+  // ---- host-resident prefix ------------------------------------------------
+  const int cur = layer & 1, nxt = cur ^ 1;
+  CKV_HIP(hipMemcpyAsync(c->sel_host, sel, (size_t)k * sizeof(int32_t), hipMemcpyDeviceToHost, st));
+  CKV_HIP(hipEventRecord(c->ev_sel, st));
+  CKV_HIP(hipEventSynchronize(c->ev_sel));
+
+  // slot table: predicted chunks sit in slots 0..|P|-1 (in P order), misses follow
+  const std::vector<int32_t>& P = c->pred;
+  std::vector<int32_t> miss;
+  miss.reserve((size_t)k);
+  int32_t* tab = c->slot_tab_host[cur];
+  size_t pi = 0;
+  int64_t hits = 0;
+  for (int64_t u = 0; u < k; ++u) {
+    const int32_t j = c->sel_host[u];
+    while (pi < P.size() && P[pi] < j) ++pi;
+    if (pi < P.size() && P[pi] == j) {
+      tab[u] = (int32_t)pi;
+      ++hits;
+    } else {
+      tab[u] = (int32_t)(P.size() + miss.size());
+      miss.push_back(j);
+      stv.bytes_demand += 2 * chunk_len(d, j) * d->n_kv_heads * d->head_dim * eb;
+    }
+    stv.bytes_gathered += 2 * chunk_len(d, j) * d->n_kv_heads * d->head_dim * eb;
+  }
+  stv.hits = hits;
+  stv.misses = (int64_t)miss.size();
+  stv.wasted = (int64_t)P.size() - hits;
+
+  // demand copies into this layer's buffer (after the attention that last used it)
+  if (c->attn_recorded[cur]) CKV_HIP(hipStreamWaitEvent(c->demand, c->ev_attn[cur], 0));
+  s = copy_runs(c, miss.data(), (int64_t)miss.size(), (int64_t)P.size(), io->kv_host, c->slots[cur],
+                c->demand);
+  if (s != CKV_OK) return s;
+  CKV_HIP(hipMemcpyAsync(c->slot_tab_dev[cur], tab, (size_t)k * sizeof(int32_t),
+                         hipMemcpyHostToDevice, c->demand));
+  CKV_HIP(hipEventRecord(c->ev_dem, c->demand));
+
+  CKV_HIP(hipStreamWaitEvent(st, c->ev_dem, 0));
+  if (c->pref_pending[cur]) CKV_HIP(hipStreamWaitEvent(st, c->ev_pref[cur], 0));
+  c->pref_pending[cur] = false;
+  if ((s = mark(4)) != CKV_OK) return s;
+  ChunkSource src{c->slots[cur], static_cast<char*>(c->slots[cur]) + span_elems * eb,
+                  2 * span_elems, c->slot_tab_dev[cur], 0};
+  s = launch_attn(d, io->q, src, sel, k, io->k_suffix, io->v_suffix, io->out, ws + c->off_attn,
+                  c->ws_attn, st);
+  if (s != CKV_OK) return s;
+  if ((s = mark(5)) != CKV_OK) return s;
+  if (tev) ++c->t_issued;
+  CKV_HIP(hipEventRecord(c->ev_attn[cur], st));
+  c->attn_recorded[cur] = true;
+
+  // prefetch the next layer's copy of this layer's selection (P_{l+1} = S_l)
+  c->pred.assign(c->sel_host, c->sel_host + k);
+  if (io->kv_host_next) {
+    if (c->attn_recorded[nxt]) CKV_HIP(hipStreamWaitEvent(c->prefetch, c->ev_attn[nxt], 0));
+    s = copy_runs(c, c->pred.data(), k, 0, io->kv_host_next, c->slots[nxt], c->prefetch);
+    if (s != CKV_OK) return s;
+    CKV_HIP(hipEventRecord(c->ev_pref[nxt], c->prefetch));
+    c->pref_pending[nxt] = true;
+    for (int64_t u = 0; u < k; ++u)
+      stv.bytes_prefetch += 2 * chunk_len(d, c->pred[u]) * d->n_kv_heads * d->head_dim * eb;
+  } else {
+    c->pred.clear();
+  }
+  c->next_layer = layer + 1;
+  if (stats) *stats = stv;
+  return CKV_OK;
+}
+
+}  // extern "C"

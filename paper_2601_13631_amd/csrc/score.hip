@@ -1,0 +1,653 @@
+// score.hip -- chunk scoring (Sec. 4.4, Eq. 1) for gfx950.
+//
+// A_j = sum over rows r=(t,h) of sum_{i in chunk j} p_{r,i},
+// p_{r,i} = softmax_i(sm_scale * q_r . k_i) over the n prefix keys.
+//
+// Work split.  Rows of one KV head g are r = t*G + i (query t, head g*G+i).  A
+// workgroup owns 256 rows (4 waves x 64) of one KV head and one key range of
+// `key_range` keys.  Each wave keeps its 64 query rows in registers as the B
+// operand of bf16 MFMA 32x32x16 and streams the range's keys through LDS in
+// 32-key subtiles, computing S^T = K Q^T so that every lane owns one query row
+// and holds 16 of the 32 keys of a subtile (its partner lane l^32 the other 16).
+//
+// Softmax without a second pass.  Each (row, range) takes as reference mc the
+// scaled maximum of the range's first subtile and accumulates, per chunk,
+// P = sum exp2(c1*dot - mc) (c1 = sm_scale*log2 e) in fp32 over at most one
+// chunk, plus z = sum of the range's chunk sums in fp64.  A finalize kernel
+// folds the ranges of a row together in fp64: Mc = max mc, w = exp2(mc-Mc)/Z
+// with Z = sum exp2(mc-Mc) z, and A_j = sum_r w P in fp64.  The result is
+// exact in real arithmetic for any reference; the first-subtile reference only
+// has to keep exp2 finite.  If any chunk sum of a range is not finite the
+// workgroup recomputes that range with its true maximum (two passes), so the
+// fast path never trades correctness for speed.
+//
+// All sums have a fixed order: results are bitwise reproducible run to run.
+
+#include <cfloat>
+
+#include "ckv_internal.h"
+
+namespace ckv {
+namespace {
+
+constexpr int kWaves = 4;
+constexpr int kWaveRows = 64;
+constexpr int kBlockRows = kWaves * kWaveRows;  // 256
+constexpr int kSub = 32;                        // keys per subtile
+constexpr float kOverflowGuard = 0x1p100f;      // a chunk sum above this forces the exact pass
+
+enum ChunkMode { kC4 = 0, kC8 = 1, kC16 = 2, kC32x = 3 };
+
+__device__ __forceinline__ float partner_f(float x) {
+  // value of the same register in lane l^32
+  int v = __float_as_int(x);
+  auto r = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+  return __int_as_float(threadIdx.x & 32 ? r[0] : r[1]);
+}
+
+__device__ __forceinline__ double partner_d(double x) {
+  int2 v = *reinterpret_cast<int2*>(&x);
+  auto rx = __builtin_amdgcn_permlane32_swap(v.x, v.x, false, false);
+  auto ry = __builtin_amdgcn_permlane32_swap(v.y, v.y, false, false);
+  int2 o;
+  o.x = threadIdx.x & 32 ? rx[0] : rx[1];
+  o.y = threadIdx.x & 32 ? ry[0] : ry[1];
+  return *reinterpret_cast<double*>(&o);
+}
+
+// ---------------------------------------------------------------------------
+// bf16 main kernel
+// ---------------------------------------------------------------------------
+// LDS subtile: 32 keys x D bf16, 16-byte segments XOR-swizzled by key so that
+// the MFMA operand reads (consecutive lanes = consecutive keys, same segment)
+// hit distinct banks for both 8- and 16-lane bank cycles.
+template <int D>
+struct SubtileLds {
+  static constexpr int kSegs = D / 8;  // 16-byte segments per key row
+  __device__ static int offset(int key, int seg) {  // in bf16 elements
+    return key * D + ((seg ^ ((key ^ (key >> 3)) & (kSegs - 1))) * 8);
+  }
+};
+
+struct ScoreArgs {
+  const uint16_t* q;   // [S][Hq][D] bf16 bits
+  const uint16_t* k;   // [n][Hkv][D]
+  float* part;         // [Hkv][NR][CPR][R]
+  float* mc;           // [Hkv][NR][R]
+  double* z;           // [Hkv][NR][R]
+  int64_t n;
+  int S, Hq, Hkv, G, R, c, key_range, n_ranges, cpr, n_row_blocks;
+  float c1;            // sm_scale * log2(e)
+  uint32_t nblocks, nblocks_padded;
+};
+
+template <int D>
+__device__ __forceinline__ void load_subtile(const ScoreArgs& a, int g, int64_t key0,
+                                             uint16_t* lds) {
+  constexpr int kSegs = D / 8;
+  constexpr int kPer = kSub * kSegs / (kWaves * 64);  // 16-byte loads per thread
+  static_assert(kPer >= 1, "subtile too small");
+#pragma unroll
+  for (int p = 0; p < kPer; ++p) {
+    int idx = threadIdx.x + p * kWaves * 64;
+    int key = idx / kSegs, seg = idx % kSegs;
+    int64_t tok = key0 + key;
+    u32x4 v = {0u, 0u, 0u, 0u};
+    if (tok < a.n)
+      v = *reinterpret_cast<const u32x4*>(a.k + ((tok * a.Hkv + g) * D + seg * 8));
+    *reinterpret_cast<u32x4*>(lds + SubtileLds<D>::offset(key, seg)) = v;
+  }
+}
+
+// Per-chunk sums of one subtile for one row tile, combined across the lane pair.
+// Fills sums[] (how many depends on the mode) in the order of chunk index.
+template <int MODE>
+__device__ __forceinline__ void chunk_sums(const f32x16& p, float* sums) {
+  if constexpr (MODE == kC32x) {
+    float s = 0.f;
+#pragma unroll
+    for (int v = 0; v < 16; ++v) s += p[v];
+    sums[0] = s + partner_f(s);
+  } else if constexpr (MODE == kC16) {
+    float s0 = 0.f, s1 = 0.f;
+#pragma unroll
+    for (int v = 0; v < 8; ++v) { s0 += p[v]; s1 += p[v + 8]; }
+    sums[0] = s0 + partner_f(s0);
+    sums[1] = s1 + partner_f(s1);
+  } else if constexpr (MODE == kC8) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      float s = (p[4 * i] + p[4 * i + 1]) + (p[4 * i + 2] + p[4 * i + 3]);
+      sums[i] = s + partner_f(s);
+    }
+  } else {  // kC4: chunk 2i+h lives entirely in lane half h
+#pragma unroll
+    for (int i = 0; i < 4; ++i) sums[i] = (p[4 * i] + p[4 * i + 1]) + (p[4 * i + 2] + p[4 * i + 3]);
+  }
+}
+
+template <int MODE>
+constexpr int sums_per_lane() {
+  return MODE == kC32x ? 1 : MODE == kC16 ? 2 : 4;
+}
+
+// Processes the workgroup's key range once.  PASS 0: reference = first
+// subtile's maximum, writes partials.  PASS 1: only the exact range maximum
+// (into mref).  PASS 2: writes partials with mref as reference.
+template <int D, int MODE, int PASS>
+__device__ bool run_range(const ScoreArgs& a, int g, int range, int row0, const bf16x8 (&qf)[2][D / 16],
+                          uint16_t* lds, float (&mref)[2], double (&zsum)[2]) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int half = lane >> 5;
+  const int64_t kbeg = (int64_t)range * a.key_range;
+  const int64_t kend = min<int64_t>(kbeg + a.key_range, a.n);
+  const int nsub = (int)((kend - kbeg + kSub - 1) / kSub);
+  const int my_row0 = row0 + wave * kWaveRows;
+  bool overflow = false;
+  float chunk_acc[2] = {0.f, 0.f};  // kC32x with c > 32: running sum of the open chunk
+  if (PASS != 1) { zsum[0] = 0.0; zsum[1] = 0.0; }
+  if (PASS == 1) { mref[0] = -INFINITY; mref[1] = -INFINITY; }
+  float* part = a.part + ((int64_t)(g * a.n_ranges + range) * a.cpr) * a.R;
+
+  for (int s = 0; s < nsub; ++s) {
+    const int64_t key0 = kbeg + (int64_t)s * kSub;
+    __syncthreads();  // previous subtile fully consumed
+    load_subtile<D>(a, g, key0, lds);
+    __syncthreads();
+
+    f32x16 acc[2];
+#pragma unroll
+    for (int rt = 0; rt < 2; ++rt)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[rt][v] = 0.f;
+#pragma unroll
+    for (int ks = 0; ks < D / 16; ++ks) {
+      bf16x8 kf = *reinterpret_cast<const bf16x8*>(
+          lds + SubtileLds<D>::offset(lane & 31, 2 * ks + half));
+      acc[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[0][ks], acc[0], 0, 0, 0);
+      acc[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[1][ks], acc[1], 0, 0, 0);
+    }
+    // key of register v in this lane: key0 + 8*(v/4) + 4*half + v%4
+    const int nvalid = (int)min<int64_t>(kSub, kend - key0);
+
+    if (PASS == 1 || (PASS == 0 && s == 0)) {
+#pragma unroll
+      for (int rt = 0; rt < 2; ++rt) {
+        float mx = -INFINITY;
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          int key = 8 * (v >> 2) + 4 * half + (v & 3);
+          if (key < nvalid) mx = fmaxf(mx, acc[rt][v]);
+        }
+        mx = fmaxf(mx, partner_f(mx));
+        if (PASS == 1)
+          mref[rt] = fmaxf(mref[rt], mx * a.c1);
+        else
+          mref[rt] = mx * a.c1;
+      }
+    }
+    if (PASS == 1) continue;
+
+    // p = exp2(c1*dot - mc); invalid keys contribute 0
+#pragma unroll
+    for (int rt = 0; rt < 2; ++rt) {
+      const float nm = -mref[rt];
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        int key = 8 * (v >> 2) + 4 * half + (v & 3);
+        float e = __builtin_amdgcn_exp2f(fmaf(acc[rt][v], a.c1, nm));
+        acc[rt][v] = key < nvalid ? e : 0.f;
+      }
+    }
+
+    // per-chunk sums and their partial writes
+    if constexpr (MODE == kC32x) {
+      const int64_t chunk = key0 / a.c;                       // chunk of this subtile
+      const bool closes = ((key0 + kSub) % a.c == 0) || (s == nsub - 1);
+#pragma unroll
+      for (int rt = 0; rt < 2; ++rt) {
+        float sum;
+        chunk_sums<MODE>(acc[rt], &sum);
+        chunk_acc[rt] += sum;
+      }
+      if (closes) {
+        const int jl = (int)(chunk - kbeg / a.c);
+        const int row = my_row0 + lane;  // lane l writes row tile l/32, row l%32
+        float mine = half ? chunk_acc[1] : chunk_acc[0];
+        if (row < a.R) part[(int64_t)jl * a.R + row] = mine;
+#pragma unroll
+        for (int rt = 0; rt < 2; ++rt) {
+          overflow |= !(chunk_acc[rt] <= kOverflowGuard);
+          zsum[rt] += (double)chunk_acc[rt];
+          chunk_acc[rt] = 0.f;
+        }
+      }
+    } else {
+      constexpr int kN = sums_per_lane<MODE>();
+      const int jl0 = (int)((key0 - kbeg) / a.c);  // first chunk of this subtile
+#pragma unroll
+      for (int rt = 0; rt < 2; ++rt) {
+        float sums[kN];
+        chunk_sums<MODE>(acc[rt], sums);
+#pragma unroll
+        for (int i = 0; i < kN; ++i) {
+          overflow |= !(sums[i] <= kOverflowGuard);
+          zsum[rt] += (double)sums[i];
+        }
+        if constexpr (MODE == kC4) {
+          // lane half h holds chunks 2i+h of rows (row tile rt, row lane%32)
+          const int row = my_row0 + rt * 32 + (lane & 31);
+#pragma unroll
+          for (int i = 0; i < kN; ++i) {
+            int jl = jl0 + 2 * i + half;
+            int key_first = 8 * i + 4 * half;
+            if (row < a.R && key_first < nvalid) part[(int64_t)jl * a.R + row] = sums[i];
+          }
+        } else {
+          // both halves hold all sums: half h writes row tile h
+          if (rt == half) {
+            const int row = my_row0 + rt * 32 + (lane & 31);
+#pragma unroll
+            for (int i = 0; i < kN; ++i) {
+              int key_first = i * (kSub / kN);
+              if (row < a.R && key_first < nvalid) part[(int64_t)(jl0 + i) * a.R + row] = sums[i];
+            }
+          }
+        }
+      }
+    }
+  }
+  if constexpr (MODE == kC4) {
+    // each half summed different chunks: combine in a fixed order (half 0 + half 1)
+#pragma unroll
+    for (int rt = 0; rt < 2; ++rt) {
+      double o = partner_d(zsum[rt]);
+      zsum[rt] = half ? (o + zsum[rt]) : (zsum[rt] + o);
+    }
+  }
+  return overflow;
+}
+
+template <int D, int MODE>
+__global__ __launch_bounds__(kWaves * 64, 2) void score_bf16_kernel(ScoreArgs a) {
+  __shared__ __attribute__((aligned(16))) uint16_t lds[kSub * D];
+  const uint32_t L = xcd_remap(blockIdx.x, a.nblocks_padded);
+  if (L >= a.nblocks) return;
+  const int rb = (int)(L % a.n_row_blocks);
+  const int range = (int)((L / a.n_row_blocks) % a.n_ranges);
+  const int g = (int)(L / ((uint32_t)a.n_row_blocks * a.n_ranges));
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, half = lane >> 5;
+  const int row0 = rb * kBlockRows;
+
+  // Q^T fragments: B operand, lane l holds row l%32 and d = 16*ks + 8*half .. +7
+  bf16x8 qf[2][D / 16];
+#pragma unroll
+  for (int rt = 0; rt < 2; ++rt) {
+    const int row = row0 + wave * kWaveRows + rt * 32 + (lane & 31);
+    const bool ok = row < a.R;
+    const int t = ok ? row / a.G : 0, hi = ok ? row % a.G : 0;
+    const uint16_t* src = a.q + ((int64_t)t * a.Hq + (int64_t)g * a.G + hi) * D + 8 * half;
+#pragma unroll
+    for (int ks = 0; ks < D / 16; ++ks) {
+      u32x4 v = {0u, 0u, 0u, 0u};
+      if (ok) v = *reinterpret_cast<const u32x4*>(src + 16 * ks);
+      qf[rt][ks] = *reinterpret_cast<bf16x8*>(&v);
+    }
+  }
+
+  float mref[2];
+  double zsum[2];
+  bool of = run_range<D, MODE, 0>(a, g, range, row0, qf, lds, mref, zsum);
+  if (__syncthreads_or(of ? 1 : 0)) {
+    run_range<D, MODE, 1>(a, g, range, row0, qf, lds, mref, zsum);
+    run_range<D, MODE, 2>(a, g, range, row0, qf, lds, mref, zsum);
+  }
+  const int row = row0 + wave * kWaveRows + lane;  // lane l reports row tile l/32
+  if (row < a.R) {
+    const int64_t o = (int64_t)(g * a.n_ranges + range) * a.R + row;
+    a.mc[o] = half ? mref[1] : mref[0];
+    a.z[o] = half ? zsum[1] : zsum[0];
+  }
+}
+
+// ---------------------------------------------------------------------------
+// fp32 kernel (v_mfma_f32_32x32x2_f32), same structure without LDS staging:
+// K fragments are read straight from global memory (the fp32 workloads are
+// small).  One wave per workgroup, 64 rows.
+// ---------------------------------------------------------------------------
+struct ScoreArgsF32 {
+  const float* q;
+  const float* k;
+  float* part;
+  float* mc;
+  double* z;
+  int64_t n;
+  int S, Hq, Hkv, G, R, c, key_range, n_ranges, cpr, n_row_blocks;
+  float c1;
+  uint32_t nblocks;
+};
+
+template <int D, int MODE, int PASS>
+__device__ bool run_range_f32(const ScoreArgsF32& a, int g, int range, int row0,
+                              const float (&qf)[2][D / 2], float (&mref)[2], double (&zsum)[2]) {
+  const int lane = threadIdx.x & 63, half = lane >> 5;
+  const int64_t kbeg = (int64_t)range * a.key_range;
+  const int64_t kend = min<int64_t>(kbeg + a.key_range, a.n);
+  const int nsub = (int)((kend - kbeg + kSub - 1) / kSub);
+  bool overflow = false;
+  float chunk_acc[2] = {0.f, 0.f};
+  if (PASS != 1) { zsum[0] = 0.0; zsum[1] = 0.0; }
+  if (PASS == 1) { mref[0] = -INFINITY; mref[1] = -INFINITY; }
+  float* part = a.part + ((int64_t)(g * a.n_ranges + range) * a.cpr) * a.R;
+  for (int s = 0; s < nsub; ++s) {
+    const int64_t key0 = kbeg + (int64_t)s * kSub;
+    const int nvalid = (int)min<int64_t>(kSub, kend - key0);
+    const int64_t mykey = key0 + (lane & 31);
+    const float* krow = a.k + (min<int64_t>(mykey, a.n - 1) * a.Hkv + g) * D;
+    f32x16 acc[2];
+#pragma unroll
+    for (int rt = 0; rt < 2; ++rt)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[rt][v] = 0.f;
+#pragma unroll
+    for (int ks = 0; ks < D / 2; ++ks) {
+      float kf = krow[2 * ks + half];
+      acc[0] = __builtin_amdgcn_mfma_f32_32x32x2f32(kf, qf[0][ks], acc[0], 0, 0, 0);
+      acc[1] = __builtin_amdgcn_mfma_f32_32x32x2f32(kf, qf[1][ks], acc[1], 0, 0, 0);
+    }
+    if (PASS == 1 || (PASS == 0 && s == 0)) {
+#pragma unroll
+      for (int rt = 0; rt < 2; ++rt) {
+        float mx = -INFINITY;
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          int key = 8 * (v >> 2) + 4 * half + (v & 3);
+          if (key < nvalid) mx = fmaxf(mx, acc[rt][v]);
+        }
+        mx = fmaxf(mx, partner_f(mx));
+        if (PASS == 1)
+          mref[rt] = fmaxf(mref[rt], mx * a.c1);
+        else
+          mref[rt] = mx * a.c1;
+      }
+    }
+    if (PASS == 1) continue;
+#pragma unroll
+    for (int rt = 0; rt < 2; ++rt) {
+      const float nm = -mref[rt];
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        int key = 8 * (v >> 2) + 4 * half + (v & 3);
+        float e = __builtin_amdgcn_exp2f(fmaf(acc[rt][v], a.c1, nm));
+        acc[rt][v] = key < nvalid ? e : 0.f;
+      }
+    }
+    if constexpr (MODE == kC32x) {
+      const int64_t chunk = key0 / a.c;
+      const bool closes = ((key0 + kSub) % a.c == 0) || (s == nsub - 1);
+#pragma unroll
+      for (int rt = 0; rt < 2; ++rt) {
+        float sum;
+        chunk_sums<MODE>(acc[rt], &sum);
+        chunk_acc[rt] += sum;
+      }
+      if (closes) {
+        const int jl = (int)(chunk - kbeg / a.c);
+        const int row = row0 + lane;
+        float mine = half ? chunk_acc[1] : chunk_acc[0];
+        if (row < a.R) part[(int64_t)jl * a.R + row] = mine;
+#pragma unroll
+        for (int rt = 0; rt < 2; ++rt) {
+          overflow |= !(chunk_acc[rt] <= kOverflowGuard);
+          zsum[rt] += (double)chunk_acc[rt];
+          chunk_acc[rt] = 0.f;
+        }
+      }
+    } else {
+      constexpr int kN = sums_per_lane<MODE>();
+      const int jl0 = (int)((key0 - kbeg) / a.c);
+#pragma unroll
+      for (int rt = 0; rt < 2; ++rt) {
+        float sums[kN];
+        chunk_sums<MODE>(acc[rt], sums);
+#pragma unroll
+        for (int i = 0; i < kN; ++i) {
+          overflow |= !(sums[i] <= kOverflowGuard);
+          zsum[rt] += (double)sums[i];
+        }
+        if constexpr (MODE == kC4) {
+          const int row = row0 + rt * 32 + (lane & 31);
+#pragma unroll
+          for (int i = 0; i < kN; ++i) {
+            int jl = jl0 + 2 * i + half;
+            int key_first = 8 * i + 4 * half;
+            if (row < a.R && key_first < nvalid) part[(int64_t)jl * a.R + row] = sums[i];
+          }
+        } else if (rt == half) {
+          const int row = row0 + rt * 32 + (lane & 31);
+#pragma unroll
+          for (int i = 0; i < kN; ++i) {
+            int key_first = i * (kSub / kN);
+            if (row < a.R && key_first < nvalid) part[(int64_t)(jl0 + i) * a.R + row] = sums[i];
+          }
+        }
+      }
+    }
+  }
+  if constexpr (MODE == kC4) {
+#pragma unroll
+    for (int rt = 0; rt < 2; ++rt) {
+      double o = partner_d(zsum[rt]);
+      zsum[rt] = half ? (o + zsum[rt]) : (zsum[rt] + o);
+    }
+  }
+  return overflow;
+}
+
+template <int D, int MODE>
+__global__ __launch_bounds__(64) void score_f32_kernel(ScoreArgsF32 a) {
+  const uint32_t L = blockIdx.x;
+  if (L >= a.nblocks) return;
+  const int rb = (int)(L % a.n_row_blocks);
+  const int range = (int)((L / a.n_row_blocks) % a.n_ranges);
+  const int g = (int)(L / ((uint32_t)a.n_row_blocks * a.n_ranges));
+  const int lane = threadIdx.x & 63, half = lane >> 5;
+  const int row0 = rb * kWaveRows;
+  float qf[2][D / 2];
+#pragma unroll
+  for (int rt = 0; rt < 2; ++rt) {
+    const int row = row0 + rt * 32 + (lane & 31);
+    const bool ok = row < a.R;
+    const int t = ok ? row / a.G : 0, hi = ok ? row % a.G : 0;
+    const float* src = a.q + ((int64_t)t * a.Hq + (int64_t)g * a.G + hi) * D + half;
+#pragma unroll
+    for (int ks = 0; ks < D / 2; ++ks) qf[rt][ks] = ok ? src[2 * ks] : 0.f;
+  }
+  float mref[2];
+  double zsum[2];
+  bool of = run_range_f32<D, MODE, 0>(a, g, range, row0, qf, mref, zsum);
+  // one wave: the decision is wave-uniform via a ballot
+  if (__any(of)) {
+    run_range_f32<D, MODE, 1>(a, g, range, row0, qf, mref, zsum);
+    run_range_f32<D, MODE, 2>(a, g, range, row0, qf, mref, zsum);
+  }
+  const int row = row0 + lane;
+  if (row < a.R) {
+    const int64_t o = (int64_t)(g * a.n_ranges + range) * a.R + row;
+    a.mc[o] = half ? mref[1] : mref[0];
+    a.z[o] = half ? zsum[1] : zsum[0];
+  }
+}
+
+// ---------------------------------------------------------------------------
+// finalize
+// ---------------------------------------------------------------------------
+// F1: per (g, row): Mc = max over ranges of mc, Z = sum exp2(mc - Mc) z; the z
+// slot of every range is overwritten with w = exp2(mc - Mc) / Z.
+__global__ __launch_bounds__(256) void row_norm_kernel(const float* __restrict__ mc,
+                                                      double* __restrict__ z, int Hkv, int R,
+                                                      int NR) {
+  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (idx >= (int64_t)Hkv * R) return;
+  const int g = (int)(idx / R), row = (int)(idx % R);
+  const int64_t base = (int64_t)g * NR * R + row;
+  float M = -INFINITY;
+  for (int r = 0; r < NR; ++r) M = fmaxf(M, mc[base + (int64_t)r * R]);
+  double Z = 0.0;
+  for (int r = 0; r < NR; ++r)
+    Z += exp2((double)mc[base + (int64_t)r * R] - (double)M) * z[base + (int64_t)r * R];
+  const double inv = 1.0 / Z;
+  for (int r = 0; r < NR; ++r)
+    z[base + (int64_t)r * R] = exp2((double)mc[base + (int64_t)r * R] - (double)M) * inv;
+}
+
+// F2: per (g, chunk): wpart[g][j] = sum_r w[g][range(j)][r] * P[g][range][jl][r] in
+// fp64.  A workgroup of 256 threads serves 8 chunks, 32 lanes per chunk; each
+// lane sums rows lane, lane+32, ... in order, then a fixed butterfly reduces
+// the 32 lanes.
+__global__ __launch_bounds__(256) void chunk_reduce_kernel(const float* __restrict__ part,
+                                                          const double* __restrict__ w,
+                                                          double* __restrict__ wpart, int R,
+                                                          int NR, int cpr, int64_t m,
+                                                          int64_t m_pad) {
+  const int g = blockIdx.y;
+  const int64_t j = (int64_t)blockIdx.x * 8 + (threadIdx.x >> 5);
+  const int lane = threadIdx.x & 31;
+  if (j >= m) return;  // whole 32-lane groups exit together
+  const int range = (int)(j / cpr), jl = (int)(j % cpr);
+  const float* p = part + (((int64_t)g * NR + range) * cpr + jl) * R;
+  const double* wr = w + ((int64_t)g * NR + range) * R;
+  double s = 0.0;
+  for (int r = lane; r < R; r += 32) s += (double)p[r] * wr[r];
+#pragma unroll
+  for (int off = 16; off >= 1; off >>= 1) s += __shfl_xor(s, off, 32);
+  if (lane == 0) wpart[(int64_t)g * m_pad + j] = s;
+}
+
+// F3: A_j = sum over KV heads in order.
+__global__ __launch_bounds__(256) void head_sum_kernel(const double* __restrict__ wpart,
+                                                      double* __restrict__ A, int Hkv, int64_t m,
+                                                      int64_t m_pad) {
+  const int64_t j = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (j >= m) return;
+  double s = 0.0;
+  for (int g = 0; g < Hkv; ++g) s += wpart[(int64_t)g * m_pad + j];
+  A[j] = s;
+}
+
+int chunk_mode(int c) {
+  if (c == 4) return kC4;
+  if (c == 8) return kC8;
+  if (c == 16) return kC16;
+  if (c % 32 == 0) return kC32x;
+  return -1;
+}
+
+}  // namespace
+
+ScorePlan make_score_plan(const ckv_dims* d) {
+  ScorePlan p{};
+  const int G = d->n_q_heads / d->n_kv_heads;
+  p.m = ceil_div(d->n_prefix, d->chunk_size);
+  p.rows = G * d->n_suffix;
+  const int unit = d->chunk_size % 32 == 0 ? d->chunk_size : 32;  // lcm(32, c) for supported c
+  const bool f32 = d->dtype == CKV_DTYPE_F32;
+  const int64_t row_blocks = ceil_div(p.rows, f32 ? kWaveRows : kBlockRows);
+  // grow the key range while the grid keeps >= 1024 workgroups (4 per CU)
+  int64_t kr = unit * ceil_div(256, unit);
+  while (kr * 2 <= 4096 && (int64_t)d->n_kv_heads * row_blocks * ceil_div(d->n_prefix, kr * 2) >= 1024)
+    kr *= 2;
+  p.key_range = (int32_t)kr;
+  p.n_ranges = (int32_t)ceil_div(d->n_prefix, kr);
+  p.cpr = (int32_t)(kr / d->chunk_size);
+  const size_t R = (size_t)p.rows, H = (size_t)d->n_kv_heads, NR = (size_t)p.n_ranges;
+  size_t off = 0;
+  p.off_part = off;
+  off = align_up(off + H * NR * p.cpr * R * sizeof(float), 256);
+  p.off_mc = off;
+  off = align_up(off + H * NR * R * sizeof(float), 256);
+  p.off_z = off;
+  off = align_up(off + H * NR * R * sizeof(double), 256);
+  p.off_wpart = off;
+  off = align_up(off + H * (size_t)align_up(p.m, 64) * sizeof(double), 256);
+  p.bytes = off;
+  return p;
+}
+
+ckv_status launch_score(const ckv_dims* d, const void* q, const void* k, double* scores, void* ws,
+                        size_t ws_bytes, hipStream_t st, hipEvent_t after_main) {
+  const ScorePlan p = make_score_plan(d);
+  if (ws_bytes < p.bytes) CKV_FAIL(CKV_EINVAL, "score workspace too small: %zu < %zu", ws_bytes, p.bytes);
+  const int mode = chunk_mode(d->chunk_size);
+  char* base = static_cast<char*>(ws);
+  float* part = reinterpret_cast<float*>(base + p.off_part);
+  float* mc = reinterpret_cast<float*>(base + p.off_mc);
+  double* z = reinterpret_cast<double*>(base + p.off_z);
+  double* wpart = reinterpret_cast<double*>(base + p.off_wpart);
+  const int G = d->n_q_heads / d->n_kv_heads;
+  const float c1 = resolve_scale(d) * 1.4426950408889634f;
+  const int64_t m_pad = (int64_t)align_up(p.m, 64);
+
+  if (d->dtype == CKV_DTYPE_BF16) {
+    ScoreArgs a;
+    a.q = static_cast<const uint16_t*>(q);
+    a.k = static_cast<const uint16_t*>(k);
+    a.part = part; a.mc = mc; a.z = z;
+    a.n = d->n_prefix; a.S = d->n_suffix; a.Hq = d->n_q_heads; a.Hkv = d->n_kv_heads; a.G = G;
+    a.R = p.rows; a.c = d->chunk_size; a.key_range = p.key_range; a.n_ranges = p.n_ranges;
+    a.cpr = p.cpr; a.n_row_blocks = (int)ceil_div(p.rows, kBlockRows); a.c1 = c1;
+    a.nblocks = (uint32_t)((int64_t)a.Hkv * a.n_ranges * a.n_row_blocks);
+    a.nblocks_padded = (uint32_t)align_up(a.nblocks, 8);
+    dim3 grid(a.nblocks_padded), block(kWaves * 64);
+#define CKV_SCORE_LAUNCH(DD, MM) hipLaunchKernelGGL((score_bf16_kernel<DD, MM>), grid, block, 0, st, a)
+    if (d->head_dim == 128) {
+      switch (mode) {
+        case kC4: CKV_SCORE_LAUNCH(128, kC4); break;
+        case kC8: CKV_SCORE_LAUNCH(128, kC8); break;
+        case kC16: CKV_SCORE_LAUNCH(128, kC16); break;
+        default: CKV_SCORE_LAUNCH(128, kC32x); break;
+      }
+    } else {
+      switch (mode) {
+        case kC4: CKV_SCORE_LAUNCH(64, kC4); break;
+        case kC8: CKV_SCORE_LAUNCH(64, kC8); break;
+        case kC16: CKV_SCORE_LAUNCH(64, kC16); break;
+        default: CKV_SCORE_LAUNCH(64, kC32x); break;
+      }
+    }
+#undef CKV_SCORE_LAUNCH
+  } else {
+    ScoreArgsF32 a;
+    a.q = static_cast<const float*>(q);
+    a.k = static_cast<const float*>(k);
+    a.part = part; a.mc = mc; a.z = z;
+    a.n = d->n_prefix; a.S = d->n_suffix; a.Hq = d->n_q_heads; a.Hkv = d->n_kv_heads; a.G = G;
+    a.R = p.rows; a.c = d->chunk_size; a.key_range = p.key_range; a.n_ranges = p.n_ranges;
+    a.cpr = p.cpr; a.n_row_blocks = (int)ceil_div(p.rows, kWaveRows); a.c1 = c1;
+    a.nblocks = (uint32_t)((int64_t)a.Hkv * a.n_ranges * a.n_row_blocks);
+    dim3 grid(a.nblocks), block(64);
+    switch (mode) {
+      case kC4: hipLaunchKernelGGL((score_f32_kernel<64, kC4>), grid, block, 0, st, a); break;
+      case kC8: hipLaunchKernelGGL((score_f32_kernel<64, kC8>), grid, block, 0, st, a); break;
+      case kC16: hipLaunchKernelGGL((score_f32_kernel<64, kC16>), grid, block, 0, st, a); break;
+      default: hipLaunchKernelGGL((score_f32_kernel<64, kC32x>), grid, block, 0, st, a); break;
+    }
+  }
+  CKV_HIP(hipGetLastError());
+  if (after_main) CKV_HIP(hipEventRecord(after_main, st));
+  {
+    const int64_t nthreads = (int64_t)d->n_kv_heads * p.rows;
+    hipLaunchKernelGGL(row_norm_kernel, dim3((unsigned)ceil_div(nthreads, 256)), dim3(256), 0, st,
+                       mc, z, d->n_kv_heads, p.rows, p.n_ranges);
+    CKV_HIP(hipGetLastError());
+  }
+  hipLaunchKernelGGL(chunk_reduce_kernel, dim3((unsigned)ceil_div(p.m, 8), d->n_kv_heads), dim3(256),
+                     0, st, part, z, wpart, p.rows, p.n_ranges, p.cpr, p.m, m_pad);
+  CKV_HIP(hipGetLastError());
+  hipLaunchKernelGGL(head_sum_kernel, dim3((unsigned)ceil_div(p.m, 256)), dim3(256), 0, st, wpart,
+                     scores, d->n_kv_heads, p.m, m_pad);
+  CKV_HIP(hipGetLastError());
+  return CKV_OK;
+}
+
+}  // namespace ckv

@@ -218,3 +218,18 @@ def all_layers(w: Workload, layers=None, threads: int = 8) -> list:
     layers = list(range(w.n_layers)) if layers is None else list(layers)
     with ThreadPoolExecutor(max_workers=threads) as ex:
         return list(ex.map(lambda l: layer_tensors(w, l, hs[l]), layers))
+
+
+def chunk_major(k_prefix: np.ndarray, v_prefix: np.ndarray, chunk_size: int) -> np.ndarray:
+    """Host store layout of one layer: chunk j is one span [K rows; V rows] of
+    chunk_size rows each (rows past n of the last chunk are zero padding).
+    Returns an array of shape [m][2][c][Hkv][d]."""
+    n, Hkv, d = k_prefix.shape
+    m = -(-n // chunk_size)
+    out = np.zeros((m, 2, chunk_size, Hkv, d), k_prefix.dtype)
+    pad = m * chunk_size - n
+    kk = np.concatenate([k_prefix, np.zeros((pad, Hkv, d), k_prefix.dtype)]) if pad else k_prefix
+    vv = np.concatenate([v_prefix, np.zeros((pad, Hkv, d), v_prefix.dtype)]) if pad else v_prefix
+    out[:, 0] = kk.reshape(m, chunk_size, Hkv, d)
+    out[:, 1] = vv.reshape(m, chunk_size, Hkv, d)
+    return out

@@ -1,0 +1,105 @@
+"""The C-ABI library loads, exports every declared symbol, and validates on the host.
+
+No GPU work is launched here: only pure host helpers and argument checks that
+fail before anything is enqueued.
+"""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "ckv.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(ckv_[a-z_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def ckv():
+    import paper_2601_13631_amd as ckv
+    return ckv
+
+
+def test_every_declared_symbol_is_exported(ckv):
+    names = declared_functions()
+    assert len(names) >= 15, names
+    lib = ctypes.CDLL(ckv.LIB_PATH)
+    missing = [n for n in names if not hasattr(lib, n)]
+    assert not missing, missing
+    assert set(ckv.EXPORTED) == set(names)
+
+
+def test_host_helpers(ckv):
+    assert ckv.num_chunks(5, 2) == 3 and ckv.num_chunks(32768, 32) == 1024
+    assert ckv.num_chunks(-1, 4) == -1 and ckv.num_chunks(4, 0) == -1
+    # keep counts of the five workloads
+    assert ckv.num_keep(64, 0.25) == 16
+    assert ckv.num_keep(512, 0.20) == 103 and ckv.num_keep(1024, 0.10) == 103
+    assert [ckv.num_keep(m, 0.15) for m in (8192, 4096, 2048, 1024)] == [1229, 615, 308, 154]
+    assert ckv.num_keep(4096, 0.10) == 410
+    assert ckv.num_keep(0, 0.5) == 0 and ckv.num_keep(10, 0.0) == -1 and ckv.num_keep(10, 1.5) == -1
+    assert "gfx950" in ckv.version()
+
+
+def test_keep_matches_oracle(ckv):
+    import oracle
+    for m in (1, 2, 3, 7, 64, 100, 1000, 4096, 8192):
+        for r in (1e-6, 0.05, 0.1, 0.15, 0.2, 0.25, 1 / 3, 0.5, 0.999, 1.0):
+            assert ckv.num_keep(m, r) == oracle.num_keep(m, r), (m, r)
+
+
+def _status(fn, *args):
+    return fn(*args)
+
+
+def test_validation_before_launch(ckv):
+    L = ckv._lib
+    good = ckv.make_dims(1024, 32, 4, 1, 64, 16, ckv.DTYPE_BF16)
+    bad_hd = ckv.make_dims(1024, 32, 4, 1, 96, 16, ckv.DTYPE_BF16)
+    bad_c = ckv.make_dims(1024, 32, 4, 1, 64, 12, ckv.DTYPE_BF16)
+    bad_gqa = ckv.make_dims(1024, 32, 6, 4, 64, 16, ckv.DTYPE_BF16)
+    bad_n = ckv.make_dims(0, 32, 4, 1, 64, 16, ckv.DTYPE_BF16)
+    P = 4096  # a fake aligned address: never dereferenced, every call below fails validation
+    ws = ckv.score_workspace_bytes(good)
+    assert ws > 0 and ckv.score_workspace_bytes(bad_hd) == 0
+    assert L.ckv_score_chunks(None, P, P, P, P, ws, None) == ckv.EINVAL
+    assert L.ckv_score_chunks(ctypes.byref(bad_hd), P, P, P, P, ws, None) == ckv.EUNSUPPORTED
+    assert "head_dim" in ckv.last_error()
+    assert L.ckv_score_chunks(ctypes.byref(bad_c), P, P, P, P, ws, None) == ckv.EUNSUPPORTED
+    assert L.ckv_score_chunks(ctypes.byref(bad_gqa), P, P, P, P, ws, None) == ckv.EINVAL
+    assert L.ckv_score_chunks(ctypes.byref(bad_n), P, P, P, P, ws, None) == ckv.EINVAL
+    assert L.ckv_score_chunks(ctypes.byref(good), P, None, P, P, ws, None) == ckv.EINVAL
+    assert L.ckv_score_chunks(ctypes.byref(good), P + 2, P, P, P, ws, None) == ckv.EINVAL
+    assert L.ckv_score_chunks(ctypes.byref(good), P, P, P, P, ws - 1, None) == ckv.EINVAL
+    assert "workspace" in ckv.last_error()
+    assert L.ckv_select_topk_chunks(P, 0, 1, P, None, 0, None) == ckv.EINVAL
+    assert L.ckv_select_topk_chunks(P, 10, 11, P, None, 0, None) == ckv.EINVAL
+    assert L.ckv_select_topk_chunks(P, 10, 0, P, None, 0, None) == ckv.EINVAL
+    assert L.ckv_select_topk_chunks(None, 10, 1, P, None, 0, None) == ckv.EINVAL
+    assert L.ckv_gather_chunks(ctypes.byref(good), P, P, P, 65, P, P, None) == ckv.EINVAL
+    assert L.ckv_gather_chunks(ctypes.byref(good), P, P, P, 0, P, P, None) == ckv.OK  # nothing to do
+    assert L.ckv_sparse_prefill_attn(ctypes.byref(good), P, P, P, P, -1, P, P, P, None, 0, None) == ckv.EINVAL
+    assert L.ckv_sparse_prefill_attn(ctypes.byref(good), P, None, P, P, 3, P, P, P, None, 0, None) == ckv.EINVAL
+    h = ctypes.c_void_p()
+    assert L.ckv_ctx_create(ctypes.byref(good), 0.0, 0, ctypes.byref(h)) == ckv.EINVAL
+    assert L.ckv_ctx_create(ctypes.byref(good), 0.5, 0x80, ctypes.byref(h)) == ckv.EINVAL
+    assert L.ckv_ctx_create(ctypes.byref(bad_hd), 0.5, 0, ctypes.byref(h)) == ckv.EUNSUPPORTED
+    assert not h.value
+    assert L.ckv_reprefill_layer(None, 0, None, None) == ckv.EINVAL
+    assert L.ckv_ctx_destroy(None) == ckv.OK
+
+
+def test_product_does_not_touch_oracle():
+    """The product package and its sources never reference the oracle."""
+    pkg = os.path.join(ROOT, "paper_2601_13631_amd")
+    for dirpath, _, files in os.walk(pkg):
+        for f in files:
+            if f.endswith((".py", ".hip", ".h", ".cpp")):
+                text = open(os.path.join(dirpath, f)).read()
+                assert "oracle" not in text.lower(), f
+                assert "ckvo_" not in text, f
