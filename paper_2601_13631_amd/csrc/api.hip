@@ -43,7 +43,7 @@ ckv_status check_dims(const ckv_dims* d) {
   if (!(c == 4 || c == 8 || c == 16 || c % 32 == 0))
     CKV_FAIL(CKV_EUNSUPPORTED, "chunk_size must be 4, 8, 16 or a multiple of 32 (got %d)", c);
   const int64_t rows = (int64_t)(d->n_q_heads / d->n_kv_heads) * d->n_suffix;
-  if (rows > (1 << 24) || d->n_prefix > (int64_t(1) << 34))
+  if (rows > (1 << 24) || d->n_prefix > (int64_t(1) << 30))
     CKV_FAIL(CKV_EUNSUPPORTED, "shape too large");
   return CKV_OK;
 }

@@ -27,8 +27,10 @@ namespace {
 constexpr int kWaves = 4;
 constexpr int kWaveRows = 32;
 constexpr int kBlockRows = kWaves * kWaveRows;  // 128
-constexpr int kTile = 32;
+constexpr int kTile = 64;  // keys per LDS stage
+constexpr int kSub = 32;   // keys per MFMA product
 constexpr int kNoKey = 0x7fffffff;  // visibility limit of a masked key
+constexpr float kLazy = 8.f;        // headroom of the lazy softmax reference (log2 units)
 
 // MFMA row p of the K operand holds key kappa(p); afterwards register v of a
 // lane in half h holds key 16*(v/8) + 8*h + v%8.
@@ -72,9 +74,11 @@ struct AttnArgs {
   const int32_t* chunk_off;
   int32_t direct;
   const int32_t* sel;      // [k]
-  int64_t kc;              // k * c prefix positions
+  int kc;                  // k * c prefix positions (< 2^31)
   int64_t n;
   int c;
+  int log2c;               // log2(c) when c is a power of two, else -1
+  int short_tail;          // c - n % c when the last chunk is short, else 0
   const uint16_t* ks;      // [S][Hkv][D]
   const uint16_t* vs;
   uint16_t* out;           // [S][Hq][D]
@@ -85,60 +89,107 @@ struct AttnArgs {
   uint32_t nblocks, nblocks_padded;
 };
 
-// Loads tile `tile` of positions into LDS and writes each key's visibility
-// limit (a row with query t sees the key iff t >= lim).  Returns true if every
-// key of the tile is visible to every row.
+// The K/V rows of one 64-key stage, fetched into registers (while the previous
+// stage is consumed from LDS) and then written to the other LDS buffer.
 template <int D>
-__device__ __forceinline__ bool load_tile(const AttnArgs& a, int g, int64_t tile, uint16_t* lk,
-                                          uint16_t* lv, int* lim) {
+struct TileRegs {
+  static constexpr int kPer = kTile * (D / 8) / (kWaves * 64);  // 16-byte pieces per thread
+  u32x4 k[kPer], v[kPer];
+  int lim[kPer];
+};
+
+// Chunk index (and slot-table entry) of each piece's key, fetched one stage
+// ahead of its K/V rows so that the row loads never wait on the index loads.
+// The loads are unconditional (clamped to the last kept chunk) and their values
+// are only interpreted by tile_load.
+template <int D>
+struct TileIdx {
+  int32_t j[TileRegs<D>::kPer];     // sel[u] of the piece's chunk u
+  int32_t slot[TileRegs<D>::kPer];  // chunk_off[u] when a slot table is used
+};
+
+// Kept chunk u holding compact position pos.  A power-of-two c uses a shift;
+// any other supported c is a multiple of 64 or 32, and u is then computed per
+// piece with a 32-bit division.
+__device__ __forceinline__ int chunk_of(const AttnArgs& a, int pos) {
+  return a.log2c >= 0 ? (pos >> a.log2c) : (int)((uint32_t)pos / (uint32_t)a.c);
+}
+
+template <int D>
+__device__ __forceinline__ void tile_index(const AttnArgs& a, int tile, TileIdx<D>& x) {
   constexpr int kSegs = D / 8;
-  constexpr int kPer = kTile * kSegs / (kWaves * 64);
-  bool all_vis = true;
+  if (a.kc == 0) return;
+  const int pos0 = tile * kTile;
+  const int last = a.kc / a.c - 1;
 #pragma unroll
-  for (int p = 0; p < kPer; ++p) {
+  for (int p = 0; p < TileRegs<D>::kPer; ++p) {
+    const int key = (threadIdx.x + p * kWaves * 64) / kSegs;
+    const int u = min(chunk_of(a, pos0 + key), last);
+    x.j[p] = a.sel[u];
+    if (a.chunk_off) x.slot[p] = a.chunk_off[u];
+  }
+}
+
+// Fetches stage `tile` of key positions and each key's visibility limit (a row
+// with query t sees the key iff t >= lim).  Loads are unconditional: a masked
+// key reads suffix row 0 of this KV head instead (finite data; its probability
+// is forced to zero, so it contributes nothing).
+template <int D>
+__device__ __forceinline__ void tile_load(const AttnArgs& a, int g, int tile, const TileIdx<D>& x,
+                                          TileRegs<D>& r) {
+  constexpr int kSegs = D / 8;
+  const int pos0 = tile * kTile;
+#pragma unroll
+  for (int p = 0; p < TileRegs<D>::kPer; ++p) {
     const int idx = threadIdx.x + p * kWaves * 64;
     const int key = idx / kSegs, seg = idx % kSegs;
-    const int64_t pos = tile * kTile + key;
-    const uint16_t* ksrc = nullptr;
-    const uint16_t* vsrc = nullptr;
+    const int pos = pos0 + key;
+    const int col = g * D + seg * 8;
+    const uint16_t* ksrc = a.ks + col;
+    const uint16_t* vsrc = a.vs + col;
     int limit = kNoKey;
     if (pos < a.kc) {
-      const int64_t u = pos / a.c;
-      const int off = (int)(pos - u * a.c);
-      const int64_t j = a.sel[u];
-      const int64_t len = j >= 0 ? min<int64_t>(a.c, a.n - j * a.c) : 0;  // index outside [0, m): empty
+      const int u = chunk_of(a, pos);
+      const int off = pos - u * a.c;
+      const int j = x.j[p];
+      const int len = j >= 0 ? (int)min<int64_t>(a.c, a.n - (int64_t)j * a.c) : 0;  // outside [0, m): empty
       if (off < len) {
-        const int64_t slot = a.chunk_off ? (int64_t)a.chunk_off[u] : (a.direct ? j : u);
-        const int64_t e = slot * a.chunk_stride + ((int64_t)off * a.Hkv + g) * D + seg * 8;
+        const int slot = a.chunk_off ? x.slot[p] : (a.direct ? j : u);
+        const int64_t e = (int64_t)slot * a.chunk_stride + (off * a.Hkv * D + col);
         ksrc = a.kbase + e;
         vsrc = a.vbase + e;
         limit = -1;
       }
     } else if (pos < a.kc + a.S) {
-      const int64_t tok = pos - a.kc;
-      const int64_t e = (tok * a.Hkv + g) * D + seg * 8;
-      ksrc = a.ks + e;
-      vsrc = a.vs + e;
-      limit = (int)tok;
+      const int tok = pos - a.kc;
+      ksrc += tok * a.Hkv * D;
+      vsrc += tok * a.Hkv * D;
+      limit = tok;
     }
-    u32x4 kv = {0u, 0u, 0u, 0u}, vv = {0u, 0u, 0u, 0u};
-    if (ksrc) {
-      kv = *reinterpret_cast<const u32x4*>(ksrc);
-      vv = *reinterpret_cast<const u32x4*>(vsrc);
-    }
-    *reinterpret_cast<u32x4*>(lk + k_off<D>(key, seg)) = kv;
-    *reinterpret_cast<u32x4*>(lv + v_off<D>(key, seg)) = vv;
-    if (seg == 0) lim[key] = limit;
-    all_vis = all_vis && (limit == -1);
+    r.k[p] = *reinterpret_cast<const u32x4*>(ksrc);
+    r.v[p] = *reinterpret_cast<const u32x4*>(vsrc);
+    r.lim[p] = limit;
   }
-  return all_vis;
+}
+
+template <int D>
+__device__ __forceinline__ void tile_store(const TileRegs<D>& r, uint16_t* lk, uint16_t* lv, int* lim) {
+  constexpr int kSegs = D / 8;
+#pragma unroll
+  for (int p = 0; p < TileRegs<D>::kPer; ++p) {
+    const int idx = threadIdx.x + p * kWaves * 64;
+    const int key = idx / kSegs, seg = idx % kSegs;
+    *reinterpret_cast<u32x4*>(lk + k_off<D>(key, seg)) = r.k[p];
+    *reinterpret_cast<u32x4*>(lv + v_off<D>(key, seg)) = r.v[p];
+    if (seg == 0) lim[key] = r.lim[p];
+  }
 }
 
 template <int D>
 __global__ __launch_bounds__(kWaves * 64, 2) void attn_kernel(AttnArgs a) {
-  __shared__ __attribute__((aligned(16))) uint16_t lk[kTile * D];
-  __shared__ __attribute__((aligned(16))) uint16_t lv[kTile * D];
-  __shared__ int lim[kTile];
+  __shared__ __attribute__((aligned(16))) uint16_t lk[2][kTile * D];
+  __shared__ __attribute__((aligned(16))) uint16_t lv[2][kTile * D];
+  __shared__ int lim[2][kTile];
 
   // logical order (g, split, row block): blocks reading the same K/V tiles are
   // adjacent, hence on the same XCD and its L2
@@ -155,22 +206,45 @@ __global__ __launch_bounds__(kWaves * 64, 2) void attn_kernel(AttnArgs a) {
   const int hi = row_ok ? row % a.G : 0;
 
   // last query of the block bounds the suffix keys anyone here can see
+  const int first_t = (rb * kBlockRows) / a.G;
   const int last_row = min(a.R - 1, rb * kBlockRows + kBlockRows - 1);
-  const int64_t np_block = a.kc + last_row / a.G + 1;
-  const int64_t ntiles = (np_block + kTile - 1) / kTile;
-  const int64_t tile0 = (int64_t)split * a.tiles_per_split;
-  const int64_t tile1 = min<int64_t>(ntiles, tile0 + a.tiles_per_split);
+  const int np_block = a.kc + last_row / a.G + 1;
+  const int ntiles = (np_block + kTile - 1) / kTile;
+  const int tile0 = split * a.tiles_per_split;
+  const int tile1 = min(ntiles, tile0 + a.tiles_per_split);
+  // prefix positions before vis_end are real tokens whatever chunks were kept
+  const int vis_end = a.kc - a.short_tail;
 
   bf16x8 qf[D / 16];
   {
     const uint16_t* src = a.q + ((int64_t)(row_ok ? t : 0) * a.Hq + (int64_t)g * a.G + hi) * D + 8 * half;
 #pragma unroll
     for (int ks = 0; ks < D / 16; ++ks) {
-      u32x4 v = {0u, 0u, 0u, 0u};
-      if (row_ok) v = *reinterpret_cast<const u32x4*>(src + 16 * ks);
+      u32x4 v = *reinterpret_cast<const u32x4*>(src + 16 * ks);
+      if (!row_ok) v = u32x4{0u, 0u, 0u, 0u};
       qf[ks] = *reinterpret_cast<bf16x8*>(&v);
     }
   }
+
+  // per-lane LDS element offsets of the operand reads (the same for every stage)
+  const int krow = kappa(lane & 31);
+  int koff[D / 16];
+#pragma unroll
+  for (int ks = 0; ks < D / 16; ++ks) koff[ks] = k_off<D>(krow, 2 * ks + half);
+  const int s16 = lane & 15, g4 = (lane >> 4) & 1;
+  int voff[D / 32][2][2];
+#pragma unroll
+  for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int rd = 0; rd < 2; ++rd) {
+        // V^T fragment piece: lane (group g4 = (lane/16)%2, s16 = lane%16) supplies
+        // row 16*kb + 8*half + 4*rd + s16/4, columns 32*db + 16*g4 + 4*(s16%4) .. +3
+        const int vrow = 16 * kb + 8 * half + 4 * rd + (s16 >> 2);
+        const int col = 32 * db + 16 * g4 + 4 * (s16 & 3);
+        voff[db][kb][rd] = v_off<D>(vrow, col >> 3) + (col & 7);
+      }
 
   f32x16 o[D / 32];
 #pragma unroll
@@ -179,76 +253,110 @@ __global__ __launch_bounds__(kWaves * 64, 2) void attn_kernel(AttnArgs a) {
     for (int v = 0; v < 16; ++v) o[db][v] = 0.f;
   float m_run = -INFINITY, l_run = 0.f;
 
-  const int krow = kappa(lane & 31);
-  for (int64_t tile = tile0; tile < tile1; ++tile) {
+  TileRegs<D> regs;
+  TileIdx<D> idx_next;
+  if (tile0 < tile1) {
+    TileIdx<D> idx0;
+    tile_index<D>(a, tile0, idx0);
+    tile_load<D>(a, g, tile0, idx0, regs);
+    if (tile0 + 1 < tile1) tile_index<D>(a, tile0 + 1, idx_next);
+    tile_store<D>(regs, lk[0], lv[0], lim[0]);
     __syncthreads();
-    const bool my_vis = load_tile<D>(a, g, tile, lk, lv, lim);
-    const bool all_vis = __syncthreads_and(my_vis ? 1 : 0);
+  }
+  for (int tile = tile0; tile < tile1; ++tile) {
+    const int cur = (tile - tile0) & 1;
+    const bool has_next = tile + 1 < tile1;
+    if (has_next) {
+      tile_load<D>(a, g, tile + 1, idx_next, regs);
+      if (tile + 2 < tile1) tile_index<D>(a, tile + 2, idx_next);
+    }
+    // no key of this stage needs a mask for any row of the block when it ends
+    // before the kept prefix's possibly short tail, or when its suffix keys are
+    // seen by the block's first query and its prefix keys are all real tokens
+    const int pos0 = tile * kTile, pos_end = pos0 + kTile;
+    const bool all_vis = pos_end <= vis_end ||
+                         (pos_end <= a.kc + first_t + 1 && (pos0 >= a.kc || a.short_tail == 0));
 
-    f32x16 s;
+    // S^T for the two 32-key halves: two independent MFMA chains
+    f32x16 s[2];
 #pragma unroll
-    for (int v = 0; v < 16; ++v) s[v] = 0.f;
+    for (int sub = 0; sub < 2; ++sub)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) s[sub][v] = 0.f;
 #pragma unroll
     for (int ks = 0; ks < D / 16; ++ks) {
-      bf16x8 kf = *reinterpret_cast<const bf16x8*>(lk + k_off<D>(krow, 2 * ks + half));
-      s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[ks], s, 0, 0, 0);
-    }
-    // register v holds key 16*(v/8) + 8*half + v%8
-    if (!all_vis) {
 #pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int key = 16 * (v >> 3) + 8 * half + (v & 7);
-        if (t < lim[key]) s[v] = -INFINITY;
+      for (int sub = 0; sub < 2; ++sub) {
+        bf16x8 kf = *reinterpret_cast<const bf16x8*>(&lk[cur][sub * kSub * D + koff[ks]]);
+        s[sub] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[ks], s[sub], 0, 0, 0);
       }
     }
-    float mx = s[0];
+    // register v of half `sub` holds key 32*sub + 16*(v/8) + 8*half + v%8
+    if (!all_vis) {
 #pragma unroll
-    for (int v = 1; v < 16; ++v) mx = fmaxf(mx, s[v]);
+      for (int sub = 0; sub < 2; ++sub)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int key = kSub * sub + 16 * (v >> 3) + 8 * half + (v & 7);
+          if (t < lim[cur][key]) s[sub][v] = -INFINITY;
+        }
+    }
+    float mx = fmaxf(s[0][0], s[1][0]);
+#pragma unroll
+    for (int v = 1; v < 16; ++v) mx = fmaxf(mx, fmaxf(s[0][v], s[1][v]));
     mx = fmaxf(mx, partner_f(mx));
-    const float m_new = fmaxf(m_run, mx * a.c1);
+    // The reference m_run only moves when the stage's maximum exceeds it by more
+    // than kLazy (log2 units): weights stay below 2^kLazy, numerator and
+    // denominator share the reference, and most stages skip the O rescale.
+    const float mt = mx * a.c1;
+    const float m_new = mt > m_run + kLazy ? mt : m_run;
     const float m_use = m_new == -INFINITY ? 0.f : m_new;
     const float alpha = __builtin_amdgcn_exp2f(m_run - m_use);
     float rs = 0.f;
 #pragma unroll
-    for (int v = 0; v < 16; ++v) {
-      s[v] = __builtin_amdgcn_exp2f(fmaf(s[v], a.c1, -m_use));
-      rs += s[v];
-    }
+    for (int sub = 0; sub < 2; ++sub)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        s[sub][v] = __builtin_amdgcn_exp2f(fmaf(s[sub][v], a.c1, -m_use));
+        rs += s[sub][v];
+      }
     rs += partner_f(rs);
     l_run = l_run * alpha + rs;
     m_run = m_new;
+    if (__any(alpha != 1.f)) {
 #pragma unroll
-    for (int db = 0; db < D / 32; ++db)
+      for (int db = 0; db < D / 32; ++db)
 #pragma unroll
-      for (int v = 0; v < 16; ++v) o[db][v] *= alpha;
+        for (int v = 0; v < 16; ++v) o[db][v] *= alpha;
+    }
 
-    bf16x8 pb[2];
+    // O^T += V^T P^T, 16 keys per product
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
+    for (int sub = 0; sub < 2; ++sub) {
+      bf16x8 pb[2];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) pb[kb][e] = (__bf16)s[8 * kb + e];
-
-    // V^T fragments: lane (group G4 = lane/16, s = lane%16) supplies the address of
-    // row 16*kb + 8*half + 4*rd + s/4, columns 32*db + 16*(G4%2) + 4*(s%4) .. +3
-    const int s16 = lane & 15, g4 = (lane >> 4) & 1;
+      for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-    for (int db = 0; db < D / 32; ++db) {
+        for (int e = 0; e < 8; ++e) pb[kb][e] = (__bf16)s[sub][8 * kb + e];
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb) {
-        s16x4 part[2];
+      for (int db = 0; db < D / 32; ++db) {
 #pragma unroll
-        for (int rd = 0; rd < 2; ++rd) {
-          const int vrow = 16 * kb + 8 * half + 4 * rd + (s16 >> 2);
-          const int col = 32 * db + 16 * g4 + 4 * (s16 & 3);
-          const int off = v_off<D>(vrow, col >> 3) + (col & 7);
-          part[rd] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-              (__attribute__((address_space(3))) s16x4*)(lv + off));
+        for (int kb = 0; kb < 2; ++kb) {
+          s16x4 piece[2];
+#pragma unroll
+          for (int rd = 0; rd < 2; ++rd)
+            piece[rd] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                (__attribute__((address_space(3))) s16x4*)(&lv[cur][sub * kSub * D + voff[db][kb][rd]]));
+          bf16x8 vf;
+          *reinterpret_cast<s16x4*>(&vf) = piece[0];
+          *(reinterpret_cast<s16x4*>(&vf) + 1) = piece[1];
+          o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pb[kb], o[db], 0, 0, 0);
         }
-        bf16x8 vf;
-        *reinterpret_cast<s16x4*>(&vf) = part[0];
-        *(reinterpret_cast<s16x4*>(&vf) + 1) = part[1];
-        o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pb[kb], o[db], 0, 0, 0);
       }
+    }
+    if (has_next) {
+      tile_store<D>(regs, lk[cur ^ 1], lv[cur ^ 1], lim[cur ^ 1]);
+      __syncthreads();
     }
   }
 
@@ -462,9 +570,11 @@ ckv_status launch_attn(const ckv_dims* d, const void* q, const ChunkSource& src,
   a.chunk_off = src.chunk_off;
   a.direct = src.direct;
   a.sel = sel;
-  a.kc = k * d->chunk_size;
+  a.kc = (int)(k * d->chunk_size);
   a.n = d->n_prefix;
   a.c = d->chunk_size;
+  a.log2c = (d->chunk_size & (d->chunk_size - 1)) == 0 ? __builtin_ctz(d->chunk_size) : -1;
+  a.short_tail = d->n_prefix % d->chunk_size ? (int)(d->chunk_size - d->n_prefix % d->chunk_size) : 0;
   a.ks = static_cast<const uint16_t*>(k_suffix);
   a.vs = static_cast<const uint16_t*>(v_suffix);
   a.out = static_cast<uint16_t*>(out);

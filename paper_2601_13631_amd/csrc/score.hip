@@ -81,21 +81,44 @@ struct ScoreArgs {
   uint32_t nblocks, nblocks_padded;
 };
 
+constexpr int kStage = 64;  // keys per LDS stage: two 32-key subtiles
+
+// The next stage's K rows are fetched into registers while the current stage is
+// consumed from LDS, then written to the other LDS buffer: one barrier per stage.
+// Loads are unconditional (rows past the range end read the stage's first row
+// and are zeroed when stored), so the compiler never has to wait on them early.
 template <int D>
-__device__ __forceinline__ void load_subtile(const ScoreArgs& a, int g, int64_t key0,
-                                             uint16_t* lds) {
+struct StageRegs {
+  static constexpr int kPer = kStage * (D / 8) / (kWaves * 64);  // 16-byte loads per thread
+  u32x4 v[kPer];
+  uint32_t valid;  // bit p: piece p is inside the range
+};
+
+template <int D>
+__device__ __forceinline__ void stage_load(const uint16_t* kstage, int64_t keys_left,
+                                           const uint32_t (&voff)[StageRegs<D>::kPer],
+                                           const uint32_t (&voff0)[StageRegs<D>::kPer],
+                                           StageRegs<D>& r) {
   constexpr int kSegs = D / 8;
-  constexpr int kPer = kSub * kSegs / (kWaves * 64);  // 16-byte loads per thread
-  static_assert(kPer >= 1, "subtile too small");
+  r.valid = 0;
 #pragma unroll
-  for (int p = 0; p < kPer; ++p) {
-    int idx = threadIdx.x + p * kWaves * 64;
-    int key = idx / kSegs, seg = idx % kSegs;
-    int64_t tok = key0 + key;
-    u32x4 v = {0u, 0u, 0u, 0u};
-    if (tok < a.n)
-      v = *reinterpret_cast<const u32x4*>(a.k + ((tok * a.Hkv + g) * D + seg * 8));
-    *reinterpret_cast<u32x4*>(lds + SubtileLds<D>::offset(key, seg)) = v;
+  for (int p = 0; p < StageRegs<D>::kPer; ++p) {
+    const int key = (threadIdx.x + p * kWaves * 64) / kSegs;
+    const bool ok = key < keys_left;
+    r.valid |= (ok ? 1u : 0u) << p;
+    r.v[p] = *reinterpret_cast<const u32x4*>(kstage + (ok ? voff[p] : voff0[p]));
+  }
+}
+
+template <int D>
+__device__ __forceinline__ void stage_store(const StageRegs<D>& r, uint16_t* lds) {
+  constexpr int kSegs = D / 8;
+#pragma unroll
+  for (int p = 0; p < StageRegs<D>::kPer; ++p) {
+    const int idx = threadIdx.x + p * kWaves * 64;
+    u32x4 v = r.v[p];
+    if (!((r.valid >> p) & 1u)) v = u32x4{0u, 0u, 0u, 0u};
+    *reinterpret_cast<u32x4*>(lds + SubtileLds<D>::offset(idx / kSegs, idx % kSegs)) = v;
   }
 }
 
@@ -131,146 +154,190 @@ constexpr int sums_per_lane() {
   return MODE == kC32x ? 1 : MODE == kC16 ? 2 : 4;
 }
 
-// Processes the workgroup's key range once.  PASS 0: reference = first
-// subtile's maximum, writes partials.  PASS 1: only the exact range maximum
-// (into mref).  PASS 2: writes partials with mref as reference.
-template <int D, int MODE, int PASS>
-__device__ bool run_range(const ScoreArgs& a, int g, int range, int row0, const bf16x8 (&qf)[2][D / 16],
-                          uint16_t* lds, float (&mref)[2], double (&zsum)[2]) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int half = lane >> 5;
-  const int64_t kbeg = (int64_t)range * a.key_range;
-  const int64_t kend = min<int64_t>(kbeg + a.key_range, a.n);
-  const int nsub = (int)((kend - kbeg + kSub - 1) / kSub);
-  const int my_row0 = row0 + wave * kWaveRows;
-  bool overflow = false;
-  float chunk_acc[2] = {0.f, 0.f};  // kC32x with c > 32: running sum of the open chunk
-  if (PASS != 1) { zsum[0] = 0.0; zsum[1] = 0.0; }
-  if (PASS == 1) { mref[0] = -INFINITY; mref[1] = -INFINITY; }
-  float* part = a.part + ((int64_t)(g * a.n_ranges + range) * a.cpr) * a.R;
+struct RangeState {
+  float mref[2];       // per row tile: reference (scaled log2 units)
+  double zsum[2];      // per row tile: sum of the range's chunk sums
+  float chunk_acc[2];  // kC32x with c > 32: running sum of the open chunk
+  bool overflow;
+};
 
-  for (int s = 0; s < nsub; ++s) {
-    const int64_t key0 = kbeg + (int64_t)s * kSub;
-    __syncthreads();  // previous subtile fully consumed
-    load_subtile<D>(a, g, key0, lds);
-    __syncthreads();
+// One 32-key subtile (range-relative keys rk0 .. rk0+31 of a range holding
+// nkeys keys), read from LDS rows lrow0 .. lrow0+31.  FULL: all 32 keys valid
+// (uniform; only a range's last subtile can be short).  PASS 0: reference from
+// the range's first subtile (first == true), then partial sums.  PASS 1: exact
+// range maximum only.  PASS 2: partial sums with the exact maximum as reference.
+template <int D, int MODE, int PASS, bool FULL>
+__device__ __forceinline__ void process_subtile(const ScoreArgs& a, const bf16x8 (&qf)[2][D / 16],
+                                                const uint16_t* lds, int lrow0, int rk0, int nkeys,
+                                                bool first, float* part, int my_row0,
+                                                RangeState& st) {
+  const int lane = threadIdx.x & 63, half = lane >> 5;
+  f32x16 acc[2];
+#pragma unroll
+  for (int rt = 0; rt < 2; ++rt)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) acc[rt][v] = 0.f;
+#pragma unroll
+  for (int ks = 0; ks < D / 16; ++ks) {
+    bf16x8 kf = *reinterpret_cast<const bf16x8*>(
+        lds + SubtileLds<D>::offset(lrow0 + (lane & 31), 2 * ks + half));
+    acc[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[0][ks], acc[0], 0, 0, 0);
+    acc[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[1][ks], acc[1], 0, 0, 0);
+  }
+  // register v of this lane holds key rk0 + 8*(v/4) + 4*half + v%4
+  const int nvalid = FULL ? kSub : min(kSub, nkeys - rk0);
 
-    f32x16 acc[2];
-#pragma unroll
-    for (int rt = 0; rt < 2; ++rt)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) acc[rt][v] = 0.f;
-#pragma unroll
-    for (int ks = 0; ks < D / 16; ++ks) {
-      bf16x8 kf = *reinterpret_cast<const bf16x8*>(
-          lds + SubtileLds<D>::offset(lane & 31, 2 * ks + half));
-      acc[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[0][ks], acc[0], 0, 0, 0);
-      acc[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[1][ks], acc[1], 0, 0, 0);
-    }
-    // key of register v in this lane: key0 + 8*(v/4) + 4*half + v%4
-    const int nvalid = (int)min<int64_t>(kSub, kend - key0);
-
-    if (PASS == 1 || (PASS == 0 && s == 0)) {
-#pragma unroll
-      for (int rt = 0; rt < 2; ++rt) {
-        float mx = -INFINITY;
-#pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          int key = 8 * (v >> 2) + 4 * half + (v & 3);
-          if (key < nvalid) mx = fmaxf(mx, acc[rt][v]);
-        }
-        mx = fmaxf(mx, partner_f(mx));
-        if (PASS == 1)
-          mref[rt] = fmaxf(mref[rt], mx * a.c1);
-        else
-          mref[rt] = mx * a.c1;
-      }
-    }
-    if (PASS == 1) continue;
-
-    // p = exp2(c1*dot - mc); invalid keys contribute 0
+  if (PASS == 1 || (PASS == 0 && first)) {
 #pragma unroll
     for (int rt = 0; rt < 2; ++rt) {
-      const float nm = -mref[rt];
+      float mx = -INFINITY;
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
-        int key = 8 * (v >> 2) + 4 * half + (v & 3);
-        float e = __builtin_amdgcn_exp2f(fmaf(acc[rt][v], a.c1, nm));
+        const int key = 8 * (v >> 2) + 4 * half + (v & 3);
+        if (FULL || key < nvalid) mx = fmaxf(mx, acc[rt][v]);
+      }
+      mx = fmaxf(mx, partner_f(mx));
+      st.mref[rt] = PASS == 1 ? fmaxf(st.mref[rt], mx * a.c1) : mx * a.c1;
+    }
+  }
+  if (PASS == 1) return;
+
+  // p = exp2(c1*dot - mc); keys past the range's end contribute 0
+#pragma unroll
+  for (int rt = 0; rt < 2; ++rt) {
+    const float nm = -st.mref[rt];
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      const float e = __builtin_amdgcn_exp2f(fmaf(acc[rt][v], a.c1, nm));
+      if constexpr (FULL) {
+        acc[rt][v] = e;
+      } else {
+        const int key = 8 * (v >> 2) + 4 * half + (v & 3);
         acc[rt][v] = key < nvalid ? e : 0.f;
       }
     }
+  }
 
-    // per-chunk sums and their partial writes
-    if constexpr (MODE == kC32x) {
-      const int64_t chunk = key0 / a.c;                       // chunk of this subtile
-      const bool closes = ((key0 + kSub) % a.c == 0) || (s == nsub - 1);
+  if constexpr (MODE == kC32x) {
+    const bool closes = ((rk0 + kSub) % a.c == 0) || (rk0 + kSub >= nkeys);
+#pragma unroll
+    for (int rt = 0; rt < 2; ++rt) {
+      float sum;
+      chunk_sums<MODE>(acc[rt], &sum);
+      st.chunk_acc[rt] += sum;
+    }
+    if (closes) {
+      const int jl = rk0 / a.c;
+      const int row = my_row0 + lane;  // lane l writes row tile l/32, row l%32
+      const float mine = half ? st.chunk_acc[1] : st.chunk_acc[0];
+      if (row < a.R) part[(int64_t)jl * a.R + row] = mine;
 #pragma unroll
       for (int rt = 0; rt < 2; ++rt) {
-        float sum;
-        chunk_sums<MODE>(acc[rt], &sum);
-        chunk_acc[rt] += sum;
+        st.overflow |= !(st.chunk_acc[rt] <= kOverflowGuard);
+        st.zsum[rt] += (double)st.chunk_acc[rt];
+        st.chunk_acc[rt] = 0.f;
       }
-      if (closes) {
-        const int jl = (int)(chunk - kbeg / a.c);
-        const int row = my_row0 + lane;  // lane l writes row tile l/32, row l%32
-        float mine = half ? chunk_acc[1] : chunk_acc[0];
-        if (row < a.R) part[(int64_t)jl * a.R + row] = mine;
+    }
+  } else {
+    constexpr int kN = sums_per_lane<MODE>();
+    constexpr int kChunk = MODE == kC4 ? 4 : MODE == kC8 ? 8 : 16;
+    const int jl0 = rk0 / kChunk;  // first chunk of this subtile
 #pragma unroll
-        for (int rt = 0; rt < 2; ++rt) {
-          overflow |= !(chunk_acc[rt] <= kOverflowGuard);
-          zsum[rt] += (double)chunk_acc[rt];
-          chunk_acc[rt] = 0.f;
-        }
+    for (int rt = 0; rt < 2; ++rt) {
+      float sums[kN];
+      chunk_sums<MODE>(acc[rt], sums);
+#pragma unroll
+      for (int i = 0; i < kN; ++i) {
+        st.overflow |= !(sums[i] <= kOverflowGuard);
+        st.zsum[rt] += (double)sums[i];
       }
-    } else {
-      constexpr int kN = sums_per_lane<MODE>();
-      const int jl0 = (int)((key0 - kbeg) / a.c);  // first chunk of this subtile
-#pragma unroll
-      for (int rt = 0; rt < 2; ++rt) {
-        float sums[kN];
-        chunk_sums<MODE>(acc[rt], sums);
+      if constexpr (MODE == kC4) {
+        // lane half h holds chunks 2i+h of rows (row tile rt, row lane%32)
+        const int row = my_row0 + rt * 32 + (lane & 31);
 #pragma unroll
         for (int i = 0; i < kN; ++i) {
-          overflow |= !(sums[i] <= kOverflowGuard);
-          zsum[rt] += (double)sums[i];
+          const int key_first = 8 * i + 4 * half;
+          if (row < a.R && (FULL || key_first < nvalid))
+            part[(int64_t)(jl0 + 2 * i + half) * a.R + row] = sums[i];
         }
-        if constexpr (MODE == kC4) {
-          // lane half h holds chunks 2i+h of rows (row tile rt, row lane%32)
-          const int row = my_row0 + rt * 32 + (lane & 31);
+      } else if (rt == half) {
+        // both halves hold every sum: half h writes row tile h
+        const int row = my_row0 + rt * 32 + (lane & 31);
 #pragma unroll
-          for (int i = 0; i < kN; ++i) {
-            int jl = jl0 + 2 * i + half;
-            int key_first = 8 * i + 4 * half;
-            if (row < a.R && key_first < nvalid) part[(int64_t)jl * a.R + row] = sums[i];
-          }
-        } else {
-          // both halves hold all sums: half h writes row tile h
-          if (rt == half) {
-            const int row = my_row0 + rt * 32 + (lane & 31);
-#pragma unroll
-            for (int i = 0; i < kN; ++i) {
-              int key_first = i * (kSub / kN);
-              if (row < a.R && key_first < nvalid) part[(int64_t)(jl0 + i) * a.R + row] = sums[i];
-            }
-          }
+        for (int i = 0; i < kN; ++i) {
+          const int key_first = i * (kSub / kN);
+          if (row < a.R && (FULL || key_first < nvalid))
+            part[(int64_t)(jl0 + i) * a.R + row] = sums[i];
         }
       }
     }
+  }
+}
+
+// Processes the workgroup's key range once (see process_subtile for PASS).
+template <int D, int MODE, int PASS>
+__device__ bool run_range(const ScoreArgs& a, int g, int range, int row0,
+                          const bf16x8 (&qf)[2][D / 16], uint16_t* lds, RangeState& st) {
+  constexpr int kSegs = D / 8;
+  constexpr int kPer = StageRegs<D>::kPer;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, half = lane >> 5;
+  const int64_t kbeg = (int64_t)range * a.key_range;
+  const int nkeys = (int)(min<int64_t>(kbeg + a.key_range, a.n) - kbeg);
+  const int nstage = (nkeys + kStage - 1) / kStage;
+  const int my_row0 = row0 + wave * kWaveRows;
+  st.overflow = false;
+  st.chunk_acc[0] = st.chunk_acc[1] = 0.f;
+  if (PASS != 1) st.zsum[0] = st.zsum[1] = 0.0;
+  if (PASS == 1) st.mref[0] = st.mref[1] = -INFINITY;
+  float* part = a.part + ((int64_t)(g * a.n_ranges + range) * a.cpr) * a.R;
+
+  // per-thread element offsets of its pieces inside a stage (and of the stage's
+  // first row, read in place of rows past the range end)
+  uint32_t voff[kPer], voff0[kPer];
+#pragma unroll
+  for (int p = 0; p < kPer; ++p) {
+    const int idx = threadIdx.x + p * kWaves * 64;
+    const int key = idx / kSegs, seg = idx % kSegs;
+    voff[p] = (uint32_t)(((int64_t)key * a.Hkv + g) * D + seg * 8);
+    voff0[p] = (uint32_t)(g * D + seg * 8);
+  }
+  const int64_t stage_elems = (int64_t)kStage * a.Hkv * D;
+  const uint16_t* kbase = a.k + kbeg * a.Hkv * D;
+
+  StageRegs<D> r;
+  stage_load<D>(kbase, nkeys, voff, voff0, r);
+  stage_store<D>(r, lds);
+  __syncthreads();
+  for (int s = 0; s < nstage; ++s) {
+    const int rk0 = s * kStage;
+    if (s + 1 < nstage) stage_load<D>(kbase + (s + 1) * stage_elems, nkeys - rk0 - kStage, voff, voff0, r);
+    const uint16_t* cur = lds + (s & 1) * kStage * D;
+    if (rk0 + kStage <= nkeys) {
+      process_subtile<D, MODE, PASS, true>(a, qf, cur, 0, rk0, nkeys, s == 0, part, my_row0, st);
+      process_subtile<D, MODE, PASS, true>(a, qf, cur, kSub, rk0 + kSub, nkeys, false, part, my_row0, st);
+    } else {
+      process_subtile<D, MODE, PASS, false>(a, qf, cur, 0, rk0, nkeys, s == 0, part, my_row0, st);
+      if (rk0 + kSub < nkeys)
+        process_subtile<D, MODE, PASS, false>(a, qf, cur, kSub, rk0 + kSub, nkeys, false, part,
+                                              my_row0, st);
+    }
+    if (s + 1 < nstage) stage_store<D>(r, lds + ((s + 1) & 1) * kStage * D);
+    __syncthreads();
   }
   if constexpr (MODE == kC4) {
     // each half summed different chunks: combine in a fixed order (half 0 + half 1)
 #pragma unroll
     for (int rt = 0; rt < 2; ++rt) {
-      double o = partner_d(zsum[rt]);
-      zsum[rt] = half ? (o + zsum[rt]) : (zsum[rt] + o);
+      const double o = partner_d(st.zsum[rt]);
+      st.zsum[rt] = half ? (o + st.zsum[rt]) : (st.zsum[rt] + o);
     }
   }
-  return overflow;
+  return st.overflow;
 }
 
 template <int D, int MODE>
 __global__ __launch_bounds__(kWaves * 64, 2) void score_bf16_kernel(ScoreArgs a) {
-  __shared__ __attribute__((aligned(16))) uint16_t lds[kSub * D];
+  __shared__ __attribute__((aligned(16))) uint16_t lds[2 * kStage * D];
   const uint32_t L = xcd_remap(blockIdx.x, a.nblocks_padded);
   if (L >= a.nblocks) return;
   const int rb = (int)(L % a.n_row_blocks);
@@ -289,24 +356,23 @@ __global__ __launch_bounds__(kWaves * 64, 2) void score_bf16_kernel(ScoreArgs a)
     const uint16_t* src = a.q + ((int64_t)t * a.Hq + (int64_t)g * a.G + hi) * D + 8 * half;
 #pragma unroll
     for (int ks = 0; ks < D / 16; ++ks) {
-      u32x4 v = {0u, 0u, 0u, 0u};
-      if (ok) v = *reinterpret_cast<const u32x4*>(src + 16 * ks);
+      u32x4 v = *reinterpret_cast<const u32x4*>(src + 16 * ks);
+      if (!ok) v = u32x4{0u, 0u, 0u, 0u};
       qf[rt][ks] = *reinterpret_cast<bf16x8*>(&v);
     }
   }
 
-  float mref[2];
-  double zsum[2];
-  bool of = run_range<D, MODE, 0>(a, g, range, row0, qf, lds, mref, zsum);
+  RangeState st;
+  const bool of = run_range<D, MODE, 0>(a, g, range, row0, qf, lds, st);
   if (__syncthreads_or(of ? 1 : 0)) {
-    run_range<D, MODE, 1>(a, g, range, row0, qf, lds, mref, zsum);
-    run_range<D, MODE, 2>(a, g, range, row0, qf, lds, mref, zsum);
+    run_range<D, MODE, 1>(a, g, range, row0, qf, lds, st);
+    run_range<D, MODE, 2>(a, g, range, row0, qf, lds, st);
   }
   const int row = row0 + wave * kWaveRows + lane;  // lane l reports row tile l/32
   if (row < a.R) {
     const int64_t o = (int64_t)(g * a.n_ranges + range) * a.R + row;
-    a.mc[o] = half ? mref[1] : mref[0];
-    a.z[o] = half ? zsum[1] : zsum[0];
+    a.mc[o] = half ? st.mref[1] : st.mref[0];
+    a.z[o] = half ? st.zsum[1] : st.zsum[0];
   }
 }
 
@@ -482,57 +548,75 @@ __global__ __launch_bounds__(64) void score_f32_kernel(ScoreArgsF32 a) {
 // ---------------------------------------------------------------------------
 // finalize
 // ---------------------------------------------------------------------------
-// F1: per (g, row): Mc = max over ranges of mc, Z = sum exp2(mc - Mc) z; the z
-// slot of every range is overwritten with w = exp2(mc - Mc) / Z.
-__global__ __launch_bounds__(256) void row_norm_kernel(const float* __restrict__ mc,
-                                                      double* __restrict__ z, int Hkv, int R,
-                                                      int NR) {
-  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (idx >= (int64_t)Hkv * R) return;
-  const int g = (int)(idx / R), row = (int)(idx % R);
+// F1: per (g, row): Mc = max over ranges of mc, Z = sum exp2(mc - Mc) z, and the
+// z slot of every range is overwritten with w = exp2(mc - Mc) / Z (all fp64).
+// A workgroup serves 64 rows (one per lane, coalesced) with its 4 waves splitting
+// the ranges; the waves' partial maxima and sums are combined through LDS in
+// wave order.
+constexpr int kNormWaves = 4;
+
+__global__ __launch_bounds__(kNormWaves * 64) void row_norm_kernel(const float* __restrict__ mc,
+                                                                  double* __restrict__ z, int Hkv,
+                                                                  int R, int NR) {
+  __shared__ float smax[kNormWaves][64];
+  __shared__ double ssum[kNormWaves][64];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int blocks_per_head = (R + 63) / 64;
+  const int g = blockIdx.x / blocks_per_head;
+  const int row = (blockIdx.x % blocks_per_head) * 64 + lane;
+  const bool ok = row < R;
   const int64_t base = (int64_t)g * NR * R + row;
   float M = -INFINITY;
-  for (int r = 0; r < NR; ++r) M = fmaxf(M, mc[base + (int64_t)r * R]);
+  for (int r = wave; r < NR; r += kNormWaves)
+    if (ok) M = fmaxf(M, mc[base + (int64_t)r * R]);
+  smax[wave][lane] = M;
+  __syncthreads();
+  M = smax[0][lane];
+  for (int w = 1; w < kNormWaves; ++w) M = fmaxf(M, smax[w][lane]);
   double Z = 0.0;
-  for (int r = 0; r < NR; ++r)
-    Z += exp2((double)mc[base + (int64_t)r * R] - (double)M) * z[base + (int64_t)r * R];
+  for (int r = wave; r < NR; r += kNormWaves)
+    if (ok) Z += exp2((double)mc[base + (int64_t)r * R] - (double)M) * z[base + (int64_t)r * R];
+  ssum[wave][lane] = Z;
+  __syncthreads();
+  Z = ssum[0][lane];
+  for (int w = 1; w < kNormWaves; ++w) Z += ssum[w][lane];
+  if (!ok) return;
   const double inv = 1.0 / Z;
-  for (int r = 0; r < NR; ++r)
+  for (int r = wave; r < NR; r += kNormWaves)
     z[base + (int64_t)r * R] = exp2((double)mc[base + (int64_t)r * R] - (double)M) * inv;
 }
 
-// F2: per (g, chunk): wpart[g][j] = sum_r w[g][range(j)][r] * P[g][range][jl][r] in
-// fp64.  A workgroup of 256 threads serves 8 chunks, 32 lanes per chunk; each
-// lane sums rows lane, lane+32, ... in order, then a fixed butterfly reduces
-// the 32 lanes.
+// F2: A_j = sum over KV heads g (in order) of sum over rows r of
+// w[g][range(j)][r] * P[g][range(j)][jl][r], in fp64.  One wave per chunk: lane
+// l takes rows l, l+64, ... with four independent accumulators, then a fixed
+// butterfly reduces the wave.
 __global__ __launch_bounds__(256) void chunk_reduce_kernel(const float* __restrict__ part,
                                                           const double* __restrict__ w,
-                                                          double* __restrict__ wpart, int R,
-                                                          int NR, int cpr, int64_t m,
-                                                          int64_t m_pad) {
-  const int g = blockIdx.y;
-  const int64_t j = (int64_t)blockIdx.x * 8 + (threadIdx.x >> 5);
-  const int lane = threadIdx.x & 31;
-  if (j >= m) return;  // whole 32-lane groups exit together
+                                                          double* __restrict__ A, int Hkv, int R,
+                                                          int NR, int cpr, int64_t m) {
+  const int64_t j = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (j >= m) return;  // whole waves exit together
   const int range = (int)(j / cpr), jl = (int)(j % cpr);
-  const float* p = part + (((int64_t)g * NR + range) * cpr + jl) * R;
-  const double* wr = w + ((int64_t)g * NR + range) * R;
-  double s = 0.0;
-  for (int r = lane; r < R; r += 32) s += (double)p[r] * wr[r];
+  double total = 0.0;
+  for (int g = 0; g < Hkv; ++g) {
+    const float* p = part + (((int64_t)g * NR + range) * cpr + jl) * R;
+    const double* wr = w + ((int64_t)g * NR + range) * R;
+    double s0 = 0.0, s1 = 0.0, s2 = 0.0, s3 = 0.0;
+    int r = lane;
+    for (; r + 192 < R; r += 256) {
+      s0 += (double)p[r] * wr[r];
+      s1 += (double)p[r + 64] * wr[r + 64];
+      s2 += (double)p[r + 128] * wr[r + 128];
+      s3 += (double)p[r + 192] * wr[r + 192];
+    }
+    for (; r < R; r += 64) s0 += (double)p[r] * wr[r];
+    double s = (s0 + s1) + (s2 + s3);
 #pragma unroll
-  for (int off = 16; off >= 1; off >>= 1) s += __shfl_xor(s, off, 32);
-  if (lane == 0) wpart[(int64_t)g * m_pad + j] = s;
-}
-
-// F3: A_j = sum over KV heads in order.
-__global__ __launch_bounds__(256) void head_sum_kernel(const double* __restrict__ wpart,
-                                                      double* __restrict__ A, int Hkv, int64_t m,
-                                                      int64_t m_pad) {
-  const int64_t j = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (j >= m) return;
-  double s = 0.0;
-  for (int g = 0; g < Hkv; ++g) s += wpart[(int64_t)g * m_pad + j];
-  A[j] = s;
+    for (int off = 32; off >= 1; off >>= 1) s += __shfl_xor(s, off);
+    total += s;
+  }
+  if (lane == 0) A[j] = total;
 }
 
 int chunk_mode(int c) {
@@ -568,8 +652,6 @@ ScorePlan make_score_plan(const ckv_dims* d) {
   off = align_up(off + H * NR * R * sizeof(float), 256);
   p.off_z = off;
   off = align_up(off + H * NR * R * sizeof(double), 256);
-  p.off_wpart = off;
-  off = align_up(off + H * (size_t)align_up(p.m, 64) * sizeof(double), 256);
   p.bytes = off;
   return p;
 }
@@ -583,10 +665,8 @@ ckv_status launch_score(const ckv_dims* d, const void* q, const void* k, double*
   float* part = reinterpret_cast<float*>(base + p.off_part);
   float* mc = reinterpret_cast<float*>(base + p.off_mc);
   double* z = reinterpret_cast<double*>(base + p.off_z);
-  double* wpart = reinterpret_cast<double*>(base + p.off_wpart);
   const int G = d->n_q_heads / d->n_kv_heads;
   const float c1 = resolve_scale(d) * 1.4426950408889634f;
-  const int64_t m_pad = (int64_t)align_up(p.m, 64);
 
   if (d->dtype == CKV_DTYPE_BF16) {
     ScoreArgs a;
@@ -635,17 +715,12 @@ ckv_status launch_score(const ckv_dims* d, const void* q, const void* k, double*
   }
   CKV_HIP(hipGetLastError());
   if (after_main) CKV_HIP(hipEventRecord(after_main, st));
-  {
-    const int64_t nthreads = (int64_t)d->n_kv_heads * p.rows;
-    hipLaunchKernelGGL(row_norm_kernel, dim3((unsigned)ceil_div(nthreads, 256)), dim3(256), 0, st,
-                       mc, z, d->n_kv_heads, p.rows, p.n_ranges);
-    CKV_HIP(hipGetLastError());
-  }
-  hipLaunchKernelGGL(chunk_reduce_kernel, dim3((unsigned)ceil_div(p.m, 8), d->n_kv_heads), dim3(256),
-                     0, st, part, z, wpart, p.rows, p.n_ranges, p.cpr, p.m, m_pad);
+  const int norm_blocks = d->n_kv_heads * (int)ceil_div(p.rows, 64);
+  hipLaunchKernelGGL(row_norm_kernel, dim3(norm_blocks), dim3(kNormWaves * 64), 0, st, mc, z,
+                     d->n_kv_heads, p.rows, p.n_ranges);
   CKV_HIP(hipGetLastError());
-  hipLaunchKernelGGL(head_sum_kernel, dim3((unsigned)ceil_div(p.m, 256)), dim3(256), 0, st, wpart,
-                     scores, d->n_kv_heads, p.m, m_pad);
+  hipLaunchKernelGGL(chunk_reduce_kernel, dim3((unsigned)ceil_div(p.m, 4)), dim3(256), 0, st, part,
+                     z, scores, d->n_kv_heads, p.rows, p.n_ranges, p.cpr, p.m);
   CKV_HIP(hipGetLastError());
   return CKV_OK;
 }

@@ -33,17 +33,24 @@ __device__ __forceinline__ uint64_t order_key(double x) {
   return (u >> 63) ? ~u : (u | 0x8000000000000000ull);
 }
 
-template <typename T, typename Op>
-__device__ T block_reduce(T v, Op op, T* red) {
+// block-wide minimum of lo and maximum of hi (every thread gets both)
+__device__ void block_minmax(uint64_t& lo, uint64_t& hi, uint64_t* red_lo, uint64_t* red_hi) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
 #pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) v = op(v, __shfl_xor(v, off));
+  for (int off = 32; off >= 1; off >>= 1) {
+    const uint64_t l2 = __shfl_xor(lo, off), h2 = __shfl_xor(hi, off);
+    lo = l2 < lo ? l2 : lo;
+    hi = h2 > hi ? h2 : hi;
+  }
   __syncthreads();
-  if (lane == 0) red[wave] = v;
+  if (lane == 0) { red_lo[wave] = lo; red_hi[wave] = hi; }
   __syncthreads();
-  T r = red[0];
-  for (int w = 1; w < kWavesSel; ++w) r = op(r, red[w]);
-  return r;
+  lo = red_lo[0];
+  hi = red_hi[0];
+  for (int w = 1; w < kWavesSel; ++w) {
+    lo = red_lo[w] < lo ? red_lo[w] : lo;
+    hi = red_hi[w] > hi ? red_hi[w] : hi;
+  }
 }
 
 // exclusive prefix sum over the block (returns this thread's exclusive prefix)
@@ -75,7 +82,9 @@ __global__ __launch_bounds__(kThreads) void select_kernel(const double* __restri
                                                           int use_lds) {
   extern __shared__ uint64_t key_cache[];
   __shared__ uint32_t hist[256];
+  __shared__ uint32_t wsum[4];
   __shared__ uint64_t red_u[kWavesSel];
+  __shared__ uint64_t red_u2[kWavesSel];
   __shared__ int64_t red_i[kWavesSel];
   __shared__ SelState st;
 
@@ -101,8 +110,7 @@ __global__ __launch_bounds__(kThreads) void select_kernel(const double* __restri
       uint64_t x = key_at(i);
       if ((x & mask) == prefix) { lo = x < lo ? x : lo; hi = x > hi ? x : hi; }
     }
-    lo = block_reduce(lo, [](uint64_t a, uint64_t b) { return a < b ? a : b; }, red_u);
-    hi = block_reduce(hi, [](uint64_t a, uint64_t b) { return a > b ? a : b; }, red_u);
+    block_minmax(lo, hi, red_u, red_u2);
     if (lo == hi) {  // every candidate equal: the lowest indices among them win
       if (tid == 0) { st.prefix = lo; st.mask = ~0ull; st.done = 1; }
       __syncthreads();
@@ -117,19 +125,33 @@ __global__ __launch_bounds__(kThreads) void select_kernel(const double* __restri
       if ((x & mask) == prefix) atomicAdd(&hist[(x >> shift) & 255], 1u);
     }
     __syncthreads();
-    if (tid == 0) {
-      int64_t need = st.remaining, above = 0;
-      int b = 255;
-      for (; b > 0; --b) {
-        if (above + hist[b] >= need) break;
-        above += hist[b];
+    // counts of keys in bins >= b, as an inclusive scan over t = 255 - b by the
+    // first four waves; the bin where that count first reaches `need` is chosen
+    const int64_t need = st.remaining;
+    uint32_t cum = 0, mine = 0;
+    if (tid < 256) {
+      mine = hist[255 - tid];
+      cum = mine;
+#pragma unroll
+      for (int off = 1; off < 64; off <<= 1) {
+        const uint32_t y = __shfl_up(cum, off);
+        if ((tid & 63) >= off) cum += y;
       }
-      const uint64_t digit_mask = 255ull << shift;
-      const uint64_t keep_hi = shift + 8 >= 64 ? 0 : ~((1ull << (shift + 8)) - 1);
-      st.prefix = (lo & keep_hi) | ((uint64_t)b << shift);
-      st.mask = keep_hi | digit_mask;
-      st.remaining = need - above;
-      st.done = (hist[b] == (uint32_t)st.remaining) || shift == 0;
+      if ((tid & 63) == 63) wsum[tid >> 6] = cum;
+    }
+    __syncthreads();
+    if (tid < 256) {
+      for (int w = 0; w < (tid >> 6); ++w) cum += wsum[w];
+      const uint32_t before = cum - mine;
+      if (before < need && cum >= need) {  // exactly one thread
+        const int b = 255 - tid;
+        const uint64_t digit_mask = 255ull << shift;
+        const uint64_t keep_hi = shift + 8 >= 64 ? 0 : ~((1ull << (shift + 8)) - 1);
+        st.prefix = (lo & keep_hi) | ((uint64_t)b << shift);
+        st.mask = keep_hi | digit_mask;
+        st.remaining = need - before;
+        st.done = (mine == (uint32_t)st.remaining) || shift == 0;
+      }
     }
     __syncthreads();
     if (st.done) break;
