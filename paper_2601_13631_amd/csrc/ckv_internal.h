@@ -69,7 +69,8 @@ struct ScorePlan {
   int32_t key_range;  // keys per range (multiple of 32 and of c)
   int32_t n_ranges;   // ceil(n / key_range)
   int32_t cpr;        // chunks per range
-  size_t off_part, off_mc, off_z, bytes;  // workspace layout
+  int32_t ldp;        // row stride of the partial sums (rows padded to whole row blocks)
+  size_t off_part, off_mc, off_z, off_flags, bytes;  // workspace layout
 };
 ScorePlan make_score_plan(const ckv_dims* d);
 // after_main (optional) is recorded between the main kernel and the finalize kernels.
