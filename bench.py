@@ -9,12 +9,20 @@ each with its own seeded synthetic Q/K/V resident in HBM before timing starts.
 Prints one JSON line.  ``roofline`` describes the scoring kernel (the dominant
 kernel): its algorithmic flops per launch (2*S*Hq*n*d) over its average
 duration, taken from HIP events recorded on the layer's stream around that
-kernel inside the timed region.  ``cpu_baseline`` times the oracle (plain C,
-fp64) on a bounded sample of the same workload on this host's cores.
+kernel inside the timed region (two events per step; the context records no
+others there).  ``roofline.traffic`` is the kernel's HBM bytes per launch from
+the committed rocprofv3 counter summary (FETCH_SIZE and WRITE_SIZE, each scaled
+by what the counter reads for a plain copy of known size); it is null when the
+kernel's sources no longer match the hash recorded with those counters.
+``cpu_baseline`` times the oracle (plain C, fp64) on a bounded sample of the
+same workload on this host's cores.  ``detail`` holds an untimed diagnostic
+pass after the timed region: per-stage times from events between every stage,
+and the step time with no events at all.
 """
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import os
 import sys
@@ -25,11 +33,43 @@ sys.path.insert(0, ROOT)
 
 METRIC = "prefix tokens/sec per Re-Prefill layer step"
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_F32_TFLOPS = 157.3     # MI355X fp32 (matrix and vector)
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
 
 
 def log(msg: str) -> None:
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+SCORE_SOURCES = ("paper_2601_13631_amd/csrc/score.hip", "paper_2601_13631_amd/csrc/ckv_internal.h")
+
+
+def score_source_hash() -> str:
+    h = hashlib.sha256()
+    for f in SCORE_SOURCES:
+        with open(os.path.join(ROOT, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def counter_traffic(workload: str):
+    """HBM bytes per launch of score_bf16_kernel from the committed counter
+    summary, or (None, reason) if there is none for this workload or the
+    kernel's sources changed since the counters were taken."""
+    path = os.path.join(ROOT, "profiles", f"score_bf16_kernel_{workload}_pmc.txt")
+    if not os.path.exists(path):
+        return None, "no counter summary for this workload"
+    kv = {}
+    with open(path) as fh:
+        for line in fh:
+            if ":" in line and not line.startswith((" ", "#")):
+                k, v = line.split(":", 1)
+                kv[k.strip()] = v.strip()
+    if kv.get("source_sha256") != score_source_hash():
+        return None, "kernel sources changed since the counters were taken"
+    fetch = float(kv["fetch_size_kib_per_dispatch"]) * float(kv["fetch_scale"])
+    write = float(kv["write_size_kib_per_dispatch"]) * float(kv["write_scale"])
+    return (fetch + write) * 1024.0, os.path.relpath(path, ROOT)
 
 
 def main() -> int:
@@ -56,7 +96,9 @@ def main() -> int:
 
     w = synth.WORKLOADS[args.workload]
     if w.host_resident:
-        print("host-resident workloads are measured by tests/bench_host.py", file=sys.stderr)
+        print(f"{w.name} keeps its prefix in pinned host memory; bench.py measures the "
+              "HBM-resident workloads (the host-resident layer path is exercised by the GPU tests)",
+              file=sys.stderr)
         return 2
     torch.cuda.set_device(0)
     dev = torch.device("cuda:0")
@@ -75,44 +117,71 @@ def main() -> int:
     layers = [{k: up(v) for k, v in h.items()} for h in host]
     dims = ckv.make_dims(w.n_prefix, w.n_suffix, w.n_q_heads, w.n_kv_heads, w.head_dim,
                          w.chunk_size, ckv.DTYPE_F32 if w.dtype == "f32" else ckv.DTYPE_BF16)
-    flags = ckv.CTX_STAGE_TIMING | (ckv.CTX_MATERIALIZE if args.materialize else 0)
-    ctx = ckv.Context(dims, w.keep_ratio, flags)
+    mat = ckv.CTX_MATERIALIZE if args.materialize else 0
+    ctx = ckv.Context(dims, w.keep_ratio, ckv.CTX_SCORE_TIMING | mat)
     k = ctx.k
     outs = [torch.empty_like(l["q"]) for l in layers]
     stream = torch.cuda.current_stream()
 
-    def step(i: int) -> None:
+    def step(c, i: int) -> None:
         l = layers[i % L]
-        ctx.reprefill_layer(i % L, l["q"], l["k_suffix"], l["v_suffix"], l["k_prefix"], outs[i % L],
-                            k_prefix=l["k_prefix"], v_prefix=l["v_prefix"], stream=stream)
+        c.reprefill_layer(i % L, l["q"], l["k_suffix"], l["v_suffix"], l["k_prefix"], outs[i % L],
+                          k_prefix=l["k_prefix"], v_prefix=l["v_prefix"], stream=stream)
 
     log(f"warmup {args.warmup} steps")
     for i in range(args.warmup):
-        step(i)
+        step(ctx, i)
     torch.cuda.synchronize()
-    ctx.reset()  # stage times restart with the timed region
+    ctx.reset()  # score times restart with the timed region
     log(f"timing {args.steps} steps")
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
-        step(i)
+        step(ctx, i)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
-    stage_ms, n_timed = ctx.stage_times()
+    score_ms, n_timed = ctx.stage_times()
     ctx.close()
+    assert n_timed == args.steps, (n_timed, args.steps)
     ms_per_step = elapsed * 1e3 / args.steps
     value = w.n_prefix * args.steps / elapsed
-    per_layer = {s: stage_ms[s] / n_timed for s in stage_ms}
-    log(f"{ms_per_step * 1e3:.1f} us/step; stages (us): " +
-        ", ".join(f"{s} {v * 1e3:.1f}" for s, v in per_layer.items()))
+    score_s = score_ms["score"] / n_timed * 1e-3
+    log(f"{ms_per_step * 1e3:.1f} us/step; score kernel {score_s * 1e6:.1f} us")
+
+    # untimed diagnostics: every stage bracketed by events, then no events at all
+    n_diag = min(args.steps, 4 * L)
+    diag = ckv.Context(dims, w.keep_ratio, ckv.CTX_STAGE_TIMING | mat)
+    for i in range(min(args.warmup, L)):
+        step(diag, i)
+    torch.cuda.synchronize()
+    diag.reset()
+    for i in range(n_diag):
+        step(diag, i)
+    stage_ms, n_st = diag.stage_times()
+    diag.close()
+    per_layer = {s_: stage_ms[s_] / n_st for s_ in stage_ms}
+    plain = ckv.Context(dims, w.keep_ratio, mat)
+    for i in range(min(args.warmup, L)):
+        step(plain, i)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    for i in range(n_diag):
+        step(plain, i)
+    torch.cuda.synchronize()
+    plain_us = (time.perf_counter() - t1) * 1e6 / n_diag
+    plain.close()
+    log("diagnostic stages (us): " + ", ".join(f"{s_} {v * 1e3:.1f}" for s_, v in per_layer.items()) +
+        f"; step without events {plain_us:.1f} us")
 
     # scoring: algorithmic flops per launch / average launch duration
     score_flops = 2.0 * w.n_suffix * w.n_q_heads * w.n_prefix * w.head_dim
-    score_s = per_layer["score"] * 1e-3
     achieved = score_flops / score_s / 1e12
-    roofline = {"kernel": "score_bf16_kernel", "bound": "mfma", "achieved": round(achieved, 2),
-                "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
-                "traffic": None,
+    traffic, traffic_src = counter_traffic(w.name) if w.dtype == "bf16" else (None, "fp32 kernel")
+    roofline = {"kernel": "score_bf16_kernel" if w.dtype == "bf16" else "score_f32_kernel",
+                "bound": "mfma", "achieved": round(achieved, 2),
+                "peak": PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_F32_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(achieved / (PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_F32_TFLOPS), 4),
+                "traffic": round(traffic) if traffic else None, "traffic_source": traffic_src,
                 "flops_per_launch": score_flops, "avg_launch_us": round(score_s * 1e6, 2)}
     # attention and kept-chunk bytes, as context
     T = k * w.chunk_size
@@ -123,7 +192,9 @@ def main() -> int:
         "attn_tflops": round(attn_flops / attn_s / 1e12, 2),
         "attn_frac_mfma": round(attn_flops / attn_s / 1e12 / PEAK_BF16_TFLOPS, 4),
         "attn_kept_kv_gbs": round(kept_bytes / attn_s / 1e9, 1),
-        "stage_us_per_layer": {s: round(v * 1e3, 2) for s, v in per_layer.items()},
+        "stage_us_per_layer": {s_: round(v * 1e3, 2) for s_, v in per_layer.items()},
+        "stage_events_note": "diagnostic pass with events between all stages; each event adds a gap",
+        "us_per_step_without_events": round(plain_us, 2),
     }
     if args.materialize and per_layer["move"] > 0:
         others["gather_gbs"] = round(2 * kept_bytes / (per_layer["move"] * 1e-3) / 1e9, 1)

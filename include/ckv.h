@@ -182,6 +182,10 @@ typedef struct ckv_ctx ckv_ctx;
                                        attention instead of reading spans in place */
 #define CKV_CTX_STAGE_TIMING 0x4    /* record HIP events between the stages of every
                                        layer (see ckv_ctx_stage_times) */
+#define CKV_CTX_SCORE_TIMING 0x8    /* record HIP events only around the chunk-scoring
+                                       main kernel: two events per layer instead of six;
+                                       ckv_ctx_stage_times then reports the score stage
+                                       and zero for the others */
 
 /* Stages timed with CKV_CTX_STAGE_TIMING. */
 #define CKV_STAGE_SCORE 0     /* chunk-scoring main kernel                         */
@@ -235,7 +239,8 @@ typedef struct ckv_layer_stats {
 
 /* Sum of the GPU time of each stage (ms[CKV_N_STAGES], milliseconds) over
  * every layer run since the context was created or last reset, and that
- * number of layers in *n_layers.  Requires CKV_CTX_STAGE_TIMING; waits for the
+ * number of layers in *n_layers.  Requires CKV_CTX_STAGE_TIMING or
+ * CKV_CTX_SCORE_TIMING (then only ms[CKV_STAGE_SCORE] is filled); waits for the
  * events of the layers not yet accounted.  Stage times come from events
  * recorded on each layer's compute stream between its kernel launches. */
 ckv_status ckv_ctx_stage_times(ckv_ctx* ctx, double* ms, int64_t* n_layers);

@@ -20,11 +20,11 @@ LIB_PATH = os.path.join(_HERE, "libckv.so")
 
 OK, EINVAL, EUNSUPPORTED, EHIP, ENOMEM, ESTATE = range(6)
 DTYPE_F32, DTYPE_BF16 = 0, 1
-CTX_HOST_PREFIX, CTX_MATERIALIZE, CTX_STAGE_TIMING = 0x1, 0x2, 0x4
+CTX_HOST_PREFIX, CTX_MATERIALIZE, CTX_STAGE_TIMING, CTX_SCORE_TIMING = 0x1, 0x2, 0x4, 0x8
 STAGES = ("score", "finalize", "select", "move", "attn")
 
 if not os.path.exists(LIB_PATH):
-    raise ImportError(f"libckv.so not built at {LIB_PATH}; run `python -m paper_2601_13631_amd.build`")
+    raise ImportError(f"libckv.so not built at {LIB_PATH}; run `python paper_2601_13631_amd/build.py`")
 _lib = ctypes.CDLL(LIB_PATH)
 
 

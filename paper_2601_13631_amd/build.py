@@ -1,6 +1,6 @@
 """Builds libckv.so (all HIP sources, gfx950) next to this file.
 
-Run as ``python -m paper_2601_13631_amd.build`` or call ``build()``.  Every
+Run as ``python paper_2601_13631_amd/build.py`` or call ``build()``.  Every
 source is compiled with hipcc for gfx950 only, with packed-fp32 instruction
 selection disabled, then linked into one shared library.
 """

@@ -63,14 +63,36 @@ __device__ __forceinline__ uint32_t xcd_remap(uint32_t bid, uint32_t nblocks_pad
 }
 
 // ---- kernels' host-side launchers (each file owns its kernels) ----------------
+// Work decomposition of chunk scoring.  Each (KV head g, row block rb) pair --
+// rbh = g*RB + rb, a block of rpb rows of that head -- spans the whole key axis,
+// cut into U units of UK keys (UK = lcm(64, c): whole 64-key stages and whole
+// chunks).  The units of every rbh are split into NS segments of floor or ceil
+// of U/NS units: segment s holds units [s*U/NS, (s+1)*U/NS).  One workgroup
+// runs one segment, so the grid is Hkv*RB*NS workgroups of equal work (within
+// one unit); NS is chosen so that the grid fills two workgroups per CU.
+struct ScoreWork {
+  int32_t rpb;  // rows per row block (a power of two)
+  int32_t RB;   // row blocks per KV head
+  int32_t UK;   // keys per unit
+  int32_t U;    // units per rbh: ceil(n / UK)
+  int32_t NS;   // segments per rbh
+  int32_t ldp;  // row stride of the partial sums: RB * rpb
+  __host__ __device__ int seg_begin(int s) const {  // first unit of segment s
+    return (int)((int64_t)s * U / NS);
+  }
+  __host__ __device__ int seg_of_unit(int u) const {  // segment holding unit u
+    return (int)((((int64_t)u + 1) * NS - 1) / U);
+  }
+};
+
 struct ScorePlan {
-  int64_t m;          // chunks
-  int32_t rows;       // G*S rows per KV head
-  int32_t key_range;  // keys per range (multiple of 32 and of c)
-  int32_t n_ranges;   // ceil(n / key_range)
-  int32_t cpr;        // chunks per range
-  int32_t ldp;        // row stride of the partial sums (rows padded to whole row blocks)
-  size_t off_part, off_mc, off_z, off_flags, bytes;  // workspace layout
+  int64_t m;      // chunks
+  int32_t rows;   // G*S rows per KV head
+  ScoreWork w;
+  // workspace layout: partial sums [Hkv][U*UK/c][ldp] (fp32), references
+  // [Hkv*RB][NS][rpb] (fp32), sums / weights [Hkv*RB][NS][rpb] (fp64),
+  // overflow flags [Hkv*RB][NS]
+  size_t off_part, off_mc, off_z, off_flags, bytes;
 };
 ScorePlan make_score_plan(const ckv_dims* d);
 // after_main (optional) is recorded between the main kernel and the finalize kernels.

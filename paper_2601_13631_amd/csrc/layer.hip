@@ -106,11 +106,14 @@ ckv_status copy_runs(ckv_ctx* c, const int32_t* chunks, int64_t cnt, int64_t slo
   return CKV_OK;
 }
 
+bool all_stages(const ckv_ctx* c) { return c->flags & CKV_CTX_STAGE_TIMING; }
+
 // Adds the stage times of the oldest unaccounted layer to the totals.
 ckv_status harvest_one(ckv_ctx* c) {
   hipEvent_t* e = c->tev[c->t_done % ckv_ctx::kRing];
-  CKV_HIP(hipEventSynchronize(e[CKV_N_STAGES]));
-  for (int s = 0; s < CKV_N_STAGES; ++s) {
+  const int n = all_stages(c) ? CKV_N_STAGES : 1;
+  CKV_HIP(hipEventSynchronize(e[n]));
+  for (int s = 0; s < n; ++s) {
     float ms = 0.f;
     CKV_HIP(hipEventElapsedTime(&ms, e[s], e[s + 1]));
     c->t_ms[s] += ms;
@@ -136,7 +139,8 @@ ckv_status ckv_ctx_create(const ckv_dims* dims, double keep_ratio, int32_t flags
     if (s != CKV_OK) return s;
   }
   if (!(keep_ratio > 0.0 && keep_ratio <= 1.0)) CKV_FAIL(CKV_EINVAL, "keep_ratio must be in (0, 1]");
-  if (flags & ~(CKV_CTX_HOST_PREFIX | CKV_CTX_MATERIALIZE | CKV_CTX_STAGE_TIMING))
+  if (flags & ~(CKV_CTX_HOST_PREFIX | CKV_CTX_MATERIALIZE | CKV_CTX_STAGE_TIMING |
+                CKV_CTX_SCORE_TIMING))
     CKV_FAIL(CKV_EINVAL, "unknown flags");
   ckv_ctx* c = new (std::nothrow) ckv_ctx();
   if (!c) CKV_FAIL(CKV_ENOMEM, "host allocation failed");
@@ -150,6 +154,10 @@ ckv_status ckv_ctx_create(const ckv_dims* dims, double keep_ratio, int32_t flags
   const int eb = elem_bytes(dims->dtype);
   const int64_t span = (int64_t)dims->chunk_size * dims->n_kv_heads * dims->head_dim * eb;
   c->ws_score = make_score_plan(dims).bytes;
+  if (c->ws_score == 0) {
+    free_ctx(c);
+    CKV_FAIL(CKV_EUNSUPPORTED, "shape too large for the scoring decomposition");
+  }
   c->ws_attn = make_attn_plan(dims, c->k).bytes;
   // scoring and attention scratch are used one after the other on one stream,
   // so both start at the front of the workspace
@@ -186,7 +194,7 @@ ckv_status ckv_ctx_create(const ckv_dims* dims, double keep_ratio, int32_t flags
     CKV_HIP_ALLOC(hipEventCreateWithFlags(&c->ev_sel, hipEventDisableTiming));
     CKV_HIP_ALLOC(hipEventCreateWithFlags(&c->ev_dem, hipEventDisableTiming));
   }
-  if (flags & CKV_CTX_STAGE_TIMING)
+  if (flags & (CKV_CTX_STAGE_TIMING | CKV_CTX_SCORE_TIMING))
     for (auto& set : c->tev)
       for (auto& e : set) CKV_HIP_ALLOC(hipEventCreate(&e));
   *out = c;
@@ -196,7 +204,8 @@ ckv_status ckv_ctx_create(const ckv_dims* dims, double keep_ratio, int32_t flags
 ckv_status ckv_ctx_stage_times(ckv_ctx* ctx, double* ms, int64_t* n_layers) {
   clear_error();
   if (!ctx || !ms || !n_layers) CKV_FAIL(CKV_EINVAL, "NULL argument");
-  if (!(ctx->flags & CKV_CTX_STAGE_TIMING)) CKV_FAIL(CKV_ESTATE, "context created without CKV_CTX_STAGE_TIMING");
+  if (!(ctx->flags & (CKV_CTX_STAGE_TIMING | CKV_CTX_SCORE_TIMING)))
+    CKV_FAIL(CKV_ESTATE, "context created without CKV_CTX_STAGE_TIMING or CKV_CTX_SCORE_TIMING");
   while (ctx->t_done < ctx->t_issued) {
     ckv_status s = harvest_one(ctx);
     if (s != CKV_OK) return s;
@@ -254,7 +263,7 @@ ckv_status ckv_reprefill_layer(ckv_ctx* c, int32_t layer, const ckv_layer_io* io
   const int64_t span_elems = (int64_t)d->chunk_size * d->n_kv_heads * d->head_dim;
 
   hipEvent_t* tev = nullptr;
-  if (c->flags & CKV_CTX_STAGE_TIMING) {
+  if (c->flags & (CKV_CTX_STAGE_TIMING | CKV_CTX_SCORE_TIMING)) {
     if (c->t_issued - c->t_done >= ckv_ctx::kRing) {  // reuse the oldest set: account it first
       ckv_status s = harvest_one(c);
       if (s != CKV_OK) return s;
@@ -263,7 +272,7 @@ ckv_status ckv_reprefill_layer(ckv_ctx* c, int32_t layer, const ckv_layer_io* io
     CKV_HIP(hipEventRecord(tev[0], st));
   }
   auto mark = [&](int i) -> ckv_status {
-    if (tev) CKV_HIP(hipEventRecord(tev[i], st));
+    if (tev && all_stages(c)) CKV_HIP(hipEventRecord(tev[i], st));
     return CKV_OK;
   };
 

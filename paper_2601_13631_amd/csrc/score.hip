@@ -3,24 +3,28 @@
 // A_j = sum over rows r=(t,h) of sum_{i in chunk j} p_{r,i},
 // p_{r,i} = softmax_i(sm_scale * q_r . k_i) over the n prefix keys.
 //
-// Work split.  Rows of one KV head g are r = t*G + i (query t, head g*G+i).  A
-// workgroup owns 256 rows (4 waves x 64) of one KV head and one key range of
-// `key_range` keys.  Each wave keeps its 64 query rows in registers as the B
-// operand of bf16 MFMA 32x32x16 and streams the range's keys through LDS in
-// 32-key subtiles, computing S^T = K Q^T so that every lane owns one query row
-// and holds 16 of the 32 keys of a subtile (its partner lane l^32 the other 16).
+// Work split.  Rows of one KV head g are r = t*G + i (query t, head g*G+i),
+// grouped in blocks of 256 rows (4 waves x 64).  Each (KV head, row block) pair
+// spans the whole key axis, cut into 256-key items; the items are dealt out in
+// equal contiguous runs to a fixed grid of workgroups, so every workgroup (and
+// CU) does the same work.  The items of one workgroup that share a row block
+// form a segment.  Each wave keeps its 64 query rows in registers as the B
+// operand of bf16 MFMA 32x32x16 and streams the segment's keys through LDS in
+// 64-key stages of two 32-key subtiles, computing S^T = K Q^T so that every
+// lane holds one query row and 16 of the 32 keys of a subtile (its partner lane
+// l^32 the other 16).
 //
-// Softmax without a second pass.  Each row takes as reference mc the scaled
-// maximum of its logits over the prefix's first 32 keys (every workgroup of
-// the row computes the same value) and each (row, range) accumulates, per
-// chunk, P = sum exp2(c1*dot - mc) (c1 = sm_scale*log2 e) in fp32 over at most
-// one chunk, plus z = sum of the range's chunk sums in fp64.  Finalize kernels
-// fold the ranges of a row in fp64: Z = sum z, w = 1/Z, A_j = sum_r w P.  The
-// result is exact in real arithmetic for any reference; the reference only has
-// to keep exp2 finite.  If any chunk sum of a range is not finite the
-// workgroup recomputes that range against its own exact maximum (two passes),
-// and the fold rescales that range by exp2(mc - max mc), so the fast path never
-// trades correctness for speed.
+// Softmax without a second pass.  A segment takes as each row's reference mc
+// the scaled maximum of its logits over the segment's first 32 keys and
+// accumulates, per chunk, P = sum exp2(c1*dot - mc) (c1 = sm_scale*log2 e) in
+// fp32 over at most one chunk, plus z = sum of the segment's chunk sums in
+// fp64.  Finalize kernels fold the segments of a row in fp64: M = max mc,
+// Z = sum exp2(mc - M) z, w = exp2(mc - M)/Z, A_j = sum_r w P.  The result is
+// exact in real arithmetic for any reference; the reference only has to keep
+// exp2 finite.  If a segment's z leaves the guard (some chunk sum is above it
+// or not finite) the fallback kernel recomputes that segment against its own
+// exact maximum (two passes), so the fast path never trades correctness for
+// speed.
 //
 // All sums have a fixed order: results are bitwise reproducible run to run.
 
@@ -47,6 +51,15 @@ __device__ __forceinline__ float partner_f(float x) {
   return __int_as_float(threadIdx.x & 32 ? r[0] : r[1]);
 }
 
+// x + (x of lane l^32), the same value in both lanes of the pair.  The swap
+// leaves (own, partner) in lanes 0..31 and (partner, own) in lanes 32..63, and
+// fp32 addition is commutative, so no lane select is needed.
+__device__ __forceinline__ float pair_sum(float x) {
+  int v = __float_as_int(x);
+  auto r = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+  return __int_as_float(r[0]) + __int_as_float(r[1]);
+}
+
 __device__ __forceinline__ double partner_d(double x) {
   int2 v = *reinterpret_cast<int2*>(&x);
   auto rx = __builtin_amdgcn_permlane32_swap(v.x, v.x, false, false);
@@ -60,67 +73,97 @@ __device__ __forceinline__ double partner_d(double x) {
 // ---------------------------------------------------------------------------
 // bf16 main kernel
 // ---------------------------------------------------------------------------
-// LDS subtile: 32 keys x D bf16, 16-byte segments XOR-swizzled by key so that
-// the MFMA operand reads (consecutive lanes = consecutive keys, same segment)
-// hit distinct banks for both 8- and 16-lane bank cycles.
+// LDS stage: key rows of D bf16 padded by one 16-byte segment, so that the MFMA
+// operand reads (consecutive lanes = consecutive keys, same segment) start 4
+// banks apart and every 16-lane group covers all 64 banks once.  The padding
+// keeps each fragment's address a compile-time offset from one base register.
 template <int D>
 struct SubtileLds {
-  static constexpr int kSegs = D / 8;  // 16-byte segments per key row
+  static constexpr int kRow = D + 8;  // elements per key row
   __device__ static int offset(int key, int seg) {  // in bf16 elements
-    return key * D + ((seg ^ ((key ^ (key >> 3)) & (kSegs - 1))) * 8);
+    return key * kRow + seg * 8;
   }
 };
 
 struct ScoreArgs {
   const uint16_t* q;   // [S][Hq][D] bf16 bits
   const uint16_t* k;   // [n][Hkv][D]
-  float* part;         // [Hkv][NR][CPR][ldp]: rows padded to whole row blocks
-  float* mc;           // [Hkv][NR][R]
-  double* z;           // [Hkv][NR][R]
-  int* flags;          // [nblocks]: the range overflowed in the main pass
-  int64_t n;
-  int S, Hq, Hkv, G, R, ldp, c, key_range, n_ranges, cpr, n_row_blocks;
+  float* part;         // [Hkv][m_pad][ldp]
+  float* mc;           // [Hkv*RB][NS][rpb]
+  double* z;           // [Hkv*RB][NS][rpb]
+  int* flags;          // [Hkv*RB][NS]: the segment overflowed in the main pass
+  int64_t n, m_pad;    // keys; chunk slots per KV head (U*UK/c)
+  int S, Hq, Hkv, G, R, c;
   float c1;            // sm_scale * log2(e)
-  uint32_t nblocks, nblocks_padded;
+  ScoreWork w;
+  uint32_t nwg, nwg_padded;  // Hkv*RB*NS workgroups (the flags are indexed by workgroup)
 };
 
 constexpr int kStage = 64;  // keys per LDS stage: two 32-key subtiles
 
 // The next stage's K rows are fetched into registers while the current stage is
 // consumed from LDS, then written to the other LDS buffer: one barrier per stage.
-// Loads are unconditional (rows past the range end read the stage's first row
+// Loads are unconditional (rows past the segment end read the stage's first row
 // and are zeroed when stored), so the compiler never has to wait on them early.
 template <int D>
 struct StageRegs {
   static constexpr int kPer = kStage * (D / 8) / (kWaves * 64);  // 16-byte loads per thread
   u32x4 v[kPer];
-  uint32_t valid;  // bit p: piece p is inside the range
+  uint32_t valid;  // bit p: piece p is inside the segment
 };
 
+// Byte offsets of a thread's pieces inside a stage (boff) and of the same
+// segment of the stage's first key (boff0).
+template <int D>
+struct StageOffsets {
+  uint32_t boff[StageRegs<D>::kPer], boff0[StageRegs<D>::kPer];
+  __device__ StageOffsets(int Hkv, int g) {
+    constexpr int kSegs = D / 8;
+#pragma unroll
+    for (int p = 0; p < StageRegs<D>::kPer; ++p) {
+      const int idx = threadIdx.x + p * kWaves * 64;
+      const int key = idx / kSegs, seg = idx % kSegs;
+      boff[p] = (uint32_t)((((int64_t)key * Hkv + g) * D + seg * 8) * 2);
+      boff0[p] = (uint32_t)((g * D + seg * 8) * 2);
+    }
+  }
+};
+
+// A stage that lies wholly inside the segment: plain loads from a uniform base.
+template <int D>
+__device__ __forceinline__ void stage_load_full(const uint16_t* kstage, const StageOffsets<D>& o,
+                                                StageRegs<D>& r) {
+  const char* base = reinterpret_cast<const char*>(kstage);
+#pragma unroll
+  for (int p = 0; p < StageRegs<D>::kPer; ++p)
+    r.v[p] = *reinterpret_cast<const u32x4*>(base + o.boff[p]);
+}
+
+// A stage that may run past the segment end: rows past it read the stage's first
+// row (always valid) and are zeroed by stage_store.
 template <int D>
 __device__ __forceinline__ void stage_load(const uint16_t* kstage, int64_t keys_left,
-                                           const uint32_t (&voff)[StageRegs<D>::kPer],
-                                           const uint32_t (&voff0)[StageRegs<D>::kPer],
-                                           StageRegs<D>& r) {
+                                           const StageOffsets<D>& o, StageRegs<D>& r) {
   constexpr int kSegs = D / 8;
+  const char* base = reinterpret_cast<const char*>(kstage);
   r.valid = 0;
 #pragma unroll
   for (int p = 0; p < StageRegs<D>::kPer; ++p) {
     const int key = (threadIdx.x + p * kWaves * 64) / kSegs;
     const bool ok = key < keys_left;
     r.valid |= (ok ? 1u : 0u) << p;
-    r.v[p] = *reinterpret_cast<const u32x4*>(kstage + (ok ? voff[p] : voff0[p]));
+    r.v[p] = *reinterpret_cast<const u32x4*>(base + (ok ? o.boff[p] : o.boff0[p]));
   }
 }
 
-template <int D>
+template <int D, bool FULL>
 __device__ __forceinline__ void stage_store(const StageRegs<D>& r, uint16_t* lds) {
   constexpr int kSegs = D / 8;
 #pragma unroll
   for (int p = 0; p < StageRegs<D>::kPer; ++p) {
     const int idx = threadIdx.x + p * kWaves * 64;
     u32x4 v = r.v[p];
-    if (!((r.valid >> p) & 1u)) v = u32x4{0u, 0u, 0u, 0u};
+    if (!FULL && !((r.valid >> p) & 1u)) v = u32x4{0u, 0u, 0u, 0u};
     *reinterpret_cast<u32x4*>(lds + SubtileLds<D>::offset(idx / kSegs, idx % kSegs)) = v;
   }
 }
@@ -130,21 +173,22 @@ __device__ __forceinline__ void stage_store(const StageRegs<D>& r, uint16_t* lds
 template <int MODE>
 __device__ __forceinline__ void chunk_sums(const f32x16& p, float* sums) {
   if constexpr (MODE == kC32 || MODE == kC32x) {
-    float s = 0.f;
+    float t[8];
 #pragma unroll
-    for (int v = 0; v < 16; ++v) s += p[v];
-    sums[0] = s + partner_f(s);
+    for (int v = 0; v < 8; ++v) t[v] = p[v] + p[v + 8];
+#pragma unroll
+    for (int v = 0; v < 4; ++v) t[v] += t[v + 4];
+    sums[0] = pair_sum((t[0] + t[2]) + (t[1] + t[3]));
   } else if constexpr (MODE == kC16) {
-    float s0 = 0.f, s1 = 0.f;
+    float s0 = p[0], s1 = p[8];
 #pragma unroll
-    for (int v = 0; v < 8; ++v) { s0 += p[v]; s1 += p[v + 8]; }
-    sums[0] = s0 + partner_f(s0);
-    sums[1] = s1 + partner_f(s1);
+    for (int v = 1; v < 8; ++v) { s0 += p[v]; s1 += p[v + 8]; }
+    sums[0] = pair_sum(s0);
+    sums[1] = pair_sum(s1);
   } else if constexpr (MODE == kC8) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      float s = (p[4 * i] + p[4 * i + 1]) + (p[4 * i + 2] + p[4 * i + 3]);
-      sums[i] = s + partner_f(s);
+      sums[i] = pair_sum((p[4 * i] + p[4 * i + 1]) + (p[4 * i + 2] + p[4 * i + 3]));
     }
   } else {  // kC4: chunk 2i+h lives entirely in lane half h
 #pragma unroll
@@ -157,22 +201,121 @@ constexpr int sums_per_lane() {
   return MODE >= kC32 ? 1 : MODE == kC16 ? 2 : 4;
 }
 
+// Lane l of a wave holds logits of rows l%32 of both row tiles (mref[0..1]),
+// and after pooling owns row l of the wave (row tile l/32): zsum and chunk_acc
+// belong to that row.
 struct RangeState {
-  float mref[2];       // per row tile: reference (scaled log2 units)
-  double zsum[2];      // per row tile: sum of the range's chunk sums
-  float chunk_acc[2];  // kC32x with c > 32: running sum of the open chunk
+  float mref[2];    // references of rows (tile 0, l%32) and (tile 1, l%32), scaled log2 units
+  double zsum;      // own row: sum of the segment's chunk sums
+  float chunk_acc;  // kC32x (c = 64, 96, ...): own row's running sum of the open chunk
   bool overflow;
 };
 
-// One 32-key subtile (range-relative keys rk0 .. rk0+31 of a range holding
+// Sum over the lane pair (l, l^32) of one tile's value x0 (row tile 0) and
+// x1 (row tile 1), delivered to the lane that owns the row: lanes 0..31 get
+// x0[l] + x0[l+32], lanes 32..63 get x1[l-32] + x1[l].
+__device__ __forceinline__ float own_row_sum(float x0, float x1) {
+  auto r = __builtin_amdgcn_permlane32_swap(__float_as_int(x0), __float_as_int(x1), false, false);
+  return __int_as_float(r[0]) + __int_as_float(r[1]);
+}
+
+// kC4: chunk 2i+h of a subtile lives in lane half h.  After the swap lane l
+// holds, for its own row, chunk 2i in lo and chunk 2i+1 in hi.
+__device__ __forceinline__ void own_row_pair(float x0, float x1, float& lo, float& hi) {
+  auto r = __builtin_amdgcn_permlane32_swap(__float_as_int(x0), __float_as_int(x1), false, false);
+  lo = __int_as_float(r[0]);
+  hi = __int_as_float(r[1]);
+}
+
+// Pools the numerators p[rt] (keys past the segment end already zero) of one
+// 32-key subtile starting at segment-relative key rk0 into per-chunk sums of the
+// lane's own row, writes them to the partials and adds them to z.  Register v
+// holds key 8*(v/4) + 4*half + v%4.  A short subtile writes zeros to chunk
+// slots past the segment's last key; those slots exist (a row-block-head owns
+// U*UK/c of them, UK a multiple of 64 and c) and nothing reads them.
+template <int MODE>
+__device__ __forceinline__ void pool_subtile(const ScoreArgs& a, const f32x16 (&p)[2], int rk0,
+                                             int nkeys, float* part, int row, RangeState& st) {
+  if constexpr (MODE == kC32 || MODE == kC32x) {
+    float t[2];
+#pragma unroll
+    for (int rt = 0; rt < 2; ++rt) {
+      float u[8];
+#pragma unroll
+      for (int v = 0; v < 8; ++v) u[v] = p[rt][v] + p[rt][v + 8];
+#pragma unroll
+      for (int v = 0; v < 4; ++v) u[v] += u[v + 4];
+      t[rt] = (u[0] + u[2]) + (u[1] + u[3]);
+    }
+    const float c = own_row_sum(t[0], t[1]);
+    if constexpr (MODE == kC32) {
+      part[(int64_t)(rk0 >> 5) * a.w.ldp + row] = c;
+      st.zsum += (double)c;
+    } else {
+      st.chunk_acc += c;
+      if ((rk0 + kSub) % a.c == 0 || rk0 + kSub >= nkeys) {  // uniform: the chunk closes
+        part[(int64_t)(rk0 / a.c) * a.w.ldp + row] = st.chunk_acc;
+        st.zsum += (double)st.chunk_acc;
+        st.chunk_acc = 0.f;
+      }
+    }
+  } else if constexpr (MODE == kC16) {
+    // chunk 0: registers 0..7, chunk 1: registers 8..15
+    float t[2][2];
+#pragma unroll
+    for (int rt = 0; rt < 2; ++rt)
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const int b = 8 * h;
+        t[rt][h] = ((p[rt][b] + p[rt][b + 1]) + (p[rt][b + 2] + p[rt][b + 3])) +
+                   ((p[rt][b + 4] + p[rt][b + 5]) + (p[rt][b + 6] + p[rt][b + 7]));
+      }
+    const int jl0 = rk0 >> 4;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const float c = own_row_sum(t[0][h], t[1][h]);
+      part[(int64_t)(jl0 + h) * a.w.ldp + row] = c;
+      st.zsum += (double)c;
+    }
+  } else if constexpr (MODE == kC8) {
+    // chunk i: registers 4i..4i+3
+    const int jl0 = rk0 >> 3;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      float t[2];
+#pragma unroll
+      for (int rt = 0; rt < 2; ++rt)
+        t[rt] = (p[rt][4 * i] + p[rt][4 * i + 1]) + (p[rt][4 * i + 2] + p[rt][4 * i + 3]);
+      const float c = own_row_sum(t[0], t[1]);
+      part[(int64_t)(jl0 + i) * a.w.ldp + row] = c;
+      st.zsum += (double)c;
+    }
+  } else {  // kC4: registers 4i..4i+3 of half h are chunk 2i+h
+    const int jl0 = rk0 >> 2;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      float t[2];
+#pragma unroll
+      for (int rt = 0; rt < 2; ++rt)
+        t[rt] = (p[rt][4 * i] + p[rt][4 * i + 1]) + (p[rt][4 * i + 2] + p[rt][4 * i + 3]);
+      float lo, hi;
+      own_row_pair(t[0], t[1], lo, hi);
+      part[(int64_t)(jl0 + 2 * i) * a.w.ldp + row] = lo;
+      part[(int64_t)(jl0 + 2 * i + 1) * a.w.ldp + row] = hi;
+      st.zsum += (double)lo;
+      st.zsum += (double)hi;
+    }
+  }
+}
+
+// One 32-key subtile (segment-relative keys rk0 .. rk0+31 of a segment holding
 // nkeys keys), read from LDS rows lrow0 .. lrow0+31.  FULL: all 32 keys valid
-// (uniform; only a range's last subtile can be short).  PASS 0 and PASS 2:
-// partial sums against st.mref.  PASS 1: exact range maximum only.
-template <int D, int MODE, int PASS, bool FULL, bool QMEM = false>
+// (uniform; only a segment's last subtile can be short).  PASS 0 and PASS 2:
+// partial sums against st.mref.  PASS 1: exact segment maximum only.
+template <int D, int MODE, int PASS, bool FULL>
 __device__ __forceinline__ void process_subtile(const ScoreArgs& a, const bf16x8 (&qf)[2][D / 16],
                                                 const uint16_t* lds, int lrow0, int rk0, int nkeys,
-                                                float* part, int my_row0, RangeState& st,
-                                                int g = 0) {
+                                                float* part, int my_row0, RangeState& st) {
   const int lane = threadIdx.x & 63, half = lane >> 5;
   f32x16 acc[2];
 #pragma unroll
@@ -204,7 +347,7 @@ __device__ __forceinline__ void process_subtile(const ScoreArgs& a, const bf16x8
     return;
   }
 
-  // p = exp2(c1*dot - mc); keys past the range's end contribute 0
+  // p = exp2(c1*dot - mc); keys past the segment's end contribute 0
 #pragma unroll
   for (int rt = 0; rt < 2; ++rt) {
     const float nm = -st.mref[rt];
@@ -219,113 +362,14 @@ __device__ __forceinline__ void process_subtile(const ScoreArgs& a, const bf16x8
       }
     }
   }
-
-  if constexpr (MODE >= kC32) {
-    const bool closes = ((rk0 + kSub) % a.c == 0) || (rk0 + kSub >= nkeys);
-#pragma unroll
-    for (int rt = 0; rt < 2; ++rt) {
-      float sum;
-      chunk_sums<MODE>(acc[rt], &sum);
-      st.chunk_acc[rt] += sum;
-    }
-    if (closes) {
-      const int jl = rk0 / a.c;
-      const int row = my_row0 + lane;  // lane l writes row tile l/32, row l%32
-      const float mine = half ? st.chunk_acc[1] : st.chunk_acc[0];
-      part[(int64_t)jl * a.ldp + row] = mine;
-#pragma unroll
-      for (int rt = 0; rt < 2; ++rt) {
-        st.overflow |= !(st.chunk_acc[rt] <= kOverflowGuard);
-        st.zsum[rt] += (double)st.chunk_acc[rt];
-        st.chunk_acc[rt] = 0.f;
-      }
-    }
-  } else {
-    constexpr int kN = sums_per_lane<MODE>();
-    constexpr int kChunk = MODE == kC4 ? 4 : MODE == kC8 ? 8 : 16;
-    const int jl0 = rk0 / kChunk;  // first chunk of this subtile
-#pragma unroll
-    for (int rt = 0; rt < 2; ++rt) {
-      float sums[kN];
-      chunk_sums<MODE>(acc[rt], sums);
-#pragma unroll
-      for (int i = 0; i < kN; ++i) {
-        st.overflow |= !(sums[i] <= kOverflowGuard);
-        st.zsum[rt] += (double)sums[i];
-      }
-      if constexpr (MODE == kC4) {
-        // lane half h holds chunks 2i+h of rows (row tile rt, row lane%32)
-        const int row = my_row0 + rt * 32 + (lane & 31);
-#pragma unroll
-        for (int i = 0; i < kN; ++i) {
-          const int key_first = 8 * i + 4 * half;
-          if (FULL || key_first < nvalid) part[(int64_t)(jl0 + 2 * i + half) * a.ldp + row] = sums[i];
-        }
-      } else if (rt == half) {
-        // both halves hold every sum: half h writes row tile h
-        const int row = my_row0 + rt * 32 + (lane & 31);
-#pragma unroll
-        for (int i = 0; i < kN; ++i) {
-          const int key_first = i * (kSub / kN);
-          if (FULL || key_first < nvalid) part[(int64_t)(jl0 + i) * a.ldp + row] = sums[i];
-        }
-      }
-    }
-  }
-}
-
-// Common softmax reference of each row: the scaled maximum of its logits over
-// the prefix's first 32 keys.  Every workgroup of a row computes the same value,
-// so all key ranges of a row share one reference and the fold across ranges
-// needs no rescaling (unless a range fell back to its exact maximum).
-template <int D>
-__device__ void row_reference(const ScoreArgs& a, int g, const bf16x8 (&qf)[2][D / 16],
-                              uint16_t* lds, RangeState& st) {
-  constexpr int kSegs = D / 8;
-  constexpr int kPer = StageRegs<D>::kPer;
-  const int lane = threadIdx.x & 63, half = lane >> 5;
-  const int nkeys = (int)min<int64_t>(kSub, a.n);
-  uint32_t voff[kPer], voff0[kPer];
-#pragma unroll
-  for (int p = 0; p < kPer; ++p) {
-    const int idx = threadIdx.x + p * kWaves * 64;
-    voff[p] = (uint32_t)(((int64_t)(idx / kSegs) * a.Hkv + g) * D + (idx % kSegs) * 8);
-    voff0[p] = (uint32_t)(g * D + (idx % kSegs) * 8);
-  }
-  StageRegs<D> r;
-  stage_load<D>(a.k, nkeys, voff, voff0, r);
-  stage_store<D>(r, lds);
-  __syncthreads();
-  f32x16 acc[2];
-#pragma unroll
-  for (int rt = 0; rt < 2; ++rt)
-#pragma unroll
-    for (int v = 0; v < 16; ++v) acc[rt][v] = 0.f;
-#pragma unroll
-  for (int ks = 0; ks < D / 16; ++ks) {
-    bf16x8 kf = *reinterpret_cast<const bf16x8*>(lds + SubtileLds<D>::offset(lane & 31, 2 * ks + half));
-    acc[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[0][ks], acc[0], 0, 0, 0);
-    acc[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[1][ks], acc[1], 0, 0, 0);
-  }
-#pragma unroll
-  for (int rt = 0; rt < 2; ++rt) {
-    float mx = -INFINITY;
-#pragma unroll
-    for (int v = 0; v < 16; ++v) {
-      const int key = 8 * (v >> 2) + 4 * half + (v & 3);
-      if (key < nkeys) mx = fmaxf(mx, acc[rt][v]);
-    }
-    mx = fmaxf(mx, partner_f(mx));
-    st.mref[rt] = mx * a.c1;
-  }
-  __syncthreads();  // LDS is reused by the range
+  pool_subtile<MODE>(a, acc, rk0, nkeys, part, my_row0 + lane, st);
 }
 
 // ---- software-pipelined steady state (PASS 0, full 64-key stages) ----------
-// A stage is four units (subtile 0/1 x row tile 0/1).  Each unit's 8 MFMAs are
-// issued while the previous unit's softmax VALU work runs, in one basic block,
-// and the last unit's VALU work is carried over the stage barrier into the next
-// stage.  Scheduling-group hints ask the scheduler to alternate the two.
+// A stage is two subtiles.  Each subtile's 16 MFMAs are issued in the same
+// scheduling region as the previous subtile's softmax VALU work (the compiler
+// interleaves the two), and the last subtile's VALU work is carried over the
+// stage barrier into the next stage.
 
 // All 16 MFMAs of one subtile (both row tiles share each K fragment).
 template <int D>
@@ -345,54 +389,21 @@ __device__ __forceinline__ void mfma_subtile(const uint16_t* lds, int lrow0,
   }
 }
 
-// Softmax numerators, per-chunk sums, partial writes and z for one unit: row
-// tile RT of a full 32-key subtile starting at range-relative key rk0.  Both
-// lane halves hold the combined sums; each pair of lanes writes the same value
-// to the same row (rows are padded, so no guard is needed).
-template <int MODE, int RT>
-__device__ __forceinline__ void valu_unit(const ScoreArgs& a, f32x16& acc, int rk0, float* part,
-                                          int my_row0, RangeState& st) {
-  const int lane = threadIdx.x & 63, half = lane >> 5;
-  const float nm = -st.mref[RT];
+// Softmax numerators of both row tiles of a full 32-key subtile starting at
+// segment-relative key rk0, then pooling into the lane's own row.  Chunk sums
+// are not checked here: all terms are >= 0, so z exceeds the guard (or is not
+// finite) whenever one of its chunk sums does, and the segment is checked once
+// at its end.
+template <int MODE>
+__device__ __forceinline__ void valu_subtile(const ScoreArgs& a, f32x16 (&acc)[2], int rk0,
+                                             int nkeys, float* part, int row, RangeState& st) {
 #pragma unroll
-  for (int v = 0; v < 16; ++v) acc[v] = __builtin_amdgcn_exp2f(fmaf(acc[v], a.c1, nm));
-  constexpr int kN = sums_per_lane<MODE>();
-  float sums[kN];
-  chunk_sums<MODE>(acc, sums);
-  const int row = my_row0 + RT * 32 + (lane & 31);
-  if constexpr (MODE == kC32) {
-    part[(int64_t)(rk0 >> 5) * a.ldp + row] = sums[0];
-    st.overflow |= !(sums[0] <= kOverflowGuard);
-    st.zsum[RT] += (double)sums[0];
-  } else if constexpr (MODE == kC32x) {
-    st.chunk_acc[RT] += sums[0];
-    if ((rk0 + kSub) % a.c == 0) {  // uniform
-      part[(int64_t)(rk0 / a.c) * a.ldp + row] = st.chunk_acc[RT];
-      st.overflow |= !(st.chunk_acc[RT] <= kOverflowGuard);
-      st.zsum[RT] += (double)st.chunk_acc[RT];
-      st.chunk_acc[RT] = 0.f;
-    }
-  } else {
-    constexpr int kChunk = MODE == kC4 ? 4 : MODE == kC8 ? 8 : 16;
-    const int jl0 = rk0 / kChunk;
+  for (int rt = 0; rt < 2; ++rt) {
+    const float nm = -st.mref[rt];
 #pragma unroll
-    for (int i = 0; i < kN; ++i) {
-      st.overflow |= !(sums[i] <= kOverflowGuard);
-      st.zsum[RT] += (double)sums[i];
-      // kC4: lane half h holds chunks 2i+h; otherwise both halves hold chunk i
-      const int jl = MODE == kC4 ? jl0 + 2 * i + half : jl0 + i;
-      part[(int64_t)jl * a.ldp + row] = sums[i];
-    }
+    for (int v = 0; v < 16; ++v) acc[rt][v] = __builtin_amdgcn_exp2f(fmaf(acc[rt][v], a.c1, nm));
   }
-}
-
-// Asks the scheduler to alternate the 16 MFMAs of a slot with VALU work.
-__device__ __forceinline__ void interleave_hint() {
-#pragma unroll
-  for (int i = 0; i < 16; ++i) {
-    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
-    __builtin_amdgcn_sched_group_barrier(0x002, 6, 0);  // then VALU
-  }
+  pool_subtile<MODE>(a, acc, rk0, nkeys, part, row, st);
 }
 
 // One full 64-key stage as two slots.  Slot 0: MFMAs of subtile 0 with the
@@ -400,131 +411,125 @@ __device__ __forceinline__ void interleave_hint() {
 // subtile 1 (into `carry`) with the VALU work of subtile 0.
 template <int D, int MODE, bool CARRY>
 __device__ __forceinline__ void fast_stage(const ScoreArgs& a, const bf16x8 (&qf)[2][D / 16],
-                                           const uint16_t* cur, int rk0, float* part, int my_row0,
-                                           RangeState& st, f32x16 (&carry)[2], int& carry_rk) {
+                                           const uint16_t* cur, int rk0, int nkeys, float* part,
+                                           int row, RangeState& st, f32x16 (&carry)[2],
+                                           int& carry_rk) {
   f32x16 acc[2];
   __builtin_amdgcn_sched_barrier(0);
   mfma_subtile<D>(cur, 0, qf, acc);
   if constexpr (CARRY) {
-    valu_unit<MODE, 0>(a, carry[0], carry_rk, part, my_row0, st);
-    valu_unit<MODE, 1>(a, carry[1], carry_rk, part, my_row0, st);
-    interleave_hint();
+    valu_subtile<MODE>(a, carry, carry_rk, nkeys, part, row, st);
   }
   __builtin_amdgcn_sched_barrier(0);
   mfma_subtile<D>(cur, kSub, qf, carry);
-  valu_unit<MODE, 0>(a, acc[0], rk0, part, my_row0, st);
-  valu_unit<MODE, 1>(a, acc[1], rk0, part, my_row0, st);
-  interleave_hint();
+  valu_subtile<MODE>(a, acc, rk0, nkeys, part, row, st);
   __builtin_amdgcn_sched_barrier(0);
   carry_rk = rk0 + kSub;
 }
 
-// PASS 0 over the range: pipelined full stages, then the short tail stage (if
-// any) through process_subtile.
+// Segment reference: the scaled maximum of each row's logits over the
+// segment's first 32 keys (already in LDS buffer 0).
 template <int D, int MODE>
-__device__ bool run_range_fast(const ScoreArgs& a, int g, int range, int row0,
-                               const bf16x8 (&qf)[2][D / 16], uint16_t* lds, RangeState& st) {
-  constexpr int kSegs = D / 8;
-  constexpr int kPer = StageRegs<D>::kPer;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, half = lane >> 5;
-  const int64_t kbeg = (int64_t)range * a.key_range;
-  const int nkeys = (int)(min<int64_t>(kbeg + a.key_range, a.n) - kbeg);
+__device__ __forceinline__ void segment_reference(const ScoreArgs& a, const bf16x8 (&qf)[2][D / 16],
+                                                  const uint16_t* lds, int nkeys, int my_row0,
+                                                  RangeState& st) {
+  st.mref[0] = st.mref[1] = -INFINITY;
+  process_subtile<D, MODE, 1, false>(a, qf, lds, 0, 0, nkeys, nullptr, my_row0, st);
+}
+
+// PASS 0 over one segment (keys kbeg .. kbeg+nkeys-1 of KV head g): the
+// reference from the first subtile, pipelined full stages, then the short tail
+// stage (if any) through process_subtile.  Returns whether a chunk sum may have
+// left the guard (then the fallback kernel redoes the segment exactly).
+template <int D, int MODE>
+__device__ __forceinline__ bool run_segment_fast(const ScoreArgs& a, int g, int64_t kbeg, int nkeys,
+                                                 int row0, const bf16x8 (&qf)[2][D / 16],
+                                                 uint16_t* lds, RangeState& st) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int nstage = (nkeys + kStage - 1) / kStage;
   const int nfull = nkeys / kStage;
   const int my_row0 = row0 + wave * kWaveRows;
   st.overflow = false;
-  st.chunk_acc[0] = st.chunk_acc[1] = 0.f;
-  st.zsum[0] = st.zsum[1] = 0.0;
-  float* part = a.part + ((int64_t)(g * a.n_ranges + range) * a.cpr) * a.ldp;
+  st.chunk_acc = 0.f;
+  st.zsum = 0.0;
+  float* part = a.part + ((int64_t)g * a.m_pad + kbeg / a.c) * a.w.ldp;
 
-  uint32_t voff[kPer], voff0[kPer];
-#pragma unroll
-  for (int p = 0; p < kPer; ++p) {
-    const int idx = threadIdx.x + p * kWaves * 64;
-    const int key = idx / kSegs, seg = idx % kSegs;
-    voff[p] = (uint32_t)(((int64_t)key * a.Hkv + g) * D + seg * 8);
-    voff0[p] = (uint32_t)(g * D + seg * 8);
-  }
+  const StageOffsets<D> o(a.Hkv, g);
   const int64_t stage_elems = (int64_t)kStage * a.Hkv * D;
   const uint16_t* kbase = a.k + kbeg * a.Hkv * D;
+  constexpr int kBuf = kStage * SubtileLds<D>::kRow;  // elements per LDS stage buffer
 
   StageRegs<D> r;
-  stage_load<D>(kbase, nkeys, voff, voff0, r);
-  stage_store<D>(r, lds);
+  if (nfull > 0) {
+    stage_load_full<D>(kbase, o, r);
+    stage_store<D, true>(r, lds);
+  } else {
+    stage_load<D>(kbase, nkeys, o, r);
+    stage_store<D, false>(r, lds);
+  }
   __syncthreads();
+  segment_reference<D, MODE>(a, qf, lds, nkeys, my_row0, st);
   f32x16 carry[2];
   int carry_rk = 0;
   for (int s = 0; s < nfull; ++s) {
     const int rk0 = s * kStage;
-    if (s + 1 < nstage) stage_load<D>(kbase + (s + 1) * stage_elems, nkeys - rk0 - kStage, voff, voff0, r);
-    const uint16_t* cur = lds + (s & 1) * kStage * D;
+    const uint16_t* next = kbase + (s + 1) * stage_elems;
+    // uniform: the next stage is full, the short tail, or absent
+    if (s + 1 < nfull)
+      stage_load_full<D>(next, o, r);
+    else if (s + 1 < nstage)
+      stage_load<D>(next, nkeys - rk0 - kStage, o, r);
+    const uint16_t* cur = lds + (s & 1) * kBuf;
     if (s == 0)
-      fast_stage<D, MODE, false>(a, qf, cur, rk0, part, my_row0, st, carry, carry_rk);
+      fast_stage<D, MODE, false>(a, qf, cur, rk0, nkeys, part, my_row0 + lane, st, carry, carry_rk);
     else
-      fast_stage<D, MODE, true>(a, qf, cur, rk0, part, my_row0, st, carry, carry_rk);
-    if (s + 1 < nstage) stage_store<D>(r, lds + ((s + 1) & 1) * kStage * D);
+      fast_stage<D, MODE, true>(a, qf, cur, rk0, nkeys, part, my_row0 + lane, st, carry, carry_rk);
+    uint16_t* nbuf = lds + ((s + 1) & 1) * kBuf;
+    if (s + 1 < nfull)
+      stage_store<D, true>(r, nbuf);
+    else if (s + 1 < nstage)
+      stage_store<D, false>(r, nbuf);
     __syncthreads();
   }
-  if (nfull > 0) {
-    valu_unit<MODE, 0>(a, carry[0], carry_rk, part, my_row0, st);
-    valu_unit<MODE, 1>(a, carry[1], carry_rk, part, my_row0, st);
-  }
+  if (nfull > 0) valu_subtile<MODE>(a, carry, carry_rk, nkeys, part, my_row0 + lane, st);
   if (nfull < nstage) {  // short last stage
     const int rk0 = nfull * kStage;
-    const uint16_t* cur = lds + (nfull & 1) * kStage * D;
+    const uint16_t* cur = lds + (nfull & 1) * kBuf;
     process_subtile<D, MODE, 0, false>(a, qf, cur, 0, rk0, nkeys, part, my_row0, st);
     if (rk0 + kSub < nkeys)
       process_subtile<D, MODE, 0, false>(a, qf, cur, kSub, rk0 + kSub, nkeys, part, my_row0, st);
   }
-  if constexpr (MODE == kC4) {
-#pragma unroll
-    for (int rt = 0; rt < 2; ++rt) {
-      const double o = partner_d(st.zsum[rt]);
-      st.zsum[rt] = half ? (o + st.zsum[rt]) : (st.zsum[rt] + o);
-    }
-  }
+  st.overflow |= !(st.zsum <= (double)kOverflowGuard);
   return st.overflow;
 }
 
-// Processes the workgroup's key range once (see process_subtile for PASS); used
-// by the exact fallback kernel.
+// One plain pass over a segment (see process_subtile for PASS); used by the
+// exact fallback kernel.
 template <int D, int MODE, int PASS>
-__device__ bool run_range(const ScoreArgs& a, int g, int range, int row0,
-                          const bf16x8 (&qf)[2][D / 16], uint16_t* lds, RangeState& st) {
-  constexpr int kSegs = D / 8;
-  constexpr int kPer = StageRegs<D>::kPer;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, half = lane >> 5;
-  const int64_t kbeg = (int64_t)range * a.key_range;
-  const int nkeys = (int)(min<int64_t>(kbeg + a.key_range, a.n) - kbeg);
+__device__ __forceinline__ void run_segment(const ScoreArgs& a, int g, int64_t kbeg, int nkeys,
+                                            int row0, const bf16x8 (&qf)[2][D / 16], uint16_t* lds,
+                                            RangeState& st) {
+  const int wave = threadIdx.x >> 6;
   const int nstage = (nkeys + kStage - 1) / kStage;
   const int my_row0 = row0 + wave * kWaveRows;
-  st.overflow = false;
-  st.chunk_acc[0] = st.chunk_acc[1] = 0.f;
-  if (PASS != 1) st.zsum[0] = st.zsum[1] = 0.0;
+  st.chunk_acc = 0.f;
+  if (PASS != 1) st.zsum = 0.0;
   if (PASS == 1) st.mref[0] = st.mref[1] = -INFINITY;
-  float* part = a.part + ((int64_t)(g * a.n_ranges + range) * a.cpr) * a.ldp;
+  float* part = a.part + ((int64_t)g * a.m_pad + kbeg / a.c) * a.w.ldp;
 
-  // per-thread element offsets of its pieces inside a stage (and of the stage's
-  // first row, read in place of rows past the range end)
-  uint32_t voff[kPer], voff0[kPer];
-#pragma unroll
-  for (int p = 0; p < kPer; ++p) {
-    const int idx = threadIdx.x + p * kWaves * 64;
-    const int key = idx / kSegs, seg = idx % kSegs;
-    voff[p] = (uint32_t)(((int64_t)key * a.Hkv + g) * D + seg * 8);
-    voff0[p] = (uint32_t)(g * D + seg * 8);
-  }
+  const StageOffsets<D> o(a.Hkv, g);
   const int64_t stage_elems = (int64_t)kStage * a.Hkv * D;
   const uint16_t* kbase = a.k + kbeg * a.Hkv * D;
+  constexpr int kBuf = kStage * SubtileLds<D>::kRow;
 
   StageRegs<D> r;
-  stage_load<D>(kbase, nkeys, voff, voff0, r);
-  stage_store<D>(r, lds);
+  stage_load<D>(kbase, nkeys, o, r);
+  stage_store<D, false>(r, lds);
   __syncthreads();
   for (int s = 0; s < nstage; ++s) {
     const int rk0 = s * kStage;
-    if (s + 1 < nstage) stage_load<D>(kbase + (s + 1) * stage_elems, nkeys - rk0 - kStage, voff, voff0, r);
-    const uint16_t* cur = lds + (s & 1) * kStage * D;
+    if (s + 1 < nstage) stage_load<D>(kbase + (s + 1) * stage_elems, nkeys - rk0 - kStage, o, r);
+    const uint16_t* cur = lds + (s & 1) * kBuf;
     if (rk0 + kStage <= nkeys) {
       process_subtile<D, MODE, PASS, true>(a, qf, cur, 0, rk0, nkeys, part, my_row0, st);
       process_subtile<D, MODE, PASS, true>(a, qf, cur, kSub, rk0 + kSub, nkeys, part, my_row0, st);
@@ -533,22 +538,13 @@ __device__ bool run_range(const ScoreArgs& a, int g, int range, int row0,
       if (rk0 + kSub < nkeys)
         process_subtile<D, MODE, PASS, false>(a, qf, cur, kSub, rk0 + kSub, nkeys, part, my_row0, st);
     }
-    if (s + 1 < nstage) stage_store<D>(r, lds + ((s + 1) & 1) * kStage * D);
+    if (s + 1 < nstage) stage_store<D, false>(r, lds + ((s + 1) & 1) * kBuf);
     __syncthreads();
   }
-  if constexpr (MODE == kC4) {
-    // each half summed different chunks: combine in a fixed order (half 0 + half 1)
-#pragma unroll
-    for (int rt = 0; rt < 2; ++rt) {
-      const double o = partner_d(st.zsum[rt]);
-      st.zsum[rt] = half ? (o + st.zsum[rt]) : (st.zsum[rt] + o);
-    }
-  }
-  return st.overflow;
 }
 
-// Q^T fragments of the workgroup's rows: B operand, lane l holds row l%32 of a
-// row tile and d = 16*ks + 8*half .. +7 (zero past R).
+// Q^T fragments of a row block: B operand, lane l holds row l%32 of a row tile
+// and d = 16*ks + 8*half .. +7 (zero past R).
 template <int D>
 __device__ __forceinline__ void load_q(const ScoreArgs& a, int g, int row0, bf16x8 (&qf)[2][D / 16]) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, half = lane >> 5;
@@ -567,63 +563,73 @@ __device__ __forceinline__ void load_q(const ScoreArgs& a, int g, int row0, bf16
   }
 }
 
-__device__ __forceinline__ void store_stats(const ScoreArgs& a, int g, int range, int row0,
-                                            const RangeState& st) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, half = lane >> 5;
-  const int row = row0 + wave * kWaveRows + lane;  // lane l reports row tile l/32
-  if (row < a.R) {
-    const int64_t o = (int64_t)(g * a.n_ranges + range) * a.R + row;
-    a.mc[o] = half ? st.mref[1] : st.mref[0];
-    a.z[o] = half ? st.zsum[1] : st.zsum[0];
-  }
+// Reference and sum of every row of the block for segment slot s of rbh (rows
+// past R hold zero queries and are written too: the arrays span whole blocks).
+__device__ __forceinline__ void store_stats(const ScoreArgs& a, int rbh, int s, const RangeState& st) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  // both lane halves hold both references: the swap hands lane l its own row's
+  float ref, unused;
+  own_row_pair(st.mref[0], st.mref[1], ref, unused);
+  const int64_t o = ((int64_t)rbh * a.w.NS + s) * kBlockRows + wave * kWaveRows + lane;
+  a.mc[o] = ref;
+  a.z[o] = st.zsum;
 }
 
-// Main pass: every (KV head, key range, 256-row block) workgroup, pipelined,
-// against the rows' common reference.  Records in flags[L] whether a chunk sum
-// of its range overflowed (then the fallback kernel redoes the range).
+// Workgroup w runs segment s = w % NS of rbh = w / NS: keys kbeg .. kbeg+nkeys-1.
+struct Segment {
+  int rbh, s;
+  int64_t kbeg;
+  int nkeys;
+};
+__device__ __forceinline__ Segment segment_of(const ScoreWork& wk, int64_t n, int w) {
+  Segment g;
+  g.rbh = w / wk.NS;
+  g.s = w % wk.NS;
+  g.kbeg = (int64_t)wk.seg_begin(g.s) * wk.UK;
+  g.nkeys = (int)(min<int64_t>((int64_t)wk.seg_begin(g.s + 1) * wk.UK, n) - g.kbeg);
+  return g;
+}
+
+// Main pass: every workgroup runs its segment, pipelined, against the
+// segment's own reference, and records whether a chunk sum left the guard
+// (then the fallback kernel redoes the segment).
 template <int D, int MODE>
 __global__ __launch_bounds__(kWaves * 64, 2) void score_bf16_kernel(ScoreArgs a) {
-  __shared__ __attribute__((aligned(16))) uint16_t lds[2 * kStage * D];
-  const uint32_t L = xcd_remap(blockIdx.x, a.nblocks_padded);
-  if (L >= a.nblocks) return;
-  const int rb = (int)(L % a.n_row_blocks);
-  const int range = (int)((L / a.n_row_blocks) % a.n_ranges);
-  const int g = (int)(L / ((uint32_t)a.n_row_blocks * a.n_ranges));
-  const int row0 = rb * kBlockRows;
+  __shared__ __attribute__((aligned(16))) uint16_t lds[2 * kStage * SubtileLds<D>::kRow];
+  const uint32_t w = xcd_remap(blockIdx.x, a.nwg_padded);
+  if (w >= a.nwg) return;
+  const Segment sg = segment_of(a.w, a.n, (int)w);
+  const int g = sg.rbh / a.w.RB, row0 = (sg.rbh % a.w.RB) * kBlockRows;
   bf16x8 qf[2][D / 16];
   load_q<D>(a, g, row0, qf);
   RangeState st;
-  row_reference<D>(a, g, qf, lds, st);
-  const bool of = run_range_fast<D, MODE>(a, g, range, row0, qf, lds, st);
+  const bool of = run_segment_fast<D, MODE>(a, g, sg.kbeg, sg.nkeys, row0, qf, lds, st);
   const int any_of = __syncthreads_or(of ? 1 : 0);
-  if (threadIdx.x == 0) a.flags[L] = any_of;
-  store_stats(a, g, range, row0, st);
+  if (threadIdx.x == 0) a.flags[w] = any_of;
+  store_stats(a, sg.rbh, sg.s, st);
 }
 
 // Exact fallback, almost always a no-op: a grid-stride loop over the main
-// pass's workgroups; a flagged range is recomputed against its own exact
+// pass's workgroups; a flagged segment is recomputed against its own exact
 // maximum (first pass: maximum only, second pass: partial sums and z).
 template <int D, int MODE>
 __global__ __launch_bounds__(kWaves * 64, 2) void score_fallback_kernel(ScoreArgs a) {
-  __shared__ __attribute__((aligned(16))) uint16_t lds[2 * kStage * D];
-  // all threads scan this block's share of the flags at once; nothing to do is
-  // the common case
+  __shared__ __attribute__((aligned(16))) uint16_t lds[2 * kStage * SubtileLds<D>::kRow];
+  // all threads scan a share of the flags at once; nothing to do is the common case
   int mine = 0;
-  for (uint32_t L = blockIdx.x + gridDim.x * threadIdx.x; L < a.nblocks; L += gridDim.x * blockDim.x)
-    mine |= a.flags[L];
+  for (uint32_t i = blockIdx.x + gridDim.x * threadIdx.x; i < a.nwg; i += gridDim.x * blockDim.x)
+    mine |= a.flags[i];
   if (!__syncthreads_or(mine)) return;
-  for (uint32_t L = blockIdx.x; L < a.nblocks; L += gridDim.x) {
-    if (!a.flags[L]) continue;  // uniform
-    const int rb = (int)(L % a.n_row_blocks);
-    const int range = (int)((L / a.n_row_blocks) % a.n_ranges);
-    const int g = (int)(L / ((uint32_t)a.n_row_blocks * a.n_ranges));
-    const int row0 = rb * kBlockRows;
+  for (uint32_t w = blockIdx.x; w < a.nwg; w += gridDim.x) {
+    if (!a.flags[w]) continue;  // uniform
+    const Segment sg = segment_of(a.w, a.n, (int)w);
+    const int g = sg.rbh / a.w.RB, row0 = (sg.rbh % a.w.RB) * kBlockRows;
     bf16x8 qf[2][D / 16];
     load_q<D>(a, g, row0, qf);
     RangeState st;
-    run_range<D, MODE, 1>(a, g, range, row0, qf, lds, st);
-    run_range<D, MODE, 2>(a, g, range, row0, qf, lds, st);
-    store_stats(a, g, range, row0, st);
+    run_segment<D, MODE, 1>(a, g, sg.kbeg, sg.nkeys, row0, qf, lds, st);
+    run_segment<D, MODE, 2>(a, g, sg.kbeg, sg.nkeys, row0, qf, lds, st);
+    store_stats(a, sg.rbh, sg.s, st);
     __syncthreads();
   }
 }
@@ -639,24 +645,23 @@ struct ScoreArgsF32 {
   float* part;
   float* mc;
   double* z;
-  int64_t n;
-  int S, Hq, Hkv, G, R, ldp, c, key_range, n_ranges, cpr, n_row_blocks;
+  int64_t n, m_pad;
+  int S, Hq, Hkv, G, R, c;
   float c1;
-  uint32_t nblocks;
+  ScoreWork w;
+  int nwg;
 };
 
 template <int D, int MODE, int PASS>
-__device__ bool run_range_f32(const ScoreArgsF32& a, int g, int range, int row0,
-                              const float (&qf)[2][D / 2], float (&mref)[2], double (&zsum)[2]) {
+__device__ bool run_span_f32(const ScoreArgsF32& a, int g, int64_t kbeg, int64_t kend, int row0,
+                             const float (&qf)[2][D / 2], float (&mref)[2], double (&zsum)[2]) {
   const int lane = threadIdx.x & 63, half = lane >> 5;
-  const int64_t kbeg = (int64_t)range * a.key_range;
-  const int64_t kend = min<int64_t>(kbeg + a.key_range, a.n);
   const int nsub = (int)((kend - kbeg + kSub - 1) / kSub);
   bool overflow = false;
   float chunk_acc[2] = {0.f, 0.f};
   if (PASS != 1) { zsum[0] = 0.0; zsum[1] = 0.0; }
   if (PASS == 1) { mref[0] = -INFINITY; mref[1] = -INFINITY; }
-  float* part = a.part + ((int64_t)(g * a.n_ranges + range) * a.cpr) * a.ldp;
+  float* part = a.part + ((int64_t)g * a.m_pad + kbeg / a.c) * a.w.ldp;
   for (int s = 0; s < nsub; ++s) {
     const int64_t key0 = kbeg + (int64_t)s * kSub;
     const int nvalid = (int)min<int64_t>(kSub, kend - key0);
@@ -713,7 +718,7 @@ __device__ bool run_range_f32(const ScoreArgsF32& a, int g, int range, int row0,
         const int jl = (int)(chunk - kbeg / a.c);
         const int row = row0 + lane;
         float mine = half ? chunk_acc[1] : chunk_acc[0];
-        if (row < a.R) part[(int64_t)jl * a.ldp + row] = mine;
+        if (row < a.R) part[(int64_t)jl * a.w.ldp + row] = mine;
 #pragma unroll
         for (int rt = 0; rt < 2; ++rt) {
           overflow |= !(chunk_acc[rt] <= kOverflowGuard);
@@ -739,14 +744,14 @@ __device__ bool run_range_f32(const ScoreArgsF32& a, int g, int range, int row0,
           for (int i = 0; i < kN; ++i) {
             int jl = jl0 + 2 * i + half;
             int key_first = 8 * i + 4 * half;
-            if (row < a.R && key_first < nvalid) part[(int64_t)jl * a.ldp + row] = sums[i];
+            if (row < a.R && key_first < nvalid) part[(int64_t)jl * a.w.ldp + row] = sums[i];
           }
         } else if (rt == half) {
           const int row = row0 + rt * 32 + (lane & 31);
 #pragma unroll
           for (int i = 0; i < kN; ++i) {
             int key_first = i * (kSub / kN);
-            if (row < a.R && key_first < nvalid) part[(int64_t)(jl0 + i) * a.ldp + row] = sums[i];
+            if (row < a.R && key_first < nvalid) part[(int64_t)(jl0 + i) * a.w.ldp + row] = sums[i];
           }
         }
       }
@@ -764,13 +769,11 @@ __device__ bool run_range_f32(const ScoreArgsF32& a, int g, int range, int row0,
 
 template <int D, int MODE>
 __global__ __launch_bounds__(64) void score_f32_kernel(ScoreArgsF32 a) {
-  const uint32_t L = blockIdx.x;
-  if (L >= a.nblocks) return;
-  const int rb = (int)(L % a.n_row_blocks);
-  const int range = (int)((L / a.n_row_blocks) % a.n_ranges);
-  const int g = (int)(L / ((uint32_t)a.n_row_blocks * a.n_ranges));
+  const int w = blockIdx.x;
+  if (w >= a.nwg) return;
   const int lane = threadIdx.x & 63, half = lane >> 5;
-  const int row0 = rb * kWaveRows;
+  const Segment sg = segment_of(a.w, a.n, w);
+  const int g = sg.rbh / a.w.RB, row0 = (sg.rbh % a.w.RB) * kWaveRows;
   float qf[2][D / 2];
 #pragma unroll
   for (int rt = 0; rt < 2; ++rt) {
@@ -783,86 +786,88 @@ __global__ __launch_bounds__(64) void score_f32_kernel(ScoreArgsF32 a) {
   }
   float mref[2];
   double zsum[2];
-  bool of = run_range_f32<D, MODE, 0>(a, g, range, row0, qf, mref, zsum);
+  const int64_t kend = sg.kbeg + sg.nkeys;
+  bool of = run_span_f32<D, MODE, 0>(a, g, sg.kbeg, kend, row0, qf, mref, zsum);
   // one wave: the decision is wave-uniform via a ballot
   if (__any(of)) {
-    run_range_f32<D, MODE, 1>(a, g, range, row0, qf, mref, zsum);
-    run_range_f32<D, MODE, 2>(a, g, range, row0, qf, mref, zsum);
+    run_span_f32<D, MODE, 1>(a, g, sg.kbeg, kend, row0, qf, mref, zsum);
+    run_span_f32<D, MODE, 2>(a, g, sg.kbeg, kend, row0, qf, mref, zsum);
   }
-  const int row = row0 + lane;
-  if (row < a.R) {
-    const int64_t o = (int64_t)(g * a.n_ranges + range) * a.R + row;
-    a.mc[o] = half ? mref[1] : mref[0];
-    a.z[o] = half ? zsum[1] : zsum[0];
-  }
+  const int64_t o = ((int64_t)sg.rbh * a.w.NS + sg.s) * kWaveRows + lane;
+  a.mc[o] = half ? mref[1] : mref[0];
+  a.z[o] = half ? zsum[1] : zsum[0];
 }
 
 // ---------------------------------------------------------------------------
 // finalize
 // ---------------------------------------------------------------------------
-// F1: per (g, row): Mc = max over ranges of mc, Z = sum over ranges of
-// exp2(mc - Mc) z, and the z slot of every range is overwritten with
-// w = exp2(mc - Mc) / Z (fp64).  All ranges normally share one reference (then
-// every factor exp2(0) = 1 is exact and skipped); a range that fell back to its
-// own maximum is rescaled here.  A workgroup serves 32 rows (coalesced) with 8
-// lanes per row splitting the ranges; partial results are combined through LDS
-// in lane order.
+// F1: per (g, row): M = max over the row's segments of mc, Z = sum over them
+// of exp2(mc - M) z, and the z slot of every segment is overwritten with its
+// weight w = exp2(mc - M) / Z (fp64).  A workgroup serves 32 rows (coalesced)
+// with 8 lanes per row splitting the segments; partial results are combined
+// through LDS in lane order.
 constexpr int kNormRows = 32;
 constexpr int kNormLanes = 8;
 
-__device__ __forceinline__ double range_factor(float mc, float M) {
+__device__ __forceinline__ double seg_factor(float mc, float M) {
   return mc == M ? 1.0 : exp2((double)mc - (double)M);
 }
 
 __global__ __launch_bounds__(kNormRows * kNormLanes) void row_norm_kernel(
-    const float* __restrict__ mc, double* __restrict__ z, int Hkv, int R, int NR) {
-  __shared__ float smax[kNormLanes][kNormRows];
+    const float* __restrict__ mc, double* __restrict__ z, ScoreWork wk, int R) {
+  __shared__ float sred[kNormLanes][kNormRows];
   __shared__ double ssum[kNormLanes][kNormRows];
   const int rl = threadIdx.x % kNormRows, q = threadIdx.x / kNormRows;
   const int blocks_per_head = (R + kNormRows - 1) / kNormRows;
   const int g = blockIdx.x / blocks_per_head;
   const int row = (blockIdx.x % blocks_per_head) * kNormRows + rl;
   const bool ok = row < R;
-  const int64_t base = (int64_t)g * NR * R + row;
+  // kNormRows divides rpb: the 32 rows lie in one row block
+  const int rbh = g * wk.RB + ((blockIdx.x % blocks_per_head) * kNormRows) / wk.rpb;
+  const int nseg = wk.NS;
+  const int64_t base = (int64_t)rbh * wk.NS * wk.rpb + row % wk.rpb;
   float M = -INFINITY;
   if (ok)
-    for (int r = q; r < NR; r += kNormLanes) M = fmaxf(M, mc[base + (int64_t)r * R]);
-  smax[q][rl] = M;
+    for (int s = q; s < nseg; s += kNormLanes) M = fmaxf(M, mc[base + (int64_t)s * wk.rpb]);
+  sred[q][rl] = M;
   __syncthreads();
-  M = smax[0][rl];
-  for (int i = 1; i < kNormLanes; ++i) M = fmaxf(M, smax[i][rl]);
+  M = sred[0][rl];
+  for (int i = 1; i < kNormLanes; ++i) M = fmaxf(M, sred[i][rl]);
   double Z = 0.0;
   if (ok)
-    for (int r = q; r < NR; r += kNormLanes)
-      Z += range_factor(mc[base + (int64_t)r * R], M) * z[base + (int64_t)r * R];
+    for (int s = q; s < nseg; s += kNormLanes)
+      Z += seg_factor(mc[base + (int64_t)s * wk.rpb], M) * z[base + (int64_t)s * wk.rpb];
   ssum[q][rl] = Z;
   __syncthreads();
   Z = ssum[0][rl];
   for (int i = 1; i < kNormLanes; ++i) Z += ssum[i][rl];
   if (!ok) return;
   const double inv = 1.0 / Z;
-  for (int r = q; r < NR; r += kNormLanes)
-    z[base + (int64_t)r * R] = range_factor(mc[base + (int64_t)r * R], M) * inv;
+  for (int s = q; s < nseg; s += kNormLanes)
+    z[base + (int64_t)s * wk.rpb] = seg_factor(mc[base + (int64_t)s * wk.rpb], M) * inv;
 }
 
 // F2: A_j = sum over KV heads g (in order) of sum over rows r of
-// w[g][range(j)][r] * P[g][range(j)][jl][r], in fp64.  One workgroup of 256
-// threads per chunk: thread i takes rows i, i+256, ... of every head in order,
-// then a fixed tree over LDS reduces the 256 partial sums.
+// w[segment holding chunk j][r] * P[g][j][r], in fp64.  One workgroup
+// of 256 threads per chunk: thread i takes rows i, i+256, ... of every head in
+// order, then a fixed tree over LDS reduces the 256 partial sums.
 constexpr int kReduceThreads = 256;
 
 __global__ __launch_bounds__(kReduceThreads) void chunk_reduce_kernel(
-    const float* __restrict__ part, const double* __restrict__ w, double* __restrict__ A, int Hkv,
-    int R, int ldp, int NR, int cpr) {
+    const float* __restrict__ part, const double* __restrict__ w, double* __restrict__ A,
+    ScoreWork wk, int Hkv, int R, int64_t m_pad, int c, int log2_rpb) {
   __shared__ double red[kReduceThreads];
   const int64_t j = blockIdx.x;
   const int tid = threadIdx.x;
-  const int range = (int)(j / cpr), jl = (int)(j % cpr);
+  const int seg = wk.seg_of_unit((int)(j * c / wk.UK));  // the same for every row block
   double s = 0.0;
   for (int g = 0; g < Hkv; ++g) {
-    const float* p = part + (((int64_t)g * NR + range) * cpr + jl) * ldp;
-    const double* wr = w + ((int64_t)g * NR + range) * R;
-    for (int r = tid; r < R; r += kReduceThreads) s += (double)p[r] * wr[r];
+    const float* p = part + ((int64_t)g * m_pad + j) * wk.ldp;
+    for (int r = tid; r < R; r += kReduceThreads) {
+      const int rbh = g * wk.RB + (r >> log2_rpb);
+      const double wr = w[((int64_t)rbh * wk.NS + seg) * wk.rpb + (r & (wk.rpb - 1))];
+      s += (double)p[r] * wr;
+    }
   }
   red[tid] = s;
   __syncthreads();
@@ -893,32 +898,41 @@ int chunk_mode(int c) {
 ScorePlan make_score_plan(const ckv_dims* d) {
   ScorePlan p{};
   const int G = d->n_q_heads / d->n_kv_heads;
-  p.m = ceil_div(d->n_prefix, d->chunk_size);
-  p.rows = G * d->n_suffix;
-  const int unit = d->chunk_size % 32 == 0 ? d->chunk_size : 32;  // lcm(32, c) for supported c
   const bool f32 = d->dtype == CKV_DTYPE_F32;
-  const int64_t row_blocks = ceil_div(p.rows, f32 ? kWaveRows : kBlockRows);
-  // Longer key ranges amortise each workgroup's fixed work (Q tile, row
-  // reference, statistics) and shrink the per-range partials that the
-  // normalisation pass reads; grow the range while the grid keeps at least
-  // 1.5 workgroups per CU.
-  int64_t kr = unit * ceil_div(256, unit);
-  while (kr * 2 <= 4096 && (int64_t)d->n_kv_heads * row_blocks * ceil_div(d->n_prefix, kr * 2) >= 384)
-    kr *= 2;
-  p.key_range = (int32_t)kr;
-  p.n_ranges = (int32_t)ceil_div(d->n_prefix, kr);
-  p.cpr = (int32_t)(kr / d->chunk_size);
-  p.ldp = (int32_t)align_up(p.rows, kBlockRows);
-  const size_t R = (size_t)p.rows, H = (size_t)d->n_kv_heads, NR = (size_t)p.n_ranges;
+  const int64_t c = d->chunk_size;
+  p.m = ceil_div(d->n_prefix, c);
+  p.rows = G * d->n_suffix;
+  ScoreWork& w = p.w;
+  w.rpb = f32 ? kWaveRows : kBlockRows;
+  w.RB = (int32_t)ceil_div(p.rows, w.rpb);
+  int64_t g64 = 64, cc = c;  // gcd(64, c)
+  while (cc) { const int64_t t = g64 % cc; g64 = cc; cc = t; }
+  const int64_t UK = 64 / g64 * c;  // lcm(64, c)
+  const int64_t U = ceil_div(d->n_prefix, UK);
+  const int64_t H_RB = (int64_t)d->n_kv_heads * w.RB;
+  // A fixed grid target (two 256-thread workgroups per CU of a 256-CU MI355X
+  // for bf16) keeps the decomposition, and so every rounding, independent of
+  // the device the library runs on.  Segments keep at least 8 stages.
+  const int64_t target = f32 ? 1024 : 512;
+  const int64_t min_units = std::max<int64_t>(1, 512 / UK);
+  int64_t NS = std::max<int64_t>(1, target / H_RB);
+  NS = std::min<int64_t>(NS, std::max<int64_t>(1, U / min_units));
+  if (UK > INT32_MAX || U > INT32_MAX || H_RB * NS >= (int64_t(1) << 31)) return p;  // bytes == 0
+  w.UK = (int32_t)UK;
+  w.U = (int32_t)U;
+  w.NS = (int32_t)NS;
+  w.ldp = w.RB * w.rpb;
+  const size_t H = (size_t)d->n_kv_heads, m_pad = (size_t)(U * UK / c);
+  const size_t stats = (size_t)H_RB * NS * (size_t)w.rpb;
   size_t off = 0;
   p.off_part = off;
-  off = align_up(off + H * NR * p.cpr * (size_t)p.ldp * sizeof(float), 256);
+  off = align_up(off + H * m_pad * (size_t)w.ldp * sizeof(float), 256);
   p.off_mc = off;
-  off = align_up(off + H * NR * R * sizeof(float), 256);
+  off = align_up(off + stats * sizeof(float), 256);
   p.off_z = off;
-  off = align_up(off + H * NR * R * sizeof(double), 256);
+  off = align_up(off + stats * sizeof(double), 256);
   p.off_flags = off;
-  off = align_up(off + H * NR * (size_t)ceil_div(p.rows, kBlockRows) * sizeof(int), 256);
+  off = align_up(off + (size_t)H_RB * NS * sizeof(int), 256);
   p.bytes = off;
   return p;
 }
@@ -926,6 +940,7 @@ ScorePlan make_score_plan(const ckv_dims* d) {
 ckv_status launch_score(const ckv_dims* d, const void* q, const void* k, double* scores, void* ws,
                         size_t ws_bytes, hipStream_t st, hipEvent_t after_main) {
   const ScorePlan p = make_score_plan(d);
+  if (p.bytes == 0) CKV_FAIL(CKV_EUNSUPPORTED, "shape too large for the scoring decomposition");
   if (ws_bytes < p.bytes) CKV_FAIL(CKV_EINVAL, "score workspace too small: %zu < %zu", ws_bytes, p.bytes);
   const int mode = chunk_mode(d->chunk_size);
   char* base = static_cast<char*>(ws);
@@ -934,6 +949,8 @@ ckv_status launch_score(const ckv_dims* d, const void* q, const void* k, double*
   double* z = reinterpret_cast<double*>(base + p.off_z);
   const int G = d->n_q_heads / d->n_kv_heads;
   const float c1 = resolve_scale(d) * 1.4426950408889634f;
+  const int64_t m_pad = (int64_t)p.w.U * p.w.UK / d->chunk_size;
+  const uint32_t nwg = (uint32_t)((int64_t)d->n_kv_heads * p.w.RB * p.w.NS);
 
   if (d->dtype == CKV_DTYPE_BF16) {
     ScoreArgs a;
@@ -941,17 +958,17 @@ ckv_status launch_score(const ckv_dims* d, const void* q, const void* k, double*
     a.k = static_cast<const uint16_t*>(k);
     a.part = part; a.mc = mc; a.z = z;
     a.flags = reinterpret_cast<int*>(base + p.off_flags);
-    a.n = d->n_prefix; a.S = d->n_suffix; a.Hq = d->n_q_heads; a.Hkv = d->n_kv_heads; a.G = G;
-    a.R = p.rows; a.ldp = p.ldp; a.c = d->chunk_size; a.key_range = p.key_range;
-    a.n_ranges = p.n_ranges; a.cpr = p.cpr; a.n_row_blocks = (int)ceil_div(p.rows, kBlockRows);
-    a.c1 = c1;
-    a.nblocks = (uint32_t)((int64_t)a.Hkv * a.n_ranges * a.n_row_blocks);
-    a.nblocks_padded = (uint32_t)align_up(a.nblocks, 8);
-    dim3 grid(a.nblocks_padded), block(kWaves * 64);
+    a.n = d->n_prefix; a.m_pad = m_pad;
+    a.S = d->n_suffix; a.Hq = d->n_q_heads; a.Hkv = d->n_kv_heads; a.G = G;
+    a.R = p.rows; a.c = d->chunk_size; a.c1 = c1; a.w = p.w;
+    a.nwg = nwg;
+    a.nwg_padded = (uint32_t)align_up(nwg, 8);
+    dim3 grid(a.nwg_padded), block(kWaves * 64);
+    dim3 fb_grid(std::min((uint32_t)kFallbackBlocks, nwg));
 #define CKV_SCORE_LAUNCH(DD, MM)                                                        \
   do {                                                                                  \
     hipLaunchKernelGGL((score_bf16_kernel<DD, MM>), grid, block, 0, st, a);             \
-    hipLaunchKernelGGL((score_fallback_kernel<DD, MM>), dim3(kFallbackBlocks), block, 0, st, a); \
+    hipLaunchKernelGGL((score_fallback_kernel<DD, MM>), fb_grid, block, 0, st, a);      \
   } while (0)
     if (d->head_dim == 128) {
       switch (mode) {
@@ -976,12 +993,11 @@ ckv_status launch_score(const ckv_dims* d, const void* q, const void* k, double*
     a.q = static_cast<const float*>(q);
     a.k = static_cast<const float*>(k);
     a.part = part; a.mc = mc; a.z = z;
-    a.n = d->n_prefix; a.S = d->n_suffix; a.Hq = d->n_q_heads; a.Hkv = d->n_kv_heads; a.G = G;
-    a.R = p.rows; a.ldp = p.ldp; a.c = d->chunk_size; a.key_range = p.key_range;
-    a.n_ranges = p.n_ranges; a.cpr = p.cpr; a.n_row_blocks = (int)ceil_div(p.rows, kWaveRows);
-    a.c1 = c1;
-    a.nblocks = (uint32_t)((int64_t)a.Hkv * a.n_ranges * a.n_row_blocks);
-    dim3 grid(a.nblocks), block(64);
+    a.n = d->n_prefix; a.m_pad = m_pad;
+    a.S = d->n_suffix; a.Hq = d->n_q_heads; a.Hkv = d->n_kv_heads; a.G = G;
+    a.R = p.rows; a.c = d->chunk_size; a.c1 = c1; a.w = p.w;
+    a.nwg = (int)nwg;
+    dim3 grid(nwg), block(64);
     switch (mode) {
       case kC4: hipLaunchKernelGGL((score_f32_kernel<64, kC4>), grid, block, 0, st, a); break;
       case kC8: hipLaunchKernelGGL((score_f32_kernel<64, kC8>), grid, block, 0, st, a); break;
@@ -994,10 +1010,11 @@ ckv_status launch_score(const ckv_dims* d, const void* q, const void* k, double*
   if (after_main) CKV_HIP(hipEventRecord(after_main, st));
   const int norm_blocks = d->n_kv_heads * (int)ceil_div(p.rows, kNormRows);
   hipLaunchKernelGGL(row_norm_kernel, dim3(norm_blocks), dim3(kNormRows * kNormLanes), 0, st, mc,
-                     z, d->n_kv_heads, p.rows, p.n_ranges);
+                     z, p.w, p.rows);
   CKV_HIP(hipGetLastError());
+  const int log2_rpb = p.w.rpb == 256 ? 8 : 6;
   hipLaunchKernelGGL(chunk_reduce_kernel, dim3((unsigned)p.m), dim3(kReduceThreads), 0, st, part,
-                     z, scores, d->n_kv_heads, p.rows, p.ldp, p.n_ranges, p.cpr);
+                     z, scores, p.w, d->n_kv_heads, p.rows, m_pad, d->chunk_size, log2_rpb);
   CKV_HIP(hipGetLastError());
   return CKV_OK;
 }
