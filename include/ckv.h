@@ -107,9 +107,12 @@ int64_t ckv_num_keep(int64_t m, double r);
  *   k_prefix      device, [n][Hkv][d]
  *   chunk_scores  device, double[m] (written)
  *   ws            device workspace of ckv_score_workspace_bytes(dims) bytes
+ *                 (0 for a shape too large for the scoring decomposition);
+ *                 scratch, no initial contents needed.  Calls that share a
+ *                 workspace must not overlap in time.
  * Arithmetic: logits and exponentials in fp32 (bf16 products are exact in
  * fp32), per-chunk partial sums in fp32 over at most one chunk, every sum
- * across rows, ranges and heads in fp64, in a fixed order (run-to-run
+ * across rows, key segments and heads in fp64, in a fixed order (run-to-run
  * deterministic).
  * ------------------------------------------------------------------------- */
 size_t ckv_score_workspace_bytes(const ckv_dims* dims);

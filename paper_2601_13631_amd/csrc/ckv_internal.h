@@ -95,7 +95,7 @@ struct ScorePlan {
   size_t off_part, off_mc, off_z, off_flags, bytes;
 };
 ScorePlan make_score_plan(const ckv_dims* d);
-// after_main (optional) is recorded between the main kernel and the finalize kernels.
+// after_main (optional) is recorded between the main kernel and the fold.
 ckv_status launch_score(const ckv_dims* d, const void* q, const void* k, double* scores,
                         void* ws, size_t ws_bytes, hipStream_t st,
                         hipEvent_t after_main = nullptr);

@@ -15,16 +15,16 @@
 // l^32 the other 16).
 //
 // Softmax without a second pass.  A segment takes as each row's reference mc
-// the scaled maximum of its logits over the segment's first 32 keys and
-// accumulates, per chunk, P = sum exp2(c1*dot - mc) (c1 = sm_scale*log2 e) in
-// fp32 over at most one chunk, plus z = sum of the segment's chunk sums in
-// fp64.  Finalize kernels fold the segments of a row in fp64: M = max mc,
-// Z = sum exp2(mc - M) z, w = exp2(mc - M)/Z, A_j = sum_r w P.  The result is
-// exact in real arithmetic for any reference; the reference only has to keep
-// exp2 finite.  If a segment's z leaves the guard (some chunk sum is above it
-// or not finite) the fallback kernel recomputes that segment against its own
-// exact maximum (two passes), so the fast path never trades correctness for
-// speed.
+// the scaled maximum of its logits over the segment's first 32 keys, rounded
+// up to a whole number, and accumulates, per chunk, P = sum exp2(c1*dot - mc)
+// (c1 = sm_scale*log2 e) in fp32 over at most one chunk, plus z = sum of the
+// segment's chunk sums in fp64.  A fold kernel combines the segments of a row
+// in fp64: M = max mc, Z = sum exp2(mc - M) z, w = exp2(mc - M)/Z (exact
+// powers of two), and a reduction forms A_j = sum_r w P.  The result is exact
+// in real arithmetic for any reference; the reference only has to keep exp2
+// finite.  If a segment's z leaves the guard (some chunk sum is above it or not
+// finite) the fold kernel first recomputes that segment against its own exact
+// maximum (two passes), so the fast path never trades correctness for speed.
 //
 // All sums have a fixed order: results are bitwise reproducible run to run.
 
@@ -40,7 +40,6 @@ constexpr int kWaveRows = 64;
 constexpr int kBlockRows = kWaves * kWaveRows;  // 256
 constexpr int kSub = 32;                        // keys per subtile
 constexpr float kOverflowGuard = 0x1p100f;      // a chunk sum above this forces the exact pass
-constexpr int kFallbackBlocks = 64;             // grid of the (almost always idle) fallback kernel
 
 enum ChunkMode { kC4 = 0, kC8 = 1, kC16 = 2, kC32 = 3, kC32x = 4 };  // kC32x: c = 64, 96, ...
 
@@ -342,7 +341,9 @@ __device__ __forceinline__ void process_subtile(const ScoreArgs& a, const bf16x8
         if (FULL || key < nvalid) mx = fmaxf(mx, acc[rt][v]);
       }
       mx = fmaxf(mx, partner_f(mx));
-      st.mref[rt] = fmaxf(st.mref[rt], mx * a.c1);
+      // references are whole numbers (log2 units): the fold rescales by exact
+      // powers of two
+      st.mref[rt] = fmaxf(st.mref[rt], ceilf(mx * a.c1));
     }
     return;
   }
@@ -590,9 +591,58 @@ __device__ __forceinline__ Segment segment_of(const ScoreWork& wk, int64_t n, in
   return g;
 }
 
+// Fold of the segments of row block rbh: thread t owns row t of the block
+// (rows past R fold too; nothing reads them).  M = max mc, Z = sum
+// exp2(mc - M) z, and each segment's z slot becomes its weight exp2(mc - M)/Z.
+// Segments are read kFoldBatch at a time so their loads are in flight together
+// (one batch covers every shape with NS <= kFoldBatch).
+constexpr int kFoldBatch = 32;
+
+// exp2(mc - M) for whole-number references mc <= M: an exact power of two
+// (zero once it is below the smallest subnormal).
+__device__ __forceinline__ double seg_factor(float mc, float M) {
+  return mc == M ? 1.0 : ldexp(1.0, (int)fmaxf(mc - M, -1100.f));
+}
+
+__device__ __forceinline__ void fold_row_block(const float* mc, double* z, const ScoreWork& wk,
+                                               int rbh) {
+  const int64_t base = (int64_t)rbh * wk.NS * wk.rpb + threadIdx.x;
+  const int NS = wk.NS, rpb = wk.rpb;
+  float M = -INFINITY;
+  for (int s0 = 0; s0 < NS; s0 += kFoldBatch) {
+    float v[kFoldBatch];
+#pragma unroll
+    for (int i = 0; i < kFoldBatch; ++i)
+      v[i] = s0 + i < NS ? mc[base + (int64_t)(s0 + i) * rpb] : -INFINITY;
+#pragma unroll
+    for (int i = 0; i < kFoldBatch; ++i) M = fmaxf(M, v[i]);
+  }
+  double Z = 0.0;
+  for (int s0 = 0; s0 < NS; s0 += kFoldBatch) {
+    float v[kFoldBatch];
+    double zz[kFoldBatch];
+#pragma unroll
+    for (int i = 0; i < kFoldBatch; ++i) {
+      const bool ok = s0 + i < NS;
+      v[i] = ok ? mc[base + (int64_t)(s0 + i) * rpb] : M;
+      zz[i] = ok ? z[base + (int64_t)(s0 + i) * rpb] : 0.0;
+    }
+#pragma unroll
+    for (int i = 0; i < kFoldBatch; ++i) Z += seg_factor(v[i], M) * zz[i];
+  }
+  const double inv = 1.0 / Z;
+  for (int s0 = 0; s0 < NS; s0 += kFoldBatch) {
+    float v[kFoldBatch];
+#pragma unroll
+    for (int i = 0; i < kFoldBatch; ++i) v[i] = s0 + i < NS ? mc[base + (int64_t)(s0 + i) * rpb] : M;
+#pragma unroll
+    for (int i = 0; i < kFoldBatch; ++i)
+      if (s0 + i < NS) z[base + (int64_t)(s0 + i) * rpb] = seg_factor(v[i], M) * inv;
+  }
+}
+
 // Main pass: every workgroup runs its segment, pipelined, against the
-// segment's own reference, and records whether a chunk sum left the guard
-// (then the fallback kernel redoes the segment).
+// segment's own reference, and records whether a chunk sum left the guard.
 template <int D, int MODE>
 __global__ __launch_bounds__(kWaves * 64, 2) void score_bf16_kernel(ScoreArgs a) {
   __shared__ __attribute__((aligned(16))) uint16_t lds[2 * kStage * SubtileLds<D>::kRow];
@@ -609,29 +659,38 @@ __global__ __launch_bounds__(kWaves * 64, 2) void score_bf16_kernel(ScoreArgs a)
   store_stats(a, sg.rbh, sg.s, st);
 }
 
-// Exact fallback, almost always a no-op: a grid-stride loop over the main
-// pass's workgroups; a flagged segment is recomputed against its own exact
-// maximum (first pass: maximum only, second pass: partial sums and z).
+// Fold pass, one workgroup per row block: redoes exactly (against its own
+// maximum, two passes) any of the block's segments whose chunk sums left the
+// guard in the main pass -- almost never -- then folds the block's segments.
 template <int D, int MODE>
-__global__ __launch_bounds__(kWaves * 64, 2) void score_fallback_kernel(ScoreArgs a) {
+__global__ __launch_bounds__(kWaves * 64) void score_fold_kernel(ScoreArgs a) {
   __shared__ __attribute__((aligned(16))) uint16_t lds[2 * kStage * SubtileLds<D>::kRow];
-  // all threads scan a share of the flags at once; nothing to do is the common case
-  int mine = 0;
-  for (uint32_t i = blockIdx.x + gridDim.x * threadIdx.x; i < a.nwg; i += gridDim.x * blockDim.x)
-    mine |= a.flags[i];
-  if (!__syncthreads_or(mine)) return;
-  for (uint32_t w = blockIdx.x; w < a.nwg; w += gridDim.x) {
-    if (!a.flags[w]) continue;  // uniform
-    const Segment sg = segment_of(a.w, a.n, (int)w);
-    const int g = sg.rbh / a.w.RB, row0 = (sg.rbh % a.w.RB) * kBlockRows;
-    bf16x8 qf[2][D / 16];
-    load_q<D>(a, g, row0, qf);
-    RangeState st;
-    run_segment<D, MODE, 1>(a, g, sg.kbeg, sg.nkeys, row0, qf, lds, st);
-    run_segment<D, MODE, 2>(a, g, sg.kbeg, sg.nkeys, row0, qf, lds, st);
-    store_stats(a, sg.rbh, sg.s, st);
-    __syncthreads();
+  const int rbh = blockIdx.x;
+  const int g = rbh / a.w.RB, row0 = (rbh % a.w.RB) * kBlockRows;
+  // all flags of the block in one round trip; nothing flagged is the common case
+  int any = 0;
+  for (int s = threadIdx.x; s < a.w.NS; s += blockDim.x) any |= a.flags[rbh * a.w.NS + s];
+  if (__syncthreads_or(any)) {
+    for (int s = 0; s < a.w.NS; ++s) {
+      if (!a.flags[rbh * a.w.NS + s]) continue;  // uniform
+      const Segment o = segment_of(a.w, a.n, rbh * a.w.NS + s);
+      bf16x8 qf[2][D / 16];
+      load_q<D>(a, g, row0, qf);
+      RangeState st;
+      run_segment<D, MODE, 1>(a, g, o.kbeg, o.nkeys, row0, qf, lds, st);
+      run_segment<D, MODE, 2>(a, g, o.kbeg, o.nkeys, row0, qf, lds, st);
+      store_stats(a, rbh, s, st);
+      __syncthreads();
+    }
   }
+  fold_row_block(a.mc, a.z, a.w, rbh);
+}
+
+// fp32 path: the main kernel already redid overflowing segments; fold only.
+__global__ __launch_bounds__(kWaveRows) void score_fold_f32_kernel(const float* __restrict__ mc,
+                                                                   double* __restrict__ z,
+                                                                   ScoreWork wk) {
+  fold_row_block(mc, z, wk, blockIdx.x);
 }
 
 // ---------------------------------------------------------------------------
@@ -689,9 +748,9 @@ __device__ bool run_span_f32(const ScoreArgsF32& a, int g, int64_t kbeg, int64_t
         }
         mx = fmaxf(mx, partner_f(mx));
         if (PASS == 1)
-          mref[rt] = fmaxf(mref[rt], mx * a.c1);
+          mref[rt] = fmaxf(mref[rt], ceilf(mx * a.c1));
         else
-          mref[rt] = mx * a.c1;
+          mref[rt] = ceilf(mx * a.c1);
       }
     }
     if (PASS == 1) continue;
@@ -801,56 +860,11 @@ __global__ __launch_bounds__(64) void score_f32_kernel(ScoreArgsF32 a) {
 // ---------------------------------------------------------------------------
 // finalize
 // ---------------------------------------------------------------------------
-// F1: per (g, row): M = max over the row's segments of mc, Z = sum over them
-// of exp2(mc - M) z, and the z slot of every segment is overwritten with its
-// weight w = exp2(mc - M) / Z (fp64).  A workgroup serves 32 rows (coalesced)
-// with 8 lanes per row splitting the segments; partial results are combined
-// through LDS in lane order.
-constexpr int kNormRows = 32;
-constexpr int kNormLanes = 8;
-
-__device__ __forceinline__ double seg_factor(float mc, float M) {
-  return mc == M ? 1.0 : exp2((double)mc - (double)M);
-}
-
-__global__ __launch_bounds__(kNormRows * kNormLanes) void row_norm_kernel(
-    const float* __restrict__ mc, double* __restrict__ z, ScoreWork wk, int R) {
-  __shared__ float sred[kNormLanes][kNormRows];
-  __shared__ double ssum[kNormLanes][kNormRows];
-  const int rl = threadIdx.x % kNormRows, q = threadIdx.x / kNormRows;
-  const int blocks_per_head = (R + kNormRows - 1) / kNormRows;
-  const int g = blockIdx.x / blocks_per_head;
-  const int row = (blockIdx.x % blocks_per_head) * kNormRows + rl;
-  const bool ok = row < R;
-  // kNormRows divides rpb: the 32 rows lie in one row block
-  const int rbh = g * wk.RB + ((blockIdx.x % blocks_per_head) * kNormRows) / wk.rpb;
-  const int nseg = wk.NS;
-  const int64_t base = (int64_t)rbh * wk.NS * wk.rpb + row % wk.rpb;
-  float M = -INFINITY;
-  if (ok)
-    for (int s = q; s < nseg; s += kNormLanes) M = fmaxf(M, mc[base + (int64_t)s * wk.rpb]);
-  sred[q][rl] = M;
-  __syncthreads();
-  M = sred[0][rl];
-  for (int i = 1; i < kNormLanes; ++i) M = fmaxf(M, sred[i][rl]);
-  double Z = 0.0;
-  if (ok)
-    for (int s = q; s < nseg; s += kNormLanes)
-      Z += seg_factor(mc[base + (int64_t)s * wk.rpb], M) * z[base + (int64_t)s * wk.rpb];
-  ssum[q][rl] = Z;
-  __syncthreads();
-  Z = ssum[0][rl];
-  for (int i = 1; i < kNormLanes; ++i) Z += ssum[i][rl];
-  if (!ok) return;
-  const double inv = 1.0 / Z;
-  for (int s = q; s < nseg; s += kNormLanes)
-    z[base + (int64_t)s * wk.rpb] = seg_factor(mc[base + (int64_t)s * wk.rpb], M) * inv;
-}
-
-// F2: A_j = sum over KV heads g (in order) of sum over rows r of
-// w[segment holding chunk j][r] * P[g][j][r], in fp64.  One workgroup
-// of 256 threads per chunk: thread i takes rows i, i+256, ... of every head in
-// order, then a fixed tree over LDS reduces the 256 partial sums.
+// Reduction: A_j = sum over KV heads g (in order) of sum over rows r of
+// w[segment holding chunk j][r] * P[g][j][r], in fp64.  One workgroup of 256
+// threads per chunk: thread i takes rows 4i .. 4i+3, 4i+1024 .. of every head
+// in order (16-byte partial loads, 32-byte weight loads), then a fixed tree
+// over LDS reduces the 256 sums.
 constexpr int kReduceThreads = 256;
 
 __global__ __launch_bounds__(kReduceThreads) void chunk_reduce_kernel(
@@ -861,12 +875,25 @@ __global__ __launch_bounds__(kReduceThreads) void chunk_reduce_kernel(
   const int tid = threadIdx.x;
   const int seg = wk.seg_of_unit((int)(j * c / wk.UK));  // the same for every row block
   double s = 0.0;
+#pragma unroll 2
   for (int g = 0; g < Hkv; ++g) {
     const float* p = part + ((int64_t)g * m_pad + j) * wk.ldp;
-    for (int r = tid; r < R; r += kReduceThreads) {
+    for (int r = 4 * tid; r < R; r += 4 * kReduceThreads) {
+      // ldp and rpb are multiples of 64: the 4 rows are in bounds and in one block
+      const f32x4 pv = *reinterpret_cast<const f32x4*>(p + r);
       const int rbh = g * wk.RB + (r >> log2_rpb);
-      const double wr = w[((int64_t)rbh * wk.NS + seg) * wk.rpb + (r & (wk.rpb - 1))];
-      s += (double)p[r] * wr;
+      const double* wr = w + ((int64_t)rbh * wk.NS + seg) * wk.rpb + (r & (wk.rpb - 1));
+      const double2 w01 = *reinterpret_cast<const double2*>(wr);
+      const double2 w23 = *reinterpret_cast<const double2*>(wr + 2);
+      if (r + 3 < R) {
+        s += (double)pv[0] * w01.x;
+        s += (double)pv[1] * w01.y;
+        s += (double)pv[2] * w23.x;
+        s += (double)pv[3] * w23.y;
+      } else {
+        const double wv[4] = {w01.x, w01.y, w23.x, w23.y};
+        for (int e = 0; e < 4 && r + e < R; ++e) s += (double)pv[e] * wv[e];
+      }
     }
   }
   red[tid] = s;
@@ -917,7 +944,8 @@ ScorePlan make_score_plan(const ckv_dims* d) {
   const int64_t min_units = std::max<int64_t>(1, 512 / UK);
   int64_t NS = std::max<int64_t>(1, target / H_RB);
   NS = std::min<int64_t>(NS, std::max<int64_t>(1, U / min_units));
-  if (UK > INT32_MAX || U > INT32_MAX || H_RB * NS >= (int64_t(1) << 31)) return p;  // bytes == 0
+  // bytes == 0 marks an unsupported shape
+  if (UK > INT32_MAX || U > INT32_MAX || H_RB * NS >= (int64_t(1) << 31)) return p;
   w.UK = (int32_t)UK;
   w.U = (int32_t)U;
   w.NS = (int32_t)NS;
@@ -964,11 +992,13 @@ ckv_status launch_score(const ckv_dims* d, const void* q, const void* k, double*
     a.nwg = nwg;
     a.nwg_padded = (uint32_t)align_up(nwg, 8);
     dim3 grid(a.nwg_padded), block(kWaves * 64);
-    dim3 fb_grid(std::min((uint32_t)kFallbackBlocks, nwg));
-#define CKV_SCORE_LAUNCH(DD, MM)                                                        \
-  do {                                                                                  \
-    hipLaunchKernelGGL((score_bf16_kernel<DD, MM>), grid, block, 0, st, a);             \
-    hipLaunchKernelGGL((score_fallback_kernel<DD, MM>), fb_grid, block, 0, st, a);      \
+    const dim3 fold_grid((unsigned)(d->n_kv_heads * p.w.RB));
+    // the event (if any) goes between the main kernel and the fold
+#define CKV_SCORE_LAUNCH(DD, MM)                                                   \
+  do {                                                                             \
+    hipLaunchKernelGGL((score_bf16_kernel<DD, MM>), grid, block, 0, st, a);        \
+    if (after_main) CKV_HIP(hipEventRecord(after_main, st));                      \
+    hipLaunchKernelGGL((score_fold_kernel<DD, MM>), fold_grid, block, 0, st, a);   \
   } while (0)
     if (d->head_dim == 128) {
       switch (mode) {
@@ -1005,12 +1035,10 @@ ckv_status launch_score(const ckv_dims* d, const void* q, const void* k, double*
       case kC32: hipLaunchKernelGGL((score_f32_kernel<64, kC32>), grid, block, 0, st, a); break;
       default: hipLaunchKernelGGL((score_f32_kernel<64, kC32x>), grid, block, 0, st, a); break;
     }
+    if (after_main) CKV_HIP(hipEventRecord(after_main, st));
+    hipLaunchKernelGGL(score_fold_f32_kernel, dim3((unsigned)(d->n_kv_heads * p.w.RB)),
+                       dim3(kWaveRows), 0, st, mc, z, p.w);
   }
-  CKV_HIP(hipGetLastError());
-  if (after_main) CKV_HIP(hipEventRecord(after_main, st));
-  const int norm_blocks = d->n_kv_heads * (int)ceil_div(p.rows, kNormRows);
-  hipLaunchKernelGGL(row_norm_kernel, dim3(norm_blocks), dim3(kNormRows * kNormLanes), 0, st, mc,
-                     z, p.w, p.rows);
   CKV_HIP(hipGetLastError());
   const int log2_rpb = p.w.rpb == 256 ? 8 : 6;
   hipLaunchKernelGGL(chunk_reduce_kernel, dim3((unsigned)p.m), dim3(kReduceThreads), 0, st, part,

@@ -1,0 +1,193 @@
+// select_block.h -- top-k ContiguousChunk selection (Sec. 4.4) by one
+// workgroup of kSelThreads threads (a device function, so that any kernel can
+// end with a selection).
+//
+// Keeps the k largest of m fp64 chunk scores under the total order (score
+// descending, index ascending) and writes their indices in ascending order.
+// Radix select on 64-bit order-preserving keys (sign-flipped IEEE bits, -0.0
+// folded onto +0.0, NaN below -inf).  Each round histograms an 8-bit digit that
+// starts at the highest bit where the smallest and largest candidate differ, so
+// no round is spent on bits every candidate shares; the same pass records each
+// bin's smallest and largest key, which bound the next round's candidates.  The
+// search ends when the chosen bin holds exactly the keys still needed or all
+// candidates are equal; the lowest indices then win among equal keys.  Output
+// is an in-order compaction with block-wide exclusive scans, so the indices
+// come out ascending.  Every count is an integer (LDS atomics): the result
+// depends only on the score bits.  With a key cache (LDS, m entries) the
+// scores are read from global memory once; without one, every pass re-reads
+// them (they stay in L2).
+
+#pragma once
+
+#include "ckv_internal.h"
+
+namespace ckv {
+
+constexpr int kSelThreads = 256;
+constexpr int kSelWaves = kSelThreads / 64;
+
+__device__ __forceinline__ uint64_t order_key(double x) {
+  uint64_t u = (uint64_t)__double_as_longlong(x);
+  if ((u << 1) == 0) u = 0;  // -0.0 -> +0.0
+  if ((u & 0x7FF0000000000000ull) == 0x7FF0000000000000ull && (u & 0x000FFFFFFFFFFFFFull))
+    return 0;  // NaN: below everything
+  return (u >> 63) ? ~u : (u | 0x8000000000000000ull);
+}
+
+struct SelShared {
+  uint32_t hist[256];
+  unsigned long long bmin[256], bmax[256];
+  uint32_t wsum[kSelWaves];
+  uint64_t red_lo[kSelWaves], red_hi[kSelWaves];
+  int64_t red_i[kSelWaves];
+  uint64_t prefix, mask, lo, hi;
+  int64_t remaining;
+  int done;
+};
+
+// Block-wide minimum of lo and maximum of hi, left in sh.lo / sh.hi.
+__device__ __forceinline__ void sel_block_minmax(uint64_t lo, uint64_t hi, SelShared& sh) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) {
+    const uint64_t l2 = __shfl_xor(lo, off), h2 = __shfl_xor(hi, off);
+    lo = l2 < lo ? l2 : lo;
+    hi = h2 > hi ? h2 : hi;
+  }
+  if (lane == 0) { sh.red_lo[wave] = lo; sh.red_hi[wave] = hi; }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    for (int w = 1; w < kSelWaves; ++w) {
+      lo = sh.red_lo[w] < lo ? sh.red_lo[w] : lo;
+      hi = sh.red_hi[w] > hi ? sh.red_hi[w] : hi;
+    }
+    sh.lo = lo;
+    sh.hi = hi;
+  }
+  __syncthreads();
+}
+
+// Exclusive prefix sum over the block (this thread's exclusive prefix).
+__device__ __forceinline__ int64_t sel_block_exclusive_scan(int64_t v, SelShared& sh) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  int64_t x = v;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const int64_t y = __shfl_up(x, off);
+    if (lane >= off) x += y;
+  }
+  __syncthreads();  // red_i may still be read by a previous scan
+  if (lane == 63) sh.red_i[wave] = x;
+  __syncthreads();
+  int64_t before = 0;
+  for (int w = 0; w < wave; ++w) before += sh.red_i[w];
+  return before + x - v;
+}
+
+// Called by all kSelThreads threads of the workgroup; 1 <= k <= m.  cache:
+// nullptr, or LDS room for m keys.
+__device__ __forceinline__ void select_topk_block(const double* scores, int64_t m, int64_t k,
+                                                  int32_t* sel, SelShared& sh, uint64_t* cache) {
+  const int tid = threadIdx.x;
+  auto key_at = [&](int64_t i) -> uint64_t { return cache ? cache[i] : order_key(scores[i]); };
+  {
+    uint64_t lo = ~0ull, hi = 0;
+    for (int64_t i = tid; i < m; i += kSelThreads) {
+      const uint64_t x = order_key(scores[i]);
+      if (cache) cache[i] = x;
+      lo = x < lo ? x : lo;
+      hi = x > hi ? x : hi;
+    }
+    sel_block_minmax(lo, hi, sh);  // its barriers also publish the cache
+  }
+  if (tid == 0) {
+    sh.prefix = 0;
+    sh.mask = 0;
+    sh.remaining = k;
+    sh.done = 0;
+  }
+  __syncthreads();
+  for (int round = 0; round < 64; ++round) {
+    const uint64_t lo = sh.lo, hi = sh.hi, prefix = sh.prefix, mask = sh.mask;
+    if (lo == hi) {  // every candidate equal: the lowest indices among them win
+      __syncthreads();
+      if (tid == 0) { sh.prefix = lo; sh.mask = ~0ull; }
+      __syncthreads();
+      break;
+    }
+    const int top = 63 - __clzll(lo ^ hi);
+    const int shift = top >= 7 ? top - 7 : 0;
+    for (int b = tid; b < 256; b += kSelThreads) {
+      sh.hist[b] = 0;
+      sh.bmin[b] = ~0ull;
+      sh.bmax[b] = 0;
+    }
+    __syncthreads();
+    for (int64_t i = tid; i < m; i += kSelThreads) {
+      const uint64_t x = key_at(i);
+      if ((x & mask) == prefix) {
+        const int b = (int)((x >> shift) & 255);
+        atomicAdd(&sh.hist[b], 1u);
+        atomicMin(&sh.bmin[b], (unsigned long long)x);
+        atomicMax(&sh.bmax[b], (unsigned long long)x);
+      }
+    }
+    __syncthreads();
+    // count of candidates in bins >= b as an inclusive scan over t = 255 - b;
+    // the bin where that count first reaches `need` is chosen (one thread)
+    const int64_t need = sh.remaining;
+    uint32_t cum = 0, mine = 0;
+    if (tid < 256) {
+      mine = sh.hist[255 - tid];
+      cum = mine;
+#pragma unroll
+      for (int off = 1; off < 64; off <<= 1) {
+        const uint32_t y = __shfl_up(cum, off);
+        if ((tid & 63) >= off) cum += y;
+      }
+      if ((tid & 63) == 63) sh.wsum[tid >> 6] = cum;
+    }
+    __syncthreads();
+    if (tid < 256) {
+      for (int w = 0; w < (tid >> 6); ++w) cum += sh.wsum[w];
+      const uint32_t before = cum - mine;
+      if (before < need && cum >= need) {
+        const int b = 255 - tid;
+        const uint64_t keep_hi = shift + 8 >= 64 ? 0 : ~((1ull << (shift + 8)) - 1);
+        sh.prefix = (lo & keep_hi) | ((uint64_t)b << shift);
+        sh.mask = keep_hi | (255ull << shift);
+        sh.remaining = need - before;
+        sh.done = (mine == (uint32_t)sh.remaining) || shift == 0;
+        sh.lo = sh.bmin[b];
+        sh.hi = sh.bmax[b];
+      }
+    }
+    __syncthreads();
+    if (sh.done) break;
+  }
+
+  // ascending compaction: i is kept if (key & mask) > prefix, or equal and among
+  // the first `remaining` equal keys by index
+  const uint64_t prefix = sh.prefix, mask = sh.mask;
+  const int64_t remaining = sh.remaining;
+  const int64_t per = (m + kSelThreads - 1) / kSelThreads;
+  const int64_t i0 = min(m, (int64_t)tid * per), i1 = min(m, i0 + per);
+  int64_t n_gt = 0, n_eq = 0;
+  for (int64_t i = i0; i < i1; ++i) {
+    const uint64_t x = key_at(i) & mask;
+    n_gt += x > prefix;
+    n_eq += x == prefix;
+  }
+  const int64_t gt_before = sel_block_exclusive_scan(n_gt, sh);
+  const int64_t eq_before = sel_block_exclusive_scan(n_eq, sh);
+  int64_t eq_rank = eq_before;
+  int64_t pos = gt_before + min(eq_before, remaining);
+  for (int64_t i = i0; i < i1; ++i) {
+    const uint64_t x = key_at(i) & mask;
+    bool take = x > prefix;
+    if (x == prefix) take = eq_rank++ < remaining;
+    if (take) sel[pos++] = (int32_t)i;
+  }
+}
+
+}  // namespace ckv
