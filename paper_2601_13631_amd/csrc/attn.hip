@@ -7,17 +7,20 @@
 // Rows of one KV head are r = t*G + i (query t, head g*G + i), so the G query
 // heads that share a KV head share every K/V tile.  A workgroup owns 128 rows
 // (4 waves x 32) and one contiguous slice ("split") of the key positions.  Per
-// 32-key tile:
+// 64-key stage:
 //   S^T = K Q^T   bf16 MFMA 32x32x16, A = K rows from LDS, B = Q^T in
 //                 registers: every lane owns one query row and 16 keys;
-//   online softmax in fp32 (exp2 with sm_scale*log2 e folded in);
+//   online softmax in fp32 (exp2 with sm_scale*log2 e folded in) with a lazy
+//                 reference: it moves only when a stage's maximum exceeds it
+//                 by more than 2^8, so most stages skip the O rescale;
 //   O^T += V^T P^T  A = V^T read from LDS with the transposing
 //                 ds_read_tr16_b64, B = P^T straight from the softmax registers.
 // The K operand rows are loaded in a permuted order so that the registers a
 // lane holds after the first product are exactly the 8 consecutive keys the
 // second product needs from it -- no register shuffles between the two.
-// Splits write unnormalised fp32 partials and (max, sum); a combine kernel
-// merges them in split order (deterministic).
+// Splits write their normalised partial output O/l in bf16 (the output's own
+// type and range) plus (reference, l) in fp32; a combine kernel merges them in
+// split order (deterministic).
 
 #include "ckv_internal.h"
 
@@ -82,7 +85,7 @@ struct AttnArgs {
   const uint16_t* ks;      // [S][Hkv][D]
   const uint16_t* vs;
   uint16_t* out;           // [S][Hq][D]
-  float* o_part;           // [splits][Hkv][R][D]
+  uint16_t* o_part;        // [splits][Hkv][R][D]: O / l, bf16
   float2* ml_part;         // [splits][Hkv][R]
   int S, Hq, Hkv, G, R, n_splits, tiles_per_split, n_row_blocks;
   float c1;
@@ -376,21 +379,27 @@ __global__ __launch_bounds__(kWaves * 64, 2) void attn_kernel(AttnArgs a) {
       }
   } else {
     const int64_t prow = ((int64_t)split * a.Hkv + g) * a.R + row;
-    float* dst = a.o_part + prow * D + 4 * half;
+    uint16_t* dst = a.o_part + prow * D + 4 * half;
+    const float inv = l_run > 0.f ? 1.f / l_run : 0.f;
 #pragma unroll
     for (int db = 0; db < D / 32; ++db)
 #pragma unroll
-      for (int q4 = 0; q4 < 4; ++q4)
-        *reinterpret_cast<f32x4*>(dst + 32 * db + 8 * q4) =
-            f32x4{o[db][4 * q4], o[db][4 * q4 + 1], o[db][4 * q4 + 2], o[db][4 * q4 + 3]};
-    if (half == 0) a.ml_part[prow] = make_float2(m_run, l_run);
+      for (int q4 = 0; q4 < 4; ++q4) {
+        __bf16 b[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) b[j] = (__bf16)(o[db][4 * q4 + j] * inv);
+        *reinterpret_cast<uint2*>(dst + 32 * db + 8 * q4) = *reinterpret_cast<uint2*>(b);
+      }
+    // the reference the numerators were taken against (0 while no key was seen)
+    if (half == 0) a.ml_part[prow] = make_float2(m_run == -INFINITY ? 0.f : m_run, l_run);
   }
 }
 
-// Merges the splits of each row in split order: out = sum_s e_s O_s / sum_s e_s l_s
-// with e_s = exp2(m_s - max m).  One thread per (row, 8 columns).
+// Merges the splits of each row in split order: out = sum_s w_s Ohat_s with
+// w_s = e_s l_s / sum_s e_s l_s, e_s = exp2(m_s - max m), Ohat_s = O_s / l_s.
+// One thread per (row, 8 columns).
 template <int D>
-__global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ o_part,
+__global__ __launch_bounds__(256) void combine_kernel(const uint16_t* __restrict__ o_part,
                                                       const float2* __restrict__ ml_part,
                                                       uint16_t* __restrict__ out, int n_splits,
                                                       int Hkv, int R, int G, int Hq) {
@@ -400,18 +409,21 @@ __global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ 
   const int64_t grow = idx / (D / 8);
   const int c8 = (int)(idx % (D / 8)) * 8;
   float M = -INFINITY;
-  for (int s = 0; s < n_splits; ++s) M = fmaxf(M, ml_part[s * rows + grow].x);
+  for (int s = 0; s < n_splits; ++s) {
+    const float2 ml = ml_part[s * rows + grow];
+    if (ml.y > 0.f) M = fmaxf(M, ml.x);
+  }
   float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
   float Lsum = 0.f;
   for (int s = 0; s < n_splits; ++s) {
     const float2 ml = ml_part[s * rows + grow];
-    const float e = ml.x == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(ml.x - M);
-    Lsum += e * ml.y;
-    const float* src = o_part + (s * rows + grow) * D + c8;
-    const f32x4 x0 = *reinterpret_cast<const f32x4*>(src);
-    const f32x4 x1 = *reinterpret_cast<const f32x4*>(src + 4);
+    if (!(ml.y > 0.f)) continue;  // the split saw no key of this row
+    const float wgt = __builtin_amdgcn_exp2f(ml.x - M) * ml.y;
+    Lsum += wgt;
+    const uint4 raw = *reinterpret_cast<const uint4*>(o_part + (s * rows + grow) * D + c8);
+    const __bf16* h = reinterpret_cast<const __bf16*>(&raw);
 #pragma unroll
-    for (int j = 0; j < 4; ++j) { acc[j] += e * x0[j]; acc[4 + j] += e * x1[j]; }
+    for (int j = 0; j < 8; ++j) acc[j] += wgt * (float)h[j];
   }
   const int g = (int)(grow / R), row = (int)(grow % R);
   const int t = row / G, i = row % G;
@@ -518,16 +530,17 @@ AttnPlan make_attn_plan(const ckv_dims* d, int64_t k) {
   const int64_t np = k * d->chunk_size + d->n_suffix;
   const int64_t ntiles = ceil_div(np, kTile);
   const int64_t base = (int64_t)d->n_kv_heads * ceil_div(p.rows, kBlockRows);
-  // enough workgroups for ~2 per CU, keeping >= 8 tiles per split
-  int64_t splits = ceil_div(512, base);
-  splits = std::min<int64_t>(splits, std::max<int64_t>(1, ntiles / 8));
-  splits = std::max<int64_t>(1, std::min<int64_t>(splits, 64));
+  // at most ~2 workgroups per CU, keeping >= 4 stages per split; then the
+  // fewest splits that give the same stages per split
+  int64_t splits = std::max<int64_t>(1, 512 / base);
+  splits = std::min<int64_t>(splits, std::max<int64_t>(1, ntiles / 4));
+  splits = ceil_div(ntiles, ceil_div(ntiles, splits));
   p.n_splits = (int32_t)splits;
   size_t off = 0;
   if (splits > 1) {
     const size_t rows = (size_t)d->n_kv_heads * p.rows;
     p.off_o = off;
-    off = align_up(off + (size_t)splits * rows * d->head_dim * sizeof(float), 256);
+    off = align_up(off + (size_t)splits * rows * d->head_dim * sizeof(uint16_t), 256);
     p.off_ml = off;
     off = align_up(off + (size_t)splits * rows * sizeof(float2), 256);
   }
@@ -578,7 +591,7 @@ ckv_status launch_attn(const ckv_dims* d, const void* q, const ChunkSource& src,
   a.ks = static_cast<const uint16_t*>(k_suffix);
   a.vs = static_cast<const uint16_t*>(v_suffix);
   a.out = static_cast<uint16_t*>(out);
-  a.o_part = p.n_splits > 1 ? reinterpret_cast<float*>(static_cast<char*>(ws) + p.off_o) : nullptr;
+  a.o_part = p.n_splits > 1 ? reinterpret_cast<uint16_t*>(static_cast<char*>(ws) + p.off_o) : nullptr;
   a.ml_part = p.n_splits > 1 ? reinterpret_cast<float2*>(static_cast<char*>(ws) + p.off_ml) : nullptr;
   a.S = d->n_suffix; a.Hq = d->n_q_heads; a.Hkv = d->n_kv_heads;
   a.G = d->n_q_heads / d->n_kv_heads; a.R = p.rows;
