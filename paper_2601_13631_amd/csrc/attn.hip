@@ -6,15 +6,18 @@
 //
 // Rows of one KV head are r = t*G + i (query t, head g*G + i), so the G query
 // heads that share a KV head share every K/V tile.  A workgroup owns 128 rows
-// (4 waves x 32) and one contiguous slice ("split") of the key positions.  Per
-// 64-key stage:
+// (4 waves x 32) and one contiguous slice ("split") of the key positions.  At
+// its start it resolves every key of its slice to a source code (a prefix row
+// of the K/V source, a suffix token, or no key) in LDS, so the tile loads are
+// branch-free.  Per 64-key stage:
 //   S^T = K Q^T   bf16 MFMA 32x32x16, A = K rows from LDS, B = Q^T in
 //                 registers: every lane owns one query row and 16 keys;
 //   online softmax in fp32 (exp2 with sm_scale*log2 e folded in) with a lazy
 //                 reference: it moves only when a stage's maximum exceeds it
 //                 by more than 2^8, so most stages skip the O rescale;
 //   O^T += V^T P^T  A = V^T read from LDS with the transposing
-//                 ds_read_tr16_b64, B = P^T straight from the softmax registers.
+//                 ds_read_b64_tr_b16, B = P^T straight from the softmax
+//                 registers.
 // The K operand rows are loaded in a permuted order so that the registers a
 // lane holds after the first product are exactly the 8 consecutive keys the
 // second product needs from it -- no register shuffles between the two.
@@ -30,10 +33,12 @@ namespace {
 constexpr int kWaves = 4;
 constexpr int kWaveRows = 32;
 constexpr int kBlockRows = kWaves * kWaveRows;  // 128
-constexpr int kTile = 64;  // keys per LDS stage
-constexpr int kSub = 32;   // keys per MFMA product
-constexpr int kNoKey = 0x7fffffff;  // visibility limit of a masked key
-constexpr float kLazy = 8.f;        // headroom of the lazy softmax reference (log2 units)
+constexpr int kTile = 64;                       // keys per LDS stage
+constexpr int kSub = 32;                        // keys per MFMA product
+constexpr int kMaxSliceKeys = 2048;             // key codes per workgroup slice (8 KiB)
+constexpr float kLazy = 8.f;                    // headroom of the lazy softmax reference (log2 units)
+// key codes: >= 0 row of the prefix K/V source, -1 no key, <= -2 suffix token -2-code
+constexpr int kNoKey = -1;
 
 // MFMA row p of the K operand holds key kappa(p); afterwards register v of a
 // lane in half h holds key 16*(v/8) + 8*h + v%8.
@@ -42,15 +47,16 @@ __device__ __forceinline__ int kappa(int p) {
   return 16 * (i >> 1) + 8 * h + 4 * (i & 1) + j;
 }
 
-// LDS swizzles (XOR of 16-byte segment index), conflict-free for the access
-// patterns of the two operand reads.
+// K stage: rows padded by one 16-byte segment, so the operand reads (16
+// consecutive lanes = 16 distinct rows, same segment) start 4 banks apart and
+// every fragment is an immediate offset from one per-lane base.
 template <int D>
-__device__ __forceinline__ int k_swz(int row) {
-  if constexpr (D == 128)
-    return ((row & 1) ? 1 : 0) ^ ((row & 2) ? 2 : 0) ^ ((row & 4) ? 8 : 0) ^ ((row & 8) ? 4 : 0);
-  else
-    return ((row & 1) ? 1 : 0) ^ ((row & 2) ? 2 : 0) ^ ((row & 4) ? 1 : 0) ^ ((row & 8) ? 4 : 0);
-}
+struct KLds {
+  static constexpr int kRow = D + 8;
+};
+
+// V stage: XOR swizzle of 16-byte segments, conflict-free for the transposing
+// reads.
 template <int D>
 __device__ __forceinline__ int v_swz(int row) {
   if constexpr (D == 128)
@@ -58,8 +64,6 @@ __device__ __forceinline__ int v_swz(int row) {
   else
     return ((row & 1) ? 2 : 0) ^ ((row & 2) ? 4 : 0);
 }
-template <int D>
-__device__ __forceinline__ int k_off(int row, int seg) { return row * D + ((seg ^ k_swz<D>(row)) << 3); }
 template <int D>
 __device__ __forceinline__ int v_off(int row, int seg) { return row * D + ((seg ^ v_swz<D>(row)) << 3); }
 
@@ -73,126 +77,223 @@ struct AttnArgs {
   const uint16_t* q;       // [S][Hq][D]
   const uint16_t* kbase;   // prefix chunks (see ChunkSource)
   const uint16_t* vbase;
-  int64_t chunk_stride;    // elements
   const int32_t* chunk_off;
   int32_t direct;
+  int rows_per_slot;       // chunk slot stride of the source in rows of Hkv*D elements
   const int32_t* sel;      // [k]
   int kc;                  // k * c prefix positions (< 2^31)
-  int64_t n;
+  int64_t n, m;
   int c;
   int log2c;               // log2(c) when c is a power of two, else -1
-  int short_tail;          // c - n % c when the last chunk is short, else 0
   const uint16_t* ks;      // [S][Hkv][D]
   const uint16_t* vs;
   uint16_t* out;           // [S][Hq][D]
   uint16_t* o_part;        // [splits][Hkv][R][D]: O / l, bf16
-  float2* ml_part;         // [splits][Hkv][R]
+  float2* ml_part;         // [splits][Hkv][R]: (reference, sum)
   int S, Hq, Hkv, G, R, n_splits, tiles_per_split, n_row_blocks;
   float c1;
   uint32_t nblocks, nblocks_padded;
 };
 
-// The K/V rows of one 64-key stage, fetched into registers (while the previous
-// stage is consumed from LDS) and then written to the other LDS buffer.
-template <int D>
-struct TileRegs {
-  static constexpr int kPer = kTile * (D / 8) / (kWaves * 64);  // 16-byte pieces per thread
-  u32x4 k[kPer], v[kPer];
-  int lim[kPer];
-};
-
-// Chunk index (and slot-table entry) of each piece's key, fetched one stage
-// ahead of its K/V rows so that the row loads never wait on the index loads.
-// The loads are unconditional (clamped to the last kept chunk) and their values
-// are only interpreted by tile_load.
-template <int D>
-struct TileIdx {
-  int32_t j[TileRegs<D>::kPer];     // sel[u] of the piece's chunk u
-  int32_t slot[TileRegs<D>::kPer];  // chunk_off[u] when a slot table is used
-};
-
-// Kept chunk u holding compact position pos.  A power-of-two c uses a shift;
-// any other supported c is a multiple of 64 or 32, and u is then computed per
-// piece with a 32-bit division.
+// Source code of compact key position pos (see kNoKey), in two steps so that
+// a workgroup can issue all its index loads before using any: key_chunk_loads
+// fetches sel[u] (and the slot table entry) of the key's chunk u, key_code
+// finishes.  Row off of kept chunk u sits at source row slot*rows_per_slot +
+// off, slot = chunk_off[u] (slot table), sel[u] (spans read in place) or u
+// (compact copy).
 __device__ __forceinline__ int chunk_of(const AttnArgs& a, int pos) {
   return a.log2c >= 0 ? (pos >> a.log2c) : (int)((uint32_t)pos / (uint32_t)a.c);
 }
 
-template <int D>
-__device__ __forceinline__ void tile_index(const AttnArgs& a, int tile, TileIdx<D>& x) {
-  constexpr int kSegs = D / 8;
-  if (a.kc == 0) return;
-  const int pos0 = tile * kTile;
-  const int last = a.kc / a.c - 1;
-#pragma unroll
-  for (int p = 0; p < TileRegs<D>::kPer; ++p) {
-    const int key = (threadIdx.x + p * kWaves * 64) / kSegs;
-    const int u = min(chunk_of(a, pos0 + key), last);
-    x.j[p] = a.sel[u];
-    if (a.chunk_off) x.slot[p] = a.chunk_off[u];
+__device__ __forceinline__ void key_chunk_loads(const AttnArgs& a, int pos, int& j, int& slot) {
+  j = 0;
+  slot = 0;
+  if (pos < a.kc) {
+    const int u = chunk_of(a, pos);
+    j = a.sel[u];
+    if (a.chunk_off) slot = a.chunk_off[u];
   }
 }
 
-// Fetches stage `tile` of key positions and each key's visibility limit (a row
-// with query t sees the key iff t >= lim).  Loads are unconditional: a masked
-// key reads suffix row 0 of this KV head instead (finite data; its probability
-// is forced to zero, so it contributes nothing).
+__device__ __forceinline__ int key_code(const AttnArgs& a, int pos, int j, int slot_tab) {
+  if (pos < a.kc) {
+    const int u = chunk_of(a, pos);
+    const int off = pos - u * a.c;
+    if (j < 0 || (int64_t)j >= a.m) return kNoKey;
+    if ((int64_t)j * a.c + off >= a.n) return kNoKey;  // past n in a short last chunk
+    const int slot = a.chunk_off ? slot_tab : (a.direct ? j : u);
+    return slot * a.rows_per_slot + off;
+  }
+  if (pos < a.kc + a.S) return -2 - (pos - a.kc);
+  return kNoKey;
+}
+
+// The K/V rows of one 64-key stage, fetched into registers (while the previous
+// stage is consumed from LDS) and then written to the other LDS buffer.  A
+// masked key reads suffix row 0 of this KV head (always present; its weight is
+// forced to zero).
 template <int D>
-__device__ __forceinline__ void tile_load(const AttnArgs& a, int g, int tile, const TileIdx<D>& x,
-                                          TileRegs<D>& r) {
+struct TileRegs {
+  static constexpr int kPer = kTile * (D / 8) / (kWaves * 64);  // 16-byte pieces per thread
+  u32x4 k[kPer], v[kPer];
+};
+
+// Rows of the stage's keys for K (KV = 0) or V (KV = 1).
+template <int D, int KV>
+__device__ __forceinline__ void tile_load(const AttnArgs& a, int g, const int* codes, TileRegs<D>& r) {
   constexpr int kSegs = D / 8;
-  const int pos0 = tile * kTile;
+  const int64_t hd = (int64_t)a.Hkv * D;
 #pragma unroll
   for (int p = 0; p < TileRegs<D>::kPer; ++p) {
     const int idx = threadIdx.x + p * kWaves * 64;
     const int key = idx / kSegs, seg = idx % kSegs;
-    const int pos = pos0 + key;
-    const int col = g * D + seg * 8;
-    const uint16_t* ksrc = a.ks + col;
-    const uint16_t* vsrc = a.vs + col;
-    int limit = kNoKey;
-    if (pos < a.kc) {
-      const int u = chunk_of(a, pos);
-      const int off = pos - u * a.c;
-      const int j = x.j[p];
-      const int len = j >= 0 ? (int)min<int64_t>(a.c, a.n - (int64_t)j * a.c) : 0;  // outside [0, m): empty
-      if (off < len) {
-        const int slot = a.chunk_off ? x.slot[p] : (a.direct ? j : u);
-        const int64_t e = (int64_t)slot * a.chunk_stride + (off * a.Hkv * D + col);
-        ksrc = a.kbase + e;
-        vsrc = a.vbase + e;
-        limit = -1;
-      }
-    } else if (pos < a.kc + a.S) {
-      const int tok = pos - a.kc;
-      ksrc += tok * a.Hkv * D;
-      vsrc += tok * a.Hkv * D;
-      limit = tok;
-    }
-    r.k[p] = *reinterpret_cast<const u32x4*>(ksrc);
-    r.v[p] = *reinterpret_cast<const u32x4*>(vsrc);
-    r.lim[p] = limit;
+    const int code = codes[key];
+    const bool pre = code >= 0;
+    const int row = pre ? code : (code <= -2 ? -2 - code : 0);
+    const int64_t e = row * hd + (g * D + seg * 8);
+    if constexpr (KV == 0)
+      r.k[p] = *reinterpret_cast<const u32x4*>((pre ? a.kbase : a.ks) + e);
+    else
+      r.v[p] = *reinterpret_cast<const u32x4*>((pre ? a.vbase : a.vs) + e);
   }
 }
 
 template <int D>
-__device__ __forceinline__ void tile_store(const TileRegs<D>& r, uint16_t* lk, uint16_t* lv, int* lim) {
+__device__ __forceinline__ void tile_store(const TileRegs<D>& r, uint16_t* lk, uint16_t* lv) {
   constexpr int kSegs = D / 8;
 #pragma unroll
   for (int p = 0; p < TileRegs<D>::kPer; ++p) {
     const int idx = threadIdx.x + p * kWaves * 64;
     const int key = idx / kSegs, seg = idx % kSegs;
-    *reinterpret_cast<u32x4*>(lk + k_off<D>(key, seg)) = r.k[p];
+    *reinterpret_cast<u32x4*>(lk + key * KLds<D>::kRow + seg * 8) = r.k[p];
     *reinterpret_cast<u32x4*>(lv + v_off<D>(key, seg)) = r.v[p];
-    if (seg == 0) lim[key] = r.lim[p];
+  }
+}
+
+// Per-lane state of a wave's 32 rows.
+template <int D>
+struct RowState {
+  f32x16 o[D / 32];  // O^T: o[db][v] holds d = 32*db + 8*(v/4) + 4*half + v%4
+  float m_run;       // reference (scaled log2 units), -inf before any
+  float l_run;       // sum of numerators against m_run
+};
+
+// S^T of one stage for this wave's rows: two 32-key products.
+template <int D>
+__device__ __forceinline__ void stage_logits(const uint16_t* lk, int kbase_off,
+                                             const bf16x8 (&qf)[D / 16], f32x16 (&s)[2]) {
+#pragma unroll
+  for (int sub = 0; sub < 2; ++sub)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) s[sub][v] = 0.f;
+#pragma unroll
+  for (int ks = 0; ks < D / 16; ++ks) {
+#pragma unroll
+    for (int sub = 0; sub < 2; ++sub) {
+      const bf16x8 kf = *reinterpret_cast<const bf16x8*>(
+          lk + kbase_off + sub * kSub * KLds<D>::kRow + ks * 16);
+      s[sub] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[ks], s[sub], 0, 0, 0);
+    }
+  }
+}
+
+// Logits of one stage with the masked keys at -inf.
+template <int D>
+__device__ __forceinline__ void stage_masked_logits(const uint16_t* lk, int kbase_off,
+                                                    const bf16x8 (&qf)[D / 16], const int* codes,
+                                                    bool need_mask, int t, f32x16 (&s)[2]) {
+  const int half = (threadIdx.x >> 5) & 1;
+  stage_logits<D>(lk, kbase_off, qf, s);
+  // register v of product `sub` holds key 32*sub + 16*(v/8) + 8*half + v%8
+  if (need_mask) {
+#pragma unroll
+    for (int sub = 0; sub < 2; ++sub)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int code = codes[kSub * sub + 16 * (v >> 3) + 8 * half + (v & 7)];
+        const bool vis = code >= 0 || (code <= -2 && t >= -2 - code);
+        if (!vis) s[sub][v] = -INFINITY;
+      }
+  }
+}
+
+// Softmax part of one 64-key stage from the K buffer lk whose codes are
+// `codes`: numerators into s.  The reference moves only when the stage's
+// maximum exceeds it by more than kLazy (log2 units): numerators stay below
+// 2^kLazy, numerator and denominator share the reference, and most stages skip
+// the O rescale.
+template <int D>
+__device__ __forceinline__ void stage_softmax(const AttnArgs& a, const uint16_t* lk, const int* codes,
+                                              bool need_mask, int t, int kbase_off,
+                                              const bf16x8 (&qf)[D / 16], RowState<D>& rs,
+                                              f32x16 (&s)[2]) {
+  stage_masked_logits<D>(lk, kbase_off, qf, codes, need_mask, t, s);
+  float mx = fmaxf(s[0][0], s[1][0]);
+#pragma unroll
+  for (int v = 1; v < 16; ++v) mx = fmaxf(mx, fmaxf(s[0][v], s[1][v]));
+  mx = fmaxf(mx, partner_f(mx));
+  const float mt = mx * a.c1;
+  const float m_new = mt > rs.m_run + kLazy ? mt : rs.m_run;
+  const float m_use = m_new == -INFINITY ? 0.f : m_new;
+  const float alpha = __builtin_amdgcn_exp2f(rs.m_run - m_use);
+  float sum = 0.f;
+#pragma unroll
+  for (int sub = 0; sub < 2; ++sub)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      s[sub][v] = __builtin_amdgcn_exp2f(fmaf(s[sub][v], a.c1, -m_use));
+      sum += s[sub][v];
+    }
+  sum += partner_f(sum);
+  rs.l_run = rs.l_run * alpha + sum;
+  rs.m_run = m_new;
+  if (__any(alpha != 1.f)) {
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) rs.o[db][v] *= alpha;
+  }
+}
+
+// O^T += V^T P^T from the V buffer lv, 16 keys per product.
+template <int D>
+__device__ __forceinline__ void stage_pv(const uint16_t* lv, const int (&voff)[D / 32],
+                                         const f32x16 (&s)[2], RowState<D>& rs) {
+#pragma unroll
+  for (int sub = 0; sub < 2; ++sub) {
+    bf16x8 pb[2];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) pb[kb][e] = (__bf16)s[sub][8 * kb + e];
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db) {
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb) {
+        s16x4 piece[2];
+#pragma unroll
+        for (int rd = 0; rd < 2; ++rd)
+          piece[rd] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+              (__attribute__((address_space(3))) s16x4*)(lv + voff[db] +
+                                                         (sub * kSub + 16 * kb + 4 * rd) * D));
+        bf16x8 vf;
+        *reinterpret_cast<s16x4*>(&vf) = piece[0];
+        *(reinterpret_cast<s16x4*>(&vf) + 1) = piece[1];
+        rs.o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pb[kb], rs.o[db], 0, 0, 0);
+      }
+    }
   }
 }
 
 template <int D>
 __global__ __launch_bounds__(kWaves * 64, 2) void attn_kernel(AttnArgs a) {
-  __shared__ __attribute__((aligned(16))) uint16_t lk[2][kTile * D];
+  __shared__ __attribute__((aligned(16))) uint16_t lk[2][kTile * KLds<D>::kRow];
   __shared__ __attribute__((aligned(16))) uint16_t lv[2][kTile * D];
-  __shared__ int lim[2][kTile];
+  // codes of the slice's keys, then one need-mask flag per stage (dynamic:
+  // tiles_per_split * (kTile + 1) ints)
+  extern __shared__ int slice_lds[];
+  int* codes = slice_lds;
+  int* need_mask = slice_lds + a.tiles_per_split * kTile;
 
   // logical order (g, split, row block): blocks reading the same K/V tiles are
   // adjacent, hence on the same XCD and its L2
@@ -208,15 +309,14 @@ __global__ __launch_bounds__(kWaves * 64, 2) void attn_kernel(AttnArgs a) {
   const int t = row_ok ? row / a.G : -1;
   const int hi = row_ok ? row % a.G : 0;
 
-  // last query of the block bounds the suffix keys anyone here can see
+  // keys the block's last query can see; the block's first query sees every
+  // suffix key up to its own position
   const int first_t = (rb * kBlockRows) / a.G;
   const int last_row = min(a.R - 1, rb * kBlockRows + kBlockRows - 1);
   const int np_block = a.kc + last_row / a.G + 1;
   const int ntiles = (np_block + kTile - 1) / kTile;
   const int tile0 = split * a.tiles_per_split;
-  const int tile1 = min(ntiles, tile0 + a.tiles_per_split);
-  // prefix positions before vis_end are real tokens whatever chunks were kept
-  const int vis_end = a.kc - a.short_tail;
+  const int nt = max(0, min(ntiles, tile0 + a.tiles_per_split) - tile0);
 
   bf16x8 qf[D / 16];
   {
@@ -229,136 +329,73 @@ __global__ __launch_bounds__(kWaves * 64, 2) void attn_kernel(AttnArgs a) {
     }
   }
 
-  // per-lane LDS element offsets of the operand reads (the same for every stage)
-  const int krow = kappa(lane & 31);
-  int koff[D / 16];
+  // key codes of the slice, one stage per wave at a time, and whether a stage
+  // has a key some row of the block must not see; all index loads first
+  constexpr int kMaxIt = kMaxSliceKeys / kTile / kWaves;
+  int jv[kMaxIt], sv[kMaxIt];
 #pragma unroll
-  for (int ks = 0; ks < D / 16; ++ks) koff[ks] = k_off<D>(krow, 2 * ks + half);
-  const int s16 = lane & 15, g4 = (lane >> 4) & 1;
-  int voff[D / 32][2][2];
+  for (int it = 0; it < kMaxIt; ++it) {
+    const int st = wave + it * kWaves;
+    jv[it] = 0;
+    sv[it] = 0;
+    if (st < nt) key_chunk_loads(a, (tile0 + st) * kTile + lane, jv[it], sv[it]);
+  }
 #pragma unroll
-  for (int db = 0; db < D / 32; ++db)
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int rd = 0; rd < 2; ++rd) {
-        // V^T fragment piece: lane (group g4 = (lane/16)%2, s16 = lane%16) supplies
-        // row 16*kb + 8*half + 4*rd + s16/4, columns 32*db + 16*g4 + 4*(s16%4) .. +3
-        const int vrow = 16 * kb + 8 * half + 4 * rd + (s16 >> 2);
-        const int col = 32 * db + 16 * g4 + 4 * (s16 & 3);
-        voff[db][kb][rd] = v_off<D>(vrow, col >> 3) + (col & 7);
-      }
+  for (int it = 0; it < kMaxIt; ++it) {
+    const int st = wave + it * kWaves;
+    if (st >= nt) break;  // uniform
+    const int pos = (tile0 + st) * kTile + lane;
+    const int code = pos < np_block ? key_code(a, pos, jv[it], sv[it]) : kNoKey;
+    codes[st * kTile + lane] = code;
+    const bool vis_all = code >= 0 || (code <= -2 && -2 - code <= first_t);
+    const uint64_t bad = __ballot(!vis_all);
+    if (lane == 0) need_mask[st] = bad != 0;
+  }
+  __syncthreads();
 
-  f32x16 o[D / 32];
+  // per-lane LDS element offsets of the operand reads (the same for every stage)
+  const int kbase_off = kappa(lane & 31) * KLds<D>::kRow + 8 * half;
+  // V^T fragment pieces: lane (group g4 = (lane/16)%2, s16 = lane%16) supplies
+  // row 16*kb + 8*half + 4*rd + s16/4, columns 32*db + 16*g4 + 4*(s16%4) .. +3.
+  // The swizzle depends on the row modulo 4 only, so (kb, rd) add whole rows:
+  // voff[db] is the offset for kb = rd = 0 and the rest are immediate offsets.
+  const int s16 = lane & 15, g4 = (lane >> 4) & 1;
+  int voff[D / 32];
+#pragma unroll
+  for (int db = 0; db < D / 32; ++db) {
+    const int vrow = 8 * half + (s16 >> 2);
+    const int col = 32 * db + 16 * g4 + 4 * (s16 & 3);
+    voff[db] = v_off<D>(vrow, col >> 3) + (col & 7);
+  }
+
+  RowState<D> rs;
 #pragma unroll
   for (int db = 0; db < D / 32; ++db)
 #pragma unroll
-    for (int v = 0; v < 16; ++v) o[db][v] = 0.f;
-  float m_run = -INFINITY, l_run = 0.f;
+    for (int v = 0; v < 16; ++v) rs.o[db][v] = 0.f;
+  rs.m_run = -INFINITY;
+  rs.l_run = 0.f;
 
   TileRegs<D> regs;
-  TileIdx<D> idx_next;
-  if (tile0 < tile1) {
-    TileIdx<D> idx0;
-    tile_index<D>(a, tile0, idx0);
-    tile_load<D>(a, g, tile0, idx0, regs);
-    if (tile0 + 1 < tile1) tile_index<D>(a, tile0 + 1, idx_next);
-    tile_store<D>(regs, lk[0], lv[0], lim[0]);
+  if (nt > 0) {
+    tile_load<D, 0>(a, g, codes, regs);
+    tile_load<D, 1>(a, g, codes, regs);
+    tile_store<D>(regs, lk[0], lv[0]);
     __syncthreads();
   }
-  for (int tile = tile0; tile < tile1; ++tile) {
-    const int cur = (tile - tile0) & 1;
-    const bool has_next = tile + 1 < tile1;
+  for (int st = 0; st < nt; ++st) {
+    const int cur = st & 1;
+    const bool has_next = st + 1 < nt;
+    // the next stage's K/V rows load during this stage
     if (has_next) {
-      tile_load<D>(a, g, tile + 1, idx_next, regs);
-      if (tile + 2 < tile1) tile_index<D>(a, tile + 2, idx_next);
+      tile_load<D, 0>(a, g, codes + (st + 1) * kTile, regs);
+      tile_load<D, 1>(a, g, codes + (st + 1) * kTile, regs);
     }
-    // no key of this stage needs a mask for any row of the block when it ends
-    // before the kept prefix's possibly short tail, or when its suffix keys are
-    // seen by the block's first query and its prefix keys are all real tokens
-    const int pos0 = tile * kTile, pos_end = pos0 + kTile;
-    const bool all_vis = pos_end <= vis_end ||
-                         (pos_end <= a.kc + first_t + 1 && (pos0 >= a.kc || a.short_tail == 0));
-
-    // S^T for the two 32-key halves: two independent MFMA chains
     f32x16 s[2];
-#pragma unroll
-    for (int sub = 0; sub < 2; ++sub)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) s[sub][v] = 0.f;
-#pragma unroll
-    for (int ks = 0; ks < D / 16; ++ks) {
-#pragma unroll
-      for (int sub = 0; sub < 2; ++sub) {
-        bf16x8 kf = *reinterpret_cast<const bf16x8*>(&lk[cur][sub * kSub * D + koff[ks]]);
-        s[sub] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[ks], s[sub], 0, 0, 0);
-      }
-    }
-    // register v of half `sub` holds key 32*sub + 16*(v/8) + 8*half + v%8
-    if (!all_vis) {
-#pragma unroll
-      for (int sub = 0; sub < 2; ++sub)
-#pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          const int key = kSub * sub + 16 * (v >> 3) + 8 * half + (v & 7);
-          if (t < lim[cur][key]) s[sub][v] = -INFINITY;
-        }
-    }
-    float mx = fmaxf(s[0][0], s[1][0]);
-#pragma unroll
-    for (int v = 1; v < 16; ++v) mx = fmaxf(mx, fmaxf(s[0][v], s[1][v]));
-    mx = fmaxf(mx, partner_f(mx));
-    // The reference m_run only moves when the stage's maximum exceeds it by more
-    // than kLazy (log2 units): weights stay below 2^kLazy, numerator and
-    // denominator share the reference, and most stages skip the O rescale.
-    const float mt = mx * a.c1;
-    const float m_new = mt > m_run + kLazy ? mt : m_run;
-    const float m_use = m_new == -INFINITY ? 0.f : m_new;
-    const float alpha = __builtin_amdgcn_exp2f(m_run - m_use);
-    float rs = 0.f;
-#pragma unroll
-    for (int sub = 0; sub < 2; ++sub)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        s[sub][v] = __builtin_amdgcn_exp2f(fmaf(s[sub][v], a.c1, -m_use));
-        rs += s[sub][v];
-      }
-    rs += partner_f(rs);
-    l_run = l_run * alpha + rs;
-    m_run = m_new;
-    if (__any(alpha != 1.f)) {
-#pragma unroll
-      for (int db = 0; db < D / 32; ++db)
-#pragma unroll
-        for (int v = 0; v < 16; ++v) o[db][v] *= alpha;
-    }
-
-    // O^T += V^T P^T, 16 keys per product
-#pragma unroll
-    for (int sub = 0; sub < 2; ++sub) {
-      bf16x8 pb[2];
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int e = 0; e < 8; ++e) pb[kb][e] = (__bf16)s[sub][8 * kb + e];
-#pragma unroll
-      for (int db = 0; db < D / 32; ++db) {
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb) {
-          s16x4 piece[2];
-#pragma unroll
-          for (int rd = 0; rd < 2; ++rd)
-            piece[rd] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-                (__attribute__((address_space(3))) s16x4*)(&lv[cur][sub * kSub * D + voff[db][kb][rd]]));
-          bf16x8 vf;
-          *reinterpret_cast<s16x4*>(&vf) = piece[0];
-          *(reinterpret_cast<s16x4*>(&vf) + 1) = piece[1];
-          o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pb[kb], o[db], 0, 0, 0);
-        }
-      }
-    }
+    stage_softmax<D>(a, lk[cur], codes + st * kTile, need_mask[st], t, kbase_off, qf, rs, s);
+    stage_pv<D>(lv[cur], voff, s, rs);
     if (has_next) {
-      tile_store<D>(regs, lk[cur ^ 1], lv[cur ^ 1], lim[cur ^ 1]);
+      tile_store<D>(regs, lk[cur ^ 1], lv[cur ^ 1]);
       __syncthreads();
     }
   }
@@ -366,7 +403,7 @@ __global__ __launch_bounds__(kWaves * 64, 2) void attn_kernel(AttnArgs a) {
   // o[db][v] holds d = 32*db + 8*(v/4) + 4*half + v%4 of this lane's row
   if (!row_ok) return;
   if (a.n_splits == 1) {
-    const float inv = 1.f / l_run;
+    const float inv = 1.f / rs.l_run;
     uint16_t* dst = a.out + ((int64_t)t * a.Hq + (int64_t)g * a.G + hi) * D + 4 * half;
 #pragma unroll
     for (int db = 0; db < D / 32; ++db)
@@ -374,30 +411,33 @@ __global__ __launch_bounds__(kWaves * 64, 2) void attn_kernel(AttnArgs a) {
       for (int q4 = 0; q4 < 4; ++q4) {
         __bf16 b[4];
 #pragma unroll
-        for (int j = 0; j < 4; ++j) b[j] = (__bf16)(o[db][4 * q4 + j] * inv);
+        for (int j = 0; j < 4; ++j) b[j] = (__bf16)(rs.o[db][4 * q4 + j] * inv);
         *reinterpret_cast<uint2*>(dst + 32 * db + 8 * q4) = *reinterpret_cast<uint2*>(b);
       }
   } else {
     const int64_t prow = ((int64_t)split * a.Hkv + g) * a.R + row;
     uint16_t* dst = a.o_part + prow * D + 4 * half;
-    const float inv = l_run > 0.f ? 1.f / l_run : 0.f;
+    const float inv = rs.l_run > 0.f ? 1.f / rs.l_run : 0.f;
 #pragma unroll
     for (int db = 0; db < D / 32; ++db)
 #pragma unroll
       for (int q4 = 0; q4 < 4; ++q4) {
         __bf16 b[4];
 #pragma unroll
-        for (int j = 0; j < 4; ++j) b[j] = (__bf16)(o[db][4 * q4 + j] * inv);
+        for (int j = 0; j < 4; ++j) b[j] = (__bf16)(rs.o[db][4 * q4 + j] * inv);
         *reinterpret_cast<uint2*>(dst + 32 * db + 8 * q4) = *reinterpret_cast<uint2*>(b);
       }
     // the reference the numerators were taken against (0 while no key was seen)
-    if (half == 0) a.ml_part[prow] = make_float2(m_run == -INFINITY ? 0.f : m_run, l_run);
+    if (half == 0) a.ml_part[prow] = make_float2(rs.m_run == -INFINITY ? 0.f : rs.m_run, rs.l_run);
   }
 }
 
 // Merges the splits of each row in split order: out = sum_s w_s Ohat_s with
-// w_s = e_s l_s / sum_s e_s l_s, e_s = exp2(m_s - max m), Ohat_s = O_s / l_s.
-// One thread per (row, 8 columns).
+// w_s = e_s l_s / sum_s e_s l_s, e_s = exp2(m_s - max m), Ohat_s = O_s / l_s,
+// as a running merge over batches of kCombineBatch splits whose loads are in
+// flight together.  One thread per (row, 8 columns).
+constexpr int kCombineBatch = 8;
+
 template <int D>
 __global__ __launch_bounds__(256) void combine_kernel(const uint16_t* __restrict__ o_part,
                                                       const float2* __restrict__ ml_part,
@@ -408,22 +448,36 @@ __global__ __launch_bounds__(256) void combine_kernel(const uint16_t* __restrict
   if (idx >= rows * (D / 8)) return;
   const int64_t grow = idx / (D / 8);
   const int c8 = (int)(idx % (D / 8)) * 8;
-  float M = -INFINITY;
-  for (int s = 0; s < n_splits; ++s) {
-    const float2 ml = ml_part[s * rows + grow];
-    if (ml.y > 0.f) M = fmaxf(M, ml.x);
-  }
+  float M = -INFINITY, Lsum = 0.f;
   float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-  float Lsum = 0.f;
-  for (int s = 0; s < n_splits; ++s) {
-    const float2 ml = ml_part[s * rows + grow];
-    if (!(ml.y > 0.f)) continue;  // the split saw no key of this row
-    const float wgt = __builtin_amdgcn_exp2f(ml.x - M) * ml.y;
-    Lsum += wgt;
-    const uint4 raw = *reinterpret_cast<const uint4*>(o_part + (s * rows + grow) * D + c8);
-    const __bf16* h = reinterpret_cast<const __bf16*>(&raw);
+  for (int s0 = 0; s0 < n_splits; s0 += kCombineBatch) {
+    float2 ml[kCombineBatch];
+    uint4 raw[kCombineBatch];
 #pragma unroll
-    for (int j = 0; j < 8; ++j) acc[j] += wgt * (float)h[j];
+    for (int i = 0; i < kCombineBatch; ++i) {
+      if (s0 + i < n_splits) {
+        ml[i] = ml_part[(s0 + i) * rows + grow];
+        raw[i] = *reinterpret_cast<const uint4*>(o_part + ((s0 + i) * rows + grow) * D + c8);
+      } else {
+        ml[i] = make_float2(0.f, 0.f);
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < kCombineBatch; ++i) {
+      if (!(ml[i].y > 0.f)) continue;  // absent, or the split saw no key of this row
+      if (ml[i].x > M) {
+        const float scale = M == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(M - ml[i].x);
+        Lsum *= scale;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) acc[j] *= scale;
+        M = ml[i].x;
+      }
+      const float wgt = __builtin_amdgcn_exp2f(ml[i].x - M) * ml[i].y;
+      Lsum += wgt;
+      const __bf16* h = reinterpret_cast<const __bf16*>(&raw[i]);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) acc[j] += wgt * (float)h[j];
+    }
   }
   const int g = (int)(grow / R), row = (int)(grow % R);
   const int t = row / G, i = row % G;
@@ -530,10 +584,12 @@ AttnPlan make_attn_plan(const ckv_dims* d, int64_t k) {
   const int64_t np = k * d->chunk_size + d->n_suffix;
   const int64_t ntiles = ceil_div(np, kTile);
   const int64_t base = (int64_t)d->n_kv_heads * ceil_div(p.rows, kBlockRows);
-  // at most ~2 workgroups per CU, keeping >= 4 stages per split; then the
-  // fewest splits that give the same stages per split
+  // at most ~2 workgroups per CU, keeping >= 4 stages per split and no more
+  // keys per split than the workgroup's code table holds; then the fewest
+  // splits that give the same stages per split
   int64_t splits = std::max<int64_t>(1, 512 / base);
   splits = std::min<int64_t>(splits, std::max<int64_t>(1, ntiles / 4));
+  splits = std::max<int64_t>(splits, ceil_div(ntiles, kMaxSliceKeys / kTile));
   splits = ceil_div(ntiles, ceil_div(ntiles, splits));
   p.n_splits = (int32_t)splits;
   size_t off = 0;
@@ -579,15 +635,23 @@ ckv_status launch_attn(const ckv_dims* d, const void* q, const ChunkSource& src,
   a.q = static_cast<const uint16_t*>(q);
   a.kbase = static_cast<const uint16_t*>(src.k_base);
   a.vbase = static_cast<const uint16_t*>(src.v_base);
-  a.chunk_stride = src.chunk_stride;
   a.chunk_off = src.chunk_off;
   a.direct = src.direct;
+  {
+    const int64_t hd = (int64_t)d->n_kv_heads * d->head_dim;
+    if (src.chunk_stride % hd != 0) CKV_FAIL(CKV_EINVAL, "chunk stride is not a whole number of rows");
+    const int64_t rps = src.chunk_stride / hd;
+    // largest source row a key can name: every slot index is below max(m, 2k)
+    const int64_t slots = std::max<int64_t>(ceil_div(d->n_prefix, d->chunk_size), 2 * k);
+    if (slots * rps >= (int64_t(1) << 31)) CKV_FAIL(CKV_EUNSUPPORTED, "chunk source too large");
+    a.rows_per_slot = (int)rps;
+  }
   a.sel = sel;
   a.kc = (int)(k * d->chunk_size);
   a.n = d->n_prefix;
+  a.m = ceil_div(d->n_prefix, d->chunk_size);
   a.c = d->chunk_size;
   a.log2c = (d->chunk_size & (d->chunk_size - 1)) == 0 ? __builtin_ctz(d->chunk_size) : -1;
-  a.short_tail = d->n_prefix % d->chunk_size ? (int)(d->chunk_size - d->n_prefix % d->chunk_size) : 0;
   a.ks = static_cast<const uint16_t*>(k_suffix);
   a.vs = static_cast<const uint16_t*>(v_suffix);
   a.out = static_cast<uint16_t*>(out);
@@ -597,15 +661,16 @@ ckv_status launch_attn(const ckv_dims* d, const void* q, const ChunkSource& src,
   a.G = d->n_q_heads / d->n_kv_heads; a.R = p.rows;
   a.n_splits = p.n_splits;
   const int64_t ntiles = ceil_div(a.kc + a.S, kTile);
-  a.tiles_per_split = (int)ceil_div(ntiles, p.n_splits);
+  a.tiles_per_split = (int)ceil_div(ntiles, p.n_splits);  // <= kMaxSliceKeys / kTile
   a.n_row_blocks = (int)ceil_div(p.rows, kBlockRows);
   a.c1 = resolve_scale(d) * 1.4426950408889634f;
   a.nblocks = (uint32_t)((int64_t)a.Hkv * a.n_row_blocks * a.n_splits);
   a.nblocks_padded = (uint32_t)align_up(a.nblocks, 8);
+  const size_t slice_bytes = (size_t)a.tiles_per_split * (kTile + 1) * sizeof(int);
   if (d->head_dim == 128)
-    hipLaunchKernelGGL(attn_kernel<128>, dim3(a.nblocks_padded), dim3(kWaves * 64), 0, st, a);
+    hipLaunchKernelGGL(attn_kernel<128>, dim3(a.nblocks_padded), dim3(kWaves * 64), slice_bytes, st, a);
   else
-    hipLaunchKernelGGL(attn_kernel<64>, dim3(a.nblocks_padded), dim3(kWaves * 64), 0, st, a);
+    hipLaunchKernelGGL(attn_kernel<64>, dim3(a.nblocks_padded), dim3(kWaves * 64), slice_bytes, st, a);
   CKV_HIP(hipGetLastError());
   if (p.n_splits > 1) {
     const int64_t work = (int64_t)a.Hkv * a.R * (d->head_dim / 8);

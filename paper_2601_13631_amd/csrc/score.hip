@@ -576,19 +576,27 @@ __device__ __forceinline__ void store_stats(const ScoreArgs& a, int rbh, int s, 
   a.z[o] = st.zsum;
 }
 
-// Workgroup w runs segment s = w % NS of rbh = w / NS: keys kbeg .. kbeg+nkeys-1.
+// Segment s of row block rbh: keys kbeg .. kbeg+nkeys-1.
 struct Segment {
   int rbh, s;
   int64_t kbeg;
   int nkeys;
 };
-__device__ __forceinline__ Segment segment_of(const ScoreWork& wk, int64_t n, int w) {
+__device__ __forceinline__ Segment segment_at(const ScoreWork& wk, int64_t n, int rbh, int s) {
   Segment g;
-  g.rbh = w / wk.NS;
-  g.s = w % wk.NS;
-  g.kbeg = (int64_t)wk.seg_begin(g.s) * wk.UK;
-  g.nkeys = (int)(min<int64_t>((int64_t)wk.seg_begin(g.s + 1) * wk.UK, n) - g.kbeg);
+  g.rbh = rbh;
+  g.s = s;
+  g.kbeg = (int64_t)wk.seg_begin(s) * wk.UK;
+  g.nkeys = (int)(min<int64_t>((int64_t)wk.seg_begin(s + 1) * wk.UK, n) - g.kbeg);
   return g;
+}
+
+// Workgroup w (logical) runs row block rb of KV head g at segment s, with rb
+// varying fastest: the workgroups that read the same keys are adjacent, hence
+// on the same XCD and its L2.
+__device__ __forceinline__ Segment segment_of(const ScoreWork& wk, int64_t n, int w) {
+  const int rb = w % wk.RB, s = (w / wk.RB) % wk.NS, g = w / (wk.RB * wk.NS);
+  return segment_at(wk, n, g * wk.RB + rb, s);
 }
 
 // Fold of the segments of row block rbh: thread t owns row t of the block
@@ -655,7 +663,7 @@ __global__ __launch_bounds__(kWaves * 64, 2) void score_bf16_kernel(ScoreArgs a)
   RangeState st;
   const bool of = run_segment_fast<D, MODE>(a, g, sg.kbeg, sg.nkeys, row0, qf, lds, st);
   const int any_of = __syncthreads_or(of ? 1 : 0);
-  if (threadIdx.x == 0) a.flags[w] = any_of;
+  if (threadIdx.x == 0) a.flags[sg.rbh * a.w.NS + sg.s] = any_of;
   store_stats(a, sg.rbh, sg.s, st);
 }
 
@@ -673,7 +681,7 @@ __global__ __launch_bounds__(kWaves * 64) void score_fold_kernel(ScoreArgs a) {
   if (__syncthreads_or(any)) {
     for (int s = 0; s < a.w.NS; ++s) {
       if (!a.flags[rbh * a.w.NS + s]) continue;  // uniform
-      const Segment o = segment_of(a.w, a.n, rbh * a.w.NS + s);
+      const Segment o = segment_at(a.w, a.n, rbh, s);
       bf16x8 qf[2][D / 16];
       load_q<D>(a, g, row0, qf);
       RangeState st;

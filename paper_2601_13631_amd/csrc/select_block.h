@@ -1,6 +1,6 @@
 // select_block.h -- top-k ContiguousChunk selection (Sec. 4.4) by one
-// workgroup of kSelThreads threads (a device function, so that any kernel can
-// end with a selection).
+// workgroup of THREADS threads (a multiple of 64; one wave suits small m, where
+// the workgroup barriers then cost almost nothing).
 //
 // Keeps the k largest of m fp64 chunk scores under the total order (score
 // descending, index ascending) and writes their indices in ascending order.
@@ -23,8 +23,7 @@
 
 namespace ckv {
 
-constexpr int kSelThreads = 256;
-constexpr int kSelWaves = kSelThreads / 64;
+constexpr int kSelMaxWaves = 4;
 
 __device__ __forceinline__ uint64_t order_key(double x) {
   uint64_t u = (uint64_t)__double_as_longlong(x);
@@ -37,15 +36,16 @@ __device__ __forceinline__ uint64_t order_key(double x) {
 struct SelShared {
   uint32_t hist[256];
   unsigned long long bmin[256], bmax[256];
-  uint32_t wsum[kSelWaves];
-  uint64_t red_lo[kSelWaves], red_hi[kSelWaves];
-  int64_t red_i[kSelWaves];
+  uint32_t wsum[4];
+  uint64_t red_lo[kSelMaxWaves], red_hi[kSelMaxWaves];
+  int64_t red_i[kSelMaxWaves];
   uint64_t prefix, mask, lo, hi;
   int64_t remaining;
   int done;
 };
 
 // Block-wide minimum of lo and maximum of hi, left in sh.lo / sh.hi.
+template <int THREADS>
 __device__ __forceinline__ void sel_block_minmax(uint64_t lo, uint64_t hi, SelShared& sh) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
 #pragma unroll
@@ -57,7 +57,7 @@ __device__ __forceinline__ void sel_block_minmax(uint64_t lo, uint64_t hi, SelSh
   if (lane == 0) { sh.red_lo[wave] = lo; sh.red_hi[wave] = hi; }
   __syncthreads();
   if (threadIdx.x == 0) {
-    for (int w = 1; w < kSelWaves; ++w) {
+    for (int w = 1; w < THREADS / 64; ++w) {
       lo = sh.red_lo[w] < lo ? sh.red_lo[w] : lo;
       hi = sh.red_hi[w] > hi ? sh.red_hi[w] : hi;
     }
@@ -68,6 +68,7 @@ __device__ __forceinline__ void sel_block_minmax(uint64_t lo, uint64_t hi, SelSh
 }
 
 // Exclusive prefix sum over the block (this thread's exclusive prefix).
+template <int THREADS>
 __device__ __forceinline__ int64_t sel_block_exclusive_scan(int64_t v, SelShared& sh) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   int64_t x = v;
@@ -84,21 +85,23 @@ __device__ __forceinline__ int64_t sel_block_exclusive_scan(int64_t v, SelShared
   return before + x - v;
 }
 
-// Called by all kSelThreads threads of the workgroup; 1 <= k <= m.  cache:
+// Called by all THREADS threads of the workgroup; 1 <= k <= m.  cache:
 // nullptr, or LDS room for m keys.
+template <int THREADS>
 __device__ __forceinline__ void select_topk_block(const double* scores, int64_t m, int64_t k,
                                                   int32_t* sel, SelShared& sh, uint64_t* cache) {
+  static_assert(THREADS % 64 == 0 && THREADS <= 64 * kSelMaxWaves, "1 to 4 waves");
   const int tid = threadIdx.x;
   auto key_at = [&](int64_t i) -> uint64_t { return cache ? cache[i] : order_key(scores[i]); };
   {
     uint64_t lo = ~0ull, hi = 0;
-    for (int64_t i = tid; i < m; i += kSelThreads) {
+    for (int64_t i = tid; i < m; i += THREADS) {
       const uint64_t x = order_key(scores[i]);
       if (cache) cache[i] = x;
       lo = x < lo ? x : lo;
       hi = x > hi ? x : hi;
     }
-    sel_block_minmax(lo, hi, sh);  // its barriers also publish the cache
+    sel_block_minmax<THREADS>(lo, hi, sh);  // its barriers also publish the cache
   }
   if (tid == 0) {
     sh.prefix = 0;
@@ -117,13 +120,13 @@ __device__ __forceinline__ void select_topk_block(const double* scores, int64_t 
     }
     const int top = 63 - __clzll(lo ^ hi);
     const int shift = top >= 7 ? top - 7 : 0;
-    for (int b = tid; b < 256; b += kSelThreads) {
+    for (int b = tid; b < 256; b += THREADS) {
       sh.hist[b] = 0;
       sh.bmin[b] = ~0ull;
       sh.bmax[b] = 0;
     }
     __syncthreads();
-    for (int64_t i = tid; i < m; i += kSelThreads) {
+    for (int64_t i = tid; i < m; i += THREADS) {
       const uint64_t x = key_at(i);
       if ((x & mask) == prefix) {
         const int b = (int)((x >> shift) & 255);
@@ -133,34 +136,44 @@ __device__ __forceinline__ void select_topk_block(const double* scores, int64_t 
       }
     }
     __syncthreads();
-    // count of candidates in bins >= b as an inclusive scan over t = 255 - b;
-    // the bin where that count first reaches `need` is chosen (one thread)
+    // count of candidates in bins >= b as an inclusive scan over t = 255 - b
+    // (thread i holds t = i*kPer .. i*kPer+kPer-1); the bin where that count
+    // first reaches `need` is chosen (one thread)
+    constexpr int kPer = 256 / THREADS;
     const int64_t need = sh.remaining;
-    uint32_t cum = 0, mine = 0;
-    if (tid < 256) {
-      mine = sh.hist[255 - tid];
-      cum = mine;
+    uint32_t cnt[kPer];
+    uint32_t own = 0;
 #pragma unroll
-      for (int off = 1; off < 64; off <<= 1) {
-        const uint32_t y = __shfl_up(cum, off);
-        if ((tid & 63) >= off) cum += y;
-      }
-      if ((tid & 63) == 63) sh.wsum[tid >> 6] = cum;
+    for (int q = 0; q < kPer; ++q) {
+      cnt[q] = sh.hist[255 - (tid * kPer + q)];
+      own += cnt[q];
     }
-    __syncthreads();
-    if (tid < 256) {
+    uint32_t cum = own;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+      const uint32_t y = __shfl_up(cum, off);
+      if ((tid & 63) >= off) cum += y;
+    }
+    if (THREADS > 64) {
+      if ((tid & 63) == 63) sh.wsum[tid >> 6] = cum;
+      __syncthreads();
       for (int w = 0; w < (tid >> 6); ++w) cum += sh.wsum[w];
-      const uint32_t before = cum - mine;
-      if (before < need && cum >= need) {
-        const int b = 255 - tid;
+    }
+    uint32_t before = cum - own;
+#pragma unroll
+    for (int q = 0; q < kPer; ++q) {
+      const uint32_t after = before + cnt[q];
+      if (before < need && after >= need) {
+        const int b = 255 - (tid * kPer + q);
         const uint64_t keep_hi = shift + 8 >= 64 ? 0 : ~((1ull << (shift + 8)) - 1);
         sh.prefix = (lo & keep_hi) | ((uint64_t)b << shift);
         sh.mask = keep_hi | (255ull << shift);
         sh.remaining = need - before;
-        sh.done = (mine == (uint32_t)sh.remaining) || shift == 0;
+        sh.done = (cnt[q] == (uint32_t)sh.remaining) || shift == 0;
         sh.lo = sh.bmin[b];
         sh.hi = sh.bmax[b];
       }
+      before = after;
     }
     __syncthreads();
     if (sh.done) break;
@@ -170,7 +183,7 @@ __device__ __forceinline__ void select_topk_block(const double* scores, int64_t 
   // the first `remaining` equal keys by index
   const uint64_t prefix = sh.prefix, mask = sh.mask;
   const int64_t remaining = sh.remaining;
-  const int64_t per = (m + kSelThreads - 1) / kSelThreads;
+  const int64_t per = (m + THREADS - 1) / THREADS;
   const int64_t i0 = min(m, (int64_t)tid * per), i1 = min(m, i0 + per);
   int64_t n_gt = 0, n_eq = 0;
   for (int64_t i = i0; i < i1; ++i) {
@@ -178,8 +191,8 @@ __device__ __forceinline__ void select_topk_block(const double* scores, int64_t 
     n_gt += x > prefix;
     n_eq += x == prefix;
   }
-  const int64_t gt_before = sel_block_exclusive_scan(n_gt, sh);
-  const int64_t eq_before = sel_block_exclusive_scan(n_eq, sh);
+  const int64_t gt_before = sel_block_exclusive_scan<THREADS>(n_gt, sh);
+  const int64_t eq_before = sel_block_exclusive_scan<THREADS>(n_eq, sh);
   int64_t eq_rank = eq_before;
   int64_t pos = gt_before + min(eq_before, remaining);
   for (int64_t i = i0; i < i1; ++i) {
