@@ -372,21 +372,25 @@ __device__ __forceinline__ void process_subtile(const ScoreArgs& a, const bf16x8
 // interleaves the two), and the last subtile's VALU work is carried over the
 // stage barrier into the next stage.
 
-// All 16 MFMAs of one subtile (both row tiles share each K fragment).
+// All 16 MFMAs of one subtile (both row tiles share each K fragment).  All
+// fragments are read first, so only the first MFMA waits on LDS latency.
 template <int D>
 __device__ __forceinline__ void mfma_subtile(const uint16_t* lds, int lrow0,
                                              const bf16x8 (&qf)[2][D / 16], f32x16 (&acc)[2]) {
   const int lane = threadIdx.x & 63, half = lane >> 5;
+  bf16x8 kf[D / 16];
+#pragma unroll
+  for (int ks = 0; ks < D / 16; ++ks)
+    kf[ks] = *reinterpret_cast<const bf16x8*>(
+        lds + SubtileLds<D>::offset(lrow0 + (lane & 31), 2 * ks + half));
 #pragma unroll
   for (int rt = 0; rt < 2; ++rt)
 #pragma unroll
     for (int v = 0; v < 16; ++v) acc[rt][v] = 0.f;
 #pragma unroll
   for (int ks = 0; ks < D / 16; ++ks) {
-    const bf16x8 kf = *reinterpret_cast<const bf16x8*>(
-        lds + SubtileLds<D>::offset(lrow0 + (lane & 31), 2 * ks + half));
-    acc[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[0][ks], acc[0], 0, 0, 0);
-    acc[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[1][ks], acc[1], 0, 0, 0);
+    acc[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[ks], qf[0][ks], acc[0], 0, 0, 0);
+    acc[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[ks], qf[1][ks], acc[1], 0, 0, 0);
   }
 }
 
