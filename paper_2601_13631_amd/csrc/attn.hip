@@ -35,10 +35,15 @@ constexpr int kWaveRows = 32;
 constexpr int kBlockRows = kWaves * kWaveRows;  // 128
 constexpr int kTile = 64;                       // keys per LDS stage
 constexpr int kSub = 32;                        // keys per MFMA product
-constexpr int kMaxSliceKeys = 2048;             // key codes per workgroup slice (8 KiB)
+constexpr int kMaxSliceKeys = 1024;             // keys per workgroup slice (8 KiB of key tables)
 constexpr float kLazy = 8.f;                    // headroom of the lazy softmax reference (log2 units)
-// key codes: >= 0 row of the prefix K/V source, -1 no key, <= -2 suffix token -2-code
-constexpr int kNoKey = -1;
+// Key tables: for every key of a slice, the row of its K/V source and its
+// visibility threshold -- a query t sees the key iff t >= thr.  thr = -1 marks
+// a row of the prefix source (seen by every query); a suffix token p has
+// thr = p (causal) and a row of the suffix source; a padding key has
+// thr = kNever and suffix row 0 (always present; its weight is forced to 0).
+constexpr int kPrefix = -1;
+constexpr int kNever = 0x7fffffff;
 
 // MFMA row p of the K operand holds key kappa(p); afterwards register v of a
 // lane in half h holds key 16*(v/8) + 8*h + v%8.
@@ -95,12 +100,12 @@ struct AttnArgs {
   uint32_t nblocks, nblocks_padded;
 };
 
-// Source code of compact key position pos (see kNoKey), in two steps so that
-// a workgroup can issue all its index loads before using any: key_chunk_loads
-// fetches sel[u] (and the slot table entry) of the key's chunk u, key_code
-// finishes.  Row off of kept chunk u sits at source row slot*rows_per_slot +
-// off, slot = chunk_off[u] (slot table), sel[u] (spans read in place) or u
-// (compact copy).
+// Table entries of compact key position pos, in two steps so that a workgroup
+// can issue all its index loads before using any: key_chunk_loads fetches
+// sel[u] (and the slot table entry) of the key's chunk u, key_entry finishes.
+// Row off of kept chunk u sits at source row slot*rows_per_slot + off, slot =
+// chunk_off[u] (slot table), sel[u] (spans read in place) or u (compact
+// copy).
 __device__ __forceinline__ int chunk_of(const AttnArgs& a, int pos) {
   return a.log2c >= 0 ? (pos >> a.log2c) : (int)((uint32_t)pos / (uint32_t)a.c);
 }
@@ -115,52 +120,70 @@ __device__ __forceinline__ void key_chunk_loads(const AttnArgs& a, int pos, int&
   }
 }
 
-__device__ __forceinline__ int key_code(const AttnArgs& a, int pos, int j, int slot_tab) {
+__device__ __forceinline__ void key_entry(const AttnArgs& a, int pos, int j, int slot_tab, int& row,
+                                          int& thr) {
+  row = 0;
+  thr = kNever;
   if (pos < a.kc) {
     const int u = chunk_of(a, pos);
     const int off = pos - u * a.c;
-    if (j < 0 || (int64_t)j >= a.m) return kNoKey;
-    if ((int64_t)j * a.c + off >= a.n) return kNoKey;  // past n in a short last chunk
+    if (j < 0 || (int64_t)j >= a.m) return;
+    if ((int64_t)j * a.c + off >= a.n) return;  // past n in a short last chunk
     const int slot = a.chunk_off ? slot_tab : (a.direct ? j : u);
-    return slot * a.rows_per_slot + off;
+    row = slot * a.rows_per_slot + off;
+    thr = kPrefix;
+  } else if (pos < a.kc + a.S) {
+    row = pos - a.kc;
+    thr = row;
   }
-  if (pos < a.kc + a.S) return -2 - (pos - a.kc);
-  return kNoKey;
 }
 
 // The K/V rows of one 64-key stage, fetched into registers (while the previous
-// stage is consumed from LDS) and then written to the other LDS buffer.  A
-// masked key reads suffix row 0 of this KV head (always present; its weight is
-// forced to zero).
+// stage is consumed from LDS) and then written to the other LDS buffer.  Each
+// thread moves kPer 16-byte pieces of K and of V: piece p is segment tid %
+// kSegs of key tid / kSegs + p * kKeyStep.
 template <int D>
 struct TileRegs {
-  static constexpr int kPer = kTile * (D / 8) / (kWaves * 64);  // 16-byte pieces per thread
+  static constexpr int kSegs = D / 8;
+  static constexpr int kPer = kTile * kSegs / (kWaves * 64);  // 16-byte pieces per thread
+  static constexpr int kKeyStep = kWaves * 64 / kSegs;
   u32x4 k[kPer], v[kPer];
 };
 
-// Rows of the stage's keys for K (KV = 0) or V (KV = 1).
-template <int D, int KV>
-__device__ __forceinline__ void tile_load(const AttnArgs& a, int g, const int* codes, TileRegs<D>& r) {
-  constexpr int kSegs = D / 8;
-  const int64_t hd = (int64_t)a.Hkv * D;
+// The table entries of this thread's keys of one stage (read one stage ahead,
+// so the row loads never wait on LDS).
+template <int D>
+struct TileKeys {
+  int row[TileRegs<D>::kPer], thr[TileRegs<D>::kPer];
+};
+
+template <int D>
+__device__ __forceinline__ void tile_keys(const int* rows, const int* thrs, TileKeys<D>& tk) {
+  const int key0 = threadIdx.x / TileRegs<D>::kSegs;
 #pragma unroll
   for (int p = 0; p < TileRegs<D>::kPer; ++p) {
-    const int idx = threadIdx.x + p * kWaves * 64;
-    const int key = idx / kSegs, seg = idx % kSegs;
-    const int code = codes[key];
-    const bool pre = code >= 0;
-    const int row = pre ? code : (code <= -2 ? -2 - code : 0);
-    const int64_t e = row * hd + (g * D + seg * 8);
-    if constexpr (KV == 0)
-      r.k[p] = *reinterpret_cast<const u32x4*>((pre ? a.kbase : a.ks) + e);
-    else
-      r.v[p] = *reinterpret_cast<const u32x4*>((pre ? a.vbase : a.vs) + e);
+    tk.row[p] = rows[key0 + p * TileRegs<D>::kKeyStep];
+    tk.thr[p] = thrs[key0 + p * TileRegs<D>::kKeyStep];
+  }
+}
+
+template <int D>
+__device__ __forceinline__ void tile_load(const AttnArgs& a, int g, const TileKeys<D>& tk,
+                                          TileRegs<D>& r) {
+  const uint32_t hd = (uint32_t)(a.Hkv * D);
+  const uint64_t col = (uint64_t)(g * D + (threadIdx.x % TileRegs<D>::kSegs) * 8);
+#pragma unroll
+  for (int p = 0; p < TileRegs<D>::kPer; ++p) {
+    const uint64_t e = (uint64_t)(uint32_t)tk.row[p] * hd + col;
+    const bool pre = tk.thr[p] == kPrefix;
+    r.k[p] = *reinterpret_cast<const u32x4*>((pre ? a.kbase : a.ks) + e);
+    r.v[p] = *reinterpret_cast<const u32x4*>((pre ? a.vbase : a.vs) + e);
   }
 }
 
 template <int D>
 __device__ __forceinline__ void tile_store(const TileRegs<D>& r, uint16_t* lk, uint16_t* lv) {
-  constexpr int kSegs = D / 8;
+  constexpr int kSegs = TileRegs<D>::kSegs;
 #pragma unroll
   for (int p = 0; p < TileRegs<D>::kPer; ++p) {
     const int idx = threadIdx.x + p * kWaves * 64;
@@ -197,37 +220,42 @@ __device__ __forceinline__ void stage_logits(const uint16_t* lk, int kbase_off,
   }
 }
 
-// Logits of one stage with the masked keys at -inf.
+// Logits of one stage with the keys this lane's query must not see at -inf.
 template <int D>
 __device__ __forceinline__ void stage_masked_logits(const uint16_t* lk, int kbase_off,
-                                                    const bf16x8 (&qf)[D / 16], const int* codes,
+                                                    const bf16x8 (&qf)[D / 16], const int* thrs,
                                                     bool need_mask, int t, f32x16 (&s)[2]) {
   const int half = (threadIdx.x >> 5) & 1;
   stage_logits<D>(lk, kbase_off, qf, s);
-  // register v of product `sub` holds key 32*sub + 16*(v/8) + 8*half + v%8
+  // register v of product `sub` holds key 32*sub + 16*(v/8) + 8*half + v%8:
+  // runs of 8 consecutive keys, read as two 16-byte words each
   if (need_mask) {
 #pragma unroll
     for (int sub = 0; sub < 2; ++sub)
 #pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int code = codes[kSub * sub + 16 * (v >> 3) + 8 * half + (v & 7)];
-        const bool vis = code >= 0 || (code <= -2 && t >= -2 - code);
-        if (!vis) s[sub][v] = -INFINITY;
+      for (int v8 = 0; v8 < 2; ++v8) {
+        const int* tp = thrs + kSub * sub + 16 * v8 + 8 * half;
+        const int4 t0 = *reinterpret_cast<const int4*>(tp);
+        const int4 t1 = *reinterpret_cast<const int4*>(tp + 4);
+        const int th[8] = {t0.x, t0.y, t0.z, t0.w, t1.x, t1.y, t1.z, t1.w};
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          if (t < th[e]) s[sub][8 * v8 + e] = -INFINITY;
       }
   }
 }
 
-// Softmax part of one 64-key stage from the K buffer lk whose codes are
-// `codes`: numerators into s.  The reference moves only when the stage's
+// Softmax part of one 64-key stage from the K buffer lk whose visibility
+// thresholds are `thrs`: numerators into s.  The reference moves only when the stage's
 // maximum exceeds it by more than kLazy (log2 units): numerators stay below
 // 2^kLazy, numerator and denominator share the reference, and most stages skip
 // the O rescale.
 template <int D>
-__device__ __forceinline__ void stage_softmax(const AttnArgs& a, const uint16_t* lk, const int* codes,
+__device__ __forceinline__ void stage_softmax(const AttnArgs& a, const uint16_t* lk, const int* thrs,
                                               bool need_mask, int t, int kbase_off,
                                               const bf16x8 (&qf)[D / 16], RowState<D>& rs,
                                               f32x16 (&s)[2]) {
-  stage_masked_logits<D>(lk, kbase_off, qf, codes, need_mask, t, s);
+  stage_masked_logits<D>(lk, kbase_off, qf, thrs, need_mask, t, s);
   float mx = fmaxf(s[0][0], s[1][0]);
 #pragma unroll
   for (int v = 1; v < 16; ++v) mx = fmaxf(mx, fmaxf(s[0][v], s[1][v]));
@@ -289,11 +317,12 @@ template <int D>
 __global__ __launch_bounds__(kWaves * 64, 2) void attn_kernel(AttnArgs a) {
   __shared__ __attribute__((aligned(16))) uint16_t lk[2][kTile * KLds<D>::kRow];
   __shared__ __attribute__((aligned(16))) uint16_t lv[2][kTile * D];
-  // codes of the slice's keys, then one need-mask flag per stage (dynamic:
-  // tiles_per_split * (kTile + 1) ints)
+  // key tables of the slice (rows, thresholds), then one need-mask flag per
+  // stage (dynamic: tiles_per_split * (2 * kTile + 1) ints)
   extern __shared__ int slice_lds[];
-  int* codes = slice_lds;
-  int* need_mask = slice_lds + a.tiles_per_split * kTile;
+  int* rows = slice_lds;
+  int* thrs = slice_lds + a.tiles_per_split * kTile;
+  int* need_mask = slice_lds + 2 * a.tiles_per_split * kTile;
 
   // logical order (g, split, row block): blocks reading the same K/V tiles are
   // adjacent, hence on the same XCD and its L2
@@ -329,7 +358,7 @@ __global__ __launch_bounds__(kWaves * 64, 2) void attn_kernel(AttnArgs a) {
     }
   }
 
-  // key codes of the slice, one stage per wave at a time, and whether a stage
+  // key tables of the slice, one stage per wave at a time, and whether a stage
   // has a key some row of the block must not see; all index loads first
   constexpr int kMaxIt = kMaxSliceKeys / kTile / kWaves;
   int jv[kMaxIt], sv[kMaxIt];
@@ -345,10 +374,11 @@ __global__ __launch_bounds__(kWaves * 64, 2) void attn_kernel(AttnArgs a) {
     const int st = wave + it * kWaves;
     if (st >= nt) break;  // uniform
     const int pos = (tile0 + st) * kTile + lane;
-    const int code = pos < np_block ? key_code(a, pos, jv[it], sv[it]) : kNoKey;
-    codes[st * kTile + lane] = code;
-    const bool vis_all = code >= 0 || (code <= -2 && -2 - code <= first_t);
-    const uint64_t bad = __ballot(!vis_all);
+    int krow = 0, kthr = kNever;
+    if (pos < np_block) key_entry(a, pos, jv[it], sv[it], krow, kthr);
+    rows[st * kTile + lane] = krow;
+    thrs[st * kTile + lane] = kthr;
+    const uint64_t bad = __ballot(kthr > first_t);
     if (lane == 0) need_mask[st] = bad != 0;
   }
   __syncthreads();
@@ -377,22 +407,25 @@ __global__ __launch_bounds__(kWaves * 64, 2) void attn_kernel(AttnArgs a) {
   rs.l_run = 0.f;
 
   TileRegs<D> regs;
+  TileKeys<D> tk;
   if (nt > 0) {
-    tile_load<D, 0>(a, g, codes, regs);
-    tile_load<D, 1>(a, g, codes, regs);
+    tile_keys<D>(rows, thrs, tk);
+    tile_load<D>(a, g, tk, regs);
+    if (nt > 1) tile_keys<D>(rows + kTile, thrs + kTile, tk);
     tile_store<D>(regs, lk[0], lv[0]);
     __syncthreads();
   }
   for (int st = 0; st < nt; ++st) {
     const int cur = st & 1;
     const bool has_next = st + 1 < nt;
-    // the next stage's K/V rows load during this stage
+    // the next stage's K/V rows load during this stage; the table entries of
+    // the stage after it are read now, for the next iteration
     if (has_next) {
-      tile_load<D, 0>(a, g, codes + (st + 1) * kTile, regs);
-      tile_load<D, 1>(a, g, codes + (st + 1) * kTile, regs);
+      tile_load<D>(a, g, tk, regs);
+      if (st + 2 < nt) tile_keys<D>(rows + (st + 2) * kTile, thrs + (st + 2) * kTile, tk);
     }
     f32x16 s[2];
-    stage_softmax<D>(a, lk[cur], codes + st * kTile, need_mask[st], t, kbase_off, qf, rs, s);
+    stage_softmax<D>(a, lk[cur], thrs + st * kTile, need_mask[st], t, kbase_off, qf, rs, s);
     stage_pv<D>(lv[cur], voff, s, rs);
     if (has_next) {
       tile_store<D>(regs, lk[cur ^ 1], lv[cur ^ 1]);
@@ -666,7 +699,7 @@ ckv_status launch_attn(const ckv_dims* d, const void* q, const ChunkSource& src,
   a.c1 = resolve_scale(d) * 1.4426950408889634f;
   a.nblocks = (uint32_t)((int64_t)a.Hkv * a.n_row_blocks * a.n_splits);
   a.nblocks_padded = (uint32_t)align_up(a.nblocks, 8);
-  const size_t slice_bytes = (size_t)a.tiles_per_split * (kTile + 1) * sizeof(int);
+  const size_t slice_bytes = (size_t)a.tiles_per_split * (2 * kTile + 1) * sizeof(int);
   if (d->head_dim == 128)
     hipLaunchKernelGGL(attn_kernel<128>, dim3(a.nblocks_padded), dim3(kWaves * 64), slice_bytes, st, a);
   else

@@ -372,25 +372,23 @@ __device__ __forceinline__ void process_subtile(const ScoreArgs& a, const bf16x8
 // interleaves the two), and the last subtile's VALU work is carried over the
 // stage barrier into the next stage.
 
-// All 16 MFMAs of one subtile (both row tiles share each K fragment).  All
-// fragments are read first, so only the first MFMA waits on LDS latency.
+// All 16 MFMAs of one subtile (both row tiles share each K fragment).  The
+// fragment reads are left to the scheduler: reading all of them ahead costs
+// 32 more VGPRs and measured slower.
 template <int D>
 __device__ __forceinline__ void mfma_subtile(const uint16_t* lds, int lrow0,
                                              const bf16x8 (&qf)[2][D / 16], f32x16 (&acc)[2]) {
   const int lane = threadIdx.x & 63, half = lane >> 5;
-  bf16x8 kf[D / 16];
-#pragma unroll
-  for (int ks = 0; ks < D / 16; ++ks)
-    kf[ks] = *reinterpret_cast<const bf16x8*>(
-        lds + SubtileLds<D>::offset(lrow0 + (lane & 31), 2 * ks + half));
 #pragma unroll
   for (int rt = 0; rt < 2; ++rt)
 #pragma unroll
     for (int v = 0; v < 16; ++v) acc[rt][v] = 0.f;
 #pragma unroll
   for (int ks = 0; ks < D / 16; ++ks) {
-    acc[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[ks], qf[0][ks], acc[0], 0, 0, 0);
-    acc[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[ks], qf[1][ks], acc[1], 0, 0, 0);
+    const bf16x8 kf = *reinterpret_cast<const bf16x8*>(
+        lds + SubtileLds<D>::offset(lrow0 + (lane & 31), 2 * ks + half));
+    acc[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[0][ks], acc[0], 0, 0, 0);
+    acc[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[1][ks], acc[1], 0, 0, 0);
   }
 }
 
@@ -606,8 +604,8 @@ __device__ __forceinline__ Segment segment_of(const ScoreWork& wk, int64_t n, in
 // Fold of the segments of row block rbh: thread t owns row t of the block
 // (rows past R fold too; nothing reads them).  M = max mc, Z = sum
 // exp2(mc - M) z, and each segment's z slot becomes its weight exp2(mc - M)/Z.
-// Segments are read kFoldBatch at a time so their loads are in flight together
-// (one batch covers every shape with NS <= kFoldBatch).
+// Up to kFoldBatch segments are held in registers, loaded in one round trip;
+// more are read in batches of kFoldBatch (three passes).
 constexpr int kFoldBatch = 32;
 
 // exp2(mc - M) for whole-number references mc <= M: an exact power of two
@@ -616,8 +614,42 @@ __device__ __forceinline__ double seg_factor(float mc, float M) {
   return mc == M ? 1.0 : ldexp(1.0, (int)fmaxf(mc - M, -1100.f));
 }
 
-__device__ __forceinline__ void fold_row_block(const float* mc, double* z, const ScoreWork& wk,
-                                               int rbh) {
+struct FoldRegs {
+  float v[kFoldBatch];
+  double zz[kFoldBatch];
+};
+
+// This thread's row of every segment (NS <= kFoldBatch); absent segments read
+// as (-inf, 0), which contribute exactly 0.
+__device__ __forceinline__ void fold_load(const float* mc, const double* z, const ScoreWork& wk,
+                                          int rbh, FoldRegs& r) {
+  const int64_t base = (int64_t)rbh * wk.NS * wk.rpb + threadIdx.x;
+#pragma unroll
+  for (int i = 0; i < kFoldBatch; ++i) {
+    const bool ok = i < wk.NS;
+    r.v[i] = ok ? mc[base + (int64_t)i * wk.rpb] : -INFINITY;
+    r.zz[i] = ok ? z[base + (int64_t)i * wk.rpb] : 0.0;
+  }
+}
+
+__device__ __forceinline__ void fold_apply(double* z, const ScoreWork& wk, int rbh,
+                                           const FoldRegs& r) {
+  const int64_t base = (int64_t)rbh * wk.NS * wk.rpb + threadIdx.x;
+  float M = -INFINITY;
+#pragma unroll
+  for (int i = 0; i < kFoldBatch; ++i) M = fmaxf(M, r.v[i]);
+  double Z = 0.0;  // ascending segment order
+#pragma unroll
+  for (int i = 0; i < kFoldBatch; ++i) Z += seg_factor(r.v[i], M) * r.zz[i];
+  const double inv = 1.0 / Z;
+#pragma unroll
+  for (int i = 0; i < kFoldBatch; ++i)
+    if (i < wk.NS) z[base + (int64_t)i * wk.rpb] = seg_factor(r.v[i], M) * inv;
+}
+
+// More than kFoldBatch segments: the same sums, in the same order, in batches.
+__device__ __forceinline__ void fold_row_block_batched(const float* mc, double* z,
+                                                       const ScoreWork& wk, int rbh) {
   const int64_t base = (int64_t)rbh * wk.NS * wk.rpb + threadIdx.x;
   const int NS = wk.NS, rpb = wk.rpb;
   float M = -INFINITY;
@@ -636,7 +668,7 @@ __device__ __forceinline__ void fold_row_block(const float* mc, double* z, const
 #pragma unroll
     for (int i = 0; i < kFoldBatch; ++i) {
       const bool ok = s0 + i < NS;
-      v[i] = ok ? mc[base + (int64_t)(s0 + i) * rpb] : M;
+      v[i] = ok ? mc[base + (int64_t)(s0 + i) * rpb] : -INFINITY;
       zz[i] = ok ? z[base + (int64_t)(s0 + i) * rpb] : 0.0;
     }
 #pragma unroll
@@ -650,6 +682,17 @@ __device__ __forceinline__ void fold_row_block(const float* mc, double* z, const
 #pragma unroll
     for (int i = 0; i < kFoldBatch; ++i)
       if (s0 + i < NS) z[base + (int64_t)(s0 + i) * rpb] = seg_factor(v[i], M) * inv;
+  }
+}
+
+__device__ __forceinline__ void fold_row_block(const float* mc, double* z, const ScoreWork& wk,
+                                               int rbh) {
+  if (wk.NS <= kFoldBatch) {
+    FoldRegs r;
+    fold_load(mc, z, wk, rbh, r);
+    fold_apply(z, wk, rbh, r);
+  } else {
+    fold_row_block_batched(mc, z, wk, rbh);
   }
 }
 
@@ -679,10 +722,15 @@ __global__ __launch_bounds__(kWaves * 64) void score_fold_kernel(ScoreArgs a) {
   __shared__ __attribute__((aligned(16))) uint16_t lds[2 * kStage * SubtileLds<D>::kRow];
   const int rbh = blockIdx.x;
   const int g = rbh / a.w.RB, row0 = (rbh % a.w.RB) * kBlockRows;
-  // all flags of the block in one round trip; nothing flagged is the common case
+  // all flags of the block, and (speculatively) the block's statistics, in one
+  // round trip; nothing flagged is the common case
+  const bool in_regs = a.w.NS <= kFoldBatch;
+  FoldRegs r;
+  if (in_regs) fold_load(a.mc, a.z, a.w, rbh, r);
   int any = 0;
   for (int s = threadIdx.x; s < a.w.NS; s += blockDim.x) any |= a.flags[rbh * a.w.NS + s];
-  if (__syncthreads_or(any)) {
+  const bool redo = __syncthreads_or(any);
+  if (redo) {
     for (int s = 0; s < a.w.NS; ++s) {
       if (!a.flags[rbh * a.w.NS + s]) continue;  // uniform
       const Segment o = segment_at(a.w, a.n, rbh, s);
@@ -695,7 +743,12 @@ __global__ __launch_bounds__(kWaves * 64) void score_fold_kernel(ScoreArgs a) {
       __syncthreads();
     }
   }
-  fold_row_block(a.mc, a.z, a.w, rbh);
+  if (!in_regs) {
+    fold_row_block_batched(a.mc, a.z, a.w, rbh);
+    return;
+  }
+  if (redo) fold_load(a.mc, a.z, a.w, rbh, r);  // this thread's rows, as redone
+  fold_apply(a.z, a.w, rbh, r);
 }
 
 // fp32 path: the main kernel already redid overflowing segments; fold only.
