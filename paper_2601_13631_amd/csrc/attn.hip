@@ -433,24 +433,16 @@ __global__ __launch_bounds__(kWaves * 64, 2) void attn_kernel(AttnArgs a) {
     }
   }
 
-  // o[db][v] holds d = 32*db + 8*(v/4) + 4*half + v%4 of this lane's row
-  if (!row_ok) return;
-  if (a.n_splits == 1) {
-    const float inv = 1.f / rs.l_run;
-    uint16_t* dst = a.out + ((int64_t)t * a.Hq + (int64_t)g * a.G + hi) * D + 4 * half;
-#pragma unroll
-    for (int db = 0; db < D / 32; ++db)
-#pragma unroll
-      for (int q4 = 0; q4 < 4; ++q4) {
-        __bf16 b[4];
-#pragma unroll
-        for (int j = 0; j < 4; ++j) b[j] = (__bf16)(rs.o[db][4 * q4 + j] * inv);
-        *reinterpret_cast<uint2*>(dst + 32 * db + 8 * q4) = *reinterpret_cast<uint2*>(b);
-      }
-  } else {
-    const int64_t prow = ((int64_t)split * a.Hkv + g) * a.R + row;
-    uint16_t* dst = a.o_part + prow * D + 4 * half;
+  // Output rows through LDS, so that every global store is a whole 16-byte
+  // piece of a row and 16 lanes cover a row: the wave's 32 rows (O/l in
+  // bf16) go to its own slice of the K stage buffer, which every wave has
+  // finished reading after this barrier.
+  __syncthreads();
+  {
+    constexpr int kRow = KLds<D>::kRow;
+    uint16_t* tile = reinterpret_cast<uint16_t*>(lk) + wave * kWaveRows * kRow;
     const float inv = rs.l_run > 0.f ? 1.f / rs.l_run : 0.f;
+    // o[db][v] holds d = 32*db + 8*(v/4) + 4*half + v%4 of this lane's row
 #pragma unroll
     for (int db = 0; db < D / 32; ++db)
 #pragma unroll
@@ -458,11 +450,32 @@ __global__ __launch_bounds__(kWaves * 64, 2) void attn_kernel(AttnArgs a) {
         __bf16 b[4];
 #pragma unroll
         for (int j = 0; j < 4; ++j) b[j] = (__bf16)(rs.o[db][4 * q4 + j] * inv);
-        *reinterpret_cast<uint2*>(dst + 32 * db + 8 * q4) = *reinterpret_cast<uint2*>(b);
+        *reinterpret_cast<uint2*>(tile + (lane & 31) * kRow + 32 * db + 8 * q4 + 4 * half) =
+            *reinterpret_cast<uint2*>(b);
       }
-    // the reference the numerators were taken against (0 while no key was seen)
-    if (half == 0) a.ml_part[prow] = make_float2(rs.m_run == -INFINITY ? 0.f : rs.m_run, rs.l_run);
+    __builtin_amdgcn_wave_barrier();
+    constexpr int kSegs = D / 8, kRowsPerPass = 64 / kSegs;
+    const int seg = lane % kSegs;
+    const int row_base = rb * kBlockRows + wave * kWaveRows;
+#pragma unroll
+    for (int r0 = 0; r0 < kWaveRows; r0 += kRowsPerPass) {
+      const int rr = r0 + lane / kSegs;
+      const int orow = row_base + rr;
+      const uint4 v = *reinterpret_cast<const uint4*>(tile + rr * kRow + seg * 8);
+      if (orow < a.R) {
+        uint16_t* dst;
+        if (a.n_splits == 1)
+          dst = a.out + ((int64_t)(orow / a.G) * a.Hq + (int64_t)g * a.G + orow % a.G) * D;
+        else
+          dst = a.o_part + (((int64_t)split * a.Hkv + g) * a.R + orow) * D;
+        *reinterpret_cast<uint4*>(dst + seg * 8) = v;
+      }
+    }
   }
+  // the reference the numerators were taken against (0 while no key was seen)
+  if (a.n_splits > 1 && row_ok && half == 0)
+    a.ml_part[((int64_t)split * a.Hkv + g) * a.R + row] =
+        make_float2(rs.m_run == -INFINITY ? 0.f : rs.m_run, rs.l_run);
 }
 
 // Merges the splits of each row in split order: out = sum_s w_s Ohat_s with

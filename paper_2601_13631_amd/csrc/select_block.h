@@ -7,15 +7,16 @@
 // Radix select on 64-bit order-preserving keys (sign-flipped IEEE bits, -0.0
 // folded onto +0.0, NaN below -inf).  Each round histograms an 8-bit digit that
 // starts at the highest bit where the smallest and largest candidate differ, so
-// no round is spent on bits every candidate shares; the same pass records each
-// bin's smallest and largest key, which bound the next round's candidates.  The
+// no round is spent on bits every candidate shares; after the bin is chosen, a
+// block-wide min/max over its keys bounds the next round's candidates.  The
 // search ends when the chosen bin holds exactly the keys still needed or all
 // candidates are equal; the lowest indices then win among equal keys.  Output
-// is an in-order compaction with block-wide exclusive scans, so the indices
-// come out ascending.  Every count is an integer (LDS atomics): the result
-// depends only on the score bits.  With a key cache (LDS, m entries) the
-// scores are read from global memory once; without one, every pass re-reads
-// them (they stay in L2).
+// is an in-order compaction with one block-wide exclusive scan (the counts of
+// greater and of equal keys packed in one 64-bit word), so the indices come
+// out ascending.  Every count is an integer (LDS atomics): the result depends
+// only on the score bits.  With a key cache (LDS, m entries) the scores are
+// read from global memory once; without one, every pass re-reads them (they
+// stay in L2).
 
 #pragma once
 
@@ -35,7 +36,6 @@ __device__ __forceinline__ uint64_t order_key(double x) {
 
 struct SelShared {
   uint32_t hist[256];
-  unsigned long long bmin[256], bmax[256];
   uint32_t wsum[4];
   uint64_t red_lo[kSelMaxWaves], red_hi[kSelMaxWaves];
   int64_t red_i[kSelMaxWaves];
@@ -120,20 +120,11 @@ __device__ __forceinline__ void select_topk_block(const double* scores, int64_t 
     }
     const int top = 63 - __clzll(lo ^ hi);
     const int shift = top >= 7 ? top - 7 : 0;
-    for (int b = tid; b < 256; b += THREADS) {
-      sh.hist[b] = 0;
-      sh.bmin[b] = ~0ull;
-      sh.bmax[b] = 0;
-    }
+    for (int b = tid; b < 256; b += THREADS) sh.hist[b] = 0;
     __syncthreads();
     for (int64_t i = tid; i < m; i += THREADS) {
       const uint64_t x = key_at(i);
-      if ((x & mask) == prefix) {
-        const int b = (int)((x >> shift) & 255);
-        atomicAdd(&sh.hist[b], 1u);
-        atomicMin(&sh.bmin[b], (unsigned long long)x);
-        atomicMax(&sh.bmax[b], (unsigned long long)x);
-      }
+      if ((x & mask) == prefix) atomicAdd(&sh.hist[(int)((x >> shift) & 255)], 1u);
     }
     __syncthreads();
     // count of candidates in bins >= b as an inclusive scan over t = 255 - b
@@ -170,13 +161,24 @@ __device__ __forceinline__ void select_topk_block(const double* scores, int64_t 
         sh.mask = keep_hi | (255ull << shift);
         sh.remaining = need - before;
         sh.done = (cnt[q] == (uint32_t)sh.remaining) || shift == 0;
-        sh.lo = sh.bmin[b];
-        sh.hi = sh.bmax[b];
       }
       before = after;
     }
     __syncthreads();
     if (sh.done) break;
+    // bounds of the chosen bin's keys for the next round
+    {
+      const uint64_t p2 = sh.prefix, m2 = sh.mask;
+      uint64_t blo = ~0ull, bhi = 0;
+      for (int64_t i = tid; i < m; i += THREADS) {
+        const uint64_t x = key_at(i);
+        if ((x & m2) == p2) {
+          blo = x < blo ? x : blo;
+          bhi = x > bhi ? x : bhi;
+        }
+      }
+      sel_block_minmax<THREADS>(blo, bhi, sh);
+    }
   }
 
   // ascending compaction: i is kept if (key & mask) > prefix, or equal and among
@@ -191,8 +193,10 @@ __device__ __forceinline__ void select_topk_block(const double* scores, int64_t 
     n_gt += x > prefix;
     n_eq += x == prefix;
   }
-  const int64_t gt_before = sel_block_exclusive_scan<THREADS>(n_gt, sh);
-  const int64_t eq_before = sel_block_exclusive_scan<THREADS>(n_eq, sh);
+  // one scan of both counts: greater in the high 32 bits, equal in the low
+  // (m < 2^31, so neither field carries into the other)
+  const int64_t both = sel_block_exclusive_scan<THREADS>((n_gt << 32) | n_eq, sh);
+  const int64_t gt_before = both >> 32, eq_before = both & 0xffffffffll;
   int64_t eq_rank = eq_before;
   int64_t pos = gt_before + min(eq_before, remaining);
   for (int64_t i = i0; i < i1; ++i) {
