@@ -8,9 +8,9 @@ each with its own seeded synthetic Q/K/V resident in HBM before timing starts.
 
 Prints one JSON line.  ``roofline`` describes the scoring kernel (the dominant
 kernel): its algorithmic flops per launch (2*S*Hq*n*d) over its average
-duration, taken from HIP events recorded on the layer's stream around that
-kernel inside the timed region (two events per step; the context records no
-others there).  ``roofline.traffic`` is the kernel's HBM bytes per launch from
+duration, taken from HIP events inside the timed region: the kernel is
+launched on the layer's stream with two events as its own start and stop
+timestamps (two events per step; the context records no others there).  ``roofline.traffic`` is the kernel's HBM bytes per launch from
 the committed rocprofv3 counter summary (FETCH_SIZE and WRITE_SIZE, each scaled
 by what the counter reads for a plain copy of known size); it is null when the
 kernel's sources no longer match the hash recorded with those counters.

@@ -185,8 +185,10 @@ typedef struct ckv_ctx ckv_ctx;
                                        attention instead of reading spans in place */
 #define CKV_CTX_STAGE_TIMING 0x4    /* record HIP events between the stages of every
                                        layer (see ckv_ctx_stage_times) */
-#define CKV_CTX_SCORE_TIMING 0x8    /* record HIP events only around the chunk-scoring
-                                       main kernel: two events per layer instead of six;
+#define CKV_CTX_SCORE_TIMING 0x8    /* time only the chunk-scoring main kernel: two
+                                       events per layer instead of six (bf16: the
+                                       kernel's own launch start and stop timestamps,
+                                       so the interval is its execution alone);
                                        ckv_ctx_stage_times then reports the score stage
                                        and zero for the others */
 

@@ -95,10 +95,13 @@ struct ScorePlan {
   size_t off_part, off_mc, off_z, off_flags, bytes;
 };
 ScorePlan make_score_plan(const ckv_dims* d);
-// after_main (optional) is recorded between the main kernel and the fold.
+// Optional timing events of the main kernel: with both, the kernel is
+// launched with them as its own start and stop timestamps (the interval is
+// the kernel's execution alone); with only main_stop, that event is recorded
+// between the main kernel and the fold.
 ckv_status launch_score(const ckv_dims* d, const void* q, const void* k, double* scores,
                         void* ws, size_t ws_bytes, hipStream_t st,
-                        hipEvent_t after_main = nullptr);
+                        hipEvent_t main_stop = nullptr, hipEvent_t main_start = nullptr);
 
 size_t select_ws_bytes(int64_t m);
 ckv_status launch_select(const double* scores, int64_t m, int64_t k, int32_t* sel, void* ws,

@@ -269,15 +269,18 @@ ckv_status ckv_reprefill_layer(ckv_ctx* c, int32_t layer, const ckv_layer_io* io
       if (s != CKV_OK) return s;
     }
     tev = c->tev[c->t_issued % ckv_ctx::kRing];
-    CKV_HIP(hipEventRecord(tev[0], st));
+    // every stage: the set starts here; the scoring kernel alone: its own
+    // launch brackets it (bf16), else the set starts here too
+    if (all_stages(c) || d->dtype != CKV_DTYPE_BF16) CKV_HIP(hipEventRecord(tev[0], st));
   }
   auto mark = [&](int i) -> ckv_status {
     if (tev && all_stages(c)) CKV_HIP(hipEventRecord(tev[i], st));
     return CKV_OK;
   };
 
+  const bool bracket = tev && !all_stages(c) && d->dtype == CKV_DTYPE_BF16;
   ckv_status s = launch_score(d, io->q, io->k_probe, scores, ws, c->ws_score, st,
-                              tev ? tev[1] : nullptr);
+                              tev ? tev[1] : nullptr, bracket ? tev[0] : nullptr);
   if (s != CKV_OK) return s;
   if ((s = mark(2)) != CKV_OK) return s;
   s = launch_select(scores, c->m, k, sel, nullptr, 0, st);

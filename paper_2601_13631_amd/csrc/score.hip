@@ -28,6 +28,8 @@
 //
 // All sums have a fixed order: results are bitwise reproducible run to run.
 
+#include <hip/hip_ext.h>
+
 #include <cfloat>
 
 #include "ckv_internal.h"
@@ -1031,7 +1033,7 @@ ScorePlan make_score_plan(const ckv_dims* d) {
 }
 
 ckv_status launch_score(const ckv_dims* d, const void* q, const void* k, double* scores, void* ws,
-                        size_t ws_bytes, hipStream_t st, hipEvent_t after_main) {
+                        size_t ws_bytes, hipStream_t st, hipEvent_t main_stop, hipEvent_t main_start) {
   const ScorePlan p = make_score_plan(d);
   if (p.bytes == 0) CKV_FAIL(CKV_EUNSUPPORTED, "shape too large for the scoring decomposition");
   if (ws_bytes < p.bytes) CKV_FAIL(CKV_EINVAL, "score workspace too small: %zu < %zu", ws_bytes, p.bytes);
@@ -1058,12 +1060,16 @@ ckv_status launch_score(const ckv_dims* d, const void* q, const void* k, double*
     a.nwg_padded = (uint32_t)align_up(nwg, 8);
     dim3 grid(a.nwg_padded), block(kWaves * 64);
     const dim3 fold_grid((unsigned)(d->n_kv_heads * p.w.RB));
-    // the event (if any) goes between the main kernel and the fold
-#define CKV_SCORE_LAUNCH(DD, MM)                                                   \
-  do {                                                                             \
-    hipLaunchKernelGGL((score_bf16_kernel<DD, MM>), grid, block, 0, st, a);        \
-    if (after_main) CKV_HIP(hipEventRecord(after_main, st));                      \
-    hipLaunchKernelGGL((score_fold_kernel<DD, MM>), fold_grid, block, 0, st, a);   \
+#define CKV_SCORE_LAUNCH(DD, MM)                                                           \
+  do {                                                                                     \
+    if (main_start && main_stop) {                                                         \
+      hipExtLaunchKernelGGL((score_bf16_kernel<DD, MM>), grid, block, 0, st, main_start,   \
+                            main_stop, 0, a);                                              \
+    } else {                                                                               \
+      hipLaunchKernelGGL((score_bf16_kernel<DD, MM>), grid, block, 0, st, a);              \
+      if (main_stop) CKV_HIP(hipEventRecord(main_stop, st));                              \
+    }                                                                                      \
+    hipLaunchKernelGGL((score_fold_kernel<DD, MM>), fold_grid, block, 0, st, a);           \
   } while (0)
     if (d->head_dim == 128) {
       switch (mode) {
@@ -1100,7 +1106,10 @@ ckv_status launch_score(const ckv_dims* d, const void* q, const void* k, double*
       case kC32: hipLaunchKernelGGL((score_f32_kernel<64, kC32>), grid, block, 0, st, a); break;
       default: hipLaunchKernelGGL((score_f32_kernel<64, kC32x>), grid, block, 0, st, a); break;
     }
-    if (after_main) CKV_HIP(hipEventRecord(after_main, st));
+    if (main_stop) {
+      if (main_start) CKV_FAIL(CKV_EUNSUPPORTED, "kernel-bracketing timing is for the bf16 path");
+      CKV_HIP(hipEventRecord(main_stop, st));
+    }
     hipLaunchKernelGGL(score_fold_f32_kernel, dim3((unsigned)(d->n_kv_heads * p.w.RB)),
                        dim3(kWaveRows), 0, st, mc, z, p.w);
   }
