@@ -208,8 +208,22 @@ ckv_status ckv_ctx_create(const ckv_dims* dims, double keep_ratio, int32_t flags
 /* Waits for the context's streams, then frees everything the context owns. */
 ckv_status ckv_ctx_destroy(ckv_ctx* ctx);
 /* Forgets the previous layer's selection: the next layer runs without a
- * prediction (as the first layer of a request); also clears stage times. */
+ * prediction (as the first layer of a request); also clears stage times and
+ * the set held for the current Period. */
 ckv_status ckv_ctx_reset(ckv_ctx* ctx);
+
+/* Periods -- Def. 4.2 (Sec. 4.3): consecutive layers p*i .. p*i+p-1 form a
+ * Period and share one important-chunk set, the one selected at layer p*i.
+ * With period p > 1, ckv_reprefill_layer runs scoring and selection only on
+ * a layer that is a multiple of p and keeps the set in the context; every
+ * other layer attends over the set of its Period's first layer, which must
+ * have run on this context since the last reset or set_period (else
+ * CKV_ESTATE), writes that set to io->sel_idx (if given), leaves
+ * io->chunk_scores untouched, and needs no host synchronisation even with a
+ * host-resident prefix (its prefetch prediction, the previous layer's set,
+ * is then exact).  period = 1 (the default) selects at every layer.
+ * Forgets any set held.  CKV_EINVAL if period < 1. */
+ckv_status ckv_ctx_set_period(ckv_ctx* ctx, int32_t period);
 
 typedef struct ckv_layer_io {
   const void* q;         /* device [S][Hq][d]                                        */
@@ -245,8 +259,9 @@ typedef struct ckv_layer_stats {
 /* Sum of the GPU time of each stage (ms[CKV_N_STAGES], milliseconds) over
  * every layer run since the context was created or last reset, and that
  * number of layers in *n_layers.  Requires CKV_CTX_STAGE_TIMING or
- * CKV_CTX_SCORE_TIMING (then only ms[CKV_STAGE_SCORE] is filled); waits for the
- * events of the layers not yet accounted.  Stage times come from events
+ * CKV_CTX_SCORE_TIMING (then only ms[CKV_STAGE_SCORE] is filled, and only
+ * layers that ran scoring are counted); waits for the events of the layers
+ * not yet accounted.  Stage times come from events
  * recorded on each layer's compute stream between its kernel launches. */
 ckv_status ckv_ctx_stage_times(ckv_ctx* ctx, double* ms, int64_t* n_layers);
 

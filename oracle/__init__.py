@@ -236,6 +236,25 @@ def layer_accounting(shape: Shape, sel, pred) -> dict:
     return {f: int(getattr(st, f)) for f, _ in _Stats._fields_}
 
 
+def period_first_layer(layer: int, period: int) -> int:
+    """First layer of the Period that holds `layer` (Def. 4.2, Sec. 4.3): the
+    layers are cut, from layer 0, into Periods of `period` consecutive layers,
+    and every layer of a Period uses the important-chunk set selected at the
+    Period's first layer."""
+    if period < 1 or layer < 0:
+        raise ValueError("period must be >= 1 and layer >= 0")
+    return layer - layer % period
+
+
+def period_prediction(sets: list, period: int) -> list:
+    """Prefetch prediction of every layer when each layer's set follows its
+    Period: P_0 = empty, P_l = the set layer l-1 used (Sec. 4.3.2), with
+    layer l using sets[period_first_layer(l, period)] (only the entries of
+    Period first layers are read)."""
+    used = [np.asarray(sets[period_first_layer(l, period)], np.int32) for l in range(len(sets))]
+    return [np.zeros(0, np.int32)] + used[:-1]
+
+
 def reprefill_layer(shape: Shape, keep_ratio: float, q, k_prefix, v_prefix, k_suffix, v_suffix,
                     threads: int = 0):
     """One layer: returns (chunk scores A[m], selected chunks sel[k], out[S][Hq][d])."""

@@ -81,6 +81,7 @@ _SIG = {
     "ckv_ctx_create": ([_DP, ctypes.c_double, ctypes.c_int32, ctypes.POINTER(_P)], ctypes.c_int32),
     "ckv_ctx_destroy": ([_P], ctypes.c_int32),
     "ckv_ctx_reset": ([_P], ctypes.c_int32),
+    "ckv_ctx_set_period": ([_P, ctypes.c_int32], ctypes.c_int32),
     "ckv_ctx_stage_times": ([_P, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64)],
                             ctypes.c_int32),
     "ckv_reprefill_layer": ([_P, ctypes.c_int32, ctypes.POINTER(LayerIO),
@@ -212,6 +213,10 @@ class Context:
 
     def reset(self) -> None:
         _check(_lib.ckv_ctx_reset(self._h), "ckv_ctx_reset")
+
+    def set_period(self, period: int) -> None:
+        """Layers p*i .. p*i+p-1 share the set selected at layer p*i."""
+        _check(_lib.ckv_ctx_set_period(self._h, period), "ckv_ctx_set_period")
 
     def close(self) -> None:
         if self._h:

@@ -4,7 +4,13 @@
 // spans in place (or, with CKV_CTX_MATERIALIZE, gather -> attention over the
 // compact copy), all on the caller's stream with no host synchronisation.
 //
-// Host-resident prefix (Sec. 4.3.2, with one layer per Period): the K/V store
+// Periods (Def. 4.2): with a Period of p layers (ckv_ctx_set_period), layer l
+// runs scoring and selection only when l is a multiple of p; the other layers
+// of the Period attend over the set that layer selected (kept in the context,
+// on the device and, for a host-resident prefix, on the host), with no
+// scoring, no selection and no host synchronisation.
+//
+// Host-resident prefix (Sec. 4.3.2): the K/V store
 // of every layer lives in pinned host memory, chunk-major (chunk j of a layer
 // is one span: K rows then V rows).  Two HBM slot buffers alternate between
 // layers.  While layer l computes, the chunks that layer l selected are copied
@@ -47,6 +53,12 @@ struct ckv_ctx {
   bool pref_pending[2] = {false, false}, attn_recorded[2] = {false, false};
   std::vector<int32_t> pred;  // prediction for the next layer (ascending), in slots 0..|pred|-1
   int32_t next_layer = 0;
+  // Periods: layers period_first .. period_first+period-1 attend over the set
+  // selected at period_first (device copy at off_pset, host copy pset_host)
+  int32_t period = 1;
+  int32_t period_first = -1;  // -1: no set held
+  size_t off_pset = 0;
+  std::vector<int32_t> pset_host;
   // stage timing: a ring of event sets, harvested when a set is reused or on query
   static constexpr int kRing = 64;
   hipEvent_t tev[kRing][CKV_N_STAGES + 1] = {};
@@ -167,6 +179,8 @@ ckv_status ckv_ctx_create(const ckv_dims* dims, double keep_ratio, int32_t flags
   off = align_up(off + (size_t)c->m * sizeof(double), 256);
   c->off_sel = off;
   off = align_up(off + (size_t)c->k * sizeof(int32_t), 256);
+  c->off_pset = off;
+  off = align_up(off + (size_t)c->k * sizeof(int32_t), 256);
   if (flags & CKV_CTX_MATERIALIZE) {
     c->off_ksel = off;
     off = align_up(off + (size_t)(c->k * span), 256);
@@ -217,6 +231,15 @@ ckv_status ckv_ctx_stage_times(ckv_ctx* ctx, double* ms, int64_t* n_layers) {
 
 ckv_status ckv_ctx_destroy(ckv_ctx* ctx) { return free_ctx(ctx); }
 
+ckv_status ckv_ctx_set_period(ckv_ctx* ctx, int32_t period) {
+  clear_error();
+  if (!ctx) CKV_FAIL(CKV_EINVAL, "ctx is NULL");
+  if (period < 1) CKV_FAIL(CKV_EINVAL, "period must be >= 1 (got %d)", period);
+  ctx->period = period;
+  ctx->period_first = -1;
+  return CKV_OK;
+}
+
 ckv_status ckv_ctx_reset(ckv_ctx* ctx) {
   clear_error();
   if (!ctx) CKV_FAIL(CKV_EINVAL, "ctx is NULL");
@@ -224,6 +247,7 @@ ckv_status ckv_ctx_reset(ckv_ctx* ctx) {
   ctx->pred.clear();
   ctx->pref_pending[0] = ctx->pref_pending[1] = false;
   ctx->next_layer = 0;
+  ctx->period_first = -1;
   while (ctx->t_done < ctx->t_issued) {
     ckv_status s = harvest_one(ctx);
     if (s != CKV_OK) return s;
@@ -254,16 +278,26 @@ ckv_status ckv_reprefill_layer(ckv_ctx* c, int32_t layer, const ckv_layer_io* io
     if (!aligned16(io->k_prefix) || !aligned16(io->v_prefix))
       CKV_FAIL(CKV_EINVAL, "tensors must be 16-byte aligned");
   }
+  if (layer < 0) CKV_FAIL(CKV_EINVAL, "layer must be >= 0 (got %d)", layer);
+  // a layer past the first of its Period reuses the set selected there
+  const int32_t first = layer - layer % c->period;
+  const bool reuse = first != layer;
+  if (reuse && c->period_first != first)
+    CKV_FAIL(CKV_ESTATE, "layer %d reuses the set of layer %d, the first of its Period, which has not run",
+             layer, first);
   hipStream_t st = (hipStream_t)io->stream;
   char* ws = static_cast<char*>(c->ws);
   double* scores = io->chunk_scores ? io->chunk_scores : reinterpret_cast<double*>(ws + c->off_scores);
-  int32_t* sel = io->sel_idx ? io->sel_idx : reinterpret_cast<int32_t*>(ws + c->off_sel);
+  int32_t* pset = reinterpret_cast<int32_t*>(ws + c->off_pset);
+  // the set this layer attends over: selected now, or the Period's
+  int32_t* sel = reuse ? pset : io->sel_idx ? io->sel_idx : reinterpret_cast<int32_t*>(ws + c->off_sel);
   const int64_t k = c->k;
   const int eb = elem_bytes(d->dtype);
   const int64_t span_elems = (int64_t)d->chunk_size * d->n_kv_heads * d->head_dim;
 
   hipEvent_t* tev = nullptr;
-  if (c->flags & (CKV_CTX_STAGE_TIMING | CKV_CTX_SCORE_TIMING)) {
+  // a reused layer has no scoring kernel to time alone
+  if ((c->flags & CKV_CTX_STAGE_TIMING) || ((c->flags & CKV_CTX_SCORE_TIMING) && !reuse)) {
     if (c->t_issued - c->t_done >= ckv_ctx::kRing) {  // reuse the oldest set: account it first
       ckv_status s = harvest_one(c);
       if (s != CKV_OK) return s;
@@ -278,14 +312,28 @@ ckv_status ckv_reprefill_layer(ckv_ctx* c, int32_t layer, const ckv_layer_io* io
     return CKV_OK;
   };
 
-  const bool bracket = tev && !all_stages(c) && d->dtype == CKV_DTYPE_BF16;
-  ckv_status s = launch_score(d, io->q, io->k_probe, scores, ws, c->ws_score, st,
-                              tev ? tev[1] : nullptr, bracket ? tev[0] : nullptr);
-  if (s != CKV_OK) return s;
-  if ((s = mark(2)) != CKV_OK) return s;
-  s = launch_select(scores, c->m, k, sel, nullptr, 0, st);
-  if (s != CKV_OK) return s;
-  if ((s = mark(3)) != CKV_OK) return s;
+  ckv_status s = CKV_OK;
+  if (!reuse) {
+    const bool bracket = tev && !all_stages(c) && d->dtype == CKV_DTYPE_BF16;
+    s = launch_score(d, io->q, io->k_probe, scores, ws, c->ws_score, st, tev ? tev[1] : nullptr,
+                     bracket ? tev[0] : nullptr);
+    if (s != CKV_OK) return s;
+    if ((s = mark(2)) != CKV_OK) return s;
+    s = launch_select(scores, c->m, k, sel, nullptr, 0, st);
+    if (s != CKV_OK) return s;
+    if ((s = mark(3)) != CKV_OK) return s;
+    if (c->period > 1) {  // keep the set for the rest of the Period
+      CKV_HIP(hipMemcpyAsync(pset, sel, (size_t)k * sizeof(int32_t), hipMemcpyDeviceToDevice, st));
+      c->period_first = layer;
+    }
+  } else {
+    if ((s = mark(1)) != CKV_OK) return s;
+    if ((s = mark(2)) != CKV_OK) return s;
+    if (io->sel_idx)  // the caller sees the set the layer used
+      CKV_HIP(hipMemcpyAsync(io->sel_idx, pset, (size_t)k * sizeof(int32_t),
+                             hipMemcpyDeviceToDevice, st));
+    if ((s = mark(3)) != CKV_OK) return s;
+  }
 
   ckv_layer_stats stv{};
   stv.k = k;
@@ -313,9 +361,14 @@ ckv_status ckv_reprefill_layer(ckv_ctx* c, int32_t layer, const ckv_layer_io* io
 
   // ---- host-resident prefix ------------------------------------------------
   const int cur = layer & 1, nxt = cur ^ 1;
-  CKV_HIP(hipMemcpyAsync(c->sel_host, sel, (size_t)k * sizeof(int32_t), hipMemcpyDeviceToHost, st));
-  CKV_HIP(hipEventRecord(c->ev_sel, st));
-  CKV_HIP(hipEventSynchronize(c->ev_sel));
+  if (reuse) {  // the Period's set is already on the host: no synchronisation
+    std::memcpy(c->sel_host, c->pset_host.data(), (size_t)k * sizeof(int32_t));
+  } else {
+    CKV_HIP(hipMemcpyAsync(c->sel_host, sel, (size_t)k * sizeof(int32_t), hipMemcpyDeviceToHost, st));
+    CKV_HIP(hipEventRecord(c->ev_sel, st));
+    CKV_HIP(hipEventSynchronize(c->ev_sel));
+    if (c->period > 1) c->pset_host.assign(c->sel_host, c->sel_host + k);
+  }
 
   // slot table: predicted chunks sit in slots 0..|P|-1 (in P order), misses follow
   const std::vector<int32_t>& P = c->pred;

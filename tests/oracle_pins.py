@@ -305,4 +305,33 @@ def pin_planted_chunks_found():
     assert abs(A.sum() - w.n_suffix * w.n_q_heads) < 1e-9
 
 
+def pin_period_rule():
+    """Periods (Def. 4.2): layers cut from layer 0 into runs of p share the set
+    of the run's first layer; the prefetch prediction is the previous layer's
+    set (Sec. 4.3.2), so every layer but a Period's first is predicted exactly."""
+    # brute force: enumerate the Periods
+    for p in range(1, 10):
+        for start in range(0, 60, p):
+            for layer in range(start, start + p):
+                assert oracle.period_first_layer(layer, p) == start
+    assert [oracle.period_first_layer(l, 8) for l in (0, 7, 8, 13, 16)] == [0, 0, 8, 8, 16]
+    for bad in ((3, 0), (-1, 2)):
+        try:
+            oracle.period_first_layer(*bad)
+        except ValueError:
+            continue
+        raise AssertionError("accepted an invalid period or layer")
+    sets = [np.array([1, 2]), None, np.array([3, 5]), None, np.array([0, 7])]
+    pred = oracle.period_prediction(sets, 2)
+    assert [list(x) for x in pred] == [[], [1, 2], [1, 2], [3, 5], [3, 5]]
+    s = Shape(40, 1, 2, 2, 8, 5, BF16)
+    for l in (1, 3):  # layers past a Period's first: all hits, nothing on demand
+        used = sets[oracle.period_first_layer(l, 2)]
+        st = oracle.layer_accounting(s, used, pred[l])
+        assert st["hits"] == 2 and st["misses"] == 0 and st["bytes_demand"] == 0
+    # period 1 is per-layer selection: every prediction is the previous set
+    per_layer = [np.array([i, i + 1]) for i in range(4)]
+    assert [list(x) for x in oracle.period_prediction(per_layer, 1)] == [[], [0, 1], [1, 2], [2, 3]]
+
+
 ALL_PINS = [v for k, v in sorted(globals().items()) if k.startswith("pin_")]
