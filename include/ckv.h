@@ -140,7 +140,8 @@ ckv_status ckv_select_topk_chunks(const double* chunk_scores, int64_t m, int64_t
  * Copies the K and V spans of chunks sel_idx[0..k) into k_sel / v_sel,
  * chunk u to rows [u*c, u*c+c); rows past n of a short last chunk are zeroed.
  *   k_src, v_src  [n][Hkv][d], device memory or pinned host memory mapped
- *                 into the device address space (hipHostMalloc)
+ *                 into the device address space (hipHostMalloc); pageable
+ *                 host memory is refused with CKV_EINVAL
  *   sel_idx       device, int32[k], each in [0, m) (indices are not checked on
  *                 the host; an index outside [0, m) is clamped by the kernel
  *                 and its span is zero-filled)
@@ -232,9 +233,10 @@ typedef struct ckv_layer_io {
   const void* k_probe;   /* device [n][Hkv][d]: the layer's prefix keys for scoring  */
   const void* k_prefix;  /* device [n][Hkv][d] (HBM-resident prefix), else NULL      */
   const void* v_prefix;  /* device [n][Hkv][d] (HBM-resident prefix), else NULL      */
-  const void* kv_host;   /* pinned host, chunk-major: chunk j of this layer at byte
-                            offset j * 2*c*Hkv*d*elem, K span then V span; rows past
-                            n of the last chunk are padding (host-resident prefix)  */
+  const void* kv_host;   /* pinned host (hipHostMalloc; pageable memory is refused),
+                            chunk-major: chunk j of this layer at byte offset
+                            j * 2*c*Hkv*d*elem, K span then V span; rows past n of
+                            the last chunk are padding (host-resident prefix)       */
   const void* kv_host_next; /* the next layer's kv_host, prefetched during this layer
                                with this layer's selection as the prediction; NULL
                                for the last layer                                    */

@@ -123,7 +123,10 @@ ckv_status ckv_gather_chunks(const ckv_dims* dims, const void* k_src, const void
               "pointers must be 16-byte aligned");
   const int64_t row_bytes = (int64_t)dims->n_kv_heads * dims->head_dim * elem_bytes(dims->dtype);
   CKV_REQUIRE(row_bytes % 16 == 0, "Hkv*d*elem_bytes must be a multiple of 16");
-  return launch_gather(dims, k_src, v_src, sel_idx, k, k_sel, v_sel, (hipStream_t)stream);
+  const void* ks = device_view(k_src);
+  const void* vs = device_view(v_src);
+  CKV_REQUIRE(ks && vs, "k_src/v_src must be device memory or pinned host memory");
+  return launch_gather(dims, ks, vs, sel_idx, k, k_sel, v_sel, (hipStream_t)stream);
 }
 
 size_t ckv_attn_workspace_bytes(const ckv_dims* dims, int64_t k) {

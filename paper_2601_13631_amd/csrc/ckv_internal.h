@@ -119,6 +119,15 @@ struct ChunkSource {
   int32_t direct;           // 1: off(u) = sel[u]; 0: off(u) = u (unless chunk_off)
 };
 
+// Copies whole chunk spans of span_bytes each (16-byte multiple): span chunks[i]
+// of src (pinned host memory mapped into the device address space, or device
+// memory) to span slot0 + i of dst, for i < count; chunks is a device array.
+ckv_status launch_copy_spans(const void* src, const int32_t* chunks, int64_t count, int64_t slot0,
+                             void* dst, int64_t span_bytes, hipStream_t st);
+// The address under which kernels read p: p itself for device memory, the
+// mapped address for pinned host memory; nullptr if the device cannot read it
+// (pageable host memory), which callers turn into CKV_EINVAL.
+const void* device_view(const void* p);
 ckv_status launch_gather(const ckv_dims* d, const void* k_src, const void* v_src,
                          const int32_t* sel, int64_t k, void* k_dst, void* v_dst, hipStream_t st);
 

@@ -47,7 +47,67 @@ __global__ __launch_bounds__(kThreads) void gather_kernel(const uint8_t* __restr
   }
 }
 
+// Whole-span copies for the host-resident prefix: grid x = 16 KiB pieces of a
+// span, y = list entry.  From pinned host memory every load crosses the host
+// link; thousands of 16-byte loads in flight keep it busy where one DMA copy
+// per run of chunks would pay a fixed cost per copy.
+__global__ __launch_bounds__(kThreads) void copy_spans_kernel(const uint8_t* __restrict__ src,
+                                                              const int32_t* __restrict__ chunks,
+                                                              int64_t slot0,
+                                                              uint8_t* __restrict__ dst,
+                                                              int64_t span_bytes) {
+  const int64_t i = blockIdx.y;
+  const uint8_t* s = src + (int64_t)chunks[i] * span_bytes;
+  uint8_t* d = dst + (slot0 + i) * span_bytes;
+  const int64_t base = ((int64_t)blockIdx.x * kThreads * kUnroll + threadIdx.x) * 16;
+  u32x4 v[kUnroll];
+#pragma unroll
+  for (int p = 0; p < kUnroll; ++p) {
+    const int64_t off = base + (int64_t)p * kThreads * 16;
+    if (off < span_bytes) v[p] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(s + off));
+  }
+#pragma unroll
+  for (int p = 0; p < kUnroll; ++p) {
+    const int64_t off = base + (int64_t)p * kThreads * 16;
+    if (off < span_bytes) *reinterpret_cast<u32x4*>(d + off) = v[p];
+  }
+}
+
 }  // namespace
+
+ckv_status launch_copy_spans(const void* src, const int32_t* chunks, int64_t count, int64_t slot0,
+                             void* dst, int64_t span_bytes, hipStream_t st) {
+  if (span_bytes % 16 != 0) CKV_FAIL(CKV_EINVAL, "span bytes must be a multiple of 16");
+  constexpr int64_t kMaxY = 65535;  // grid y limit: launch in batches
+  for (int64_t b = 0; b < count; b += kMaxY) {
+    const int64_t nb = std::min<int64_t>(kMaxY, count - b);
+    dim3 grid((unsigned)ceil_div(span_bytes, (int64_t)kThreads * kUnroll * 16), (unsigned)nb);
+    hipLaunchKernelGGL(copy_spans_kernel, grid, dim3(kThreads), 0, st,
+                       static_cast<const uint8_t*>(src), chunks + b, slot0 + b,
+                       static_cast<uint8_t*>(dst), span_bytes);
+    CKV_HIP(hipGetLastError());
+  }
+  return CKV_OK;
+}
+
+const void* device_view(const void* p) {
+  hipPointerAttribute_t at{};
+  if (hipPointerGetAttributes(&at, p) != hipSuccess) {
+    (void)hipGetLastError();  // pageable memory: clear the error the query left
+    return nullptr;
+  }
+  if (at.type == hipMemoryTypeDevice || at.type == hipMemoryTypeManaged ||
+      at.type == hipMemoryTypeUnified)
+    return p;
+  if (at.type == hipMemoryTypeHost) {
+    if (!at.devicePointer) return p;
+    // the device address of p itself, whether the query reported p or the
+    // start of its allocation
+    const char* hp = static_cast<const char*>(at.hostPointer ? at.hostPointer : p);
+    return static_cast<const char*>(at.devicePointer) + (static_cast<const char*>(p) - hp);
+  }
+  return nullptr;
+}
 
 ckv_status launch_gather(const ckv_dims* d, const void* k_src, const void* v_src,
                          const int32_t* sel, int64_t k, void* k_dst, void* v_dst, hipStream_t st) {

@@ -18,9 +18,10 @@
 // P_{l+1} = S_l).  When layer l+1 has selected S_{l+1}, only the difference
 // S_{l+1} \ P_{l+1} is fetched on a demand stream into the free slots behind
 // the prefetched ones, and the attention reads every kept chunk through a
-// chunk -> slot table.  Copies move whole chunk spans; runs of consecutive
-// chunks are merged into one copy.  The selection is the step's only
-// device -> host dependency.
+// chunk -> slot table.  Copies move whole chunk spans, by a kernel that reads
+// the pinned store over the host link (one launch per list of chunks instead
+// of one DMA copy per run of consecutive chunks).  The selection is the
+// step's only device -> host dependency.
 
 #include <cstring>
 #include <new>
@@ -47,6 +48,12 @@ struct ckv_ctx {
   int32_t* slot_tab_dev[2] = {nullptr, nullptr};
   int32_t* sel_host = nullptr;      // pinned [k]
   int32_t* slot_tab_host[2] = {nullptr, nullptr};  // pinned [k]
+  // chunk lists of the copy kernels: misses (demand) and the prediction
+  // (prefetch) of each slot buffer, staged in pinned memory, read on the device
+  int32_t* dem_host[2] = {nullptr, nullptr};
+  int32_t* pref_host[2] = {nullptr, nullptr};
+  int32_t* dem_dev[2] = {nullptr, nullptr};
+  int32_t* pref_dev[2] = {nullptr, nullptr};
   hipStream_t demand = nullptr, prefetch = nullptr;
   hipEvent_t ev_sel = nullptr, ev_dem = nullptr, ev_pref[2] = {nullptr, nullptr},
              ev_attn[2] = {nullptr, nullptr};
@@ -77,6 +84,10 @@ ckv_status free_ctx(ckv_ctx* c) {
     (void)hipFree(c->slots[i]);
     (void)hipFree(c->slot_tab_dev[i]);
     (void)hipHostFree(c->slot_tab_host[i]);
+    (void)hipFree(c->dem_dev[i]);
+    (void)hipFree(c->pref_dev[i]);
+    (void)hipHostFree(c->dem_host[i]);
+    (void)hipHostFree(c->pref_host[i]);
     if (c->ev_pref[i]) (void)hipEventDestroy(c->ev_pref[i]);
     if (c->ev_attn[i]) (void)hipEventDestroy(c->ev_attn[i]);
   }
@@ -101,22 +112,6 @@ ckv_status free_ctx(ckv_ctx* c) {
       return e_ == hipErrorOutOfMemory ? CKV_ENOMEM : CKV_EHIP;                          \
     }                                                                                    \
   } while (0)
-
-// Copies chunks[0..cnt) (ascending chunk indices) into consecutive slots
-// starting at slot0, one hipMemcpyAsync per run of consecutive chunk indices.
-ckv_status copy_runs(ckv_ctx* c, const int32_t* chunks, int64_t cnt, int64_t slot0,
-                     const void* host, void* buf, hipStream_t st) {
-  int64_t i = 0;
-  while (i < cnt) {
-    int64_t j = i + 1;
-    while (j < cnt && chunks[j] == chunks[j - 1] + 1) ++j;
-    const char* src = static_cast<const char*>(host) + (int64_t)chunks[i] * c->slot_bytes;
-    char* dst = static_cast<char*>(buf) + (slot0 + i) * c->slot_bytes;
-    CKV_HIP(hipMemcpyAsync(dst, src, (size_t)((j - i) * c->slot_bytes), hipMemcpyHostToDevice, st));
-    i = j;
-  }
-  return CKV_OK;
-}
 
 bool all_stages(const ckv_ctx* c) { return c->flags & CKV_CTX_STAGE_TIMING; }
 
@@ -198,6 +193,12 @@ ckv_status ckv_ctx_create(const ckv_dims* dims, double keep_ratio, int32_t flags
       CKV_HIP_ALLOC(hipMalloc((void**)&c->slot_tab_dev[i], (size_t)c->k * sizeof(int32_t)));
       CKV_HIP_ALLOC(hipHostMalloc((void**)&c->slot_tab_host[i], (size_t)c->k * sizeof(int32_t),
                                   hipHostMallocDefault));
+      CKV_HIP_ALLOC(hipMalloc((void**)&c->dem_dev[i], (size_t)c->k * sizeof(int32_t)));
+      CKV_HIP_ALLOC(hipMalloc((void**)&c->pref_dev[i], (size_t)c->k * sizeof(int32_t)));
+      CKV_HIP_ALLOC(hipHostMalloc((void**)&c->dem_host[i], (size_t)c->k * sizeof(int32_t),
+                                  hipHostMallocDefault));
+      CKV_HIP_ALLOC(hipHostMalloc((void**)&c->pref_host[i], (size_t)c->k * sizeof(int32_t),
+                                  hipHostMallocDefault));
       CKV_HIP_ALLOC(hipEventCreateWithFlags(&c->ev_pref[i], hipEventDisableTiming));
       CKV_HIP_ALLOC(hipEventCreateWithFlags(&c->ev_attn[i], hipEventDisableTiming));
     }
@@ -263,6 +264,8 @@ ckv_status ckv_reprefill_layer(ckv_ctx* c, int32_t layer, const ckv_layer_io* io
   if (!c || !io) CKV_FAIL(CKV_EINVAL, "NULL ctx or io");
   const ckv_dims* d = &c->dims;
   const bool host = c->flags & CKV_CTX_HOST_PREFIX;
+  const void* store = nullptr;       // kv_host as the device reads it
+  const void* store_next = nullptr;  // kv_host_next as the device reads it
   if (!io->q || !io->k_suffix || !io->v_suffix || !io->k_probe || !io->out)
     CKV_FAIL(CKV_EINVAL, "NULL tensor in io");
   if (!aligned16(io->q) || !aligned16(io->k_suffix) || !aligned16(io->v_suffix) ||
@@ -273,6 +276,13 @@ ckv_status ckv_reprefill_layer(ckv_ctx* c, int32_t layer, const ckv_layer_io* io
     if (layer != c->next_layer)
       CKV_FAIL(CKV_ESTATE, "host-resident layers must run in order (expected %d, got %d)",
                c->next_layer, layer);
+    // the copy kernels read the stores through the device's mapping of them
+    store = device_view(io->kv_host);
+    if (!store) CKV_FAIL(CKV_EINVAL, "kv_host must be pinned host memory (hipHostMalloc)");
+    if (io->kv_host_next) {
+      store_next = device_view(io->kv_host_next);
+      if (!store_next) CKV_FAIL(CKV_EINVAL, "kv_host_next must be pinned host memory (hipHostMalloc)");
+    }
   } else {
     if (!io->k_prefix || !io->v_prefix) CKV_FAIL(CKV_EINVAL, "HBM-resident prefix needs k/v_prefix");
     if (!aligned16(io->k_prefix) || !aligned16(io->v_prefix))
@@ -396,9 +406,14 @@ ckv_status ckv_reprefill_layer(ckv_ctx* c, int32_t layer, const ckv_layer_io* io
 
   // demand copies into this layer's buffer (after the attention that last used it)
   if (c->attn_recorded[cur]) CKV_HIP(hipStreamWaitEvent(c->demand, c->ev_attn[cur], 0));
-  s = copy_runs(c, miss.data(), (int64_t)miss.size(), (int64_t)P.size(), io->kv_host, c->slots[cur],
-                c->demand);
-  if (s != CKV_OK) return s;
+  if (!miss.empty()) {
+    std::memcpy(c->dem_host[cur], miss.data(), miss.size() * sizeof(int32_t));
+    CKV_HIP(hipMemcpyAsync(c->dem_dev[cur], c->dem_host[cur], miss.size() * sizeof(int32_t),
+                           hipMemcpyHostToDevice, c->demand));
+    s = launch_copy_spans(store, c->dem_dev[cur], (int64_t)miss.size(), (int64_t)P.size(),
+                          c->slots[cur], c->slot_bytes, c->demand);
+    if (s != CKV_OK) return s;
+  }
   CKV_HIP(hipMemcpyAsync(c->slot_tab_dev[cur], tab, (size_t)k * sizeof(int32_t),
                          hipMemcpyHostToDevice, c->demand));
   CKV_HIP(hipEventRecord(c->ev_dem, c->demand));
@@ -421,7 +436,11 @@ ckv_status ckv_reprefill_layer(ckv_ctx* c, int32_t layer, const ckv_layer_io* io
   c->pred.assign(c->sel_host, c->sel_host + k);
   if (io->kv_host_next) {
     if (c->attn_recorded[nxt]) CKV_HIP(hipStreamWaitEvent(c->prefetch, c->ev_attn[nxt], 0));
-    s = copy_runs(c, c->pred.data(), k, 0, io->kv_host_next, c->slots[nxt], c->prefetch);
+    std::memcpy(c->pref_host[nxt], c->pred.data(), (size_t)k * sizeof(int32_t));
+    CKV_HIP(hipMemcpyAsync(c->pref_dev[nxt], c->pref_host[nxt], (size_t)k * sizeof(int32_t),
+                           hipMemcpyHostToDevice, c->prefetch));
+    s = launch_copy_spans(store_next, c->pref_dev[nxt], k, 0, c->slots[nxt], c->slot_bytes,
+                          c->prefetch);
     if (s != CKV_OK) return s;
     CKV_HIP(hipEventRecord(c->ev_pref[nxt], c->prefetch));
     c->pref_pending[nxt] = true;
