@@ -47,29 +47,38 @@ __global__ __launch_bounds__(kThreads) void gather_kernel(const uint8_t* __restr
   }
 }
 
-// Whole-span copies for the host-resident prefix: grid x = 16 KiB pieces of a
-// span, y = list entry.  From pinned host memory every load crosses the host
-// link; thousands of 16-byte loads in flight keep it busy where one DMA copy
-// per run of chunks would pay a fixed cost per copy.
+// Whole-span copies for the host-resident prefix.  A small fixed grid walks
+// all 16 KiB pieces of all listed spans (grid-stride), so the copy keeps
+// thousands of 16-byte loads in flight over the host link -- one launch per
+// list instead of one DMA copy per run of chunks -- while occupying only a
+// few wave slots per CU, next to the compute kernels it overlaps.
+constexpr int kCopyBlocks = 32;
+
 __global__ __launch_bounds__(kThreads) void copy_spans_kernel(const uint8_t* __restrict__ src,
                                                               const int32_t* __restrict__ chunks,
-                                                              int64_t slot0,
+                                                              int64_t count, int64_t slot0,
                                                               uint8_t* __restrict__ dst,
                                                               int64_t span_bytes) {
-  const int64_t i = blockIdx.y;
-  const uint8_t* s = src + (int64_t)chunks[i] * span_bytes;
-  uint8_t* d = dst + (slot0 + i) * span_bytes;
-  const int64_t base = ((int64_t)blockIdx.x * kThreads * kUnroll + threadIdx.x) * 16;
-  u32x4 v[kUnroll];
+  constexpr int64_t kPiece = (int64_t)kThreads * kUnroll * 16;
+  const int64_t per_span = (span_bytes + kPiece - 1) / kPiece;
+  const int64_t total = count * per_span;
+  for (int64_t w = blockIdx.x; w < total; w += gridDim.x) {
+    const int64_t i = w / per_span, piece = w % per_span;
+    const uint8_t* s = src + (int64_t)chunks[i] * span_bytes;
+    uint8_t* d = dst + (slot0 + i) * span_bytes;
+    const int64_t base = piece * kPiece + (int64_t)threadIdx.x * 16;
+    u32x4 v[kUnroll];
 #pragma unroll
-  for (int p = 0; p < kUnroll; ++p) {
-    const int64_t off = base + (int64_t)p * kThreads * 16;
-    if (off < span_bytes) v[p] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(s + off));
-  }
+    for (int p = 0; p < kUnroll; ++p) {
+      const int64_t off = base + (int64_t)p * kThreads * 16;
+      if (off < span_bytes)
+        v[p] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(s + off));
+    }
 #pragma unroll
-  for (int p = 0; p < kUnroll; ++p) {
-    const int64_t off = base + (int64_t)p * kThreads * 16;
-    if (off < span_bytes) *reinterpret_cast<u32x4*>(d + off) = v[p];
+    for (int p = 0; p < kUnroll; ++p) {
+      const int64_t off = base + (int64_t)p * kThreads * 16;
+      if (off < span_bytes) *reinterpret_cast<u32x4*>(d + off) = v[p];
+    }
   }
 }
 
@@ -78,15 +87,13 @@ __global__ __launch_bounds__(kThreads) void copy_spans_kernel(const uint8_t* __r
 ckv_status launch_copy_spans(const void* src, const int32_t* chunks, int64_t count, int64_t slot0,
                              void* dst, int64_t span_bytes, hipStream_t st) {
   if (span_bytes % 16 != 0) CKV_FAIL(CKV_EINVAL, "span bytes must be a multiple of 16");
-  constexpr int64_t kMaxY = 65535;  // grid y limit: launch in batches
-  for (int64_t b = 0; b < count; b += kMaxY) {
-    const int64_t nb = std::min<int64_t>(kMaxY, count - b);
-    dim3 grid((unsigned)ceil_div(span_bytes, (int64_t)kThreads * kUnroll * 16), (unsigned)nb);
-    hipLaunchKernelGGL(copy_spans_kernel, grid, dim3(kThreads), 0, st,
-                       static_cast<const uint8_t*>(src), chunks + b, slot0 + b,
-                       static_cast<uint8_t*>(dst), span_bytes);
-    CKV_HIP(hipGetLastError());
-  }
+  if (count == 0) return CKV_OK;
+  const int64_t pieces = count * ceil_div(span_bytes, (int64_t)kThreads * kUnroll * 16);
+  const unsigned grid = (unsigned)std::min<int64_t>(pieces, kCopyBlocks);
+  hipLaunchKernelGGL(copy_spans_kernel, dim3(grid), dim3(kThreads), 0, st,
+                     static_cast<const uint8_t*>(src), chunks, count, slot0,
+                     static_cast<uint8_t*>(dst), span_bytes);
+  CKV_HIP(hipGetLastError());
   return CKV_OK;
 }
 

@@ -404,8 +404,11 @@ ckv_status ckv_reprefill_layer(ckv_ctx* c, int32_t layer, const ckv_layer_io* io
   stv.misses = (int64_t)miss.size();
   stv.wasted = (int64_t)P.size() - hits;
 
-  // demand copies into this layer's buffer (after the attention that last used it)
+  // demand copies into this layer's buffer (after the attention that last used it);
+  // the small index copies go first, so they never queue behind span copies
   if (c->attn_recorded[cur]) CKV_HIP(hipStreamWaitEvent(c->demand, c->ev_attn[cur], 0));
+  CKV_HIP(hipMemcpyAsync(c->slot_tab_dev[cur], tab, (size_t)k * sizeof(int32_t),
+                         hipMemcpyHostToDevice, c->demand));
   if (!miss.empty()) {
     std::memcpy(c->dem_host[cur], miss.data(), miss.size() * sizeof(int32_t));
     CKV_HIP(hipMemcpyAsync(c->dem_dev[cur], c->dem_host[cur], miss.size() * sizeof(int32_t),
@@ -414,8 +417,6 @@ ckv_status ckv_reprefill_layer(ckv_ctx* c, int32_t layer, const ckv_layer_io* io
                           c->slots[cur], c->slot_bytes, c->demand);
     if (s != CKV_OK) return s;
   }
-  CKV_HIP(hipMemcpyAsync(c->slot_tab_dev[cur], tab, (size_t)k * sizeof(int32_t),
-                         hipMemcpyHostToDevice, c->demand));
   CKV_HIP(hipEventRecord(c->ev_dem, c->demand));
 
   CKV_HIP(hipStreamWaitEvent(st, c->ev_dem, 0));
@@ -436,6 +437,9 @@ ckv_status ckv_reprefill_layer(ckv_ctx* c, int32_t layer, const ckv_layer_io* io
   c->pred.assign(c->sel_host, c->sel_host + k);
   if (io->kv_host_next) {
     if (c->attn_recorded[nxt]) CKV_HIP(hipStreamWaitEvent(c->prefetch, c->ev_attn[nxt], 0));
+    // after this layer's demand copies: those are on the critical path and get
+    // the host link to themselves
+    CKV_HIP(hipStreamWaitEvent(c->prefetch, c->ev_dem, 0));
     std::memcpy(c->pref_host[nxt], c->pred.data(), (size_t)k * sizeof(int32_t));
     CKV_HIP(hipMemcpyAsync(c->pref_dev[nxt], c->pref_host[nxt], (size_t)k * sizeof(int32_t),
                            hipMemcpyHostToDevice, c->prefetch));
