@@ -347,17 +347,6 @@ __global__ __launch_bounds__(kWaves * 64, 2) void attn_kernel(AttnArgs a) {
   const int tile0 = split * a.tiles_per_split;
   const int nt = max(0, min(ntiles, tile0 + a.tiles_per_split) - tile0);
 
-  bf16x8 qf[D / 16];
-  {
-    const uint16_t* src = a.q + ((int64_t)(row_ok ? t : 0) * a.Hq + (int64_t)g * a.G + hi) * D + 8 * half;
-#pragma unroll
-    for (int ks = 0; ks < D / 16; ++ks) {
-      u32x4 v = *reinterpret_cast<const u32x4*>(src + 16 * ks);
-      if (!row_ok) v = u32x4{0u, 0u, 0u, 0u};
-      qf[ks] = *reinterpret_cast<bf16x8*>(&v);
-    }
-  }
-
   // key tables of the slice, one stage per wave at a time, and whether a stage
   // has a key some row of the block must not see; all index loads first
   constexpr int kMaxIt = kMaxSliceKeys / kTile / kWaves;
@@ -368,6 +357,18 @@ __global__ __launch_bounds__(kWaves * 64, 2) void attn_kernel(AttnArgs a) {
     jv[it] = 0;
     sv[it] = 0;
     if (st < nt) key_chunk_loads(a, (tile0 + st) * kTile + lane, jv[it], sv[it]);
+  }
+  // Q after the index loads: loads return in order, so the key tables (on the
+  // critical path to the first K/V loads) do not wait for Q
+  bf16x8 qf[D / 16];
+  {
+    const uint16_t* src = a.q + ((int64_t)(row_ok ? t : 0) * a.Hq + (int64_t)g * a.G + hi) * D + 8 * half;
+#pragma unroll
+    for (int ks = 0; ks < D / 16; ++ks) {
+      u32x4 v = *reinterpret_cast<const u32x4*>(src + 16 * ks);
+      if (!row_ok) v = u32x4{0u, 0u, 0u, 0u};
+      qf[ks] = *reinterpret_cast<bf16x8*>(&v);
+    }
   }
 #pragma unroll
   for (int it = 0; it < kMaxIt; ++it) {

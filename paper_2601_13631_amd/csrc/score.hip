@@ -442,13 +442,16 @@ __device__ __forceinline__ void segment_reference(const ScoreArgs& a, const bf16
   process_subtile<D, MODE, 1, false>(a, qf, lds, 0, 0, nkeys, nullptr, my_row0, st);
 }
 
+template <int D>
+__device__ __forceinline__ void load_q(const ScoreArgs& a, int g, int row0, bf16x8 (&qf)[2][D / 16]);
+
 // PASS 0 over one segment (keys kbeg .. kbeg+nkeys-1 of KV head g): the
 // reference from the first subtile, pipelined full stages, then the short tail
 // stage (if any) through process_subtile.  Returns whether a chunk sum may have
 // left the guard (then the fallback kernel redoes the segment exactly).
 template <int D, int MODE>
 __device__ __forceinline__ bool run_segment_fast(const ScoreArgs& a, int g, int64_t kbeg, int nkeys,
-                                                 int row0, const bf16x8 (&qf)[2][D / 16],
+                                                 int row0, bf16x8 (&qf)[2][D / 16],
                                                  uint16_t* lds, RangeState& st) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int nstage = (nkeys + kStage - 1) / kStage;
@@ -465,13 +468,17 @@ __device__ __forceinline__ bool run_segment_fast(const ScoreArgs& a, int g, int6
   constexpr int kBuf = kStage * SubtileLds<D>::kRow;  // elements per LDS stage buffer
 
   StageRegs<D> r;
-  if (nfull > 0) {
+  if (nfull > 0)
     stage_load_full<D>(kbase, o, r);
-    stage_store<D, true>(r, lds);
-  } else {
+  else
     stage_load<D>(kbase, nkeys, o, r);
+  // Q after the first stage's loads: loads return in order, so the stage's
+  // LDS store and barrier do not wait for Q
+  load_q<D>(a, g, row0, qf);
+  if (nfull > 0)
+    stage_store<D, true>(r, lds);
+  else
     stage_store<D, false>(r, lds);
-  }
   __syncthreads();
   segment_reference<D, MODE>(a, qf, lds, nkeys, my_row0, st);
   f32x16 carry[2];
@@ -707,8 +714,7 @@ __global__ __launch_bounds__(kWaves * 64, 2) void score_bf16_kernel(ScoreArgs a)
   if (w >= a.nwg) return;
   const Segment sg = segment_of(a.w, a.n, (int)w);
   const int g = sg.rbh / a.w.RB, row0 = (sg.rbh % a.w.RB) * kBlockRows;
-  bf16x8 qf[2][D / 16];
-  load_q<D>(a, g, row0, qf);
+  bf16x8 qf[2][D / 16];  // loaded by run_segment_fast
   RangeState st;
   const bool of = run_segment_fast<D, MODE>(a, g, sg.kbeg, sg.nkeys, row0, qf, lds, st);
   const int any_of = __syncthreads_or(of ? 1 : 0);
