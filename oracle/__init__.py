@@ -57,6 +57,14 @@ class _Stats(ctypes.Structure):
                 ("k", "hits", "misses", "wasted", "bytes_prefetch", "bytes_demand", "bytes_used")]
 
 
+class _IoCounts(ctypes.Structure):
+    _fields_ = [(f, ctypes.c_int64) for f in ("tokens_selected", "runs", "blocks", "tokens_block")]
+
+
+class _CacheCounts(ctypes.Structure):
+    _fields_ = [(f, ctypes.c_int64) for f in ("hits_gpu", "hits_cpu", "misses", "demoted", "dropped")]
+
+
 @dataclass(frozen=True)
 class Shape:
     n_prefix: int
@@ -100,9 +108,18 @@ def load(path: str):
                                         ctypes.POINTER(_Stats)]
     L.ckvo_reprefill_layer.argtypes = [SP, ctypes.c_double, P, P, P, P, P, P, P,
                                        ctypes.POINTER(ctypes.c_int64), P, ctypes.c_int]
+    L.ckvo_io_account.argtypes = [ctypes.c_int64, ctypes.c_int32, P, ctypes.c_int64,
+                                  ctypes.c_int32, ctypes.POINTER(_IoCounts)]
+    L.ckvo_cache_create.argtypes = [ctypes.c_int64, ctypes.c_int64, ctypes.c_int64, ctypes.c_int]
+    L.ckvo_cache_create.restype = P
+    L.ckvo_cache_destroy.argtypes = [P]
+    L.ckvo_cache_destroy.restype = None
+    L.ckvo_cache_access.argtypes = [P, P, P, ctypes.c_int64, P, ctypes.POINTER(_CacheCounts)]
+    L.ckvo_cache_state.argtypes = [P, P, P, P]
     for f in ("ckvo_token_importance", "ckvo_chunk_scores", "ckvo_select_topk",
               "ckvo_sparse_attn", "ckvo_dense_attn", "ckvo_gather_chunks",
-              "ckvo_layer_accounting", "ckvo_reprefill_layer"):
+              "ckvo_layer_accounting", "ckvo_reprefill_layer", "ckvo_io_account",
+              "ckvo_cache_access", "ckvo_cache_state"):
         getattr(L, f).restype = ctypes.c_int
     return L
 
@@ -273,3 +290,58 @@ def reprefill_layer(shape: Shape, keep_ratio: float, q, k_prefix, v_prefix, k_su
                                       _ptr(ks), _ptr(vs), _ptr(A), _ptr(sel), ctypes.byref(kk),
                                       _ptr(out), threads), "reprefill_layer")
     return A, sel[: kk.value].copy(), out
+
+
+def io_account(n: int, c: int, sel, block_tokens: int) -> dict:
+    """Tokens a ContiguousChunk store reads for the chunk set `sel` against a
+    store of fixed `block_tokens`-token blocks (Sec. 4.2; Sec. 3)."""
+    sel = np.ascontiguousarray(sel, np.int32)
+    out = _IoCounts()
+    _check(lib().ckvo_io_account(n, c, _ptr(sel), sel.size, block_tokens, ctypes.byref(out)),
+           "io_account")
+    return {f: int(getattr(out, f)) for f, _ in _IoCounts._fields_}
+
+
+CACHE_ATTENTION, CACHE_LFU = 0, 1
+TIER_NONE, TIER_CPU, TIER_GPU = 0, 1, 2
+
+
+class Cache:
+    """Attention-guided two-tier cache of Sec. 4.5 (Eq. 2); see ckv_oracle.h."""
+
+    def __init__(self, n_keys: int, gpu_slots: int, cpu_slots: int, policy: int = CACHE_ATTENTION):
+        self.n_keys = n_keys
+        self._h = lib().ckvo_cache_create(n_keys, gpu_slots, cpu_slots, policy)
+        if not self._h:
+            raise OracleError("cache_create failed")
+
+    def access(self, keys, scores):
+        """One request's used chunks; returns (tier each key was found in, totals)."""
+        keys = np.ascontiguousarray(keys, np.int64)
+        scores = np.ascontiguousarray(scores, np.float64)
+        if keys.size != scores.size:
+            raise ValueError("keys and scores differ in length")
+        where = np.zeros(keys.size, np.int8)
+        cnt = _CacheCounts()
+        _check(lib().ckvo_cache_access(self._h, _ptr(keys), _ptr(scores), keys.size, _ptr(where),
+                                       ctypes.byref(cnt)), "cache_access")
+        return where, {f: int(getattr(cnt, f)) for f, _ in _CacheCounts._fields_}
+
+    def state(self):
+        """(I, F, tier) arrays over every key."""
+        I = np.zeros(self.n_keys, np.float64)
+        F = np.zeros(self.n_keys, np.int64)
+        tier = np.zeros(self.n_keys, np.int8)
+        _check(lib().ckvo_cache_state(self._h, _ptr(I), _ptr(F), _ptr(tier)), "cache_state")
+        return I, F, tier
+
+    def close(self) -> None:
+        if self._h:
+            lib().ckvo_cache_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

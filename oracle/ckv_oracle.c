@@ -19,6 +19,7 @@
 #define _GNU_SOURCE
 #include "ckv_oracle.h"
 
+#include <float.h>
 #include <math.h>
 #include <pthread.h>
 #include <stdlib.h>
@@ -491,4 +492,203 @@ int ckvo_reprefill_layer(const ckvo_shape* s, double keep_ratio, const void* q,
   free(a);
   *k_out = k;
   return rc;
+}
+
+/* ------------------------------------------------------------------------- */
+/* read accounting against a store of fixed blocks                           */
+/* ------------------------------------------------------------------------- */
+
+/* Sec. 4.2 and Sec. 3 (Motivation 1): mark every token of every selected
+ * chunk, then visit the store's blocks of b consecutive tokens one by one; a
+ * block with a marked token is read whole (the last block holds n mod b tokens
+ * when b does not divide n). */
+int ckvo_io_account(int64_t n, int32_t c, const int32_t* sel, int64_t k, int32_t b,
+                    ckvo_io_counts* out) {
+  if (n < 1 || c < 1 || b < 1 || k < 0 || !out || (k > 0 && !sel)) return -1;
+  int64_t m = ckvo_num_chunks(n, c);
+  if (k > m) return -1;
+  unsigned char* chunk_marked = (unsigned char*)calloc((size_t)m, 1);
+  unsigned char* token_marked = (unsigned char*)calloc((size_t)n, 1);
+  if (!chunk_marked || !token_marked) {
+    free(chunk_marked);
+    free(token_marked);
+    return -2;
+  }
+  int rc = 0;
+  for (int64_t u = 0; u < k && rc == 0; ++u) {
+    int64_t j = sel[u];
+    if (j < 0 || j >= m || chunk_marked[j]) {
+      rc = -1;
+      break;
+    }
+    chunk_marked[j] = 1;
+    for (int64_t t = j * c; t < (j + 1) * c && t < n; ++t) token_marked[t] = 1;
+  }
+  if (rc == 0) {
+    memset(out, 0, sizeof *out);
+    for (int64_t t = 0; t < n; ++t) out->tokens_selected += token_marked[t];
+    for (int64_t j = 0; j < m; ++j)
+      if (chunk_marked[j] && (j == 0 || !chunk_marked[j - 1])) out->runs++;
+    for (int64_t first = 0; first < n; first += b) {
+      int64_t last = first + b < n ? first + b : n;
+      int any = 0;
+      for (int64_t t = first; t < last; ++t) any |= token_marked[t];
+      if (any) {
+        out->blocks++;
+        out->tokens_block += last - first;
+      }
+    }
+  }
+  free(chunk_marked);
+  free(token_marked);
+  return rc;
+}
+
+/* ------------------------------------------------------------------------- */
+/* attention-guided cache                                                     */
+/* ------------------------------------------------------------------------- */
+
+struct ckvo_cache {
+  int64_t n_keys, gpu_slots, cpu_slots;
+  int policy;
+  double* I;      /* cumulative importance: sum of A over the key's accesses */
+  int64_t* F;     /* accesses */
+  int64_t* last;  /* time of the key's latest access (0: never) */
+  int8_t* tier;
+  int64_t clock;
+  ckvo_cache_counts counts;
+};
+
+ckvo_cache* ckvo_cache_create(int64_t n_keys, int64_t gpu_slots, int64_t cpu_slots, int policy) {
+  if (n_keys < 1 || gpu_slots < 0 || cpu_slots < 0) return NULL;
+  if (policy != CKVO_CACHE_ATTENTION && policy != CKVO_CACHE_LFU) return NULL;
+  ckvo_cache* c = (ckvo_cache*)calloc(1, sizeof *c);
+  if (!c) return NULL;
+  c->n_keys = n_keys;
+  c->gpu_slots = gpu_slots;
+  c->cpu_slots = cpu_slots;
+  c->policy = policy;
+  c->I = (double*)calloc((size_t)n_keys, sizeof(double));
+  c->F = (int64_t*)calloc((size_t)n_keys, sizeof(int64_t));
+  c->last = (int64_t*)calloc((size_t)n_keys, sizeof(int64_t));
+  c->tier = (int8_t*)calloc((size_t)n_keys, 1);
+  if (!c->I || !c->F || !c->last || !c->tier) {
+    ckvo_cache_destroy(c);
+    return NULL;
+  }
+  return c;
+}
+
+void ckvo_cache_destroy(ckvo_cache* c) {
+  if (!c) return;
+  free(c->I);
+  free(c->F);
+  free(c->last);
+  free(c->tier);
+  free(c);
+}
+
+/* Eq. 2: S = I * F; the frequency-only foil ranks by F alone. */
+static double cache_score(const ckvo_cache* c, int64_t x) {
+  if (c->policy == CKVO_CACHE_LFU) return (double)c->F[x];
+  return c->I[x] * (double)c->F[x];
+}
+
+/* Eviction order: the lower score leaves first; among equal scores, the key
+ * whose latest access is older. */
+static int leaves_before(const ckvo_cache* c, int64_t x, int64_t y) {
+  double sx = cache_score(c, x), sy = cache_score(c, y);
+  if (sx != sy) return sx < sy;
+  return c->last[x] < c->last[y];
+}
+
+/* The key of `tier` that leaves first (-1 if the tier is empty); *count gets
+ * the tier's occupancy.  A linear scan over every key. */
+static int64_t tier_first_out(const ckvo_cache* c, int tier, int64_t* count) {
+  int64_t best = -1, cnt = 0;
+  for (int64_t x = 0; x < c->n_keys; ++x) {
+    if (c->tier[x] != tier) continue;
+    ++cnt;
+    if (best < 0 || leaves_before(c, x, best)) best = x;
+  }
+  *count = cnt;
+  return best;
+}
+
+/* Places x in the CPU tier if there is room or x outranks the CPU tier's
+ * weakest entry (which then leaves memory); otherwise x leaves memory.
+ * Returns 1 when x was placed. */
+static int admit_cpu(ckvo_cache* c, int64_t x) {
+  int64_t cnt;
+  int64_t y = tier_first_out(c, CKVO_TIER_CPU, &cnt);
+  if (cnt < c->cpu_slots) {
+    c->tier[x] = CKVO_TIER_CPU;
+    return 1;
+  }
+  if (y >= 0 && leaves_before(c, y, x)) {
+    c->tier[y] = CKVO_TIER_NONE;
+    c->counts.dropped++;
+    c->tier[x] = CKVO_TIER_CPU;
+    return 1;
+  }
+  c->tier[x] = CKVO_TIER_NONE;
+  c->counts.dropped++;
+  return 0;
+}
+
+/* Places x in the GPU tier if there is room or x outranks the GPU tier's
+ * weakest entry, which then goes down to the CPU tier (or out of memory);
+ * otherwise x itself goes to the CPU tier. */
+static void admit_gpu(ckvo_cache* c, int64_t x) {
+  int64_t cnt;
+  int64_t y = tier_first_out(c, CKVO_TIER_GPU, &cnt);
+  if (cnt < c->gpu_slots) {
+    c->tier[x] = CKVO_TIER_GPU;
+    return;
+  }
+  if (y >= 0 && leaves_before(c, y, x)) {
+    c->tier[y] = CKVO_TIER_NONE;
+    c->tier[x] = CKVO_TIER_GPU;
+    c->counts.demoted += admit_cpu(c, y);
+    return;
+  }
+  admit_cpu(c, x);
+}
+
+/* Sec. 4.5: for each used chunk in order, note where it was found, add its
+ * attention score to I and one access to F, then re-place it by its new
+ * cache score: GPU tier first, then CPU tier, evicting the weakest entries. */
+int ckvo_cache_access(ckvo_cache* c, const int64_t* keys, const double* A, int64_t count,
+                      int8_t* tier_before, ckvo_cache_counts* counts) {
+  if (!c || count < 0 || (count > 0 && (!keys || !A))) return -1;
+  for (int64_t u = 0; u < count; ++u) {
+    if (keys[u] < 0 || keys[u] >= c->n_keys || !(A[u] >= 0.0) || A[u] > DBL_MAX) return -1;
+    for (int64_t v = 0; v < u; ++v)
+      if (keys[v] == keys[u]) return -1;
+  }
+  for (int64_t u = 0; u < count; ++u) {
+    int64_t x = keys[u];
+    int8_t was = c->tier[x];
+    if (tier_before) tier_before[u] = was;
+    if (was == CKVO_TIER_GPU) c->counts.hits_gpu++;
+    else if (was == CKVO_TIER_CPU) c->counts.hits_cpu++;
+    else c->counts.misses++;
+    c->I[x] += A[u];
+    c->F[x] += 1;
+    c->last[x] = ++c->clock;
+    c->tier[x] = CKVO_TIER_NONE;
+    admit_gpu(c, x);
+  }
+  if (counts) *counts = c->counts;
+  return 0;
+}
+
+int ckvo_cache_state(const ckvo_cache* c, double* I, int64_t* F, int8_t* tier) {
+  if (!c) return -1;
+  for (int64_t x = 0; x < c->n_keys; ++x) {
+    if (I) I[x] = c->I[x];
+    if (F) F[x] = c->F[x];
+    if (tier) tier[x] = c->tier[x];
+  }
+  return 0;
 }

@@ -103,6 +103,51 @@ typedef struct {
 int ckvo_layer_accounting(const ckvo_shape* s, const int32_t* sel, int64_t k,
                           const int32_t* pred, int64_t n_pred, ckvo_layer_stats* st);
 
+/* Read accounting (Sec. 4.2; Sec. 3, Motivation 1).  A ContiguousChunk store
+ * reads exactly the tokens of the selected chunks; a store cut into fixed
+ * blocks of b consecutive tokens (the comparison systems use 64) reads every
+ * block that holds at least one of them.  sel holds k distinct chunk indices in
+ * [0, ceil(n/c)), any order.  Counts:
+ *   tokens_selected  tokens of the selected chunks (the last chunk clamped to n)
+ *   runs             maximal runs of consecutive selected chunks
+ *   blocks           blocks holding a selected token
+ *   tokens_block     tokens in those blocks (the last block clamped to n) */
+typedef struct {
+  int64_t tokens_selected, runs, blocks, tokens_block;
+} ckvo_io_counts;
+int ckvo_io_account(int64_t n, int32_t c, const int32_t* sel, int64_t k, int32_t b,
+                    ckvo_io_counts* out);
+
+/* Attention-guided cache management (Sec. 4.5, Eq. 2).  Keys 0..n_keys-1 name
+ * cacheable ContiguousChunks.  Every key keeps I (sum of the attention scores A
+ * of its accesses), F (number of accesses) and the time of its latest access,
+ * for evicted keys too (the in-memory score table).  Two tiers of gpu_slots and
+ * cpu_slots entries hold keys by cache score S = I*F (policy ATTENTION) or S = F
+ * (policy LFU, the ablation's frequency-only foil).  Readings where the paper
+ * is silent: F counts accesses; an accessed key goes to the GPU tier when there
+ * is room or it outranks the GPU tier's weakest entry, which is then demoted to
+ * the CPU tier by the same rule, else the key goes to the CPU tier by that
+ * rule; whatever the CPU tier does not take leaves memory; ranking is by S,
+ * then by latest access (older leaves first).  This oracle finds the weakest
+ * entry by scanning every key. */
+enum { CKVO_CACHE_ATTENTION = 0, CKVO_CACHE_LFU = 1 };
+enum { CKVO_TIER_NONE = 0, CKVO_TIER_CPU = 1, CKVO_TIER_GPU = 2 };
+typedef struct {
+  int64_t hits_gpu, hits_cpu, misses; /* where each accessed key was found        */
+  int64_t demoted;                    /* GPU-tier evictions taken by the CPU tier  */
+  int64_t dropped;                    /* keys that left memory (or never entered)  */
+} ckvo_cache_counts;
+typedef struct ckvo_cache ckvo_cache;
+ckvo_cache* ckvo_cache_create(int64_t n_keys, int64_t gpu_slots, int64_t cpu_slots, int policy);
+void ckvo_cache_destroy(ckvo_cache* c);
+/* One request's used chunks: keys[count] distinct, A[count] finite and >= 0,
+ * processed in the given order.  tier_before[u] (may be NULL) receives where
+ * keys[u] was found; *counts (may be NULL) the totals since creation. */
+int ckvo_cache_access(ckvo_cache* c, const int64_t* keys, const double* A, int64_t count,
+                      int8_t* tier_before, ckvo_cache_counts* counts);
+/* Copies I, F and tier of every key (each pointer may be NULL). */
+int ckvo_cache_state(const ckvo_cache* c, double* I, int64_t* F, int8_t* tier);
+
 /* One Re-Prefill layer of the hot path: token importance, Eq. 1 pooling,
  * top-k at keep ratio r, sparse attention.  Writes A[m], sel[k] and out[S][Hq][d];
  * *k_out receives k. */

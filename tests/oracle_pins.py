@@ -334,4 +334,149 @@ def pin_period_rule():
     assert [list(x) for x in oracle.period_prediction(per_layer, 1)] == [[], [0, 1], [1, 2], [2, 3]]
 
 
+def pin_io_paper_examples():
+    """Read amplification figures the paper prints (Sec. 4.2; Sec. 3, Motivation 1)."""
+    g = json.load(open(os.path.join(GOLDEN, "paper_byte_accounting.json")))
+    b = g["block_tokens"]
+    useful = g["useful_tokens_per_block"]
+    # one 16-token ContiguousChunk inside a 64-token block: the block store reads 4x
+    r = oracle.io_account(b, useful, [1], b)
+    assert r["tokens_selected"] == useful and r["blocks"] == 1 and r["tokens_block"] == b
+    assert r["tokens_block"] // r["tokens_selected"] == g["read_amplification_block"]
+    # a store whose blocks are the ContiguousChunks reads only what is needed
+    r = oracle.io_account(b, useful, [1], useful)
+    assert r["tokens_block"] == r["tokens_selected"] == useful
+    # 11 needed tokens over 9 blocks (token-level selection, c = 1): 52x
+    nb, need = g["example_blocks"], g["example_needed_tokens"]
+    toks = list(range(need - nb + 1)) + [b * i + 7 for i in range(1, nb)]
+    r = oracle.io_account(nb * b, 1, toks, b)
+    assert r["tokens_selected"] == need and r["blocks"] == nb
+    assert int(r["tokens_block"] / r["tokens_selected"]) == g["example_read_amplification"]
+
+
+def pin_io_closed_forms():
+    """Closed forms of block read accounting."""
+    # everything selected: both stores read the whole prefix once, in one run
+    for n, c, b in ((1000, 16, 64), (1001, 32, 64), (77, 5, 9)):
+        m = -(-n // c)
+        r = oracle.io_account(n, c, np.arange(m), b)
+        assert r == {"tokens_selected": n, "runs": 1, "blocks": -(-n // b), "tokens_block": n}
+    # nothing selected
+    assert oracle.io_account(100, 8, [], 64) == dict(tokens_selected=0, runs=0, blocks=0,
+                                                     tokens_block=0)
+    # blocks of one token, or chunks that are whole aligned blocks: no amplification
+    rng = np.random.default_rng(5)
+    for n, c, b in ((4096, 16, 1), (4096, 64, 64), (4096, 128, 64), (5000, 64, 32)):
+        sel = np.sort(rng.choice(-(-n // c), size=20, replace=False))
+        r = oracle.io_account(n, c, sel, b)
+        assert r["tokens_block"] == r["tokens_selected"]
+    # a short last chunk and a short last block: n=5, c=2 (chunk 2 = token 4), b=4
+    assert oracle.io_account(5, 2, [2], 4) == dict(tokens_selected=1, runs=1, blocks=1,
+                                                   tokens_block=1)
+    assert oracle.io_account(5, 2, [1], 4) == dict(tokens_selected=2, runs=1, blocks=1,
+                                                   tokens_block=4)
+    # chunk 1 = tokens 2,3 and chunk 2 = token 4 straddle blocks 0 and 1
+    assert oracle.io_account(5, 2, [1, 2], 4) == dict(tokens_selected=3, runs=1, blocks=2,
+                                                      tokens_block=5)
+
+
+def pin_io_vs_set_algebra():
+    """Random selections against a set formulation: the distinct block ids of the
+    selected tokens, with run starts taken from index gaps."""
+    rng = np.random.default_rng(11)
+    for trial in range(40):
+        n = int(rng.integers(1, 3000))
+        c = int(rng.choice([1, 3, 4, 8, 16, 32, 64]))
+        b = int(rng.choice([1, 7, 16, 64, 100]))
+        m = -(-n // c)
+        k = int(rng.integers(0, m + 1))
+        sel = np.sort(rng.choice(m, size=k, replace=False))
+        tokens = np.concatenate([np.arange(j * c, min((j + 1) * c, n)) for j in sel]) \
+            if k else np.zeros(0, np.int64)
+        blk = np.unique(tokens // b)
+        expect = {"tokens_selected": int(tokens.size),
+                  "runs": int(k and 1 + np.count_nonzero(np.diff(sel) != 1)),
+                  "blocks": int(blk.size),
+                  "tokens_block": int(np.minimum(b, n - blk * b).sum())}
+        assert oracle.io_account(n, c, rng.permutation(sel), b) == expect, (trial, n, c, b)
+
+
+def pin_cache_hand_trace():
+    """Sec. 4.5 rules traced by hand on a 2-slot GPU tier and a 1-slot CPU tier,
+    with dyadic scores so every product is exact."""
+    T0, T1, T2 = oracle.TIER_NONE, oracle.TIER_CPU, oracle.TIER_GPU
+    c = oracle.Cache(6, 2, 1, oracle.CACHE_ATTENTION)
+    # keys 1, 2 fill the GPU tier; key 3 (S=.25) displaces key 2 (S=.125) to the CPU tier
+    w, n = c.access([1, 2, 3], [0.5, 0.125, 0.25])
+    assert list(w) == [T0, T0, T0] and n["misses"] == 3 and n["demoted"] == 1
+    assert list(c.state()[2]) == [T0, T2, T1, T2, T0, T0]
+    # key 2 found in the CPU tier: I=.25, F=2, S=.5 outranks key 3 (.25), which goes down;
+    # key 4 (S=.375) loses to the GPU tier's weakest (key 1: S=.5, older than key 2's .5),
+    # then displaces key 3 (.25) from the CPU tier, which leaves memory
+    w, n = c.access([2, 4], [0.125, 0.375])
+    assert list(w) == [T1, T0] and n == dict(hits_gpu=0, hits_cpu=1, misses=4, demoted=2,
+                                             dropped=1)
+    assert list(c.state()[2]) == [T0, T2, T2, T0, T1, T0]
+    # key 3 returns with I=.75, F=2, S=1.5: key 1 goes down, key 4 leaves memory
+    w, n = c.access([3], [0.5])
+    assert list(w) == [T0] and n == dict(hits_gpu=0, hits_cpu=1, misses=5, demoted=3, dropped=2)
+    I, F, tier = c.state()
+    assert list(tier) == [T0, T1, T2, T2, T0, T0]
+    assert list(I) == [0, 0.5, 0.25, 0.75, 0.375, 0] and list(F) == [0, 1, 2, 2, 1, 0]
+    c.close()
+    # the same stream ranked by frequency alone: ties go to the more recent access
+    c = oracle.Cache(6, 2, 1, oracle.CACHE_LFU)
+    c.access([1, 2, 3], [0.5, 0.125, 0.25])  # key 3 displaces key 1 (equal F, older)
+    assert list(c.state()[2]) == [T0, T1, T2, T2, T0, T0]
+    w, n = c.access([2, 4], [0.125, 0.375])  # key 4 displaces key 3, which displaces key 1
+    assert list(w) == [T2, T0] and n["hits_gpu"] == 1 and n["dropped"] == 1
+    assert list(c.state()[2]) == [T0, T0, T2, T1, T2, T0]
+    w, n = c.access([3], [0.5])  # key 3 (F=2) displaces key 4 (F=1) to the CPU tier
+    assert list(w) == [T1] and list(c.state()[2]) == [T0, T0, T2, T2, T1, T0]
+    c.close()
+
+
+def pin_cache_tiers_are_top_ranks():
+    """With scores that only grow (A >= 0), the cascade keeps the GPU tier equal to
+    the gpu_slots highest-ranked accessed keys under (S, latest access) and the
+    CPU tier equal to the next cpu_slots; checked after every request of random
+    streams by sorting every accessed key."""
+    rng = np.random.default_rng(3)
+    for policy in (oracle.CACHE_ATTENTION, oracle.CACHE_LFU):
+        for n_keys, g, cpu in ((40, 5, 7), (200, 16, 0), (64, 0, 10), (30, 40, 40)):
+            c = oracle.Cache(n_keys, g, cpu, policy)
+            one = oracle.Cache(n_keys, g, cpu, policy)  # fed one key per call
+            I = np.zeros(n_keys)
+            F = np.zeros(n_keys, np.int64)
+            last = np.zeros(n_keys, np.int64)
+            clock = 0
+            pop = rng.zipf(1.5, size=n_keys).astype(np.float64)
+            pop /= pop.sum()
+            for _ in range(60):
+                cnt = int(rng.integers(1, min(12, n_keys) + 1))
+                keys = rng.choice(n_keys, size=cnt, replace=False, p=pop)
+                A = rng.choice([0.0, 0.25, 0.5, 1.0, 3.0], size=cnt)
+                w, tot = c.access(keys, A)
+                for u in range(cnt):  # a request is its keys taken in order
+                    before = one.state()[2][keys[u]]
+                    w1, tot1 = one.access(keys[u:u + 1], A[u:u + 1])
+                    assert w1[0] == before == w[u]
+                assert tot1 == tot
+                for x, a in zip(keys, A):
+                    I[x] += a
+                    F[x] += 1
+                    clock += 1
+                    last[x] = clock
+                S = F.astype(np.float64) if policy == oracle.CACHE_LFU else I * F
+                seen = np.flatnonzero(F > 0)
+                order = seen[np.lexsort((-last[seen], -S[seen]))]
+                tier = c.state()[2]
+                assert set(np.flatnonzero(tier == oracle.TIER_GPU)) == set(order[:g])
+                assert set(np.flatnonzero(tier == oracle.TIER_CPU)) == set(order[g:g + cpu])
+            Io, Fo, _ = c.state()
+            assert np.array_equal(Fo, F) and np.array_equal(Io, I)
+            c.close()
+            one.close()
+
+
 ALL_PINS = [v for k, v in sorted(globals().items()) if k.startswith("pin_")]

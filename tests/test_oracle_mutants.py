@@ -39,6 +39,21 @@ MUTANTS = {
                                 "      st->wasted++;"),
     "keep_floor": ("double x = ceil(r * (double)m - 1e-9);", "double x = floor(r * (double)m);"),
     "chunk_count_floor": ("return (n + c - 1) / c;", "return n / c;"),
+    "io_runs_count_chunks": ("if (chunk_marked[j] && (j == 0 || !chunk_marked[j - 1])) out->runs++;",
+                             "if (chunk_marked[j]) out->runs++;"),
+    "io_last_block_full": ("out->tokens_block += last - first;", "out->tokens_block += b;"),
+    "io_block_decided_by_last_token": ("any |= token_marked[t];", "any = token_marked[t];"),
+    "io_chunk_one_token_short": ("for (int64_t t = j * c; t < (j + 1) * c && t < n; ++t)",
+                                 "for (int64_t t = j * c; t < (j + 1) * c - 1 && t < n; ++t)"),
+    "cache_lfu_uses_importance": ("if (c->policy == CKVO_CACHE_LFU) return (double)c->F[x];",
+                                  "if (c->policy == CKVO_CACHE_LFU) return c->I[x];"),
+    "cache_score_is_importance": ("return c->I[x] * (double)c->F[x];", "return c->I[x];"),
+    "cache_newer_leaves_first": ("return c->last[x] < c->last[y];", "return c->last[x] > c->last[y];"),
+    "cache_gpu_evictions_dropped": ("    c->counts.demoted += admit_cpu(c, y);",
+                                    "    c->counts.dropped++;"),
+    "cache_cpu_never_evicts": ("  if (y >= 0 && leaves_before(c, y, x)) {\n    c->tier[y] = CKVO_TIER_NONE;\n    c->counts.dropped++;",
+                               "  if (0) {\n    c->tier[y] = CKVO_TIER_NONE;\n    c->counts.dropped++;"),
+    "cache_frequency_not_counted": ("c->F[x] += 1;", ";"),
 }
 
 
