@@ -277,6 +277,104 @@ ckv_status ckv_ctx_stage_times(ckv_ctx* ctx, double* ms, int64_t* n_layers);
 ckv_status ckv_reprefill_layer(ckv_ctx* ctx, int32_t layer, const ckv_layer_io* io,
                                ckv_layer_stats* stats);
 
+/* ---------------------------------------------------------------------------
+ * Read accounting -- Sec. 4.2 (a ContiguousChunk store reads exactly the
+ * selected chunks) against Sec. 3, Motivation 1 (a store of fixed coarse
+ * blocks reads every block that holds a needed token: read amplification).
+ * For the selected chunks sel_idx[0..k) of an n-token prefix cut into chunks
+ * of c tokens, counts what both stores read:
+ *   tokens_selected  tokens of the selected chunks (the last chunk clamped to
+ *                    n): what the ContiguousChunk store reads
+ *   runs             maximal runs of consecutive selected chunks: contiguous
+ *                    reads when adjacent chunks are merged
+ *   blocks           blocks of block_tokens consecutive tokens (the
+ *                    comparison systems use 64) holding a selected token
+ *   tokens_block     tokens in those blocks (the last block clamped to n):
+ *                    what the block store reads
+ * Bytes are tokens times the bytes of one token's K and V in one layer; the
+ * block store's read amplification is tokens_block / tokens_selected.
+ *   sel_idx  host int32[k], strictly ascending, each in [0, ceil(n/c))
+ *   k        0 <= k <= ceil(n/c)
+ *   out      host, written
+ * Host-only, pure, O(k).  CKV_EINVAL on n < 1, c < 1, block_tokens < 1, a
+ * NULL pointer, or an index out of range or order (nothing written).
+ * ------------------------------------------------------------------------- */
+typedef struct ckv_io_counts {
+  int64_t tokens_selected;
+  int64_t runs;
+  int64_t blocks;
+  int64_t tokens_block;
+} ckv_io_counts;
+ckv_status ckv_io_account(int64_t n, int32_t c, const int32_t* sel_idx, int64_t k,
+                          int32_t block_tokens, ckv_io_counts* out);
+
+/* ---------------------------------------------------------------------------
+ * Attention-guided cache management -- Sec. 4.5, Eq. 2.
+ * Decides which ContiguousChunks stay in GPU memory and in CPU memory across
+ * requests.  Keys 0..n_keys-1 name cacheable chunks (for example
+ * layer * m + chunk).  Each key keeps, for as long as the cache lives and
+ * also after eviction (the in-memory score table):
+ *   I  cumulative importance: the sum of the attention scores A_j (Eq. 1) of
+ *      the requests that used the chunk,
+ *   F  access frequency: the number of requests that used it,
+ *   S  cache score I * F (CKV_CACHE_ATTENTION), or F alone
+ *      (CKV_CACHE_LFU, the frequency-only policy of the ablation).
+ * Two tiers of gpu_slots and cpu_slots entries are kept as min-heaps on
+ * (S, time of latest access): the weakest entry is the one with the lowest S,
+ * and among equal S the one accessed longest ago.
+ * ckv_cache_access takes one request's used chunks in the given order; for
+ * each it reports where the chunk was found (CKV_TIER_GPU: no transfer;
+ * CKV_TIER_CPU: a CPU-to-GPU transfer; CKV_TIER_NONE: a load from storage),
+ * adds A to I and one to F, and re-places it: into the GPU tier if there is
+ * room or it outranks the GPU tier's weakest entry, which then moves to the
+ * CPU tier by the same rule; otherwise into the CPU tier by that rule.  What
+ * the CPU tier does not take leaves memory.  (The paper fixes the score, the
+ * two heaps, the GPU-to-CPU cascade and the table; F counting requests, the
+ * admission rule and the tie order are this library's reading.)  As S only
+ * grows with each access, the GPU tier always holds the gpu_slots
+ * highest-ranked chunks seen so far and the CPU tier the next cpu_slots.
+ * The cache is host memory only and moves no data: the caller moves chunks
+ * as the reported tiers say.  Not thread-safe; one cache per thread.
+ * ------------------------------------------------------------------------- */
+typedef struct ckv_cache ckv_cache;
+#define CKV_CACHE_ATTENTION 0
+#define CKV_CACHE_LFU 1
+#define CKV_TIER_NONE 0
+#define CKV_TIER_CPU 1
+#define CKV_TIER_GPU 2
+
+typedef struct ckv_cache_counts {
+  int64_t hits_gpu; /* accessed chunks found in the GPU tier                 */
+  int64_t hits_cpu; /* found in the CPU tier                                 */
+  int64_t misses;   /* found in neither (loaded from storage)                */
+  int64_t demoted;  /* GPU-tier evictions taken by the CPU tier              */
+  int64_t dropped;  /* chunks that left memory or were not kept after a load */
+} ckv_cache_counts;
+
+/* n_keys >= 1, gpu_slots >= 0, cpu_slots >= 0, policy CKV_CACHE_ATTENTION or
+ * CKV_CACHE_LFU.  Host allocation of O(n_keys + slots); CKV_ENOMEM on failure. */
+ckv_status ckv_cache_create(int64_t n_keys, int64_t gpu_slots, int64_t cpu_slots, int32_t policy,
+                            ckv_cache** out);
+ckv_status ckv_cache_destroy(ckv_cache* cache);
+/* One request: keys[count] distinct and in [0, n_keys), scores[count] finite
+ * and >= 0 (the chunks' A_j).  tier_before[count] (may be NULL) receives the
+ * tier each key was found in at its turn; *counts (may be NULL) the totals
+ * since creation.  Everything is validated first: CKV_EINVAL changes nothing.
+ * O(count * log(slots)). */
+ckv_status ckv_cache_access(ckv_cache* cache, const int64_t* keys, const double* scores,
+                            int64_t count, int8_t* tier_before, ckv_cache_counts* counts);
+/* Current tier of keys[count] into tier[count]; changes nothing. */
+ckv_status ckv_cache_lookup(const ckv_cache* cache, const int64_t* keys, int64_t count,
+                            int8_t* tier);
+/* I, F and tier of every key into arrays of n_keys entries (each may be NULL). */
+ckv_status ckv_cache_state(const ckv_cache* cache, double* importance, int64_t* frequency,
+                           int8_t* tier);
+/* The keys of tier (CKV_TIER_CPU or CKV_TIER_GPU) in ascending order into
+ * keys[0..capacity); *n receives the tier's size (CKV_EINVAL, nothing
+ * written, if it exceeds capacity). */
+ckv_status ckv_cache_resident(const ckv_cache* cache, int32_t tier, int64_t* keys,
+                              int64_t capacity, int64_t* n);
+
 #ifdef __cplusplus
 }
 #endif

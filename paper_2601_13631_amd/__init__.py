@@ -21,6 +21,8 @@ LIB_PATH = os.path.join(_HERE, "libckv.so")
 OK, EINVAL, EUNSUPPORTED, EHIP, ENOMEM, ESTATE = range(6)
 DTYPE_F32, DTYPE_BF16 = 0, 1
 CTX_HOST_PREFIX, CTX_MATERIALIZE, CTX_STAGE_TIMING, CTX_SCORE_TIMING = 0x1, 0x2, 0x4, 0x8
+CACHE_ATTENTION, CACHE_LFU = 0, 1
+TIER_NONE, TIER_CPU, TIER_GPU = 0, 1, 2
 STAGES = ("score", "finalize", "select", "move", "attn")
 
 if not os.path.exists(LIB_PATH):
@@ -62,6 +64,16 @@ class LayerStats(ctypes.Structure):
         return {f: int(getattr(self, f)) for f, _ in self._fields_}
 
 
+class IoCounts(ctypes.Structure):
+    """``ckv_io_counts``."""
+    _fields_ = [(f, ctypes.c_int64) for f in ("tokens_selected", "runs", "blocks", "tokens_block")]
+
+
+class CacheCounts(ctypes.Structure):
+    """``ckv_cache_counts``."""
+    _fields_ = [(f, ctypes.c_int64) for f in ("hits_gpu", "hits_cpu", "misses", "demoted", "dropped")]
+
+
 _P = ctypes.c_void_p
 _DP = ctypes.POINTER(Dims)
 _SIG = {
@@ -86,6 +98,17 @@ _SIG = {
                             ctypes.c_int32),
     "ckv_reprefill_layer": ([_P, ctypes.c_int32, ctypes.POINTER(LayerIO),
                              ctypes.POINTER(LayerStats)], ctypes.c_int32),
+    "ckv_io_account": ([ctypes.c_int64, ctypes.c_int32, _P, ctypes.c_int64, ctypes.c_int32,
+                        ctypes.POINTER(IoCounts)], ctypes.c_int32),
+    "ckv_cache_create": ([ctypes.c_int64, ctypes.c_int64, ctypes.c_int64, ctypes.c_int32,
+                          ctypes.POINTER(_P)], ctypes.c_int32),
+    "ckv_cache_destroy": ([_P], ctypes.c_int32),
+    "ckv_cache_access": ([_P, _P, _P, ctypes.c_int64, _P, ctypes.POINTER(CacheCounts)],
+                         ctypes.c_int32),
+    "ckv_cache_lookup": ([_P, _P, ctypes.c_int64, _P], ctypes.c_int32),
+    "ckv_cache_state": ([_P, _P, _P, _P], ctypes.c_int32),
+    "ckv_cache_resident": ([_P, ctypes.c_int32, _P, ctypes.c_int64, ctypes.POINTER(ctypes.c_int64)],
+                           ctypes.c_int32),
 }
 for _name, (_args, _res) in _SIG.items():
     _f = getattr(_lib, _name)
@@ -221,6 +244,82 @@ class Context:
     def close(self) -> None:
         if self._h:
             _check(_lib.ckv_ctx_destroy(self._h), "ckv_ctx_destroy")
+            self._h = ctypes.c_void_p()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def _host_ptr(a) -> int | None:
+    """Address of a contiguous host numpy array."""
+    return a.ctypes.data if a is not None and a.size else None
+
+
+def io_account(n: int, c: int, sel_idx, block_tokens: int = 64) -> dict:
+    """``ckv_io_account``: tokens read for the ascending chunk indices sel_idx (host)
+    by a ContiguousChunk store and by a store of block_tokens-token blocks."""
+    import numpy as np
+    sel = np.ascontiguousarray(sel_idx, np.int32)
+    out = IoCounts()
+    _check(_lib.ckv_io_account(n, c, _host_ptr(sel), sel.size, block_tokens, ctypes.byref(out)),
+           "ckv_io_account")
+    return {f: int(getattr(out, f)) for f, _ in out._fields_}
+
+
+class Cache:
+    """``ckv_cache``: the attention-guided two-tier chunk cache (host memory)."""
+
+    def __init__(self, n_keys: int, gpu_slots: int, cpu_slots: int, policy: int = CACHE_ATTENTION):
+        self.n_keys = n_keys
+        self._h = ctypes.c_void_p()
+        _check(_lib.ckv_cache_create(n_keys, gpu_slots, cpu_slots, policy, ctypes.byref(self._h)),
+               "ckv_cache_create")
+
+    def access(self, keys, scores):
+        """One request's used chunks; returns (tier each was found in, totals dict)."""
+        import numpy as np
+        keys = np.ascontiguousarray(keys, np.int64)
+        scores = np.ascontiguousarray(scores, np.float64)
+        if keys.size != scores.size:
+            raise ValueError("keys and scores differ in length")
+        where = np.zeros(keys.size, np.int8)
+        cnt = CacheCounts()
+        _check(_lib.ckv_cache_access(self._h, _host_ptr(keys), _host_ptr(scores), keys.size,
+                                     _host_ptr(where), ctypes.byref(cnt)), "ckv_cache_access")
+        return where, {f: int(getattr(cnt, f)) for f, _ in cnt._fields_}
+
+    def lookup(self, keys):
+        import numpy as np
+        keys = np.ascontiguousarray(keys, np.int64)
+        tier = np.zeros(keys.size, np.int8)
+        _check(_lib.ckv_cache_lookup(self._h, _host_ptr(keys), keys.size, _host_ptr(tier)),
+               "ckv_cache_lookup")
+        return tier
+
+    def state(self):
+        """(I, F, tier) arrays over every key."""
+        import numpy as np
+        I = np.zeros(self.n_keys, np.float64)
+        F = np.zeros(self.n_keys, np.int64)
+        tier = np.zeros(self.n_keys, np.int8)
+        _check(_lib.ckv_cache_state(self._h, _host_ptr(I), _host_ptr(F), _host_ptr(tier)),
+               "ckv_cache_state")
+        return I, F, tier
+
+    def resident(self, tier: int):
+        import numpy as np
+        n = ctypes.c_int64()
+        keys = np.zeros(self.n_keys, np.int64)
+        _check(_lib.ckv_cache_resident(self._h, tier, _host_ptr(keys), keys.size, ctypes.byref(n)),
+               "ckv_cache_resident")
+        return keys[: n.value].copy()
+
+    def close(self) -> None:
+        if self._h:
+            _check(_lib.ckv_cache_destroy(self._h), "ckv_cache_destroy")
             self._h = ctypes.c_void_p()
 
     def __del__(self):
