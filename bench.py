@@ -20,6 +20,9 @@ pass after the timed region: per-stage times from events between every stage,
 the step time with no events at all, and the average time per layer when
 layers share their set over Periods of 8 layers (Def. 4.2: one layer in eight
 scores and selects) -- context only; the headline metric selects per layer.
+It also holds the kept sets' reads against a store of 64-token blocks (the
+comparison systems' granularity, Sec. 3) and the attention-guided cache's hit
+rates and host cost over a stream of requests on the same prefix (Sec. 4.5).
 """
 from __future__ import annotations
 
@@ -159,6 +162,64 @@ def host_resident(args, w, ckv, synth, np, torch) -> int:
     return 0
 
 
+def tiers_detail(args, w, ckv, synth, np, torch, layers, dims, dev) -> dict:
+    """Untimed: the layers' kept sets for several requests on the shared prefix
+    (request r's queries from synth.request_queries), their reads against a
+    64-token block store (Sec. 4.2; Sec. 3), and the attention-guided cache
+    (Sec. 4.5) against its frequency-only foil over that request stream."""
+    L, m, n, c = w.n_layers, w.n_chunks, w.n_prefix, w.chunk_size
+    ctx = ckv.Context(dims, w.keep_ratio, 0)
+    k = ctx.k
+    out = torch.empty_like(layers[0]["q"])
+    sels, scores = [], []
+    for r in range(args.requests):
+        for l in range(L):
+            q = layers[l]["q"] if r == 0 else \
+                torch.from_numpy(synth.request_queries(w, l, r)).view(torch.bfloat16).to(dev)
+            A = torch.empty(m, dtype=torch.float64, device=dev)
+            sel = torch.empty(k, dtype=torch.int32, device=dev)
+            ctx.reprefill_layer(l, q, layers[l]["k_suffix"], layers[l]["v_suffix"],
+                                layers[l]["k_prefix"], out, k_prefix=layers[l]["k_prefix"],
+                                v_prefix=layers[l]["v_prefix"], chunk_scores=A, sel_idx=sel)
+            sels.append(sel)
+            scores.append(A)
+    torch.cuda.synchronize()
+    ctx.close()
+    sels = [x.cpu().numpy() for x in sels]
+    scores = [x.cpu().numpy() for x in scores]
+    tot = {"tokens_selected": 0, "runs": 0, "blocks": 0, "tokens_block": 0}
+    for sel in sels[:L]:
+        for f, v in ckv.io_account(n, c, sel, 64).items():
+            tot[f] += v
+    io = {"layers": L, "block_tokens": 64, "tokens_contiguous": tot["tokens_selected"],
+          "tokens_block_store": tot["tokens_block"],
+          "contiguous_pct_of_block_store": round(100.0 * tot["tokens_selected"] /
+                                                 tot["tokens_block"], 2),
+          "block_store_read_amplification": round(tot["tokens_block"] / tot["tokens_selected"], 3),
+          "contiguous_runs_per_layer": round(tot["runs"] / L, 1)}
+    gpu_slots, cpu_slots = L * k // 2, L * k
+    cache = {"requests": args.requests, "keys": "layer*m+chunk", "gpu_slots": gpu_slots,
+             "cpu_slots": cpu_slots}
+    for name, policy in (("attention", ckv.CACHE_ATTENTION), ("lfu", ckv.CACHE_LFU)):
+        cm = ckv.Cache(L * m, gpu_slots, cpu_slots, policy)
+        first = None
+        t0 = time.perf_counter()
+        for i, (sel, A) in enumerate(zip(sels, scores)):
+            if i == L:
+                _, first = cm.access([], [])
+            cm.access((i % L) * m + sel.astype(np.int64), A[sel])
+        host_s = time.perf_counter() - t0
+        _, tot_c = cm.access([], [])
+        cm.close()
+        later = {f: tot_c[f] - (first[f] if first else 0) for f in ("hits_gpu", "hits_cpu", "misses")}
+        used = sum(later.values())
+        cache[name] = {"later_requests_gpu_hit_pct": round(100.0 * later["hits_gpu"] / used, 2) if used else None,
+                       "later_requests_cpu_hit_pct": round(100.0 * later["hits_cpu"] / used, 2) if used else None,
+                       "later_requests_miss_pct": round(100.0 * later["misses"] / used, 2) if used else None,
+                       "host_us_per_layer": round(host_s * 1e6 / len(sels), 2)}
+    return {"io_vs_64_token_blocks": io, "cache_manager": cache}
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -173,6 +234,8 @@ def main() -> int:
                     help="host-resident workloads: layers per pass")
     ap.add_argument("--host-reps", type=int, default=3,
                     help="host-resident workloads: timed passes over those layers")
+    ap.add_argument("--requests", type=int, default=4,
+                    help="requests on the shared prefix in the read-accounting and cache diagnostic")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs on exactly one GPU: this build has no multi-GPU path "
@@ -299,6 +362,8 @@ def main() -> int:
         f"period{PERIOD}_us_per_layer_without_events": round(period_us, 2),
         f"period{PERIOD}_prefix_tokens_per_s": round(w.n_prefix / (period_us * 1e-6), 1),
     }
+    if w.dtype == "bf16" and args.requests > 0:
+        others.update(tiers_detail(args, w, ckv, synth, np, torch, layers, dims, dev))
     if args.materialize and per_layer["move"] > 0:
         others["gather_gbs"] = round(2 * kept_bytes / (per_layer["move"] * 1e-3) / 1e9, 1)
 

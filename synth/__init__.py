@@ -212,6 +212,22 @@ def layer_tensors(w: Workload, layer: int, heavy: Optional[np.ndarray] = None) -
     return t
 
 
+def request_queries(w: Workload, layer: int, request: int) -> np.ndarray:
+    """Suffix queries Q [S][Hq][d] of request `request` on the workload's shared
+    prefix: layer_tensors' recipe for Q (noise plus the layer's per-group
+    direction u), with request 0 giving layer_tensors' own Q and every other
+    request drawing its noise from a stream of its own."""
+    S, Hq, Hkv, d = w.n_suffix, w.n_q_heads, w.n_kv_heads, w.head_dim
+    u = _normal(_rng(w, layer, _T_U), (Hkv, d)).astype(np.float64)
+    u /= np.linalg.norm(u, axis=1, keepdims=True)
+    u = u.astype(np.float32)
+    rng = _rng(w, layer, _T_Q) if request == 0 else np.random.Generator(np.random.PCG64(
+        np.random.SeedSequence([w.seed, w.cfg_id, layer, _T_Q, request])))
+    q = _normal(rng, (S, Hq, d))
+    q += np.repeat(u, Hq // Hkv, axis=0)[None, :, :]
+    return to_bf16_bits(q) if w.dtype == "bf16" else q
+
+
 def all_layers(w: Workload, layers=None, threads: int = 8) -> list:
     """layer_tensors for several layers, generated in parallel (same values)."""
     hs = heavy_sets(w)

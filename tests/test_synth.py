@@ -51,3 +51,18 @@ def test_planted_keys_align_with_queries():
     proj = k @ qbar
     tok = np.concatenate([np.arange(j * 16, j * 16 + 16) for j in heavy])
     assert proj[tok].mean() > proj.mean() + 1.0
+
+
+def test_request_queries():
+    """Request 0 is the layer's own Q; other requests draw other noise around the
+    same per-group directions, deterministically."""
+    w = synth.WORKLOADS["c2_qwen05b_8k"].scaled(n_layers=2, n_prefix=256)
+    assert np.array_equal(synth.request_queries(w, 1, 0), synth.layer_tensors(w, 1)["q"])
+    a, b = synth.request_queries(w, 1, 2), synth.request_queries(w, 1, 2)
+    assert np.array_equal(a, b)
+    c = synth.request_queries(w, 1, 3)
+    assert (a != c).mean() > 0.9
+    # the planted direction is shared: group means agree far better than noise would
+    fa = synth.bf16_bits_to_f32(a).mean(axis=0)
+    fc = synth.bf16_bits_to_f32(c).mean(axis=0)
+    assert np.abs(fa - fc).max() < 0.5 and np.abs(fa).max() > 0.05
