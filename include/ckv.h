@@ -179,6 +179,7 @@ ckv_status ckv_sparse_prefill_attn(const ckv_dims* dims, const void* q, const vo
  * host-resident prefix) HBM chunk slots.
  * ------------------------------------------------------------------------- */
 typedef struct ckv_ctx ckv_ctx;
+typedef struct ckv_cache ckv_cache; /* Sec. 4.5 cache, see ckv_cache_create */
 
 /* ctx flags */
 #define CKV_CTX_HOST_PREFIX 0x1     /* prefix K/V live in pinned host memory (Sec. 4.3.2) */
@@ -226,6 +227,34 @@ ckv_status ckv_ctx_reset(ckv_ctx* ctx);
  * Forgets any set held.  CKV_EINVAL if period < 1. */
 ckv_status ckv_ctx_set_period(ckv_ctx* ctx, int32_t period);
 
+/* Attention-guided cache on the layer step -- Sec. 4.5 (with the cache of
+ * ckv_cache_create).  Attaches `cache` to a context with a host-resident
+ * prefix (CKV_CTX_HOST_PREFIX), or detaches the current one (cache NULL).
+ * The context then keeps the chunks of the cache's GPU tier in
+ * min(gpu_slots, n_keys) HBM chunk slots that it allocates here (each slot
+ * one chunk's K span and V span), key = layer * m + chunk, so the cache's
+ * n_keys must be a multiple of m and layers beyond n_keys / m are refused.
+ * Each host-resident layer then
+ *   - reads the selected chunks held in those slots in place (stats
+ *     cache_hits): no host-link copy;
+ *   - prefetches and fetches on demand only the other chunks;
+ *   - after its attention, calls ckv_cache_access with its chunks and their
+ *     scores A_j (for a layer inside a Period, those of the Period's first
+ *     layer) and copies each chunk that entered the GPU tier from its
+ *     transient slot into a cache slot (stats bytes_cache_fill); chunks that
+ *     left the GPU tier free their slots (their bytes stay in the host store).
+ * The cache persists across requests (ckv_ctx_reset keeps it), so later
+ * requests on the same prefix find its heavily used chunks in HBM.  Every
+ * request must pass the same per-layer kv_host contents while it is
+ * attached.  Must be called before a request's first layer (or after
+ * ckv_ctx_reset), else CKV_ESTATE; the cache's GPU tier must be empty
+ * (CKV_ESTATE).  Synchronizes the device.  The context does not own the
+ * cache: detach it (or destroy the context) before destroying it or calling
+ * ckv_cache_access on it directly.  With a cache attached, a layer inside a
+ * Period waits on the host for the copies two layers back before it reuses
+ * their staging buffers. */
+ckv_status ckv_ctx_attach_cache(ckv_ctx* ctx, ckv_cache* cache);
+
 typedef struct ckv_layer_io {
   const void* q;         /* device [S][Hq][d]                                        */
   const void* k_suffix;  /* device [S][Hkv][d]                                       */
@@ -256,6 +285,10 @@ typedef struct ckv_layer_stats {
   int64_t bytes_gathered;  /* K+V bytes of the selected chunks (= bytes attended); with
                               an HBM-resident prefix the set stays on the device and a
                               kept short last chunk is counted at full length          */
+  int64_t cache_hits;      /* selected chunks read from an attached cache's HBM slots
+                              (no host-link transfer; not counted in hits or misses)   */
+  int64_t bytes_cache_fill;/* HBM->HBM bytes copied into cache slots for chunks that
+                              entered the cache's GPU tier at this layer (whole slots) */
 } ckv_layer_stats;
 
 /* Sum of the GPU time of each stage (ms[CKV_N_STAGES], milliseconds) over
@@ -336,7 +369,7 @@ ckv_status ckv_io_account(int64_t n, int32_t c, const int32_t* sel_idx, int64_t 
  * The cache is host memory only and moves no data: the caller moves chunks
  * as the reported tiers say.  Not thread-safe; one cache per thread.
  * ------------------------------------------------------------------------- */
-typedef struct ckv_cache ckv_cache;
+/* (ckv_cache is declared beside ckv_ctx above) */
 #define CKV_CACHE_ATTENTION 0
 #define CKV_CACHE_LFU 1
 #define CKV_TIER_NONE 0

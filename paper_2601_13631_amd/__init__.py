@@ -58,7 +58,8 @@ class LayerIO(ctypes.Structure):
 class LayerStats(ctypes.Structure):
     """``ckv_layer_stats``."""
     _fields_ = [(f, ctypes.c_int64) for f in (
-        "k", "hits", "misses", "wasted", "bytes_prefetch", "bytes_demand", "bytes_gathered")]
+        "k", "hits", "misses", "wasted", "bytes_prefetch", "bytes_demand", "bytes_gathered",
+        "cache_hits", "bytes_cache_fill")]
 
     def as_dict(self) -> dict:
         return {f: int(getattr(self, f)) for f, _ in self._fields_}
@@ -94,6 +95,7 @@ _SIG = {
     "ckv_ctx_destroy": ([_P], ctypes.c_int32),
     "ckv_ctx_reset": ([_P], ctypes.c_int32),
     "ckv_ctx_set_period": ([_P, ctypes.c_int32], ctypes.c_int32),
+    "ckv_ctx_attach_cache": ([_P, _P], ctypes.c_int32),
     "ckv_ctx_stage_times": ([_P, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64)],
                             ctypes.c_int32),
     "ckv_reprefill_layer": ([_P, ctypes.c_int32, ctypes.POINTER(LayerIO),
@@ -240,6 +242,13 @@ class Context:
     def set_period(self, period: int) -> None:
         """Layers p*i .. p*i+p-1 share the set selected at layer p*i."""
         _check(_lib.ckv_ctx_set_period(self._h, period), "ckv_ctx_set_period")
+
+    def attach_cache(self, cache) -> None:
+        """Keeps the GPU tier of ``cache`` (a :class:`Cache`, or None to detach)
+        in HBM slots for this host-resident context."""
+        self._cache = cache  # the context must not outlive the cache it uses
+        _check(_lib.ckv_ctx_attach_cache(self._h, cache._h if cache is not None else None),
+               "ckv_ctx_attach_cache")
 
     def close(self) -> None:
         if self._h:

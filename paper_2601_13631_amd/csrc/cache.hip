@@ -23,6 +23,10 @@ struct ckv_cache {
   std::vector<int64_t> heap[3];
   int64_t clock = 0, call = 0;
   ckv_cache_counts counts = {0, 0, 0, 0, 0};
+  // keys displaced from the GPU tier since the last drain (kept only while a
+  // layer context holds the GPU tier's chunks in HBM)
+  bool log_gpu_evictions = false;
+  std::vector<int64_t> gpu_evicted;
 };
 
 namespace {
@@ -99,12 +103,32 @@ void place(ckv_cache& c, int64_t x) {
   int64_t out = admit(c, CKV_TIER_GPU, x);
   if (out < 0) return;
   const bool demoting = out != x;  // a GPU-tier entry goes down
+  if (demoting && c.log_gpu_evictions) c.gpu_evicted.push_back(out);
   const int64_t left = admit(c, CKV_TIER_CPU, out);
   if (demoting && left != out) c.counts.demoted++;
   if (left >= 0) c.counts.dropped++;
 }
 
 }  // namespace
+
+namespace ckv {
+
+int64_t cache_keys(const ckv_cache* c) { return c->n_keys; }
+int64_t cache_gpu_slots(const ckv_cache* c) { return c->slots[CKV_TIER_GPU]; }
+int64_t cache_gpu_size(const ckv_cache* c) { return (int64_t)c->heap[CKV_TIER_GPU].size(); }
+int8_t cache_tier(const ckv_cache* c, int64_t key) { return c->tier[key]; }
+
+void cache_log_gpu_evictions(ckv_cache* c, bool on) {
+  c->log_gpu_evictions = on;
+  c->gpu_evicted.clear();
+}
+
+void cache_take_gpu_evictions(ckv_cache* c, std::vector<int64_t>& out) {
+  out.swap(c->gpu_evicted);
+  c->gpu_evicted.clear();
+}
+
+}  // namespace ckv
 
 using namespace ckv;
 

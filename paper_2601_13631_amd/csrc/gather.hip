@@ -53,10 +53,14 @@ __global__ __launch_bounds__(kThreads) void gather_kernel(const uint8_t* __restr
 // list instead of one DMA copy per run of chunks -- while occupying only a
 // few wave slots per CU, next to the compute kernels it overlaps.
 constexpr int kCopyBlocks = 32;
+// HBM-to-HBM slot moves (cache fills) run on the compute stream: a wider grid
+constexpr int kSlotCopyBlocks = 256;
 
+// dst_slots == nullptr: span i goes to slot slot0 + i
 __global__ __launch_bounds__(kThreads) void copy_spans_kernel(const uint8_t* __restrict__ src,
                                                               const int32_t* __restrict__ chunks,
                                                               int64_t count, int64_t slot0,
+                                                              const int32_t* __restrict__ dst_slots,
                                                               uint8_t* __restrict__ dst,
                                                               int64_t span_bytes) {
   constexpr int64_t kPiece = (int64_t)kThreads * kUnroll * 16;
@@ -65,7 +69,7 @@ __global__ __launch_bounds__(kThreads) void copy_spans_kernel(const uint8_t* __r
   for (int64_t w = blockIdx.x; w < total; w += gridDim.x) {
     const int64_t i = w / per_span, piece = w % per_span;
     const uint8_t* s = src + (int64_t)chunks[i] * span_bytes;
-    uint8_t* d = dst + (slot0 + i) * span_bytes;
+    uint8_t* d = dst + (dst_slots ? (int64_t)dst_slots[i] : slot0 + i) * span_bytes;
     const int64_t base = piece * kPiece + (int64_t)threadIdx.x * 16;
     u32x4 v[kUnroll];
 #pragma unroll
@@ -91,7 +95,21 @@ ckv_status launch_copy_spans(const void* src, const int32_t* chunks, int64_t cou
   const int64_t pieces = count * ceil_div(span_bytes, (int64_t)kThreads * kUnroll * 16);
   const unsigned grid = (unsigned)std::min<int64_t>(pieces, kCopyBlocks);
   hipLaunchKernelGGL(copy_spans_kernel, dim3(grid), dim3(kThreads), 0, st,
-                     static_cast<const uint8_t*>(src), chunks, count, slot0,
+                     static_cast<const uint8_t*>(src), chunks, count, slot0, nullptr,
+                     static_cast<uint8_t*>(dst), span_bytes);
+  CKV_HIP(hipGetLastError());
+  return CKV_OK;
+}
+
+ckv_status launch_copy_slots(const void* src, const int32_t* src_slots, void* dst,
+                             const int32_t* dst_slots, int64_t count, int64_t span_bytes,
+                             hipStream_t st) {
+  if (span_bytes % 16 != 0) CKV_FAIL(CKV_EINVAL, "span bytes must be a multiple of 16");
+  if (count == 0) return CKV_OK;
+  const int64_t pieces = count * ceil_div(span_bytes, (int64_t)kThreads * kUnroll * 16);
+  const unsigned grid = (unsigned)std::min<int64_t>(pieces, kSlotCopyBlocks);
+  hipLaunchKernelGGL(copy_spans_kernel, dim3(grid), dim3(kThreads), 0, st,
+                     static_cast<const uint8_t*>(src), src_slots, count, 0, dst_slots,
                      static_cast<uint8_t*>(dst), span_bytes);
   CKV_HIP(hipGetLastError());
   return CKV_OK;

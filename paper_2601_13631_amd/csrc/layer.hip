@@ -44,6 +44,10 @@ struct ckv_ctx {
   // host-resident prefix
   int64_t slot_bytes = 0;  // one chunk: K span + V span
   int64_t slots_per_buf = 0;
+  // one arena of chunk slots: two transient buffers of slots_per_buf slots
+  // (slots[0], slots[1]) then cache_slots slots holding the chunks of an
+  // attached cache's GPU tier; slot tables index the whole arena
+  void* arena = nullptr;
   void* slots[2] = {nullptr, nullptr};
   int32_t* slot_tab_dev[2] = {nullptr, nullptr};
   int32_t* sel_host = nullptr;      // pinned [k]
@@ -66,6 +70,18 @@ struct ckv_ctx {
   int32_t period_first = -1;  // -1: no set held
   size_t off_pset = 0;
   std::vector<int32_t> pset_host;
+  std::vector<double> pset_A;  // the Period set's chunk scores (attached cache only)
+  // attention-guided cache (Sec. 4.5) attached to a host-resident prefix
+  ckv_cache* cache = nullptr;
+  int64_t cache_slots = 0, cache_layers = 0;
+  std::vector<int32_t> slot_of;     // key -> cache slot, -1 if the chunk is not in HBM
+  std::vector<int32_t> free_slots;  // cache slots holding nothing
+  std::vector<int64_t> keys, evicted;
+  std::vector<double> key_scores;
+  double* scores_host = nullptr;                    // pinned [m]
+  int32_t* fill_host[2] = {nullptr, nullptr};       // pinned [2k]: source slots, then target slots
+  int32_t* fill_dev[2] = {nullptr, nullptr};
+  bool pref_recorded[2] = {false, false};
   // stage timing: a ring of event sets, harvested when a set is reused or on query
   static constexpr int kRing = 64;
   hipEvent_t tev[kRing][CKV_N_STAGES + 1] = {};
@@ -81,8 +97,9 @@ ckv_status free_ctx(ckv_ctx* c) {
   if (c->prefetch) (void)hipStreamSynchronize(c->prefetch);
   (void)hipFree(c->ws);
   for (int i = 0; i < 2; ++i) {
-    (void)hipFree(c->slots[i]);
     (void)hipFree(c->slot_tab_dev[i]);
+    (void)hipFree(c->fill_dev[i]);
+    (void)hipHostFree(c->fill_host[i]);
     (void)hipHostFree(c->slot_tab_host[i]);
     (void)hipFree(c->dem_dev[i]);
     (void)hipFree(c->pref_dev[i]);
@@ -91,7 +108,9 @@ ckv_status free_ctx(ckv_ctx* c) {
     if (c->ev_pref[i]) (void)hipEventDestroy(c->ev_pref[i]);
     if (c->ev_attn[i]) (void)hipEventDestroy(c->ev_attn[i]);
   }
+  (void)hipFree(c->arena);
   (void)hipHostFree(c->sel_host);
+  (void)hipHostFree(c->scores_host);
   for (auto& set : c->tev)
     for (auto& e : set)
       if (e) (void)hipEventDestroy(e);
@@ -188,8 +207,12 @@ ckv_status ckv_ctx_create(const ckv_dims* dims, double keep_ratio, int32_t flags
   if (flags & CKV_CTX_HOST_PREFIX) {
     c->slot_bytes = 2 * span;
     c->slots_per_buf = 2 * c->k;  // prefetched chunks plus room for a full miss set
+    CKV_HIP_ALLOC(hipMalloc(&c->arena, (size_t)(2 * c->slots_per_buf * c->slot_bytes)));
     for (int i = 0; i < 2; ++i) {
-      CKV_HIP_ALLOC(hipMalloc(&c->slots[i], (size_t)(c->slots_per_buf * c->slot_bytes)));
+      c->slots[i] = static_cast<char*>(c->arena) + i * c->slots_per_buf * c->slot_bytes;
+      CKV_HIP_ALLOC(hipMalloc((void**)&c->fill_dev[i], (size_t)(2 * c->k) * sizeof(int32_t)));
+      CKV_HIP_ALLOC(hipHostMalloc((void**)&c->fill_host[i], (size_t)(2 * c->k) * sizeof(int32_t),
+                                  hipHostMallocDefault));
       CKV_HIP_ALLOC(hipMalloc((void**)&c->slot_tab_dev[i], (size_t)c->k * sizeof(int32_t)));
       CKV_HIP_ALLOC(hipHostMalloc((void**)&c->slot_tab_host[i], (size_t)c->k * sizeof(int32_t),
                                   hipHostMallocDefault));
@@ -203,6 +226,8 @@ ckv_status ckv_ctx_create(const ckv_dims* dims, double keep_ratio, int32_t flags
       CKV_HIP_ALLOC(hipEventCreateWithFlags(&c->ev_attn[i], hipEventDisableTiming));
     }
     CKV_HIP_ALLOC(hipHostMalloc((void**)&c->sel_host, (size_t)c->k * sizeof(int32_t),
+                                hipHostMallocDefault));
+    CKV_HIP_ALLOC(hipHostMalloc((void**)&c->scores_host, (size_t)c->m * sizeof(double),
                                 hipHostMallocDefault));
     CKV_HIP_ALLOC(hipStreamCreateWithFlags(&c->demand, hipStreamNonBlocking));
     CKV_HIP_ALLOC(hipStreamCreateWithFlags(&c->prefetch, hipStreamNonBlocking));
@@ -238,6 +263,49 @@ ckv_status ckv_ctx_set_period(ckv_ctx* ctx, int32_t period) {
   if (period < 1) CKV_FAIL(CKV_EINVAL, "period must be >= 1 (got %d)", period);
   ctx->period = period;
   ctx->period_first = -1;
+  return CKV_OK;
+}
+
+ckv_status ckv_ctx_attach_cache(ckv_ctx* ctx, ckv_cache* cache) {
+  clear_error();
+  if (!ctx) CKV_FAIL(CKV_EINVAL, "ctx is NULL");
+  if (!(ctx->flags & CKV_CTX_HOST_PREFIX))
+    CKV_FAIL(CKV_EINVAL, "a cache needs a context with a host-resident prefix");
+  if (ctx->next_layer != 0)
+    CKV_FAIL(CKV_ESTATE, "attach a cache at the start of a request (before layer 0 or after a reset)");
+  int64_t G = 0;
+  if (cache) {
+    if (cache_keys(cache) % ctx->m != 0)
+      CKV_FAIL(CKV_EINVAL, "cache keys (%lld) must be a whole number of layers of %lld chunks",
+               (long long)cache_keys(cache), (long long)ctx->m);
+    if (cache_gpu_size(cache) != 0)
+      CKV_FAIL(CKV_ESTATE, "the cache's GPU tier must be empty when it is attached");
+    G = std::min(cache_gpu_slots(cache), cache_keys(cache));
+    if (2 * ctx->slots_per_buf + G > INT32_MAX)
+      CKV_FAIL(CKV_EUNSUPPORTED, "too many cache slots (%lld)", (long long)G);
+  }
+  // the arena is replaced with nothing in flight that could still read it
+  CKV_HIP(hipDeviceSynchronize());
+  const size_t bytes = (size_t)((2 * ctx->slots_per_buf + G) * ctx->slot_bytes);
+  void* arena = nullptr;
+  hipError_t e = hipMalloc(&arena, bytes);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    CKV_FAIL(e == hipErrorOutOfMemory ? CKV_ENOMEM : CKV_EHIP, "hipMalloc of %zu bytes of cache slots failed: %s",
+             bytes, hipGetErrorString(e));
+  }
+  CKV_HIP(hipFree(ctx->arena));
+  ctx->arena = arena;
+  for (int i = 0; i < 2; ++i)
+    ctx->slots[i] = static_cast<char*>(arena) + i * ctx->slots_per_buf * ctx->slot_bytes;
+  if (ctx->cache) cache_log_gpu_evictions(ctx->cache, false);
+  ctx->cache = cache;
+  ctx->cache_slots = G;
+  ctx->cache_layers = cache ? cache_keys(cache) / ctx->m : 0;
+  ctx->slot_of.assign(cache ? (size_t)cache_keys(cache) : 0, -1);
+  ctx->free_slots.clear();
+  for (int64_t i = G - 1; i >= 0; --i) ctx->free_slots.push_back((int32_t)i);
+  if (cache) cache_log_gpu_evictions(cache, true);
   return CKV_OK;
 }
 
@@ -289,6 +357,9 @@ ckv_status ckv_reprefill_layer(ckv_ctx* c, int32_t layer, const ckv_layer_io* io
       CKV_FAIL(CKV_EINVAL, "tensors must be 16-byte aligned");
   }
   if (layer < 0) CKV_FAIL(CKV_EINVAL, "layer must be >= 0 (got %d)", layer);
+  if (host && c->cache && layer >= c->cache_layers)
+    CKV_FAIL(CKV_EINVAL, "layer %d has no keys in the attached cache (%lld layers)", layer,
+             (long long)c->cache_layers);
   // a layer past the first of its Period reuses the set selected there
   const int32_t first = layer - layer % c->period;
   const bool reuse = first != layer;
@@ -371,16 +442,38 @@ ckv_status ckv_reprefill_layer(ckv_ctx* c, int32_t layer, const ckv_layer_io* io
 
   // ---- host-resident prefix ------------------------------------------------
   const int cur = layer & 1, nxt = cur ^ 1;
+  const bool cached = c->cache != nullptr;
   if (reuse) {  // the Period's set is already on the host: no synchronisation
+    if (cached) {
+      // the staging buffers written below were last read by the copies of
+      // two layers ago (and the prefetch list by the previous layer's
+      // prefetch); their contents differ from layer to layer with a cache
+      if (c->attn_recorded[cur]) CKV_HIP(hipEventSynchronize(c->ev_attn[cur]));
+      if (c->pref_recorded[nxt]) CKV_HIP(hipEventSynchronize(c->ev_pref[nxt]));
+    }
     std::memcpy(c->sel_host, c->pset_host.data(), (size_t)k * sizeof(int32_t));
   } else {
     CKV_HIP(hipMemcpyAsync(c->sel_host, sel, (size_t)k * sizeof(int32_t), hipMemcpyDeviceToHost, st));
+    if (cached)
+      CKV_HIP(hipMemcpyAsync(c->scores_host, scores, (size_t)c->m * sizeof(double),
+                             hipMemcpyDeviceToHost, st));
     CKV_HIP(hipEventRecord(c->ev_sel, st));
     CKV_HIP(hipEventSynchronize(c->ev_sel));
-    if (c->period > 1) c->pset_host.assign(c->sel_host, c->sel_host + k);
+    if (c->period > 1) {
+      c->pset_host.assign(c->sel_host, c->sel_host + k);
+      if (cached) {
+        c->pset_A.resize((size_t)k);
+        for (int64_t u = 0; u < k; ++u) c->pset_A[u] = c->scores_host[c->sel_host[u]];
+      }
+    }
   }
 
-  // slot table: predicted chunks sit in slots 0..|P|-1 (in P order), misses follow
+  // slot table, in arena slots: chunks held in the cache's HBM slots are read
+  // there; predicted chunks sit in this layer's buffer at slots 0..|P|-1 (in P
+  // order), misses follow
+  const int64_t spb = c->slots_per_buf;
+  const int64_t buf0 = cur * spb, cache0 = 2 * spb;
+  const int64_t key0 = (int64_t)layer * c->m;
   const std::vector<int32_t>& P = c->pred;
   std::vector<int32_t> miss;
   miss.reserve((size_t)k);
@@ -389,16 +482,22 @@ ckv_status ckv_reprefill_layer(ckv_ctx* c, int32_t layer, const ckv_layer_io* io
   int64_t hits = 0;
   for (int64_t u = 0; u < k; ++u) {
     const int32_t j = c->sel_host[u];
+    const int64_t chunk_bytes = 2 * chunk_len(d, j) * d->n_kv_heads * d->head_dim * eb;
+    stv.bytes_gathered += chunk_bytes;
+    if (cached && c->slot_of[key0 + j] >= 0) {
+      tab[u] = (int32_t)(cache0 + c->slot_of[key0 + j]);
+      ++stv.cache_hits;
+      continue;
+    }
     while (pi < P.size() && P[pi] < j) ++pi;
     if (pi < P.size() && P[pi] == j) {
-      tab[u] = (int32_t)pi;
+      tab[u] = (int32_t)(buf0 + pi);
       ++hits;
     } else {
-      tab[u] = (int32_t)(P.size() + miss.size());
+      tab[u] = (int32_t)(buf0 + P.size() + miss.size());
       miss.push_back(j);
-      stv.bytes_demand += 2 * chunk_len(d, j) * d->n_kv_heads * d->head_dim * eb;
+      stv.bytes_demand += chunk_bytes;
     }
-    stv.bytes_gathered += 2 * chunk_len(d, j) * d->n_kv_heads * d->head_dim * eb;
   }
   stv.hits = hits;
   stv.misses = (int64_t)miss.size();
@@ -423,35 +522,89 @@ ckv_status ckv_reprefill_layer(ckv_ctx* c, int32_t layer, const ckv_layer_io* io
   if (c->pref_pending[cur]) CKV_HIP(hipStreamWaitEvent(st, c->ev_pref[cur], 0));
   c->pref_pending[cur] = false;
   if ((s = mark(4)) != CKV_OK) return s;
-  ChunkSource src{c->slots[cur], static_cast<char*>(c->slots[cur]) + span_elems * eb,
-                  2 * span_elems, c->slot_tab_dev[cur], 0};
+  ChunkSource src{c->arena, static_cast<char*>(c->arena) + span_elems * eb, 2 * span_elems,
+                  c->slot_tab_dev[cur], 0};
   s = launch_attn(d, io->q, src, sel, k, io->k_suffix, io->v_suffix, io->out, ws + c->off_attn,
                   c->ws_attn, st);
   if (s != CKV_OK) return s;
   if ((s = mark(5)) != CKV_OK) return s;
   if (tev) ++c->t_issued;
+
+  if (cached) {
+    // Sec. 4.5: the chunks this layer used add their scores (I += A, F += 1)
+    // and are re-placed; chunks leaving the GPU tier free their HBM slots and
+    // chunks entering it are copied there from this layer's buffer, after the
+    // attention that read both
+    c->keys.resize((size_t)k);
+    c->key_scores.resize((size_t)k);
+    for (int64_t u = 0; u < k; ++u) {
+      c->keys[u] = key0 + c->sel_host[u];
+      c->key_scores[u] = reuse ? c->pset_A[u] : c->scores_host[c->sel_host[u]];
+    }
+    s = ckv_cache_access(c->cache, c->keys.data(), c->key_scores.data(), k, nullptr, nullptr);
+    if (s != CKV_OK) return s;
+    cache_take_gpu_evictions(c->cache, c->evicted);
+    // a chunk displaced by an earlier chunk of this layer and placed back at
+    // its own turn is still in the GPU tier: it keeps its slot and its bytes
+    for (int64_t x : c->evicted)
+      if (c->slot_of[x] >= 0 && cache_tier(c->cache, x) != CKV_TIER_GPU) {
+        c->free_slots.push_back(c->slot_of[x]);
+        c->slot_of[x] = -1;
+      }
+    int64_t nf = 0;
+    int32_t* fill = c->fill_host[cur];
+    for (int64_t u = 0; u < k; ++u) {
+      const int64_t x = c->keys[u];
+      if (cache_tier(c->cache, x) != CKV_TIER_GPU || c->slot_of[x] >= 0) continue;
+      if (c->free_slots.empty()) CKV_FAIL(CKV_ESTATE, "cache slots exhausted (internal)");
+      c->slot_of[x] = c->free_slots.back();
+      c->free_slots.pop_back();
+      fill[nf] = tab[u];
+      fill[k + nf] = (int32_t)(cache0 + c->slot_of[x]);
+      ++nf;
+    }
+    if (nf > 0) {
+      CKV_HIP(hipMemcpyAsync(c->fill_dev[cur], fill, (size_t)(2 * k) * sizeof(int32_t),
+                             hipMemcpyHostToDevice, st));
+      s = launch_copy_slots(c->arena, c->fill_dev[cur], c->arena, c->fill_dev[cur] + k, nf,
+                            c->slot_bytes, st);
+      if (s != CKV_OK) return s;
+      stv.bytes_cache_fill = nf * c->slot_bytes;
+    }
+  }
+  // after the cache fills too: they read this layer's buffer
   CKV_HIP(hipEventRecord(c->ev_attn[cur], st));
   c->attn_recorded[cur] = true;
 
-  // prefetch the next layer's copy of this layer's selection (P_{l+1} = S_l)
-  c->pred.assign(c->sel_host, c->sel_host + k);
+  // prefetch the next layer's copy of this layer's selection (P_{l+1} = S_l),
+  // except chunks the next layer finds in the cache's HBM slots
+  c->pred.clear();
   if (io->kv_host_next) {
+    const int64_t nkey0 = (int64_t)(layer + 1) * c->m;
+    const bool next_cached = cached && layer + 1 < c->cache_layers;
+    for (int64_t u = 0; u < k; ++u) {
+      const int32_t j = c->sel_host[u];
+      if (next_cached && c->slot_of[nkey0 + j] >= 0) continue;
+      c->pred.push_back(j);
+    }
     if (c->attn_recorded[nxt]) CKV_HIP(hipStreamWaitEvent(c->prefetch, c->ev_attn[nxt], 0));
     // after this layer's demand copies: those are on the critical path and get
     // the host link to themselves
     CKV_HIP(hipStreamWaitEvent(c->prefetch, c->ev_dem, 0));
-    std::memcpy(c->pref_host[nxt], c->pred.data(), (size_t)k * sizeof(int32_t));
-    CKV_HIP(hipMemcpyAsync(c->pref_dev[nxt], c->pref_host[nxt], (size_t)k * sizeof(int32_t),
-                           hipMemcpyHostToDevice, c->prefetch));
-    s = launch_copy_spans(store_next, c->pref_dev[nxt], k, 0, c->slots[nxt], c->slot_bytes,
-                          c->prefetch);
-    if (s != CKV_OK) return s;
+    const int64_t np = (int64_t)c->pred.size();
+    if (np > 0) {
+      std::memcpy(c->pref_host[nxt], c->pred.data(), (size_t)np * sizeof(int32_t));
+      CKV_HIP(hipMemcpyAsync(c->pref_dev[nxt], c->pref_host[nxt], (size_t)np * sizeof(int32_t),
+                             hipMemcpyHostToDevice, c->prefetch));
+      s = launch_copy_spans(store_next, c->pref_dev[nxt], np, 0, c->slots[nxt], c->slot_bytes,
+                            c->prefetch);
+      if (s != CKV_OK) return s;
+    }
     CKV_HIP(hipEventRecord(c->ev_pref[nxt], c->prefetch));
     c->pref_pending[nxt] = true;
-    for (int64_t u = 0; u < k; ++u)
+    c->pref_recorded[nxt] = true;
+    for (int64_t u = 0; u < np; ++u)
       stv.bytes_prefetch += 2 * chunk_len(d, c->pred[u]) * d->n_kv_heads * d->head_dim * eb;
-  } else {
-    c->pred.clear();
   }
   c->next_layer = layer + 1;
   if (stats) *stats = stv;

@@ -1,0 +1,163 @@
+"""The attention-guided cache (Sec. 4.5) on the host-resident layer step.
+
+Three requests on one prefix run layer by layer through a context with a
+cache attached and through one without.  Outputs and kept sets must agree bit
+for bit (the cache only changes where the chunk bytes come from); the
+chunks read from HBM cache slots, the host-link counts and the cache fills
+must equal what the oracle cache, fed the same chunk scores, predicts; the
+final tiers and scores must equal the oracle cache's.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+from gpu_common import DEV, dev, dims_of, oshape, to_f64
+
+pytestmark = pytest.mark.gpu
+
+
+def _store(w, t):
+    cm = synth.chunk_major(t["k_prefix"], t["v_prefix"], w.chunk_size)
+    h = torch.from_numpy(cm.reshape(-1))
+    if cm.dtype == np.uint16:
+        h = h.view(torch.bfloat16)
+    return h.pin_memory()
+
+
+@pytest.mark.parametrize("period", [1, 2])
+def test_layer_cache_requests(period):
+    import paper_2601_13631_amd as ckv
+    w = synth.WORKLOADS["c5_qwen32b_128k_host"].scaled(n_prefix=4096, n_suffix=24, n_layers=4)
+    L, m = w.n_layers, w.n_chunks
+    layers = [synth.layer_tensors(w, l) for l in range(L)]
+    stores = [_store(w, t) for t in layers]
+    base = [{kk: dev(v) for kk, v in t.items()} for t in layers]
+    s = oshape(w)
+    ctx = ckv.Context(dims_of(w), w.keep_ratio, ckv.CTX_HOST_PREFIX)
+    plain = ckv.Context(dims_of(w), w.keep_ratio, ckv.CTX_HOST_PREFIX)
+    ctx.set_period(period)
+    plain.set_period(period)
+    k = ctx.k
+    gpu_slots, cpu_slots = (L * k) // 2, L * k
+    cache = ckv.Cache(L * m, gpu_slots, cpu_slots)
+    ctx.attach_cache(cache)
+    ref = oracle.Cache(L * m, gpu_slots, cpu_slots)
+    per_tok = 2 * w.n_kv_heads * w.head_dim * w.elem_bytes
+    lens = np.minimum(w.chunk_size, w.n_prefix - np.arange(m) * w.chunk_size)
+    slot_bytes = w.chunk_size * per_tok
+    total_cache_hits = 0
+    for r in range(3):
+        ctx.reset()
+        plain.reset()
+        prev = np.zeros(0, np.int64)
+        A_first = None
+        for l in range(L):
+            first = l - l % period
+            print(f"period {period} request {r} layer {l}", flush=True)
+            q = dev(synth.request_queries(w, l, r))
+            outs, sels, As, stats = [], [], [], []
+            for c in (ctx, plain):
+                A = torch.full((m,), float("nan"), dtype=torch.float64, device=DEV)
+                sel = torch.empty(k, dtype=torch.int32, device=DEV)
+                out = torch.empty_like(q)
+                st = c.reprefill_layer(l, q, base[l]["k_suffix"], base[l]["v_suffix"],
+                                       base[l]["k_prefix"], out, kv_host=stores[l],
+                                       kv_host_next=stores[l + 1] if l + 1 < L else None,
+                                       chunk_scores=A, sel_idx=sel)
+                outs.append(out)
+                sels.append(sel)
+                As.append(A)
+                stats.append(st)
+            torch.cuda.synchronize()
+            sel = sels[0].cpu().numpy().astype(np.int64)
+            assert np.array_equal(sel, sels[1].cpu().numpy())
+            assert torch.equal(outs[0].view(torch.int16), outs[1].view(torch.int16))
+            if first == l:
+                A_first = As[0].cpu().numpy()
+                assert np.array_equal(A_first.view(np.int64), As[1].cpu().numpy().view(np.int64))
+            st = stats[0]
+            # expected counts from the oracle cache before and after this layer's access
+            tier = ref.state()[2]
+            resident = set(int(j) for j in sel if tier[l * m + j] == oracle.TIER_GPU)
+            S = set(int(j) for j in sel)
+            P = set(int(j) for j in prev) - resident
+            hits = (S - resident) & P
+            miss = S - resident - P
+            assert st["cache_hits"] == len(resident)
+            assert st["hits"] == len(hits) and st["misses"] == len(miss)
+            assert st["wasted"] == len(P) - len(hits)
+            assert st["bytes_demand"] == int(sum(lens[j] for j in miss)) * per_tok
+            assert st["bytes_gathered"] == int(sum(lens[j] for j in S)) * per_tok
+            before = tier[l * m + sel]
+            ref.access(l * m + sel, A_first[sel])
+            after = ref.state()[2]
+            fills = int(np.sum((after[l * m + sel] == oracle.TIER_GPU) &
+                               (before != oracle.TIER_GPU)))
+            assert st["bytes_cache_fill"] == fills * slot_bytes
+            if l + 1 < L:
+                nxt = [j for j in S if after[(l + 1) * m + j] != oracle.TIER_GPU]
+                assert st["bytes_prefetch"] == int(sum(lens[j] for j in nxt)) * per_tok
+            total_cache_hits += st["cache_hits"]
+            print(f"  cache hits {st['cache_hits']} prefetch hits {st['hits']} "
+                  f"misses {st['misses']} fills {fills}", flush=True)
+            prev = sel if l + 1 < L else np.zeros(0, np.int64)
+        # the last layer against the oracle's attention over the same set
+        t = dict(layers[L - 1], q=synth.request_queries(w, L - 1, r))
+        out_ref = oracle.sparse_attn(s, t["q"], t["k_prefix"], t["v_prefix"], sel.astype(np.int32),
+                                     t["k_suffix"], t["v_suffix"])
+        assert float(np.abs(to_f64(outs[0]) - out_ref).max()) <= 2e-2
+    assert total_cache_hits > 0  # later requests do find chunks in HBM
+    I1, F1, T1 = cache.state()
+    I2, F2, T2 = ref.state()
+    assert np.array_equal(I1.view(np.int64), I2.view(np.int64))
+    assert np.array_equal(F1, F2) and np.array_equal(T1, T2)
+    ctx.reset()
+    ctx.attach_cache(None)
+    ctx.close()
+    plain.close()
+    cache.close()
+
+
+def test_attach_cache_refusals():
+    import paper_2601_13631_amd as ckv
+    w = synth.WORKLOADS["c5_qwen32b_128k_host"].scaled(n_prefix=4096, n_suffix=24, n_layers=2)
+    m = w.n_chunks
+    t = synth.layer_tensors(w, 0)
+    tt = {kk: dev(v) for kk, v in t.items()}
+    store = _store(w, t)
+    hbm = ckv.Context(dims_of(w), w.keep_ratio, 0)
+    cache = ckv.Cache(2 * m, 8, 8)
+    with pytest.raises(ckv.CkvError) as e:  # needs a host-resident prefix
+        hbm.attach_cache(cache)
+    assert e.value.status == ckv.EINVAL
+    hbm.close()
+    ctx = ckv.Context(dims_of(w), w.keep_ratio, ckv.CTX_HOST_PREFIX)
+    odd = ckv.Cache(2 * m + 1, 8, 8)
+    with pytest.raises(ckv.CkvError) as e:  # keys not a whole number of layers
+        ctx.attach_cache(odd)
+    assert e.value.status == ckv.EINVAL
+    used = ckv.Cache(2 * m, 8, 8)
+    used.access([3], [1.0])
+    with pytest.raises(ckv.CkvError) as e:  # GPU tier not empty
+        ctx.attach_cache(used)
+    assert e.value.status == ckv.ESTATE
+    one_layer = ckv.Cache(m, 8, 8)
+    ctx.attach_cache(one_layer)
+    out = torch.empty_like(tt["q"])
+    ctx.reprefill_layer(0, tt["q"], tt["k_suffix"], tt["v_suffix"], tt["k_prefix"], out,
+                        kv_host=store, kv_host_next=store)
+    with pytest.raises(ckv.CkvError) as e:  # mid-request
+        ctx.attach_cache(cache)
+    assert e.value.status == ckv.ESTATE
+    with pytest.raises(ckv.CkvError) as e:  # layer 1 has no keys in a one-layer cache
+        ctx.reprefill_layer(1, tt["q"], tt["k_suffix"], tt["v_suffix"], tt["k_prefix"], out,
+                            kv_host=store)
+    assert e.value.status == ckv.EINVAL
+    torch.cuda.synchronize()
+    ctx.reset()
+    ctx.attach_cache(None)
+    ctx.close()
+    for c in (cache, odd, used, one_layer):
+        c.close()
