@@ -78,6 +78,58 @@ def counter_traffic(workload: str):
     return (fetch + write) * 1024.0, os.path.relpath(path, ROOT)
 
 
+def host_cache_requests(args, w, ckv, synth, np, torch, layers, stores, dims, k) -> dict:
+    """Requests on the shared host-resident prefix (request r's queries from
+    synth.request_queries), run layer by layer without a cache and with the
+    attention-guided cache (Sec. 4.5) or its frequency-only foil attached, its
+    GPU tier held in HBM slots: per request, time per layer and bytes over the
+    host link."""
+    L, m, R = len(layers), w.n_chunks, args.host_requests
+    dev = torch.device("cuda:0")
+    qs = [[torch.from_numpy(synth.request_queries(w, l, r)).view(torch.bfloat16).to(dev)
+           for l in range(L)] for r in range(R)]
+    gpu_slots = int(args.host_cache_frac * L * k)
+    out = torch.empty_like(layers[0]["q"])
+    res = {"requests": R, "layers": L, "gpu_slots": gpu_slots,
+           "slot_bytes": 2 * w.chunk_size * w.n_kv_heads * w.head_dim * w.elem_bytes}
+    for name, policy in (("none", None), ("attention", ckv.CACHE_ATTENTION), ("lfu", ckv.CACHE_LFU)):
+        ctx = ckv.Context(dims, w.keep_ratio, ckv.CTX_HOST_PREFIX)
+        cache = None
+        if policy is not None:
+            cache = ckv.Cache(L * m, gpu_slots, L * k, policy)
+            ctx.attach_cache(cache)
+        per = []
+        for r in range(R):
+            ctx.reset()
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            sts = []
+            for l in range(L):
+                t = layers[l]
+                sts.append(ctx.reprefill_layer(l, qs[r][l], t["k_suffix"], t["v_suffix"],
+                                               t["k_prefix"], out, kv_host=stores[l],
+                                               kv_host_next=stores[l + 1] if l + 1 < L else None))
+            torch.cuda.synchronize()
+            dt = time.perf_counter() - t0
+            per.append({"us_per_layer": round(dt * 1e6 / L, 1),
+                         "host_link_mb_per_layer": round(sum(s_["bytes_prefetch"] + s_["bytes_demand"]
+                                                             for s_ in sts) / L / 1e6, 2),
+                         "cache_hit_pct": round(100.0 * sum(s_["cache_hits"] for s_ in sts) /
+                                                (k * L), 2),
+                         "cache_fill_mb_per_layer": round(sum(s_["bytes_cache_fill"] for s_ in sts)
+                                                          / L / 1e6, 2)})
+        ctx.reset()
+        if cache is not None:
+            ctx.attach_cache(None)
+        ctx.close()
+        if cache is not None:
+            cache.close()
+        res[name] = per
+        log(f"requests, cache {name}: " + "; ".join(
+            f"{p_['us_per_layer']} us/layer, {p_['host_link_mb_per_layer']} MB/layer" for p_ in per))
+    return res
+
+
 def host_resident(args, w, ckv, synth, np, torch) -> int:
     """Host-resident prefix (K/V of every layer in pinned host memory, a probe
     copy of K in HBM for scoring): per-layer steps in order, each fetching only
@@ -136,6 +188,8 @@ def host_resident(args, w, ckv, synth, np, torch) -> int:
     hits = sum(s_["hits"] for s_ in stats)
     later = [s_ for i, s_ in enumerate(stats) if i % L]
     log(f"{us:.1f} us per layer including the host link; {link / elapsed / 1e9:.1f} GB/s over it")
+    cache_detail = host_cache_requests(args, w, ckv, synth, np, torch, layers, stores, dims, k) \
+        if args.host_requests > 0 else None
     line = {
         "metric": METRIC, "value": None, "unit": "tokens/s", "n_gpus": 1, "steps": n,
         "warmup": L, "ms_per_step": round(us * 1e-3, 5), "higher_is_better": True,
@@ -158,6 +212,8 @@ def host_resident(args, w, ckv, synth, np, torch) -> int:
             "hits_per_layer": round(hits / n, 1),
         },
     }
+    if cache_detail is not None:
+        line["detail"]["cache_requests"] = cache_detail
     print(json.dumps(line), flush=True)
     return 0
 
@@ -234,6 +290,12 @@ def main() -> int:
                     help="host-resident workloads: layers per pass")
     ap.add_argument("--host-reps", type=int, default=3,
                     help="host-resident workloads: timed passes over those layers")
+    ap.add_argument("--host-requests", type=int, default=4,
+                    help="host-resident workloads: requests on the shared prefix run without and "
+                         "with a cache attached (0: skip)")
+    ap.add_argument("--host-cache-frac", type=float, default=0.5,
+                    help="host-resident workloads: cache GPU slots as a fraction of one request's "
+                         "kept chunks over the layers run")
     ap.add_argument("--requests", type=int, default=4,
                     help="requests on the shared prefix in the read-accounting and cache diagnostic")
     args = ap.parse_args()
