@@ -155,6 +155,8 @@ def host_resident(args, w, ckv, synth, np, torch) -> int:
     dims = ckv.make_dims(w.n_prefix, w.n_suffix, w.n_q_heads, w.n_kv_heads, w.head_dim,
                          w.chunk_size, ckv.DTYPE_BF16)
     ctx = ckv.Context(dims, w.keep_ratio, ckv.CTX_HOST_PREFIX)
+    if args.host_period > 1:
+        ctx.set_period(args.host_period)
     k = ctx.k
     outs = [torch.empty_like(l["q"]) for l in layers]
     stream = torch.cuda.current_stream()
@@ -199,7 +201,8 @@ def host_resident(args, w, ckv, synth, np, torch) -> int:
         "config": {"workload": w.name, "layers": L, "n_prefix": w.n_prefix, "n_suffix": w.n_suffix,
                    "q_heads": w.n_q_heads, "kv_heads": w.n_kv_heads, "head_dim": w.head_dim,
                    "chunk_size": w.chunk_size, "keep_ratio": w.keep_ratio, "kept_chunks": k,
-                   "gather": "host -> HBM slots, prefetch of the previous layer's set"},
+                   "gather": "host -> HBM slots, prefetch of the previous layer's set",
+                   "period": args.host_period},
         "roofline": None, "cpu_baseline": None,
         "detail": {
             "note": "host-link-inclusive rate; value is reserved for HBM-resident inputs",
@@ -290,6 +293,8 @@ def main() -> int:
                     help="host-resident workloads: layers per pass")
     ap.add_argument("--host-reps", type=int, default=3,
                     help="host-resident workloads: timed passes over those layers")
+    ap.add_argument("--host-period", type=int, default=1,
+                    help="host-resident workloads: layers per Period (Def. 4.2) in the timed passes")
     ap.add_argument("--host-requests", type=int, default=4,
                     help="host-resident workloads: requests on the shared prefix run without and "
                          "with a cache attached (0: skip)")
