@@ -180,6 +180,7 @@ ckv_status ckv_sparse_prefill_attn(const ckv_dims* dims, const void* q, const vo
  * ------------------------------------------------------------------------- */
 typedef struct ckv_ctx ckv_ctx;
 typedef struct ckv_cache ckv_cache; /* Sec. 4.5 cache, see ckv_cache_create */
+typedef struct ckv_store ckv_store; /* storage tier, see ckv_store_open */
 
 /* ctx flags */
 #define CKV_CTX_HOST_PREFIX 0x1     /* prefix K/V live in pinned host memory (Sec. 4.3.2) */
@@ -254,6 +255,27 @@ ckv_status ckv_ctx_set_period(ckv_ctx* ctx, int32_t period);
  * Period waits on the host for the copies two layers back before it reuses
  * their staging buffers. */
 ckv_status ckv_ctx_attach_cache(ckv_ctx* ctx, ckv_cache* cache);
+
+/* Storage tier on the layer step (with a store of ckv_store_open whose
+ * span_bytes is one chunk's K and V spans and whose n_keys is a multiple of m:
+ * key = layer * m + chunk).  Attaches `store` to a context with a
+ * host-resident prefix, or detaches it (NULL).  The context then allocates two
+ * pinned staging buffers of 2k chunks and takes every chunk a layer moves to
+ * HBM from the file instead of from io->kv_host (which may be NULL;
+ * kv_host_next is ignored):
+ *   - the chunks a layer fetches on demand are read by the I/O threads into
+ *     staging (the layer waits for them) and copied to HBM;
+ *   - the prediction for layer + 1 (this layer's set less the chunks the next
+ *     layer finds in an attached cache's HBM slots) is read asynchronously
+ *     while this layer attends and the next one scores, and copied to HBM once
+ *     it has landed;
+ *   - layers past n_keys / m are refused (CKV_EINVAL).
+ * Stats bytes_prefetch and bytes_demand then count bytes read from the file.
+ * Same call rules as ckv_ctx_attach_cache (start of a request, synchronizes
+ * the device); detach or destroy the context before closing the store.  With
+ * a store attached, a layer inside a Period waits on the host for the previous
+ * layer's attention before it reuses that layer's staging buffer. */
+ckv_status ckv_ctx_attach_store(ckv_ctx* ctx, ckv_store* store);
 
 typedef struct ckv_layer_io {
   const void* q;         /* device [S][Hq][d]                                        */
@@ -340,6 +362,32 @@ typedef struct ckv_io_counts {
 } ckv_io_counts;
 ckv_status ckv_io_account(int64_t n, int32_t c, const int32_t* sel_idx, int64_t k,
                           int32_t block_tokens, ckv_io_counts* out);
+
+/* ---------------------------------------------------------------------------
+ * Storage tier -- the prefix KV kept on SSD and loaded by I/O threads
+ * (Sec. 4.3.2 steps, Sec. 4.5's "dispatch I/O threads to load them from SSD").
+ * A store is one file of n_keys spans of span_bytes bytes; span `key` starts
+ * at byte key * span_bytes.  For a layer context, key = layer * m + chunk and
+ * a span is one chunk's K rows then V rows, c rows each (the host-resident
+ * layout of ckv_layer_io.kv_host, layer after layer).  io_threads threads
+ * (1..64) read; runs of consecutive keys going to consecutive destinations
+ * are read with one pread, in pieces of at most 4 MiB.  CKV_STORE_DIRECT
+ * opens the file with O_DIRECT (reads bypass the page cache), which needs
+ * span_bytes to be a multiple of 4096; each I/O thread then reads into a
+ * 4 MiB aligned buffer of its own and copies to the destination, so any
+ * destination (pinned staging included) works.  CKV_EINVAL if the
+ * file cannot be opened or is shorter than n_keys spans.  Host code; the file
+ * is only read.
+ * ------------------------------------------------------------------------- */
+#define CKV_STORE_DIRECT 0x1
+ckv_status ckv_store_open(const char* path, int64_t n_keys, int64_t span_bytes, int32_t io_threads,
+                          int32_t flags, ckv_store** out);
+/* Waits for the I/O threads to finish their queued reads, then closes. */
+ckv_status ckv_store_close(ckv_store* store);
+/* Reads spans keys[0..count) into dst (host memory, count consecutive spans)
+ * with the I/O threads; returns when all have landed.  CKV_EINVAL on a key out
+ * of range (nothing read), CKV_EHIP on a read error. */
+ckv_status ckv_store_read(ckv_store* store, const int64_t* keys, int64_t count, void* dst);
 
 /* ---------------------------------------------------------------------------
  * Attention-guided cache management -- Sec. 4.5, Eq. 2.

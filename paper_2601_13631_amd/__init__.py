@@ -22,6 +22,7 @@ OK, EINVAL, EUNSUPPORTED, EHIP, ENOMEM, ESTATE = range(6)
 DTYPE_F32, DTYPE_BF16 = 0, 1
 CTX_HOST_PREFIX, CTX_MATERIALIZE, CTX_STAGE_TIMING, CTX_SCORE_TIMING = 0x1, 0x2, 0x4, 0x8
 CACHE_ATTENTION, CACHE_LFU = 0, 1
+STORE_DIRECT = 0x1
 TIER_NONE, TIER_CPU, TIER_GPU = 0, 1, 2
 STAGES = ("score", "finalize", "select", "move", "attn")
 
@@ -96,6 +97,11 @@ _SIG = {
     "ckv_ctx_reset": ([_P], ctypes.c_int32),
     "ckv_ctx_set_period": ([_P, ctypes.c_int32], ctypes.c_int32),
     "ckv_ctx_attach_cache": ([_P, _P], ctypes.c_int32),
+    "ckv_ctx_attach_store": ([_P, _P], ctypes.c_int32),
+    "ckv_store_open": ([ctypes.c_char_p, ctypes.c_int64, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32,
+                        ctypes.POINTER(_P)], ctypes.c_int32),
+    "ckv_store_close": ([_P], ctypes.c_int32),
+    "ckv_store_read": ([_P, _P, ctypes.c_int64, _P], ctypes.c_int32),
     "ckv_ctx_stage_times": ([_P, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64)],
                             ctypes.c_int32),
     "ckv_reprefill_layer": ([_P, ctypes.c_int32, ctypes.POINTER(LayerIO),
@@ -250,6 +256,13 @@ class Context:
         _check(_lib.ckv_ctx_attach_cache(self._h, cache._h if cache is not None else None),
                "ckv_ctx_attach_cache")
 
+    def attach_store(self, store) -> None:
+        """Takes the chunks of this host-resident context from ``store`` (a
+        :class:`Store`, or None to detach)."""
+        self._store = store  # the context must not outlive the store it reads
+        _check(_lib.ckv_ctx_attach_store(self._h, store._h if store is not None else None),
+               "ckv_ctx_attach_store")
+
     def close(self) -> None:
         if self._h:
             _check(_lib.ckv_ctx_destroy(self._h), "ckv_ctx_destroy")
@@ -329,6 +342,37 @@ class Cache:
     def close(self) -> None:
         if self._h:
             _check(_lib.ckv_cache_destroy(self._h), "ckv_cache_destroy")
+            self._h = ctypes.c_void_p()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+class Store:
+    """``ckv_store``: a file of fixed-size spans read by I/O threads (the storage tier)."""
+
+    def __init__(self, path: str, n_keys: int, span_bytes: int, io_threads: int = 8, flags: int = 0):
+        self.span_bytes = span_bytes
+        self._h = ctypes.c_void_p()
+        _check(_lib.ckv_store_open(os.fsencode(path), n_keys, span_bytes, io_threads, flags,
+                                   ctypes.byref(self._h)), "ckv_store_open")
+
+    def read(self, keys, dst) -> None:
+        """Spans ``keys`` into ``dst`` (a host numpy array or tensor of len(keys) spans)."""
+        import numpy as np
+        keys = np.ascontiguousarray(keys, np.int64)
+        nbytes = dst.nbytes if hasattr(dst, "nbytes") else dst.numel() * dst.element_size()
+        if nbytes < keys.size * self.span_bytes:
+            raise ValueError("destination smaller than the spans read")
+        ptr = dst.ctypes.data if hasattr(dst, "ctypes") else dst.data_ptr()
+        _check(_lib.ckv_store_read(self._h, _host_ptr(keys), keys.size, ptr), "ckv_store_read")
+
+    def close(self) -> None:
+        if self._h:
+            _check(_lib.ckv_store_close(self._h), "ckv_store_close")
             self._h = ctypes.c_void_p()
 
     def __del__(self):

@@ -148,6 +148,17 @@ ckv_status launch_attn(const ckv_dims* d, const void* q, const ChunkSource& src,
                        const int32_t* sel, int64_t k, const void* k_suffix, const void* v_suffix,
                        void* out, void* ws, size_t ws_bytes, hipStream_t st);
 
+// ---- storage tier, as a layer context drives it ------------------------------
+int64_t store_keys(const ckv_store* s);
+int64_t store_span_bytes(const ckv_store* s);
+bool store_direct(const ckv_store* s);
+// Queues reads of spans keys[u] into dst[u] (host memory) for the I/O threads;
+// *ticket names the request for store_wait.
+ckv_status store_submit(ckv_store* s, const int64_t* keys, int64_t count, char* const* dst,
+                        int64_t* ticket);
+// Blocks until every read of the ticket has landed (CKV_EHIP on a read error).
+ckv_status store_wait(ckv_store* s, int64_t ticket);
+
 // ---- attention-guided cache, as a layer context drives it ------------------
 int64_t cache_keys(const ckv_cache* c);
 int64_t cache_gpu_slots(const ckv_cache* c);

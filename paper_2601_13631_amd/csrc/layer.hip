@@ -82,6 +82,17 @@ struct ckv_ctx {
   int32_t* fill_host[2] = {nullptr, nullptr};       // pinned [2k]: source slots, then target slots
   int32_t* fill_dev[2] = {nullptr, nullptr};
   bool pref_recorded[2] = {false, false};
+  // storage tier: chunks come from a file through pinned staging buffers that
+  // mirror the two transient HBM buffers slot for slot
+  ckv_store* kv_store = nullptr;
+  int64_t store_layers = 0;
+  char* staging[2] = {nullptr, nullptr};       // pinned, slots_per_buf slots each
+  const void* staging_dev[2] = {nullptr, nullptr};
+  int32_t* iota_dev = nullptr;                 // 0 .. slots_per_buf-1
+  int64_t pref_ticket[2] = {0, 0};             // store reads of buffer b's prediction in flight
+  int64_t pref_count[2] = {0, 0};              // chunks they bring (staging slots 0..count-1)
+  std::vector<int64_t> io_keys;
+  std::vector<char*> io_dst;
   // stage timing: a ring of event sets, harvested when a set is reused or on query
   static constexpr int kRing = 64;
   hipEvent_t tev[kRing][CKV_N_STAGES + 1] = {};
@@ -91,8 +102,28 @@ struct ckv_ctx {
 
 namespace {
 
+// Waits for store reads into staging that are still in flight.
+void drain_store_reads(ckv_ctx* c) {
+  for (int b = 0; b < 2; ++b) {
+    if (c->kv_store && c->pref_ticket[b]) (void)store_wait(c->kv_store, c->pref_ticket[b]);
+    c->pref_ticket[b] = 0;
+    c->pref_count[b] = 0;
+  }
+}
+
+void free_staging(ckv_ctx* c) {
+  for (int b = 0; b < 2; ++b) {
+    (void)hipHostFree(c->staging[b]);
+    c->staging[b] = nullptr;
+    c->staging_dev[b] = nullptr;
+  }
+  (void)hipFree(c->iota_dev);
+  c->iota_dev = nullptr;
+}
+
 ckv_status free_ctx(ckv_ctx* c) {
   if (!c) return CKV_OK;
+  drain_store_reads(c);
   if (c->demand) (void)hipStreamSynchronize(c->demand);
   if (c->prefetch) (void)hipStreamSynchronize(c->prefetch);
   (void)hipFree(c->ws);
@@ -109,6 +140,7 @@ ckv_status free_ctx(ckv_ctx* c) {
     if (c->ev_attn[i]) (void)hipEventDestroy(c->ev_attn[i]);
   }
   (void)hipFree(c->arena);
+  free_staging(c);
   (void)hipHostFree(c->sel_host);
   (void)hipHostFree(c->scores_host);
   for (auto& set : c->tev)
@@ -309,10 +341,61 @@ ckv_status ckv_ctx_attach_cache(ckv_ctx* ctx, ckv_cache* cache) {
   return CKV_OK;
 }
 
+ckv_status ckv_ctx_attach_store(ckv_ctx* ctx, ckv_store* store) {
+  clear_error();
+  if (!ctx) CKV_FAIL(CKV_EINVAL, "ctx is NULL");
+  if (!(ctx->flags & CKV_CTX_HOST_PREFIX))
+    CKV_FAIL(CKV_EINVAL, "a store needs a context with a host-resident prefix");
+  if (ctx->next_layer != 0)
+    CKV_FAIL(CKV_ESTATE, "attach a store at the start of a request (before layer 0 or after a reset)");
+  if (store) {
+    if (store_span_bytes(store) != ctx->slot_bytes)
+      CKV_FAIL(CKV_EINVAL, "store spans of %lld bytes, chunks of %lld", (long long)store_span_bytes(store),
+               (long long)ctx->slot_bytes);
+    if (store_keys(store) % ctx->m != 0)
+      CKV_FAIL(CKV_EINVAL, "store keys (%lld) must be a whole number of layers of %lld chunks",
+               (long long)store_keys(store), (long long)ctx->m);
+  }
+  drain_store_reads(ctx);
+  CKV_HIP(hipDeviceSynchronize());
+  free_staging(ctx);
+  ctx->kv_store = nullptr;
+  ctx->store_layers = 0;
+  if (!store) return CKV_OK;
+  const int64_t spb = ctx->slots_per_buf;
+  for (int b = 0; b < 2; ++b) {
+    hipError_t e = hipHostMalloc((void**)&ctx->staging[b], (size_t)(spb * ctx->slot_bytes),
+                                 hipHostMallocDefault);
+    if (e != hipSuccess) {
+      free_staging(ctx);
+      CKV_FAIL(e == hipErrorOutOfMemory ? CKV_ENOMEM : CKV_EHIP, "pinned staging: %s",
+               hipGetErrorString(e));
+    }
+    ctx->staging_dev[b] = device_view(ctx->staging[b]);
+    if (!ctx->staging_dev[b]) {
+      free_staging(ctx);
+      CKV_FAIL(CKV_EHIP, "pinned staging is not visible to the device");
+    }
+  }
+  std::vector<int32_t> iota((size_t)spb);
+  for (int64_t i = 0; i < spb; ++i) iota[i] = (int32_t)i;
+  hipError_t e = hipMalloc((void**)&ctx->iota_dev, (size_t)spb * sizeof(int32_t));
+  if (e == hipSuccess)
+    e = hipMemcpy(ctx->iota_dev, iota.data(), (size_t)spb * sizeof(int32_t), hipMemcpyHostToDevice);
+  if (e != hipSuccess) {
+    free_staging(ctx);
+    CKV_FAIL(CKV_EHIP, "staging index table: %s", hipGetErrorString(e));
+  }
+  ctx->kv_store = store;
+  ctx->store_layers = store_keys(store) / ctx->m;
+  return CKV_OK;
+}
+
 ckv_status ckv_ctx_reset(ckv_ctx* ctx) {
   clear_error();
   if (!ctx) CKV_FAIL(CKV_EINVAL, "ctx is NULL");
   if (ctx->prefetch) CKV_HIP(hipStreamSynchronize(ctx->prefetch));
+  drain_store_reads(ctx);
   ctx->pred.clear();
   ctx->pref_pending[0] = ctx->pref_pending[1] = false;
   ctx->next_layer = 0;
@@ -339,7 +422,15 @@ ckv_status ckv_reprefill_layer(ckv_ctx* c, int32_t layer, const ckv_layer_io* io
   if (!aligned16(io->q) || !aligned16(io->k_suffix) || !aligned16(io->v_suffix) ||
       !aligned16(io->k_probe) || !aligned16(io->out))
     CKV_FAIL(CKV_EINVAL, "tensors must be 16-byte aligned");
-  if (host) {
+  const bool stored = host && c->kv_store;  // chunks come from the storage tier
+  if (stored) {
+    if (layer != c->next_layer)
+      CKV_FAIL(CKV_ESTATE, "host-resident layers must run in order (expected %d, got %d)",
+               c->next_layer, layer);
+    if (layer >= c->store_layers)
+      CKV_FAIL(CKV_EINVAL, "layer %d is not in the attached store (%lld layers)", layer,
+               (long long)c->store_layers);
+  } else if (host) {
     if (!io->kv_host) CKV_FAIL(CKV_EINVAL, "host-resident prefix needs kv_host");
     if (layer != c->next_layer)
       CKV_FAIL(CKV_ESTATE, "host-resident layers must run in order (expected %d, got %d)",
@@ -443,13 +534,31 @@ ckv_status ckv_reprefill_layer(ckv_ctx* c, int32_t layer, const ckv_layer_io* io
   // ---- host-resident prefix ------------------------------------------------
   const int cur = layer & 1, nxt = cur ^ 1;
   const bool cached = c->cache != nullptr;
+  const int64_t key0 = (int64_t)layer * c->m;
+  if (stored && c->pref_ticket[cur]) {
+    // this layer's prediction, read from the store during the previous layer:
+    // once it has landed, it moves to HBM on the prefetch stream, beside this
+    // layer's scoring
+    s = store_wait(c->kv_store, c->pref_ticket[cur]);
+    c->pref_ticket[cur] = 0;
+    if (s != CKV_OK) return s;
+    if (c->attn_recorded[cur]) CKV_HIP(hipStreamWaitEvent(c->prefetch, c->ev_attn[cur], 0));
+    CKV_HIP(hipStreamWaitEvent(c->prefetch, c->ev_dem, 0));
+    s = launch_copy_spans(c->staging_dev[cur], c->iota_dev, c->pref_count[cur], 0, c->slots[cur],
+                          c->slot_bytes, c->prefetch);
+    if (s != CKV_OK) return s;
+    CKV_HIP(hipEventRecord(c->ev_pref[cur], c->prefetch));
+    c->pref_pending[cur] = true;
+    c->pref_recorded[cur] = true;
+  }
   if (reuse) {  // the Period's set is already on the host: no synchronisation
-    if (cached) {
-      // the staging buffers written below were last read by the copies of
-      // two layers ago (and the prefetch list by the previous layer's
-      // prefetch); their contents differ from layer to layer with a cache
+    if (cached || stored) {
+      // the host staging written below was last read by the copies of two
+      // layers ago (and the prefetch list, or the store's staging buffer, by
+      // the previous layer's); their contents differ from layer to layer
       if (c->attn_recorded[cur]) CKV_HIP(hipEventSynchronize(c->ev_attn[cur]));
       if (c->pref_recorded[nxt]) CKV_HIP(hipEventSynchronize(c->ev_pref[nxt]));
+      if (stored && c->attn_recorded[nxt]) CKV_HIP(hipEventSynchronize(c->ev_attn[nxt]));
     }
     std::memcpy(c->sel_host, c->pset_host.data(), (size_t)k * sizeof(int32_t));
   } else {
@@ -473,7 +582,6 @@ ckv_status ckv_reprefill_layer(ckv_ctx* c, int32_t layer, const ckv_layer_io* io
   // order), misses follow
   const int64_t spb = c->slots_per_buf;
   const int64_t buf0 = cur * spb, cache0 = 2 * spb;
-  const int64_t key0 = (int64_t)layer * c->m;
   const std::vector<int32_t>& P = c->pred;
   std::vector<int32_t> miss;
   miss.reserve((size_t)k);
@@ -508,7 +616,25 @@ ckv_status ckv_reprefill_layer(ckv_ctx* c, int32_t layer, const ckv_layer_io* io
   if (c->attn_recorded[cur]) CKV_HIP(hipStreamWaitEvent(c->demand, c->ev_attn[cur], 0));
   CKV_HIP(hipMemcpyAsync(c->slot_tab_dev[cur], tab, (size_t)k * sizeof(int32_t),
                          hipMemcpyHostToDevice, c->demand));
-  if (!miss.empty()) {
+  if (!miss.empty() && stored) {
+    // the I/O threads read the misses into staging slots |P|.. (the layer
+    // waits for them), then they move to the same slots in HBM
+    const size_t nm = miss.size();
+    c->io_keys.resize(nm);
+    c->io_dst.resize(nm);
+    for (size_t i = 0; i < nm; ++i) {
+      c->io_keys[i] = key0 + miss[i];
+      c->io_dst[i] = c->staging[cur] + (int64_t)(P.size() + i) * c->slot_bytes;
+    }
+    int64_t ticket = 0;
+    s = store_submit(c->kv_store, c->io_keys.data(), (int64_t)nm, c->io_dst.data(), &ticket);
+    if (s == CKV_OK) s = store_wait(c->kv_store, ticket);
+    if (s != CKV_OK) return s;
+    s = launch_copy_spans(static_cast<const char*>(c->staging_dev[cur]) + (int64_t)P.size() * c->slot_bytes,
+                          c->iota_dev, (int64_t)nm, (int64_t)P.size(), c->slots[cur], c->slot_bytes,
+                          c->demand);
+    if (s != CKV_OK) return s;
+  } else if (!miss.empty()) {
     std::memcpy(c->dem_host[cur], miss.data(), miss.size() * sizeof(int32_t));
     CKV_HIP(hipMemcpyAsync(c->dem_dev[cur], c->dem_host[cur], miss.size() * sizeof(int32_t),
                            hipMemcpyHostToDevice, c->demand));
@@ -579,7 +705,7 @@ ckv_status ckv_reprefill_layer(ckv_ctx* c, int32_t layer, const ckv_layer_io* io
   // prefetch the next layer's copy of this layer's selection (P_{l+1} = S_l),
   // except chunks the next layer finds in the cache's HBM slots
   c->pred.clear();
-  if (io->kv_host_next) {
+  if (stored ? layer + 1 < c->store_layers : io->kv_host_next != nullptr) {
     const int64_t nkey0 = (int64_t)(layer + 1) * c->m;
     const bool next_cached = cached && layer + 1 < c->cache_layers;
     for (int64_t u = 0; u < k; ++u) {
@@ -587,11 +713,30 @@ ckv_status ckv_reprefill_layer(ckv_ctx* c, int32_t layer, const ckv_layer_io* io
       if (next_cached && c->slot_of[nkey0 + j] >= 0) continue;
       c->pred.push_back(j);
     }
+    const int64_t np = (int64_t)c->pred.size();
+    for (int64_t u = 0; u < np; ++u)
+      stv.bytes_prefetch += 2 * chunk_len(d, c->pred[u]) * d->n_kv_heads * d->head_dim * eb;
+    if (stored) {
+      // read into the next layer's staging buffer, whose last readers (the
+      // previous layer's copies) finished before that layer's attention
+      if (c->attn_recorded[nxt]) CKV_HIP(hipEventSynchronize(c->ev_attn[nxt]));
+      c->io_keys.resize((size_t)np);
+      c->io_dst.resize((size_t)np);
+      for (int64_t u = 0; u < np; ++u) {
+        c->io_keys[u] = nkey0 + c->pred[u];
+        c->io_dst[u] = c->staging[nxt] + u * c->slot_bytes;
+      }
+      s = store_submit(c->kv_store, c->io_keys.data(), np, c->io_dst.data(), &c->pref_ticket[nxt]);
+      if (s != CKV_OK) return s;
+      c->pref_count[nxt] = np;
+      c->next_layer = layer + 1;
+      if (stats) *stats = stv;
+      return CKV_OK;
+    }
     if (c->attn_recorded[nxt]) CKV_HIP(hipStreamWaitEvent(c->prefetch, c->ev_attn[nxt], 0));
     // after this layer's demand copies: those are on the critical path and get
     // the host link to themselves
     CKV_HIP(hipStreamWaitEvent(c->prefetch, c->ev_dem, 0));
-    const int64_t np = (int64_t)c->pred.size();
     if (np > 0) {
       std::memcpy(c->pref_host[nxt], c->pred.data(), (size_t)np * sizeof(int32_t));
       CKV_HIP(hipMemcpyAsync(c->pref_dev[nxt], c->pref_host[nxt], (size_t)np * sizeof(int32_t),
@@ -603,8 +748,6 @@ ckv_status ckv_reprefill_layer(ckv_ctx* c, int32_t layer, const ckv_layer_io* io
     CKV_HIP(hipEventRecord(c->ev_pref[nxt], c->prefetch));
     c->pref_pending[nxt] = true;
     c->pref_recorded[nxt] = true;
-    for (int64_t u = 0; u < np; ++u)
-      stv.bytes_prefetch += 2 * chunk_len(d, c->pred[u]) * d->n_kv_heads * d->head_dim * eb;
   }
   c->next_layer = layer + 1;
   if (stats) *stats = stv;

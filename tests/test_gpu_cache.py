@@ -161,3 +161,66 @@ def test_attach_cache_refusals():
     ctx.close()
     for c in (cache, odd, used, one_layer):
         c.close()
+
+
+@pytest.mark.parametrize("period,with_cache,direct", [(1, False, False), (1, True, True),
+                                                      (2, True, False)])
+def test_layer_store(tmp_path, period, with_cache, direct):
+    """Chunks read from a file by the storage tier's I/O threads: every layer's
+    output, set and counts equal those of the same layers reading the pinned
+    host store (with or without the cache, across two requests)."""
+    import paper_2601_13631_amd as ckv
+    w = synth.WORKLOADS["c5_qwen32b_128k_host"].scaled(n_prefix=4096, n_suffix=24, n_layers=4)
+    L, m = w.n_layers, w.n_chunks
+    layers = [synth.layer_tensors(w, l) for l in range(L)]
+    stores = [_store(w, t) for t in layers]
+    path = str(tmp_path / "kv.bin")
+    with open(path, "wb") as f:
+        for t in layers:
+            synth.chunk_major(t["k_prefix"], t["v_prefix"], w.chunk_size).tofile(f)
+    span = 2 * w.chunk_size * w.n_kv_heads * w.head_dim * w.elem_bytes
+    try:
+        store = ckv.Store(path, L * m, span, 4, ckv.STORE_DIRECT if direct else 0)
+    except ckv.CkvError:
+        pytest.skip("this filesystem refuses O_DIRECT")
+    base = [{kk: dev(v) for kk, v in t.items()} for t in layers]
+    ctxs = [ckv.Context(dims_of(w), w.keep_ratio, ckv.CTX_HOST_PREFIX) for _ in range(2)]
+    caches = []
+    for c in ctxs:
+        c.set_period(period)
+        if with_cache:
+            caches.append(ckv.Cache(L * m, (L * ctxs[0].k) // 2, L * ctxs[0].k))
+            c.attach_cache(caches[-1])
+    ctxs[1].attach_store(store)
+    k = ctxs[0].k
+    for r in range(2):
+        for c in ctxs:
+            c.reset()
+        for l in range(L):
+            print(f"store period {period} cache {with_cache} direct {direct} request {r} layer {l}",
+                  flush=True)
+            q = dev(synth.request_queries(w, l, r))
+            outs, sels, sts = [], [], []
+            for i, c in enumerate(ctxs):
+                sel = torch.empty(k, dtype=torch.int32, device=DEV)
+                out = torch.empty_like(q)
+                kv = dict(kv_host=stores[l], kv_host_next=stores[l + 1] if l + 1 < L else None) \
+                    if i == 0 else {}
+                sts.append(c.reprefill_layer(l, q, base[l]["k_suffix"], base[l]["v_suffix"],
+                                             base[l]["k_prefix"], out, sel_idx=sel, **kv))
+                outs.append(out)
+                sels.append(sel)
+            torch.cuda.synchronize()
+            assert torch.equal(sels[0], sels[1])
+            assert torch.equal(outs[0].view(torch.int16), outs[1].view(torch.int16))
+            assert sts[0] == sts[1], (sts[0], sts[1])
+    for c in ctxs:
+        c.reset()
+    ctxs[1].attach_store(None)
+    for c in ctxs:
+        if with_cache:
+            c.attach_cache(None)
+        c.close()
+    for cache in caches:
+        cache.close()
+    store.close()
