@@ -130,6 +130,71 @@ def host_cache_requests(args, w, ckv, synth, np, torch, layers, stores, dims, k)
     return res
 
 
+def host_store_run(args, w, ckv, synth, np, torch, host, layers, dims, k) -> dict:
+    """The same layers with their chunks on storage: the chunk-major K/V of every
+    layer written to one file under --host-store (flushed before timing), read
+    by the storage tier's I/O threads with O_DIRECT (the page cache bypassed)
+    into pinned staging and moved to HBM.  Reports the file's raw read rate
+    through the store, then per request the time per layer and the bytes read
+    from the file, without and with the attention-guided cache."""
+    L, m = len(layers), w.n_chunks
+    span = 2 * w.chunk_size * w.n_kv_heads * w.head_dim * w.elem_bytes
+    os.makedirs(args.host_store, exist_ok=True)
+    path = os.path.join(args.host_store, f"{w.name}_kv.bin")
+    with open(path, "wb") as f:
+        for h in host:
+            h.view(torch.uint8).numpy().tofile(f)
+        f.flush()
+        os.fsync(f.fileno())
+    res = {"file_gib": round(L * m * span / 2**30, 2), "direct": True, "io_threads": args.io_threads}
+    store = ckv.Store(path, L * m, span, args.io_threads, ckv.STORE_DIRECT)
+    buf = torch.empty(m * span, dtype=torch.uint8).pin_memory()
+    keys = np.arange(m, dtype=np.int64) + (L - 1) * m
+    t0 = time.perf_counter()
+    store.read(keys, buf)
+    dt = time.perf_counter() - t0
+    res["raw_read_gbs"] = round(m * span / dt / 1e9, 2)
+    out = torch.empty_like(layers[0]["q"])
+    for name, policy in (("none", None), ("attention", ckv.CACHE_ATTENTION)):
+        ctx = ckv.Context(dims, w.keep_ratio, ckv.CTX_HOST_PREFIX)
+        if args.host_period > 1:
+            ctx.set_period(args.host_period)
+        cache = None
+        if policy is not None:
+            cache = ckv.Cache(L * m, int(args.host_cache_frac * L * k), L * k, policy)
+            ctx.attach_cache(cache)
+        ctx.attach_store(store)
+        per = []
+        for r in range(max(1, args.host_requests)):
+            q = [layers[l]["q"] if r == 0 else
+                 torch.from_numpy(synth.request_queries(w, l, r)).view(torch.bfloat16).to("cuda")
+                 for l in range(L)]
+            ctx.reset()
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            sts = [ctx.reprefill_layer(l, q[l], layers[l]["k_suffix"], layers[l]["v_suffix"],
+                                       layers[l]["k_prefix"], out) for l in range(L)]
+            torch.cuda.synchronize()
+            dt = time.perf_counter() - t0
+            read = sum(s_["bytes_prefetch"] + s_["bytes_demand"] for s_ in sts)
+            per.append({"us_per_layer": round(dt * 1e6 / L, 1),
+                        "store_mb_per_layer": round(read / L / 1e6, 2),
+                        "store_gbs": round(read / dt / 1e9, 2),
+                        "cache_hit_pct": round(100.0 * sum(s_["cache_hits"] for s_ in sts) / (k * L), 2)})
+        ctx.reset()
+        ctx.attach_store(None)
+        if cache is not None:
+            ctx.attach_cache(None)
+            cache.close()
+        ctx.close()
+        res[name] = per
+        log(f"store, cache {name}: " + "; ".join(
+            f"{p_['us_per_layer']} us/layer, {p_['store_mb_per_layer']} MB/layer" for p_ in per))
+    store.close()
+    os.remove(path)
+    return res
+
+
 def host_resident(args, w, ckv, synth, np, torch) -> int:
     """Host-resident prefix (K/V of every layer in pinned host memory, a probe
     copy of K in HBM for scoring): per-layer steps in order, each fetching only
@@ -146,6 +211,7 @@ def host_resident(args, w, ckv, synth, np, torch) -> int:
         cm = synth.chunk_major(h["k_prefix"], h["v_prefix"], w.chunk_size)
         stores.append(torch.from_numpy(cm.reshape(-1)).view(torch.bfloat16).pin_memory())
         del h["v_prefix"]
+        del cm
 
     def up(a):
         return torch.from_numpy(a).view(torch.bfloat16).to(dev)
@@ -192,6 +258,8 @@ def host_resident(args, w, ckv, synth, np, torch) -> int:
     log(f"{us:.1f} us per layer including the host link; {link / elapsed / 1e9:.1f} GB/s over it")
     cache_detail = host_cache_requests(args, w, ckv, synth, np, torch, layers, stores, dims, k) \
         if args.host_requests > 0 else None
+    store_detail = host_store_run(args, w, ckv, synth, np, torch, stores, layers, dims, k) \
+        if args.host_store else None
     line = {
         "metric": METRIC, "value": None, "unit": "tokens/s", "n_gpus": 1, "steps": n,
         "warmup": L, "ms_per_step": round(us * 1e-3, 5), "higher_is_better": True,
@@ -217,6 +285,8 @@ def host_resident(args, w, ckv, synth, np, torch) -> int:
     }
     if cache_detail is not None:
         line["detail"]["cache_requests"] = cache_detail
+    if store_detail is not None:
+        line["detail"]["storage_tier"] = store_detail
     print(json.dumps(line), flush=True)
     return 0
 
@@ -301,6 +371,10 @@ def main() -> int:
     ap.add_argument("--host-cache-frac", type=float, default=0.5,
                     help="host-resident workloads: cache GPU slots as a fraction of one request's "
                          "kept chunks over the layers run")
+    ap.add_argument("--host-store", default="",
+                    help="host-resident workloads: also run the layers from a file written in this "
+                         "directory, read by the storage tier (O_DIRECT)")
+    ap.add_argument("--io-threads", type=int, default=16, help="storage tier I/O threads")
     ap.add_argument("--requests", type=int, default=4,
                     help="requests on the shared prefix in the read-accounting and cache diagnostic")
     args = ap.parse_args()
