@@ -134,7 +134,8 @@ def host_store_run(args, w, ckv, synth, np, torch, host, layers, dims, k) -> dic
     """The same layers with their chunks on storage: the chunk-major K/V of every
     layer written to one file under --host-store (flushed before timing), read
     by the storage tier's I/O threads with O_DIRECT (the page cache bypassed)
-    into pinned staging and moved to HBM.  Reports the file's raw read rate
+    into the pinned chunk pool and moved to HBM; with the cache attached the
+    pool keeps the chunks of its GPU and CPU tiers.  Reports the file's raw read rate
     through the store, then per request the time per layer and the bytes read
     from the file, without and with the attention-guided cache."""
     L, m = len(layers), w.n_chunks
@@ -176,10 +177,12 @@ def host_store_run(args, w, ckv, synth, np, torch, host, layers, dims, k) -> dic
                                        layers[l]["k_prefix"], out) for l in range(L)]
             torch.cuda.synchronize()
             dt = time.perf_counter() - t0
-            read = sum(s_["bytes_prefetch"] + s_["bytes_demand"] for s_ in sts)
+            read = sum(s_["bytes_storage"] for s_ in sts)
+            link = sum(s_["bytes_prefetch"] + s_["bytes_demand"] for s_ in sts)
             per.append({"us_per_layer": round(dt * 1e6 / L, 1),
                         "store_mb_per_layer": round(read / L / 1e6, 2),
                         "store_gbs": round(read / dt / 1e9, 2),
+                        "host_link_mb_per_layer": round(link / L / 1e6, 2),
                         "cache_hit_pct": round(100.0 * sum(s_["cache_hits"] for s_ in sts) / (k * L), 2)})
         ctx.reset()
         ctx.attach_store(None)

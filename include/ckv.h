@@ -311,6 +311,8 @@ typedef struct ckv_layer_stats {
                               (no host-link transfer; not counted in hits or misses)   */
   int64_t bytes_cache_fill;/* HBM->HBM bytes copied into cache slots for chunks that
                               entered the cache's GPU tier at this layer (whole slots) */
+  int64_t bytes_storage;   /* bytes read from an attached store at this layer (demand
+                              reads plus the next layer's prediction; whole spans)     */
 } ckv_layer_stats;
 
 /* Sum of the GPU time of each stage (ms[CKV_N_STAGES], milliseconds) over

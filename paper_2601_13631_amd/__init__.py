@@ -60,7 +60,7 @@ class LayerStats(ctypes.Structure):
     """``ckv_layer_stats``."""
     _fields_ = [(f, ctypes.c_int64) for f in (
         "k", "hits", "misses", "wasted", "bytes_prefetch", "bytes_demand", "bytes_gathered",
-        "cache_hits", "bytes_cache_fill")]
+        "cache_hits", "bytes_cache_fill", "bytes_storage")]
 
     def as_dict(self) -> dict:
         return {f: int(getattr(self, f)) for f, _ in self._fields_}

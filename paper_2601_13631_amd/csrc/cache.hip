@@ -27,6 +27,7 @@ struct ckv_cache {
   // layer context holds the GPU tier's chunks in HBM)
   bool log_gpu_evictions = false;
   std::vector<int64_t> gpu_evicted;
+  std::vector<int64_t> dropped_log;  // keys the cascade sent out of memory (same switch)
 };
 
 namespace {
@@ -106,7 +107,10 @@ void place(ckv_cache& c, int64_t x) {
   if (demoting && c.log_gpu_evictions) c.gpu_evicted.push_back(out);
   const int64_t left = admit(c, CKV_TIER_CPU, out);
   if (demoting && left != out) c.counts.demoted++;
-  if (left >= 0) c.counts.dropped++;
+  if (left >= 0) {
+    c.counts.dropped++;
+    if (c.log_gpu_evictions) c.dropped_log.push_back(left);
+  }
 }
 
 }  // namespace
@@ -121,7 +125,15 @@ int8_t cache_tier(const ckv_cache* c, int64_t key) { return c->tier[key]; }
 void cache_log_gpu_evictions(ckv_cache* c, bool on) {
   c->log_gpu_evictions = on;
   c->gpu_evicted.clear();
+  c->dropped_log.clear();
 }
+
+void cache_take_drops(ckv_cache* c, std::vector<int64_t>& out) {
+  out.swap(c->dropped_log);
+  c->dropped_log.clear();
+}
+
+int64_t cache_cpu_slots(const ckv_cache* c) { return c->slots[CKV_TIER_CPU]; }
 
 void cache_take_gpu_evictions(ckv_cache* c, std::vector<int64_t>& out) {
   out.swap(c->gpu_evicted);

@@ -168,5 +168,8 @@ int8_t cache_tier(const ckv_cache* c, int64_t key);
 void cache_log_gpu_evictions(ckv_cache* c, bool on);
 // Moves the logged keys into out (replacing its contents) and clears the log.
 void cache_take_gpu_evictions(ckv_cache* c, std::vector<int64_t>& out);
+// Moves the logged keys that left memory (or were not kept) into out.
+void cache_take_drops(ckv_cache* c, std::vector<int64_t>& out);
+int64_t cache_cpu_slots(const ckv_cache* c);
 
 }  // namespace ckv

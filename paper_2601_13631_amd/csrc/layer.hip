@@ -82,17 +82,27 @@ struct ckv_ctx {
   int32_t* fill_host[2] = {nullptr, nullptr};       // pinned [2k]: source slots, then target slots
   int32_t* fill_dev[2] = {nullptr, nullptr};
   bool pref_recorded[2] = {false, false};
-  // storage tier: chunks come from a file through pinned staging buffers that
-  // mirror the two transient HBM buffers slot for slot
+  // storage tier: chunks come from a file into a pinned chunk pool, then to
+  // HBM.  A chunk in an attached cache's GPU or CPU tier keeps its pool slot
+  // (the pool is the CPU tier of Sec. 4.5, inclusive of the GPU tier); every
+  // other slot is released, and reused only after the next layer's host
+  // synchronisation, when the copies that read it have finished.
   ckv_store* kv_store = nullptr;
   int64_t store_layers = 0;
-  char* staging[2] = {nullptr, nullptr};       // pinned, slots_per_buf slots each
-  const void* staging_dev[2] = {nullptr, nullptr};
-  int32_t* iota_dev = nullptr;                 // 0 .. slots_per_buf-1
-  int64_t pref_ticket[2] = {0, 0};             // store reads of buffer b's prediction in flight
-  int64_t pref_count[2] = {0, 0};              // chunks they bring (staging slots 0..count-1)
-  std::vector<int64_t> io_keys;
+  char* pool = nullptr;  // pinned, pool_n slots of slot_bytes
+  const void* pool_dev = nullptr;
+  int64_t pool_n = 0;
+  std::vector<int32_t> pool_of;  // key -> pool slot, -1 if its bytes are not in the pool
+  std::vector<int32_t> pool_free, pool_quarantine;
+  // copy lists (pool slots, then arena slots) of each buffer's prediction and
+  // demand copies: pinned staging and device copies, 2 * slots_per_buf entries
+  int32_t* xfer_host[2][2] = {{nullptr, nullptr}, {nullptr, nullptr}};
+  int32_t* xfer_dev[2][2] = {{nullptr, nullptr}, {nullptr, nullptr}};
+  int64_t pref_ticket[2] = {0, 0};      // store reads of buffer b's prediction in flight
+  std::vector<int64_t> pref_keys[2];    // keys of buffer b's predicted chunks, in P order
+  std::vector<int64_t> io_keys, dropped;
   std::vector<char*> io_dst;
+  std::vector<int32_t> xsrc, xdst;
   // stage timing: a ring of event sets, harvested when a set is reused or on query
   static constexpr int kRing = 64;
   hipEvent_t tev[kRing][CKV_N_STAGES + 1] = {};
@@ -102,23 +112,62 @@ struct ckv_ctx {
 
 namespace {
 
-// Waits for store reads into staging that are still in flight.
+// Waits for store reads into the pool that are still in flight.
 void drain_store_reads(ckv_ctx* c) {
   for (int b = 0; b < 2; ++b) {
     if (c->kv_store && c->pref_ticket[b]) (void)store_wait(c->kv_store, c->pref_ticket[b]);
     c->pref_ticket[b] = 0;
-    c->pref_count[b] = 0;
   }
 }
 
-void free_staging(ckv_ctx* c) {
-  for (int b = 0; b < 2; ++b) {
-    (void)hipHostFree(c->staging[b]);
-    c->staging[b] = nullptr;
-    c->staging_dev[b] = nullptr;
-  }
-  (void)hipFree(c->iota_dev);
-  c->iota_dev = nullptr;
+void free_pool(ckv_ctx* c) {
+  (void)hipHostFree(c->pool);
+  c->pool = nullptr;
+  c->pool_dev = nullptr;
+  c->pool_n = 0;
+  for (int b = 0; b < 2; ++b)
+    for (int i = 0; i < 2; ++i) {
+      (void)hipHostFree(c->xfer_host[b][i]);
+      (void)hipFree(c->xfer_dev[b][i]);
+      c->xfer_host[b][i] = nullptr;
+      c->xfer_dev[b][i] = nullptr;
+    }
+  c->pool_of.clear();
+  c->pool_free.clear();
+  c->pool_quarantine.clear();
+  c->pref_keys[0].clear();
+  c->pref_keys[1].clear();
+}
+
+// A free pool slot for the bytes of `key` (-1 if none is left).
+int32_t pool_take(ckv_ctx* c, int64_t key) {
+  if (c->pool_free.empty()) return -1;
+  const int32_t sl = c->pool_free.back();
+  c->pool_free.pop_back();
+  c->pool_of[key] = sl;
+  return sl;
+}
+
+// Releases key's pool slot; it becomes free after the next host synchronisation.
+void pool_release(ckv_ctx* c, int64_t key) {
+  if (c->pool_of[key] < 0) return;
+  c->pool_quarantine.push_back(c->pool_of[key]);
+  c->pool_of[key] = -1;
+}
+
+// Copies count chunks from pool slots src[] to arena slots dst[] on stream st,
+// with the lists staged through this buffer's pinned and device arrays.
+ckv_status pool_copy(ckv_ctx* c, int b, int which, const int32_t* src, const int32_t* dst,
+                     int64_t count, hipStream_t st) {
+  if (count == 0) return CKV_OK;
+  const int64_t spb = c->slots_per_buf;
+  int32_t* h = c->xfer_host[b][which];
+  std::memcpy(h, src, (size_t)count * sizeof(int32_t));
+  std::memcpy(h + spb, dst, (size_t)count * sizeof(int32_t));
+  CKV_HIP(hipMemcpyAsync(c->xfer_dev[b][which], h, (size_t)(2 * spb) * sizeof(int32_t),
+                         hipMemcpyHostToDevice, st));
+  return launch_copy_slots(c->pool_dev, c->xfer_dev[b][which], c->arena,
+                           c->xfer_dev[b][which] + spb, count, c->slot_bytes, st);
 }
 
 ckv_status free_ctx(ckv_ctx* c) {
@@ -140,7 +189,7 @@ ckv_status free_ctx(ckv_ctx* c) {
     if (c->ev_attn[i]) (void)hipEventDestroy(c->ev_attn[i]);
   }
   (void)hipFree(c->arena);
-  free_staging(c);
+  free_pool(c);
   (void)hipHostFree(c->sel_host);
   (void)hipHostFree(c->scores_host);
   for (auto& set : c->tev)
@@ -305,6 +354,8 @@ ckv_status ckv_ctx_attach_cache(ckv_ctx* ctx, ckv_cache* cache) {
     CKV_FAIL(CKV_EINVAL, "a cache needs a context with a host-resident prefix");
   if (ctx->next_layer != 0)
     CKV_FAIL(CKV_ESTATE, "attach a cache at the start of a request (before layer 0 or after a reset)");
+  if (ctx->kv_store)
+    CKV_FAIL(CKV_ESTATE, "attach the cache before the store (the store's chunk pool holds its tiers)");
   int64_t G = 0;
   if (cache) {
     if (cache_keys(cache) % ctx->m != 0)
@@ -355,39 +406,43 @@ ckv_status ckv_ctx_attach_store(ckv_ctx* ctx, ckv_store* store) {
     if (store_keys(store) % ctx->m != 0)
       CKV_FAIL(CKV_EINVAL, "store keys (%lld) must be a whole number of layers of %lld chunks",
                (long long)store_keys(store), (long long)ctx->m);
+    if (ctx->cache && cache_keys(ctx->cache) != store_keys(store))
+      CKV_FAIL(CKV_EINVAL, "the attached cache and the store name different key ranges");
   }
   drain_store_reads(ctx);
   CKV_HIP(hipDeviceSynchronize());
-  free_staging(ctx);
+  free_pool(ctx);
   ctx->kv_store = nullptr;
   ctx->store_layers = 0;
   if (!store) return CKV_OK;
+  // room for the cache's tiers, plus the transient chunks of two layers in
+  // flight and of the layer whose slots wait for release
+  const int64_t keys = store_keys(store), k = ctx->k;
+  const int64_t kept = ctx->cache ? std::min(keys, cache_gpu_slots(ctx->cache) + cache_cpu_slots(ctx->cache)) : 0;
+  const int64_t n = std::min(keys, kept + 6 * k) + 16;
   const int64_t spb = ctx->slots_per_buf;
-  for (int b = 0; b < 2; ++b) {
-    hipError_t e = hipHostMalloc((void**)&ctx->staging[b], (size_t)(spb * ctx->slot_bytes),
-                                 hipHostMallocDefault);
-    if (e != hipSuccess) {
-      free_staging(ctx);
-      CKV_FAIL(e == hipErrorOutOfMemory ? CKV_ENOMEM : CKV_EHIP, "pinned staging: %s",
-               hipGetErrorString(e));
+  hipError_t e = hipHostMalloc((void**)&ctx->pool, (size_t)(n * ctx->slot_bytes), hipHostMallocDefault);
+  for (int b = 0; b < 2 && e == hipSuccess; ++b)
+    for (int i = 0; i < 2 && e == hipSuccess; ++i) {
+      e = hipHostMalloc((void**)&ctx->xfer_host[b][i], (size_t)(2 * spb) * sizeof(int32_t),
+                        hipHostMallocDefault);
+      if (e == hipSuccess) e = hipMalloc((void**)&ctx->xfer_dev[b][i], (size_t)(2 * spb) * sizeof(int32_t));
     }
-    ctx->staging_dev[b] = device_view(ctx->staging[b]);
-    if (!ctx->staging_dev[b]) {
-      free_staging(ctx);
-      CKV_FAIL(CKV_EHIP, "pinned staging is not visible to the device");
-    }
-  }
-  std::vector<int32_t> iota((size_t)spb);
-  for (int64_t i = 0; i < spb; ++i) iota[i] = (int32_t)i;
-  hipError_t e = hipMalloc((void**)&ctx->iota_dev, (size_t)spb * sizeof(int32_t));
-  if (e == hipSuccess)
-    e = hipMemcpy(ctx->iota_dev, iota.data(), (size_t)spb * sizeof(int32_t), hipMemcpyHostToDevice);
   if (e != hipSuccess) {
-    free_staging(ctx);
-    CKV_FAIL(CKV_EHIP, "staging index table: %s", hipGetErrorString(e));
+    free_pool(ctx);
+    CKV_FAIL(e == hipErrorOutOfMemory ? CKV_ENOMEM : CKV_EHIP, "pinned chunk pool of %lld slots: %s",
+             (long long)n, hipGetErrorString(e));
   }
+  ctx->pool_dev = device_view(ctx->pool);
+  if (!ctx->pool_dev) {
+    free_pool(ctx);
+    CKV_FAIL(CKV_EHIP, "the pinned chunk pool is not visible to the device");
+  }
+  ctx->pool_n = n;
+  ctx->pool_of.assign((size_t)keys, -1);
+  for (int64_t i = n - 1; i >= 0; --i) ctx->pool_free.push_back((int32_t)i);
   ctx->kv_store = store;
-  ctx->store_layers = store_keys(store) / ctx->m;
+  ctx->store_layers = keys / ctx->m;
   return CKV_OK;
 }
 
@@ -396,6 +451,16 @@ ckv_status ckv_ctx_reset(ckv_ctx* ctx) {
   if (!ctx) CKV_FAIL(CKV_EINVAL, "ctx is NULL");
   if (ctx->prefetch) CKV_HIP(hipStreamSynchronize(ctx->prefetch));
   drain_store_reads(ctx);
+  if (ctx->kv_store) {
+    // predictions read for a layer that will not run: release their slots
+    // (nothing reads them any more once the device is idle)
+    CKV_HIP(hipDeviceSynchronize());
+    for (int b = 0; b < 2; ++b) {
+      for (int64_t x : ctx->pref_keys[b])
+        if (!ctx->cache || cache_tier(ctx->cache, x) == CKV_TIER_NONE) pool_release(ctx, x);
+      ctx->pref_keys[b].clear();
+    }
+  }
   ctx->pred.clear();
   ctx->pref_pending[0] = ctx->pref_pending[1] = false;
   ctx->next_layer = 0;
@@ -535,17 +600,32 @@ ckv_status ckv_reprefill_layer(ckv_ctx* c, int32_t layer, const ckv_layer_io* io
   const int cur = layer & 1, nxt = cur ^ 1;
   const bool cached = c->cache != nullptr;
   const int64_t key0 = (int64_t)layer * c->m;
-  if (stored && c->pref_ticket[cur]) {
-    // this layer's prediction, read from the store during the previous layer:
-    // once it has landed, it moves to HBM on the prefetch stream, beside this
-    // layer's scoring
+  const int64_t spb = c->slots_per_buf;
+  const int64_t buf0 = cur * spb, cache0 = 2 * spb;
+  if (stored && c->pref_ticket[cur]) {  // this layer's prediction, read during the previous one
     s = store_wait(c->kv_store, c->pref_ticket[cur]);
     c->pref_ticket[cur] = 0;
     if (s != CKV_OK) return s;
-    if (c->attn_recorded[cur]) CKV_HIP(hipStreamWaitEvent(c->prefetch, c->ev_attn[cur], 0));
+  }
+  if (stored && !c->pref_keys[cur].empty()) {
+    // the predicted chunks (read from the store, or already in the pool) move
+    // to this layer's HBM slots 0..|P|-1 on the prefetch stream, beside this
+    // layer's scoring; this buffer's copy lists were last read two layers ago
+    const std::vector<int64_t>& pk = c->pref_keys[cur];
+    const int64_t np = (int64_t)pk.size();
+    c->xsrc.resize((size_t)np);
+    c->xdst.resize((size_t)np);
+    for (int64_t i = 0; i < np; ++i) {
+      c->xsrc[i] = c->pool_of[pk[i]];
+      c->xdst[i] = (int32_t)(buf0 + i);
+      if (c->xsrc[i] < 0) CKV_FAIL(CKV_ESTATE, "predicted chunk not in the pool (internal)");
+    }
+    if (c->attn_recorded[cur]) {
+      CKV_HIP(hipEventSynchronize(c->ev_attn[cur]));
+      CKV_HIP(hipStreamWaitEvent(c->prefetch, c->ev_attn[cur], 0));
+    }
     CKV_HIP(hipStreamWaitEvent(c->prefetch, c->ev_dem, 0));
-    s = launch_copy_spans(c->staging_dev[cur], c->iota_dev, c->pref_count[cur], 0, c->slots[cur],
-                          c->slot_bytes, c->prefetch);
+    s = pool_copy(c, cur, 0, c->xsrc.data(), c->xdst.data(), np, c->prefetch);
     if (s != CKV_OK) return s;
     CKV_HIP(hipEventRecord(c->ev_pref[cur], c->prefetch));
     c->pref_pending[cur] = true;
@@ -576,12 +656,14 @@ ckv_status ckv_reprefill_layer(ckv_ctx* c, int32_t layer, const ckv_layer_io* io
       }
     }
   }
+  if (stored) {  // the previous layer's copies have finished: its released slots are free
+    c->pool_free.insert(c->pool_free.end(), c->pool_quarantine.begin(), c->pool_quarantine.end());
+    c->pool_quarantine.clear();
+  }
 
   // slot table, in arena slots: chunks held in the cache's HBM slots are read
   // there; predicted chunks sit in this layer's buffer at slots 0..|P|-1 (in P
   // order), misses follow
-  const int64_t spb = c->slots_per_buf;
-  const int64_t buf0 = cur * spb, cache0 = 2 * spb;
   const std::vector<int32_t>& P = c->pred;
   std::vector<int32_t> miss;
   miss.reserve((size_t)k);
@@ -617,22 +699,32 @@ ckv_status ckv_reprefill_layer(ckv_ctx* c, int32_t layer, const ckv_layer_io* io
   CKV_HIP(hipMemcpyAsync(c->slot_tab_dev[cur], tab, (size_t)k * sizeof(int32_t),
                          hipMemcpyHostToDevice, c->demand));
   if (!miss.empty() && stored) {
-    // the I/O threads read the misses into staging slots |P|.. (the layer
-    // waits for them), then they move to the same slots in HBM
+    // misses in the pool move from there; the others are read by the I/O
+    // threads into free pool slots first (the layer waits for them)
     const size_t nm = miss.size();
-    c->io_keys.resize(nm);
-    c->io_dst.resize(nm);
+    c->xsrc.resize(nm);
+    c->xdst.resize(nm);
+    c->io_keys.clear();
+    c->io_dst.clear();
     for (size_t i = 0; i < nm; ++i) {
-      c->io_keys[i] = key0 + miss[i];
-      c->io_dst[i] = c->staging[cur] + (int64_t)(P.size() + i) * c->slot_bytes;
+      const int64_t x = key0 + miss[i];
+      if (c->pool_of[x] < 0) {
+        if (pool_take(c, x) < 0) CKV_FAIL(CKV_ESTATE, "chunk pool exhausted (internal)");
+        c->io_keys.push_back(x);
+        c->io_dst.push_back(c->pool + (int64_t)c->pool_of[x] * c->slot_bytes);
+      }
+      c->xsrc[i] = c->pool_of[x];
+      c->xdst[i] = (int32_t)(buf0 + P.size() + i);
     }
-    int64_t ticket = 0;
-    s = store_submit(c->kv_store, c->io_keys.data(), (int64_t)nm, c->io_dst.data(), &ticket);
-    if (s == CKV_OK) s = store_wait(c->kv_store, ticket);
-    if (s != CKV_OK) return s;
-    s = launch_copy_spans(static_cast<const char*>(c->staging_dev[cur]) + (int64_t)P.size() * c->slot_bytes,
-                          c->iota_dev, (int64_t)nm, (int64_t)P.size(), c->slots[cur], c->slot_bytes,
-                          c->demand);
+    if (!c->io_keys.empty()) {
+      int64_t ticket = 0;
+      s = store_submit(c->kv_store, c->io_keys.data(), (int64_t)c->io_keys.size(), c->io_dst.data(),
+                       &ticket);
+      if (s == CKV_OK) s = store_wait(c->kv_store, ticket);
+      if (s != CKV_OK) return s;
+      stv.bytes_storage += (int64_t)c->io_keys.size() * c->slot_bytes;
+    }
+    s = pool_copy(c, cur, 1, c->xsrc.data(), c->xdst.data(), (int64_t)nm, c->demand);
     if (s != CKV_OK) return s;
   } else if (!miss.empty()) {
     std::memcpy(c->dem_host[cur], miss.data(), miss.size() * sizeof(int32_t));
@@ -698,6 +790,22 @@ ckv_status ckv_reprefill_layer(ckv_ctx* c, int32_t layer, const ckv_layer_io* io
       stv.bytes_cache_fill = nf * c->slot_bytes;
     }
   }
+  if (stored) {
+    // the pool keeps the chunks the cache holds (GPU or CPU tier); this layer's
+    // other chunks, its unused predicted chunks and the chunks the cascade sent
+    // out of memory release their slots
+    auto keep = [&](int64_t x) { return cached && cache_tier(c->cache, x) != CKV_TIER_NONE; };
+    if (cached) {
+      cache_take_drops(c->cache, c->dropped);
+      for (int64_t x : c->dropped)
+        if (!keep(x)) pool_release(c, x);
+    }
+    for (int64_t u = 0; u < k; ++u)
+      if (!keep(key0 + c->sel_host[u])) pool_release(c, key0 + c->sel_host[u]);
+    for (int64_t x : c->pref_keys[cur])
+      if (!keep(x)) pool_release(c, x);
+    c->pref_keys[cur].clear();
+  }
   // after the cache fills too: they read this layer's buffer
   CKV_HIP(hipEventRecord(c->ev_attn[cur], st));
   c->attn_recorded[cur] = true;
@@ -717,18 +825,25 @@ ckv_status ckv_reprefill_layer(ckv_ctx* c, int32_t layer, const ckv_layer_io* io
     for (int64_t u = 0; u < np; ++u)
       stv.bytes_prefetch += 2 * chunk_len(d, c->pred[u]) * d->n_kv_heads * d->head_dim * eb;
     if (stored) {
-      // read into the next layer's staging buffer, whose last readers (the
-      // previous layer's copies) finished before that layer's attention
-      if (c->attn_recorded[nxt]) CKV_HIP(hipEventSynchronize(c->ev_attn[nxt]));
-      c->io_keys.resize((size_t)np);
-      c->io_dst.resize((size_t)np);
+      // predicted chunks not in the pool are read into free pool slots by the
+      // I/O threads while this layer attends and the next one scores
+      c->pref_keys[nxt].clear();
+      c->io_keys.clear();
+      c->io_dst.clear();
       for (int64_t u = 0; u < np; ++u) {
-        c->io_keys[u] = nkey0 + c->pred[u];
-        c->io_dst[u] = c->staging[nxt] + u * c->slot_bytes;
+        const int64_t x = nkey0 + c->pred[u];
+        c->pref_keys[nxt].push_back(x);
+        if (c->pool_of[x] >= 0) continue;
+        if (pool_take(c, x) < 0) CKV_FAIL(CKV_ESTATE, "chunk pool exhausted (internal)");
+        c->io_keys.push_back(x);
+        c->io_dst.push_back(c->pool + (int64_t)c->pool_of[x] * c->slot_bytes);
       }
-      s = store_submit(c->kv_store, c->io_keys.data(), np, c->io_dst.data(), &c->pref_ticket[nxt]);
-      if (s != CKV_OK) return s;
-      c->pref_count[nxt] = np;
+      if (!c->io_keys.empty()) {
+        s = store_submit(c->kv_store, c->io_keys.data(), (int64_t)c->io_keys.size(), c->io_dst.data(),
+                         &c->pref_ticket[nxt]);
+        if (s != CKV_OK) return s;
+        stv.bytes_storage += (int64_t)c->io_keys.size() * c->slot_bytes;
+      }
       c->next_layer = layer + 1;
       if (stats) *stats = stv;
       return CKV_OK;

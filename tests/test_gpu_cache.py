@@ -166,9 +166,13 @@ def test_attach_cache_refusals():
 @pytest.mark.parametrize("period,with_cache,direct", [(1, False, False), (1, True, True),
                                                       (2, True, False)])
 def test_layer_store(tmp_path, period, with_cache, direct):
-    """Chunks read from a file by the storage tier's I/O threads: every layer's
-    output, set and counts equal those of the same layers reading the pinned
-    host store (with or without the cache, across two requests)."""
+    """Chunks read from a file by the storage tier's I/O threads into the pinned
+    chunk pool: every layer's output, set and host-link counts equal those of
+    the same layers reading the pinned host store (with or without the cache,
+    across three requests), and the bytes read from the file are exactly the
+    chunks that were neither in HBM slots nor in the pool, which holds the
+    chunks of the cache's two tiers (the oracle cache, fed the same scores,
+    says which)."""
     import paper_2601_13631_amd as ckv
     w = synth.WORKLOADS["c5_qwen32b_128k_host"].scaled(n_prefix=4096, n_suffix=24, n_layers=4)
     L, m = w.n_layers, w.n_chunks
@@ -185,35 +189,72 @@ def test_layer_store(tmp_path, period, with_cache, direct):
         pytest.skip("this filesystem refuses O_DIRECT")
     base = [{kk: dev(v) for kk, v in t.items()} for t in layers]
     ctxs = [ckv.Context(dims_of(w), w.keep_ratio, ckv.CTX_HOST_PREFIX) for _ in range(2)]
+    k = ctxs[0].k
+    gpu_slots, cpu_slots = (L * k) // 2, L * k
     caches = []
     for c in ctxs:
         c.set_period(period)
         if with_cache:
-            caches.append(ckv.Cache(L * m, (L * ctxs[0].k) // 2, L * ctxs[0].k))
+            caches.append(ckv.Cache(L * m, gpu_slots, cpu_slots))
             c.attach_cache(caches[-1])
     ctxs[1].attach_store(store)
-    k = ctxs[0].k
-    for r in range(2):
+    ref = oracle.Cache(L * m, gpu_slots, cpu_slots) if with_cache else None
+    storage_total = 0
+    for r in range(3):
         for c in ctxs:
             c.reset()
+        prev = []
+        A_first = None
         for l in range(L):
+            first = l - l % period
             print(f"store period {period} cache {with_cache} direct {direct} request {r} layer {l}",
                   flush=True)
             q = dev(synth.request_queries(w, l, r))
             outs, sels, sts = [], [], []
+            A = torch.full((m,), float("nan"), dtype=torch.float64, device=DEV)
             for i, c in enumerate(ctxs):
                 sel = torch.empty(k, dtype=torch.int32, device=DEV)
                 out = torch.empty_like(q)
                 kv = dict(kv_host=stores[l], kv_host_next=stores[l + 1] if l + 1 < L else None) \
                     if i == 0 else {}
                 sts.append(c.reprefill_layer(l, q, base[l]["k_suffix"], base[l]["v_suffix"],
-                                             base[l]["k_prefix"], out, sel_idx=sel, **kv))
+                                             base[l]["k_prefix"], out, sel_idx=sel,
+                                             chunk_scores=A if i == 1 else None, **kv))
                 outs.append(out)
                 sels.append(sel)
             torch.cuda.synchronize()
             assert torch.equal(sels[0], sels[1])
             assert torch.equal(outs[0].view(torch.int16), outs[1].view(torch.int16))
-            assert sts[0] == sts[1], (sts[0], sts[1])
+            got = dict(sts[1])
+            storage = got.pop("bytes_storage")
+            assert sts[0].pop("bytes_storage") == 0
+            assert got == sts[0], (got, sts[0])
+            sel = sels[1].cpu().numpy().astype(np.int64)
+            if first == l:
+                A_first = A.cpu().numpy()
+            # expected file reads from the oracle cache's tiers
+            if ref is None:
+                tier = np.zeros(L * m, np.int8)
+            else:
+                tier = ref.state()[2]
+            hbm = {int(j) for j in sel if tier[l * m + j] == oracle.TIER_GPU}
+            P = [j for j in prev if j not in hbm]
+            miss = [int(j) for j in sel if int(j) not in hbm and int(j) not in P]
+            reads = sum(1 for j in miss if tier[l * m + j] == oracle.TIER_NONE)
+            if ref is not None:
+                ref.access(l * m + sel, A_first[sel])
+                tier = ref.state()[2]
+            if l + 1 < L:
+                nxt = [int(j) for j in sel if tier[(l + 1) * m + j] != oracle.TIER_GPU]
+                reads += sum(1 for j in nxt if tier[(l + 1) * m + j] == oracle.TIER_NONE)
+                prev = nxt
+            else:
+                prev = []
+            assert storage == reads * span, (storage // span, reads)
+            storage_total += storage
+            print(f"  file reads {storage // span} chunks", flush=True)
+    if with_cache:  # later requests find chunks in the pool
+        assert storage_total < 3 * L * k * span
     for c in ctxs:
         c.reset()
     ctxs[1].attach_store(None)
