@@ -11,7 +11,7 @@
 #include <new>
 #include <vector>
 
-#include "ckv_internal.h"
+#include "tiers_internal.h"
 
 struct ckv_cache {
   int64_t n_keys = 0;

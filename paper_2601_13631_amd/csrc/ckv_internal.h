@@ -8,7 +8,6 @@
 #include <cstdint>
 #include <cstdio>
 #include <string>
-#include <vector>
 
 #include "../../include/ckv.h"
 
@@ -125,12 +124,6 @@ struct ChunkSource {
 // memory) to span slot0 + i of dst, for i < count; chunks is a device array.
 ckv_status launch_copy_spans(const void* src, const int32_t* chunks, int64_t count, int64_t slot0,
                              void* dst, int64_t span_bytes, hipStream_t st);
-// Copies whole spans of span_bytes each: span src_slots[i] of src to span
-// dst_slots[i] of dst, for i < count; both lists are device arrays.  For
-// device-to-device moves (wider grid than launch_copy_spans).
-ckv_status launch_copy_slots(const void* src, const int32_t* src_slots, void* dst,
-                             const int32_t* dst_slots, int64_t count, int64_t span_bytes,
-                             hipStream_t st);
 // The address under which kernels read p: p itself for device memory, the
 // mapped address for pinned host memory; nullptr if the device cannot read it
 // (pageable host memory), which callers turn into CKV_EINVAL.
@@ -147,29 +140,5 @@ AttnPlan make_attn_plan(const ckv_dims* d, int64_t k);
 ckv_status launch_attn(const ckv_dims* d, const void* q, const ChunkSource& src,
                        const int32_t* sel, int64_t k, const void* k_suffix, const void* v_suffix,
                        void* out, void* ws, size_t ws_bytes, hipStream_t st);
-
-// ---- storage tier, as a layer context drives it ------------------------------
-int64_t store_keys(const ckv_store* s);
-int64_t store_span_bytes(const ckv_store* s);
-bool store_direct(const ckv_store* s);
-// Queues reads of spans keys[u] into dst[u] (host memory) for the I/O threads;
-// *ticket names the request for store_wait.
-ckv_status store_submit(ckv_store* s, const int64_t* keys, int64_t count, char* const* dst,
-                        int64_t* ticket);
-// Blocks until every read of the ticket has landed (CKV_EHIP on a read error).
-ckv_status store_wait(ckv_store* s, int64_t ticket);
-
-// ---- attention-guided cache, as a layer context drives it ------------------
-int64_t cache_keys(const ckv_cache* c);
-int64_t cache_gpu_slots(const ckv_cache* c);
-int64_t cache_gpu_size(const ckv_cache* c);
-int8_t cache_tier(const ckv_cache* c, int64_t key);
-// Starts (or stops) logging the keys that the cascade displaces from the GPU tier.
-void cache_log_gpu_evictions(ckv_cache* c, bool on);
-// Moves the logged keys into out (replacing its contents) and clears the log.
-void cache_take_gpu_evictions(ckv_cache* c, std::vector<int64_t>& out);
-// Moves the logged keys that left memory (or were not kept) into out.
-void cache_take_drops(ckv_cache* c, std::vector<int64_t>& out);
-int64_t cache_cpu_slots(const ckv_cache* c);
 
 }  // namespace ckv

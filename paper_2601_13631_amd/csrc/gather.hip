@@ -8,7 +8,7 @@
 //
 // Grid: x = 16-byte pieces of one chunk span (4 per thread), y = chunk, z = K/V.
 
-#include "ckv_internal.h"
+#include "tiers_internal.h"
 
 namespace ckv {
 namespace {

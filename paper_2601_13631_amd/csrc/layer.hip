@@ -27,7 +27,7 @@
 #include <new>
 #include <vector>
 
-#include "ckv_internal.h"
+#include "tiers_internal.h"
 
 using namespace ckv;
 

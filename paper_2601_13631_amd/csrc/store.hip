@@ -25,7 +25,7 @@
 #include <thread>
 #include <vector>
 
-#include "ckv_internal.h"
+#include "tiers_internal.h"
 
 namespace {
 
