@@ -249,7 +249,9 @@ ckv_status ckv_ctx_set_period(ckv_ctx* ctx, int32_t period);
  * request must pass the same per-layer kv_host contents while it is
  * attached.  Must be called before a request's first layer (or after
  * ckv_ctx_reset), else CKV_ESTATE; the cache's GPU tier must be empty
- * (CKV_ESTATE).  Synchronizes the device.  The context does not own the
+ * (CKV_ESTATE); with a store attached (ckv_ctx_attach_store) it is refused
+ * (CKV_ESTATE): attach the cache first, since the store's chunk pool is sized
+ * for the cache's tiers.  Synchronizes the device.  The context does not own the
  * cache: detach it (or destroy the context) before destroying it or calling
  * ckv_cache_access on it directly.  With a cache attached, a layer inside a
  * Period waits on the host for the copies two layers back before it reuses
@@ -262,19 +264,27 @@ ckv_status ckv_ctx_attach_cache(ckv_ctx* ctx, ckv_cache* cache);
  * host-resident prefix, or detaches it (NULL).  The context then allocates two
  * pinned staging buffers of 2k chunks and takes every chunk a layer moves to
  * HBM from the file instead of from io->kv_host (which may be NULL;
- * kv_host_next is ignored):
- *   - the chunks a layer fetches on demand are read by the I/O threads into
- *     staging (the layer waits for them) and copied to HBM;
+ * kv_host_next is ignored), through a pinned chunk pool that it allocates:
+ *   - the chunks a layer fetches on demand that are not in the pool are read
+ *     by the I/O threads into free pool slots (the layer waits for them), then
+ *     copied to HBM;
  *   - the prediction for layer + 1 (this layer's set less the chunks the next
- *     layer finds in an attached cache's HBM slots) is read asynchronously
- *     while this layer attends and the next one scores, and copied to HBM once
- *     it has landed;
+ *     layer finds in an attached cache's HBM slots) is read asynchronously,
+ *     where not in the pool, while this layer attends, and copied to HBM at
+ *     the start of layer + 1, beside its scoring;
+ *   - with a cache attached, the pool keeps the chunks of the cache's GPU and
+ *     CPU tiers (min(gpu_slots + cpu_slots, n_keys) of them, plus room for two
+ *     layers in flight): a chunk in the CPU tier is copied from host memory
+ *     without a file read, as Sec. 4.5's CPU heap intends; every other pool
+ *     slot is released after its layer and reused one layer later;
  *   - layers past n_keys / m are refused (CKV_EINVAL).
- * Stats bytes_prefetch and bytes_demand then count bytes read from the file.
+ * Stats bytes_prefetch and bytes_demand count bytes moved to HBM over the
+ * host link as before; bytes_storage counts the bytes read from the file.
  * Same call rules as ckv_ctx_attach_cache (start of a request, synchronizes
- * the device); detach or destroy the context before closing the store.  With
- * a store attached, a layer inside a Period waits on the host for the previous
- * layer's attention before it reuses that layer's staging buffer. */
+ * the device); attach a cache before the store; detach or destroy the context
+ * before closing the store.  With a store attached, ckv_ctx_reset synchronizes
+ * the device, and a layer inside a Period waits on the host for the previous
+ * layer's attention before it reuses pool slots. */
 ckv_status ckv_ctx_attach_store(ckv_ctx* ctx, ckv_store* store);
 
 typedef struct ckv_layer_io {
