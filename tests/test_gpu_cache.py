@@ -163,9 +163,10 @@ def test_attach_cache_refusals():
         c.close()
 
 
-@pytest.mark.parametrize("period,with_cache,direct", [(1, False, False), (1, True, True),
-                                                      (2, True, False)])
-def test_layer_store(tmp_path, period, with_cache, direct):
+@pytest.mark.parametrize("period,with_cache,direct,n_prefix", [
+    (1, False, False, 4096), (1, True, True, 4096), (2, True, False, 4096),
+    (1, True, True, 32768)])  # the last: 1,024 chunks of 128 KiB per layer, a 512 MiB file
+def test_layer_store(tmp_path, period, with_cache, direct, n_prefix):
     """Chunks read from a file by the storage tier's I/O threads into the pinned
     chunk pool: every layer's output, set and host-link counts equal those of
     the same layers reading the pinned host store (with or without the cache,
@@ -174,7 +175,7 @@ def test_layer_store(tmp_path, period, with_cache, direct):
     chunks of the cache's two tiers (the oracle cache, fed the same scores,
     says which)."""
     import paper_2601_13631_amd as ckv
-    w = synth.WORKLOADS["c5_qwen32b_128k_host"].scaled(n_prefix=4096, n_suffix=24, n_layers=4)
+    w = synth.WORKLOADS["c5_qwen32b_128k_host"].scaled(n_prefix=n_prefix, n_suffix=24, n_layers=4)
     L, m = w.n_layers, w.n_chunks
     layers = [synth.layer_tensors(w, l) for l in range(L)]
     stores = [_store(w, t) for t in layers]
@@ -207,8 +208,8 @@ def test_layer_store(tmp_path, period, with_cache, direct):
         A_first = None
         for l in range(L):
             first = l - l % period
-            print(f"store period {period} cache {with_cache} direct {direct} request {r} layer {l}",
-                  flush=True)
+            print(f"store n {n_prefix} period {period} cache {with_cache} direct {direct} "
+                  f"request {r} layer {l}", flush=True)
             q = dev(synth.request_queries(w, l, r))
             outs, sels, sts = [], [], []
             A = torch.full((m,), float("nan"), dtype=torch.float64, device=DEV)
