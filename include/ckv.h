@@ -281,8 +281,8 @@ ckv_status ckv_ctx_attach_cache(ckv_ctx* ctx, ckv_cache* cache);
  * Stats bytes_prefetch and bytes_demand count bytes moved to HBM over the
  * host link as before; bytes_storage counts the bytes read from the file.
  * Same call rules as ckv_ctx_attach_cache (start of a request, synchronizes
- * the device); attach a cache before the store; detach or destroy the context
- * before closing the store.  With a store attached, ckv_ctx_reset synchronizes
+ * the device); attach a cache before the store and detach the store before
+ * the cache; detach or destroy the context before closing the store.  With a store attached, ckv_ctx_reset synchronizes
  * the device, and a layer inside a Period waits on the host for the previous
  * layer's attention before it reuses pool slots. */
 ckv_status ckv_ctx_attach_store(ckv_ctx* ctx, ckv_store* store);

@@ -762,6 +762,9 @@ ckv_status ckv_reprefill_layer(ckv_ctx* c, int32_t layer, const ckv_layer_io* io
     s = ckv_cache_access(c->cache, c->keys.data(), c->key_scores.data(), k, nullptr, nullptr);
     if (s != CKV_OK) return s;
     cache_take_gpu_evictions(c->cache, c->evicted);
+    // the keys sent out of memory (used by the storage tier's pool below; the
+    // log is drained every layer either way)
+    cache_take_drops(c->cache, c->dropped);
     // a chunk displaced by an earlier chunk of this layer and placed back at
     // its own turn is still in the GPU tier: it keeps its slot and its bytes
     for (int64_t x : c->evicted)
@@ -795,11 +798,9 @@ ckv_status ckv_reprefill_layer(ckv_ctx* c, int32_t layer, const ckv_layer_io* io
     // other chunks, its unused predicted chunks and the chunks the cascade sent
     // out of memory release their slots
     auto keep = [&](int64_t x) { return cached && cache_tier(c->cache, x) != CKV_TIER_NONE; };
-    if (cached) {
-      cache_take_drops(c->cache, c->dropped);
+    if (cached)
       for (int64_t x : c->dropped)
         if (!keep(x)) pool_release(c, x);
-    }
     for (int64_t u = 0; u < k; ++u)
       if (!keep(key0 + c->sel_host[u])) pool_release(c, key0 + c->sel_host[u]);
     for (int64_t x : c->pref_keys[cur])
