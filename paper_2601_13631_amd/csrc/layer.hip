@@ -173,6 +173,7 @@ ckv_status pool_copy(ckv_ctx* c, int b, int which, const int32_t* src, const int
 ckv_status free_ctx(ckv_ctx* c) {
   if (!c) return CKV_OK;
   drain_store_reads(c);
+  if (c->cache) cache_log_gpu_evictions(c->cache, false);  // the cache outlives the context
   if (c->demand) (void)hipStreamSynchronize(c->demand);
   if (c->prefetch) (void)hipStreamSynchronize(c->prefetch);
   (void)hipFree(c->ws);
