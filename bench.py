@@ -279,6 +279,7 @@ def host_resident(args, w, ckv, synth, np, torch) -> int:
             "note": "host-link-inclusive rate; value is reserved for HBM-resident inputs",
             "pcie_inclusive_prefix_tokens_per_s": round(w.n_prefix / (us * 1e-6), 1),
             "us_per_layer": round(us, 1),
+            "stack_ms_layers_run": round(us * L * 1e-3, 3),
             "host_link_gbs": round(link / elapsed / 1e9, 2),
             "host_link_bytes_per_layer": round(link / n),
             "prefetch_hit_rate_after_first_layer": round(
@@ -503,6 +504,7 @@ def main() -> int:
         "stage_us_per_layer": {s_: round(v * 1e3, 2) for s_, v in per_layer.items()},
         "stage_events_note": "diagnostic pass with events between all stages; each event adds a gap",
         "us_per_step_without_events": round(plain_us, 2),
+        "stack_ms_all_layers": round(ms_per_step * L, 4),
         f"period{PERIOD}_us_per_layer_without_events": round(period_us, 2),
         f"period{PERIOD}_prefix_tokens_per_s": round(w.n_prefix / (period_us * 1e-6), 1),
     }
