@@ -24,9 +24,15 @@ FLAGS = [
 ]
 
 
+# Attention takes softmax maxima over MFMA results, which are never NaN for
+# finite inputs: without NaN semantics the compiler drops the quieting
+# v_max_f32 x, x it otherwise puts before every fmaxf operand.
+EXTRA = {"attn.hip": ["-fno-honor-nans"]}
+
+
 def _compile(src: str, objdir: str) -> str:
     obj = os.path.join(objdir, src.replace(".hip", ".o"))
-    cmd = [HIPCC, *FLAGS, "-c", os.path.join(CSRC, src), "-o", obj]
+    cmd = [HIPCC, *FLAGS, *EXTRA.get(src, []), "-c", os.path.join(CSRC, src), "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"hipcc failed for {src}:\n{r.stderr}")
