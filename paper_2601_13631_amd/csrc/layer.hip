@@ -693,20 +693,18 @@ ckv_status ckv_reprefill_layer(ckv_ctx* c, int32_t layer, const ckv_layer_io* io
   stv.hits = hits;
   stv.misses = (int64_t)miss.size();
   stv.wasted = (int64_t)P.size() - hits;
+  // misses follow the predicted chunks in this layer's buffer (c->pred is
+  // replaced by the next layer's prediction below)
+  const int64_t n_pred = (int64_t)P.size();
 
-  // demand copies into this layer's buffer (after the attention that last used it);
-  // the small index copies go first, so they never queue behind span copies
-  if (c->attn_recorded[cur]) CKV_HIP(hipStreamWaitEvent(c->demand, c->ev_attn[cur], 0));
-  CKV_HIP(hipMemcpyAsync(c->slot_tab_dev[cur], tab, (size_t)k * sizeof(int32_t),
-                         hipMemcpyHostToDevice, c->demand));
-  if (!miss.empty() && stored) {
-    // misses in the pool move from there; the others are read by the I/O
-    // threads into free pool slots first (the layer waits for them)
+  // storage tier: the pool slots the misses move from; those not in the pool
+  // get free slots and are read from the file below
+  c->io_keys.clear();  // this layer's demand reads (none without misses)
+  c->io_dst.clear();
+  if (stored && !miss.empty()) {
     const size_t nm = miss.size();
     c->xsrc.resize(nm);
     c->xdst.resize(nm);
-    c->io_keys.clear();
-    c->io_dst.clear();
     for (size_t i = 0; i < nm; ++i) {
       const int64_t x = key0 + miss[i];
       if (c->pool_of[x] < 0) {
@@ -715,45 +713,64 @@ ckv_status ckv_reprefill_layer(ckv_ctx* c, int32_t layer, const ckv_layer_io* io
         c->io_dst.push_back(c->pool + (int64_t)c->pool_of[x] * c->slot_bytes);
       }
       c->xsrc[i] = c->pool_of[x];
-      c->xdst[i] = (int32_t)(buf0 + P.size() + i);
+      c->xdst[i] = (int32_t)(buf0 + n_pred + i);
     }
-    if (!c->io_keys.empty()) {
-      int64_t ticket = 0;
-      s = store_submit(c->kv_store, c->io_keys.data(), (int64_t)c->io_keys.size(), c->io_dst.data(),
-                       &ticket);
-      if (s == CKV_OK) s = store_wait(c->kv_store, ticket);
-      if (s != CKV_OK) return s;
-      stv.bytes_storage += (int64_t)c->io_keys.size() * c->slot_bytes;
-    }
-    s = pool_copy(c, cur, 1, c->xsrc.data(), c->xdst.data(), (int64_t)nm, c->demand);
-    if (s != CKV_OK) return s;
-  } else if (!miss.empty()) {
-    std::memcpy(c->dem_host[cur], miss.data(), miss.size() * sizeof(int32_t));
-    CKV_HIP(hipMemcpyAsync(c->dem_dev[cur], c->dem_host[cur], miss.size() * sizeof(int32_t),
-                           hipMemcpyHostToDevice, c->demand));
-    s = launch_copy_spans(store, c->dem_dev[cur], (int64_t)miss.size(), (int64_t)P.size(),
-                          c->slots[cur], c->slot_bytes, c->demand);
-    if (s != CKV_OK) return s;
   }
-  CKV_HIP(hipEventRecord(c->ev_dem, c->demand));
+  // the storage tier's demand reads start now; the layer waits for them below
+  int64_t dem_ticket = 0;
+  if (!c->io_keys.empty()) {
+    s = store_submit(c->kv_store, c->io_keys.data(), (int64_t)c->io_keys.size(), c->io_dst.data(),
+                     &dem_ticket);
+    if (s != CKV_OK) return s;
+    stv.bytes_storage += (int64_t)c->io_keys.size() * c->slot_bytes;
+  }
 
-  CKV_HIP(hipStreamWaitEvent(st, c->ev_dem, 0));
-  if (c->pref_pending[cur]) CKV_HIP(hipStreamWaitEvent(st, c->ev_pref[cur], 0));
-  c->pref_pending[cur] = false;
-  if ((s = mark(4)) != CKV_OK) return s;
-  ChunkSource src{c->arena, static_cast<char*>(c->arena) + span_elems * eb, 2 * span_elems,
-                  c->slot_tab_dev[cur], 0};
-  s = launch_attn(d, io->q, src, sel, k, io->k_suffix, io->v_suffix, io->out, ws + c->off_attn,
-                  c->ws_attn, st);
-  if (s != CKV_OK) return s;
-  if ((s = mark(5)) != CKV_OK) return s;
-  if (tev) ++c->t_issued;
+  // demand copies into this layer's buffer (after the attention that last used
+  // it; from the pool once its reads have landed), then the attention.  The
+  // small index copies go first, so they never queue behind span copies.
+  auto demand_and_attention = [&]() -> ckv_status {
+    if (dem_ticket) {
+      ckv_status w = store_wait(c->kv_store, dem_ticket);
+      if (w != CKV_OK) return w;
+    }
+    if (c->attn_recorded[cur]) CKV_HIP(hipStreamWaitEvent(c->demand, c->ev_attn[cur], 0));
+    CKV_HIP(hipMemcpyAsync(c->slot_tab_dev[cur], tab, (size_t)k * sizeof(int32_t),
+                           hipMemcpyHostToDevice, c->demand));
+    ckv_status r = CKV_OK;
+    if (!miss.empty() && stored) {
+      r = pool_copy(c, cur, 1, c->xsrc.data(), c->xdst.data(), (int64_t)miss.size(), c->demand);
+    } else if (!miss.empty()) {
+      std::memcpy(c->dem_host[cur], miss.data(), miss.size() * sizeof(int32_t));
+      CKV_HIP(hipMemcpyAsync(c->dem_dev[cur], c->dem_host[cur], miss.size() * sizeof(int32_t),
+                             hipMemcpyHostToDevice, c->demand));
+      r = launch_copy_spans(store, c->dem_dev[cur], (int64_t)miss.size(), n_pred, c->slots[cur],
+                            c->slot_bytes, c->demand);
+    }
+    if (r != CKV_OK) return r;
+    CKV_HIP(hipEventRecord(c->ev_dem, c->demand));
+    CKV_HIP(hipStreamWaitEvent(st, c->ev_dem, 0));
+    if (c->pref_pending[cur]) CKV_HIP(hipStreamWaitEvent(st, c->ev_pref[cur], 0));
+    c->pref_pending[cur] = false;
+    if ((r = mark(4)) != CKV_OK) return r;
+    ChunkSource src{c->arena, static_cast<char*>(c->arena) + span_elems * eb, 2 * span_elems,
+                    c->slot_tab_dev[cur], 0};
+    r = launch_attn(d, io->q, src, sel, k, io->k_suffix, io->v_suffix, io->out, ws + c->off_attn,
+                    c->ws_attn, st);
+    if (r != CKV_OK) return r;
+    if ((r = mark(5)) != CKV_OK) return r;
+    if (tev) ++c->t_issued;
+    return CKV_OK;
+  };
+  // from pinned host memory the attention goes out first and the host work
+  // below overlaps it; from the store the host works while the reads land
+  if (!stored && (s = demand_and_attention()) != CKV_OK) return s;
 
+  // Sec. 4.5: the chunks this layer uses add their scores (I += A, F += 1) and
+  // are re-placed.  Chunks leaving the GPU tier free their HBM slots, and
+  // chunks entering it are listed for copies from this layer's buffer, which
+  // go on the stream after the attention that reads both.
+  int64_t nf = 0;
   if (cached) {
-    // Sec. 4.5: the chunks this layer used add their scores (I += A, F += 1)
-    // and are re-placed; chunks leaving the GPU tier free their HBM slots and
-    // chunks entering it are copied there from this layer's buffer, after the
-    // attention that read both
     c->keys.resize((size_t)k);
     c->key_scores.resize((size_t)k);
     for (int64_t u = 0; u < k; ++u) {
@@ -773,7 +790,6 @@ ckv_status ckv_reprefill_layer(ckv_ctx* c, int32_t layer, const ckv_layer_io* io
         c->free_slots.push_back(c->slot_of[x]);
         c->slot_of[x] = -1;
       }
-    int64_t nf = 0;
     int32_t* fill = c->fill_host[cur];
     for (int64_t u = 0; u < k; ++u) {
       const int64_t x = c->keys[u];
@@ -785,19 +801,12 @@ ckv_status ckv_reprefill_layer(ckv_ctx* c, int32_t layer, const ckv_layer_io* io
       fill[k + nf] = (int32_t)(cache0 + c->slot_of[x]);
       ++nf;
     }
-    if (nf > 0) {
-      CKV_HIP(hipMemcpyAsync(c->fill_dev[cur], fill, (size_t)(2 * k) * sizeof(int32_t),
-                             hipMemcpyHostToDevice, st));
-      s = launch_copy_slots(c->arena, c->fill_dev[cur], c->arena, c->fill_dev[cur] + k, nf,
-                            c->slot_bytes, st);
-      if (s != CKV_OK) return s;
-      stv.bytes_cache_fill = nf * c->slot_bytes;
-    }
   }
   if (stored) {
     // the pool keeps the chunks the cache holds (GPU or CPU tier); this layer's
     // other chunks, its unused predicted chunks and the chunks the cascade sent
-    // out of memory release their slots
+    // out of memory release their slots (reused only after the next layer's
+    // host synchronisation, when this layer's copies out of them are done)
     auto keep = [&](int64_t x) { return cached && cache_tier(c->cache, x) != CKV_TIER_NONE; };
     if (cached)
       for (int64_t x : c->dropped)
@@ -808,27 +817,29 @@ ckv_status ckv_reprefill_layer(ckv_ctx* c, int32_t layer, const ckv_layer_io* io
       if (!keep(x)) pool_release(c, x);
     c->pref_keys[cur].clear();
   }
-  // after the cache fills too: they read this layer's buffer
-  CKV_HIP(hipEventRecord(c->ev_attn[cur], st));
-  c->attn_recorded[cur] = true;
 
-  // prefetch the next layer's copy of this layer's selection (P_{l+1} = S_l),
-  // except chunks the next layer finds in the cache's HBM slots
+  // the next layer's prediction (P_{l+1} = S_l) less the chunks it will find in
+  // the cache's HBM slots
   c->pred.clear();
-  if (stored ? layer + 1 < c->store_layers : io->kv_host_next != nullptr) {
-    const int64_t nkey0 = (int64_t)(layer + 1) * c->m;
+  const bool has_next = stored ? layer + 1 < c->store_layers : io->kv_host_next != nullptr;
+  const int64_t nkey0 = (int64_t)(layer + 1) * c->m;
+  if (has_next) {
     const bool next_cached = cached && layer + 1 < c->cache_layers;
     for (int64_t u = 0; u < k; ++u) {
       const int32_t j = c->sel_host[u];
       if (next_cached && c->slot_of[nkey0 + j] >= 0) continue;
       c->pred.push_back(j);
     }
-    const int64_t np = (int64_t)c->pred.size();
-    for (int64_t u = 0; u < np; ++u)
-      stv.bytes_prefetch += 2 * chunk_len(d, c->pred[u]) * d->n_kv_heads * d->head_dim * eb;
-    if (stored) {
-      // predicted chunks not in the pool are read into free pool slots by the
-      // I/O threads while this layer attends and the next one scores
+    for (int32_t j : c->pred)
+      stv.bytes_prefetch += 2 * chunk_len(d, j) * d->n_kv_heads * d->head_dim * eb;
+  }
+  const int64_t np = (int64_t)c->pred.size();
+
+  if (stored) {
+    // the next layer's prediction joins the I/O threads' queue behind this
+    // layer's demand reads and runs on while this layer attends and the next
+    // one scores
+    if (has_next) {
       c->pref_keys[nxt].clear();
       c->io_keys.clear();
       c->io_dst.clear();
@@ -846,10 +857,23 @@ ckv_status ckv_reprefill_layer(ckv_ctx* c, int32_t layer, const ckv_layer_io* io
         if (s != CKV_OK) return s;
         stv.bytes_storage += (int64_t)c->io_keys.size() * c->slot_bytes;
       }
-      c->next_layer = layer + 1;
-      if (stats) *stats = stv;
-      return CKV_OK;
     }
+    if ((s = demand_and_attention()) != CKV_OK) return s;
+  }
+
+  if (nf > 0) {  // chunks entering the GPU tier, after the attention that read their slots
+    CKV_HIP(hipMemcpyAsync(c->fill_dev[cur], c->fill_host[cur], (size_t)(2 * k) * sizeof(int32_t),
+                           hipMemcpyHostToDevice, st));
+    s = launch_copy_slots(c->arena, c->fill_dev[cur], c->arena, c->fill_dev[cur] + k, nf,
+                          c->slot_bytes, st);
+    if (s != CKV_OK) return s;
+    stv.bytes_cache_fill = nf * c->slot_bytes;
+  }
+  // after the cache fills too: they read this layer's buffer
+  CKV_HIP(hipEventRecord(c->ev_attn[cur], st));
+  c->attn_recorded[cur] = true;
+
+  if (has_next && !stored) {  // the next layer's copy, over the host link on the side stream
     if (c->attn_recorded[nxt]) CKV_HIP(hipStreamWaitEvent(c->prefetch, c->ev_attn[nxt], 0));
     // after this layer's demand copies: those are on the critical path and get
     // the host link to themselves

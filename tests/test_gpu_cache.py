@@ -99,15 +99,15 @@ def test_layer_cache_requests(period):
             if l + 1 < L:
                 nxt = [j for j in S if after[(l + 1) * m + j] != oracle.TIER_GPU]
                 assert st["bytes_prefetch"] == int(sum(lens[j] for j in nxt)) * per_tok
+            # every layer's output against the oracle's attention over the same set
+            t = dict(layers[l], q=synth.request_queries(w, l, r))
+            out_ref = oracle.sparse_attn(s, t["q"], t["k_prefix"], t["v_prefix"],
+                                         sel.astype(np.int32), t["k_suffix"], t["v_suffix"])
+            assert float(np.abs(to_f64(outs[0]) - out_ref).max()) <= 2e-2
             total_cache_hits += st["cache_hits"]
             print(f"  cache hits {st['cache_hits']} prefetch hits {st['hits']} "
                   f"misses {st['misses']} fills {fills}", flush=True)
             prev = sel if l + 1 < L else np.zeros(0, np.int64)
-        # the last layer against the oracle's attention over the same set
-        t = dict(layers[L - 1], q=synth.request_queries(w, L - 1, r))
-        out_ref = oracle.sparse_attn(s, t["q"], t["k_prefix"], t["v_prefix"], sel.astype(np.int32),
-                                     t["k_suffix"], t["v_suffix"])
-        assert float(np.abs(to_f64(outs[0]) - out_ref).max()) <= 2e-2
     assert total_cache_hits > 0  # later requests do find chunks in HBM
     I1, F1, T1 = cache.state()
     I2, F2, T2 = ref.state()
@@ -226,6 +226,11 @@ def test_layer_store(tmp_path, period, with_cache, direct, n_prefix):
             torch.cuda.synchronize()
             assert torch.equal(sels[0], sels[1])
             assert torch.equal(outs[0].view(torch.int16), outs[1].view(torch.int16))
+            if n_prefix <= 4096:  # and against the oracle over the same set
+                t = dict(layers[l], q=synth.request_queries(w, l, r))
+                out_ref = oracle.sparse_attn(oshape(w), t["q"], t["k_prefix"], t["v_prefix"],
+                                             sels[1].cpu().numpy(), t["k_suffix"], t["v_suffix"])
+                assert float(np.abs(to_f64(outs[1]) - out_ref).max()) <= 2e-2
             got = dict(sts[1])
             storage = got.pop("bytes_storage")
             assert sts[0].pop("bytes_storage") == 0
