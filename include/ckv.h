@@ -165,7 +165,8 @@ ckv_status ckv_gather_chunks(const ckv_dims* dims, const void* k_src, const void
  *   k_suffix, v_suffix  device, [S][Hkv][d]
  *   out           device, [S][Hq][d] (written)
  *   ws            device workspace of ckv_attn_workspace_bytes(dims, k) bytes
- * 0 <= k <= m.
+ * 0 <= k <= m.  Inputs must be finite: the bf16 kernel is built without NaN
+ * semantics, so a NaN in Q, K or V gives unspecified output.
  * ------------------------------------------------------------------------- */
 size_t ckv_attn_workspace_bytes(const ckv_dims* dims, int64_t k);
 ckv_status ckv_sparse_prefill_attn(const ckv_dims* dims, const void* q, const void* k_sel,
