@@ -383,7 +383,7 @@ def main() -> int:
                     help="requests on the shared prefix in the read-accounting and cache diagnostic")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py runs on exactly one GPU: this build has no multi-GPU path "
+        print("bench.py runs on exactly one GPU: the library has no multi-GPU path "
               "(the method's per-layer path is measured on one MI355X)", file=sys.stderr)
         return 2
 
