@@ -378,7 +378,8 @@ ckv_status ckv_io_account(int64_t n, int32_t c, const int32_t* sel_idx, int64_t 
 
 /* ---------------------------------------------------------------------------
  * Storage tier -- the prefix KV kept on SSD and loaded by I/O threads
- * (Sec. 4.3.2 steps, Sec. 4.5's "dispatch I/O threads to load them from SSD").
+ * (Sec. 4.3.2's loading steps; Sec. 4.5, where chunks missing from both
+ * caches are loaded from SSD by I/O threads).
  * A store is one file of n_keys spans of span_bytes bytes; span `key` starts
  * at byte key * span_bytes.  For a layer context, key = layer * m + chunk and
  * a span is one chunk's K rows then V rows, c rows each (the host-resident
