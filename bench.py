@@ -295,6 +295,41 @@ def host_resident(args, w, ckv, synth, np, torch) -> int:
     return 0
 
 
+def io_sweep(args, ckv, synth, np, torch, dev) -> dict:
+    """Untimed: read amplification of a 64-token block store against the chunk
+    size, on the kept sets the GPU selects for the 64K-token workload at c = 8,
+    16, 32 and 64 (Sec. 3's motivation; the block size of the comparison
+    systems), over the first --io-layers layers of each."""
+    res = {}
+    for name in ("c4_qwen14b_64k_c8", "c4_qwen14b_64k_c16", "c4_qwen14b_64k_c32", "c4_qwen14b_64k_c64"):
+        w = synth.WORKLOADS[name]
+        dims = ckv.make_dims(w.n_prefix, w.n_suffix, w.n_q_heads, w.n_kv_heads, w.head_dim,
+                             w.chunk_size, ckv.DTYPE_BF16)
+        ctx = ckv.Context(dims, w.keep_ratio, 0)
+        hs = synth.heavy_sets(w)
+        tot = {"tokens_selected": 0, "runs": 0, "blocks": 0, "tokens_block": 0}
+        for l in range(args.io_layers):
+            t = {k_: torch.from_numpy(v).view(torch.bfloat16).to(dev)
+                 for k_, v in synth.layer_tensors(w, l, hs[l]).items()}
+            sel = torch.empty(ctx.k, dtype=torch.int32, device=dev)
+            out = torch.empty_like(t["q"])
+            ctx.reprefill_layer(l, t["q"], t["k_suffix"], t["v_suffix"], t["k_prefix"], out,
+                                k_prefix=t["k_prefix"], v_prefix=t["v_prefix"], sel_idx=sel)
+            torch.cuda.synchronize()
+            for f, v in ckv.io_account(w.n_prefix, w.chunk_size, sel.cpu().numpy(), 64).items():
+                tot[f] += v
+            del t
+        ctx.close()
+        res[f"c{w.chunk_size}"] = {
+            "kept_chunks": ctx.k, "tokens_contiguous": tot["tokens_selected"],
+            "tokens_block_store": tot["tokens_block"],
+            "block_store_read_amplification": round(tot["tokens_block"] / tot["tokens_selected"], 3),
+            "contiguous_runs_per_layer": round(tot["runs"] / args.io_layers, 1)}
+        log(f"io sweep c={w.chunk_size}: block store reads "
+            f"{res[f'c{w.chunk_size}']['block_store_read_amplification']}x the kept tokens")
+    return res
+
+
 def tiers_detail(args, w, ckv, synth, np, torch, layers, dims, dev) -> dict:
     """Untimed: the layers' kept sets for several requests on the shared prefix
     (request r's queries from synth.request_queries), their reads against a
@@ -379,6 +414,10 @@ def main() -> int:
                     help="host-resident workloads: also run the layers from a file written in this "
                          "directory, read by the storage tier (O_DIRECT)")
     ap.add_argument("--io-threads", type=int, default=16, help="storage tier I/O threads")
+    ap.add_argument("--io-sweep", action="store_true",
+                    help="also report block-store read amplification on the 64K-token workload "
+                         "at chunk sizes 8, 16, 32 and 64")
+    ap.add_argument("--io-layers", type=int, default=4, help="layers per chunk size in --io-sweep")
     ap.add_argument("--requests", type=int, default=4,
                     help="requests on the shared prefix in the read-accounting and cache diagnostic")
     args = ap.parse_args()
@@ -510,6 +549,8 @@ def main() -> int:
     }
     if w.dtype == "bf16" and args.requests > 0:
         others.update(tiers_detail(args, w, ckv, synth, np, torch, layers, dims, dev))
+    if args.io_sweep:
+        others["io_vs_64_token_blocks_by_chunk_size"] = io_sweep(args, ckv, synth, np, torch, dev)
     if args.materialize and per_layer["move"] > 0:
         others["gather_gbs"] = round(2 * kept_bytes / (per_layer["move"] * 1e-3) / 1e9, 1)
 
