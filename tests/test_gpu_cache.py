@@ -271,3 +271,50 @@ def test_layer_store(tmp_path, period, with_cache, direct, n_prefix):
     for cache in caches:
         cache.close()
     store.close()
+
+
+def test_attach_store_refusals(tmp_path):
+    import paper_2601_13631_amd as ckv
+    w = synth.WORKLOADS["c5_qwen32b_128k_host"].scaled(n_prefix=4096, n_suffix=24, n_layers=1)
+    m = w.n_chunks
+    span = 2 * w.chunk_size * w.n_kv_heads * w.head_dim * w.elem_bytes
+    t = synth.layer_tensors(w, 0)
+    path = str(tmp_path / "kv.bin")
+    cm = synth.chunk_major(t["k_prefix"], t["v_prefix"], w.chunk_size)
+    with open(path, "wb") as f:
+        cm.tofile(f)
+        cm.tofile(f)  # two layers' worth of spans
+    tt = {kk: dev(v) for kk, v in t.items()}
+    out = torch.empty_like(tt["q"])
+    hbm = ckv.Context(dims_of(w), w.keep_ratio, 0)
+    good = ckv.Store(path, 2 * m, span, 2)
+    with pytest.raises(ckv.CkvError) as e:  # needs a host-resident prefix
+        hbm.attach_store(good)
+    assert e.value.status == ckv.EINVAL
+    hbm.close()
+    ctx = ckv.Context(dims_of(w), w.keep_ratio, ckv.CTX_HOST_PREFIX)
+    for bad in (ckv.Store(path, 2 * m, span // 2, 2),      # spans are not chunks
+                ckv.Store(path, 2 * m - 1, span, 2)):     # not a whole number of layers
+        with pytest.raises(ckv.CkvError) as e:
+            ctx.attach_store(bad)
+        assert e.value.status == ckv.EINVAL
+        bad.close()
+    cache = ckv.Cache(2 * m, 8, 8)
+    ctx.attach_store(good)
+    with pytest.raises(ckv.CkvError) as e:  # the cache goes first
+        ctx.attach_cache(cache)
+    assert e.value.status == ckv.ESTATE
+    ctx.reprefill_layer(0, tt["q"], tt["k_suffix"], tt["v_suffix"], tt["k_prefix"], out)
+    ctx.reprefill_layer(1, tt["q"], tt["k_suffix"], tt["v_suffix"], tt["k_prefix"], out)
+    with pytest.raises(ckv.CkvError) as e:  # mid-request
+        ctx.attach_store(None)
+    assert e.value.status == ckv.ESTATE
+    with pytest.raises(ckv.CkvError) as e:  # the store holds two layers
+        ctx.reprefill_layer(2, tt["q"], tt["k_suffix"], tt["v_suffix"], tt["k_prefix"], out)
+    assert e.value.status == ckv.EINVAL
+    torch.cuda.synchronize()
+    ctx.reset()
+    ctx.attach_store(None)
+    ctx.close()
+    cache.close()
+    good.close()
