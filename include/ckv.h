@@ -288,6 +288,18 @@ ckv_status ckv_ctx_attach_cache(ckv_ctx* ctx, ckv_cache* cache);
  * layer's attention before it reuses pool slots. */
 ckv_status ckv_ctx_attach_store(ckv_ctx* ctx, ckv_store* store);
 
+/* Intra-period prefetch depth -- Sec. 4.3.2 (with Def. 4.2's Periods) and the
+ * SubPeriod size of the evaluation setup.  With a store attached and a Period
+ * of p > 1 layers, a layer queues the storage reads of every later layer of
+ * its Period up to subperiod - 1 layers ahead as soon as its set is known
+ * (the set is the Period's, so these predictions are exact); a layer's
+ * computation still waits only for its own chunks.  subperiod = 1 (the
+ * default) reads one layer ahead.  The pinned-host-memory path always copies
+ * one layer ahead.  1 <= subperiod <= 16 (CKV_EINVAL); must be set before the
+ * store is attached (CKV_ESTATE), since it sizes the chunk pool (subperiod * k
+ * more slots). */
+ckv_status ckv_ctx_set_subperiod(ckv_ctx* ctx, int32_t subperiod);
+
 typedef struct ckv_layer_io {
   const void* q;         /* device [S][Hq][d]                                        */
   const void* k_suffix;  /* device [S][Hkv][d]                                       */

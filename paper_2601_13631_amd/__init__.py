@@ -98,6 +98,7 @@ _SIG = {
     "ckv_ctx_set_period": ([_P, ctypes.c_int32], ctypes.c_int32),
     "ckv_ctx_attach_cache": ([_P, _P], ctypes.c_int32),
     "ckv_ctx_attach_store": ([_P, _P], ctypes.c_int32),
+    "ckv_ctx_set_subperiod": ([_P, ctypes.c_int32], ctypes.c_int32),
     "ckv_store_open": ([ctypes.c_char_p, ctypes.c_int64, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32,
                         ctypes.POINTER(_P)], ctypes.c_int32),
     "ckv_store_close": ([_P], ctypes.c_int32),
@@ -255,6 +256,10 @@ class Context:
         self._cache = cache  # the context must not outlive the cache it uses
         _check(_lib.ckv_ctx_attach_cache(self._h, cache._h if cache is not None else None),
                "ckv_ctx_attach_cache")
+
+    def set_subperiod(self, subperiod: int) -> None:
+        """Storage reads up to subperiod - 1 layers ahead inside a Period."""
+        _check(_lib.ckv_ctx_set_subperiod(self._h, subperiod), "ckv_ctx_set_subperiod")
 
     def attach_store(self, store) -> None:
         """Takes the chunks of this host-resident context from ``store`` (a

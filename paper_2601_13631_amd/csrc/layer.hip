@@ -98,8 +98,19 @@ struct ckv_ctx {
   // demand copies: pinned staging and device copies, 2 * slots_per_buf entries
   int32_t* xfer_host[2][2] = {{nullptr, nullptr}, {nullptr, nullptr}};
   int32_t* xfer_dev[2][2] = {{nullptr, nullptr}, {nullptr, nullptr}};
-  int64_t pref_ticket[2] = {0, 0};      // store reads of buffer b's prediction in flight
-  std::vector<int64_t> pref_keys[2];    // keys of buffer b's predicted chunks, in P order
+  // predictions read ahead from the store: entry layer % kAhead holds the
+  // chunks (in P order) and keys read for that layer and the reads' ticket.
+  // One layer ahead, or with a SubPeriod of sp layers inside a Period, up to
+  // sp - 1 layers ahead (Sec. 4.3.2's intra-period prefetch).
+  static constexpr int kAhead = 16;
+  struct Ahead {
+    int32_t layer = -1;
+    int64_t ticket = 0;
+    std::vector<int32_t> chunks;
+    std::vector<int64_t> keys;
+  };
+  Ahead ahead[kAhead];
+  int32_t subperiod = 1;
   std::vector<int64_t> io_keys, dropped;
   std::vector<char*> io_dst;
   std::vector<int32_t> xsrc, xdst;
@@ -114,9 +125,9 @@ namespace {
 
 // Waits for store reads into the pool that are still in flight.
 void drain_store_reads(ckv_ctx* c) {
-  for (int b = 0; b < 2; ++b) {
-    if (c->kv_store && c->pref_ticket[b]) (void)store_wait(c->kv_store, c->pref_ticket[b]);
-    c->pref_ticket[b] = 0;
+  for (auto& a : c->ahead) {
+    if (c->kv_store && a.ticket) (void)store_wait(c->kv_store, a.ticket);
+    a.ticket = 0;
   }
 }
 
@@ -135,8 +146,11 @@ void free_pool(ckv_ctx* c) {
   c->pool_of.clear();
   c->pool_free.clear();
   c->pool_quarantine.clear();
-  c->pref_keys[0].clear();
-  c->pref_keys[1].clear();
+  for (auto& a : c->ahead) {
+    a.layer = -1;
+    a.chunks.clear();
+    a.keys.clear();
+  }
 }
 
 // A free pool slot for the bytes of `key` (-1 if none is left).
@@ -393,6 +407,17 @@ ckv_status ckv_ctx_attach_cache(ckv_ctx* ctx, ckv_cache* cache) {
   return CKV_OK;
 }
 
+ckv_status ckv_ctx_set_subperiod(ckv_ctx* ctx, int32_t subperiod) {
+  clear_error();
+  if (!ctx) CKV_FAIL(CKV_EINVAL, "ctx is NULL");
+  if (subperiod < 1 || subperiod > ckv_ctx::kAhead)
+    CKV_FAIL(CKV_EINVAL, "subperiod must be in [1, %d] (got %d)", ckv_ctx::kAhead, subperiod);
+  if (ctx->kv_store)
+    CKV_FAIL(CKV_ESTATE, "set the SubPeriod before attaching the store (it sizes the chunk pool)");
+  ctx->subperiod = subperiod;
+  return CKV_OK;
+}
+
 ckv_status ckv_ctx_attach_store(ckv_ctx* ctx, ckv_store* store) {
   clear_error();
   if (!ctx) CKV_FAIL(CKV_EINVAL, "ctx is NULL");
@@ -420,7 +445,7 @@ ckv_status ckv_ctx_attach_store(ckv_ctx* ctx, ckv_store* store) {
   // flight and of the layer whose slots wait for release
   const int64_t keys = store_keys(store), k = ctx->k;
   const int64_t kept = ctx->cache ? std::min(keys, cache_gpu_slots(ctx->cache) + cache_cpu_slots(ctx->cache)) : 0;
-  const int64_t n = std::min(keys, kept + 6 * k) + 16;
+  const int64_t n = std::min(keys, kept + (6 + ctx->subperiod) * k) + 16;
   const int64_t spb = ctx->slots_per_buf;
   hipError_t e = hipHostMalloc((void**)&ctx->pool, (size_t)(n * ctx->slot_bytes), hipHostMallocDefault);
   for (int b = 0; b < 2 && e == hipSuccess; ++b)
@@ -456,10 +481,12 @@ ckv_status ckv_ctx_reset(ckv_ctx* ctx) {
     // predictions read for a layer that will not run: release their slots
     // (nothing reads them any more once the device is idle)
     CKV_HIP(hipDeviceSynchronize());
-    for (int b = 0; b < 2; ++b) {
-      for (int64_t x : ctx->pref_keys[b])
+    for (auto& a : ctx->ahead) {
+      for (int64_t x : a.keys)
         if (!ctx->cache || cache_tier(ctx->cache, x) == CKV_TIER_NONE) pool_release(ctx, x);
-      ctx->pref_keys[b].clear();
+      a.layer = -1;
+      a.chunks.clear();
+      a.keys.clear();
     }
   }
   ctx->pred.clear();
@@ -603,16 +630,25 @@ ckv_status ckv_reprefill_layer(ckv_ctx* c, int32_t layer, const ckv_layer_io* io
   const int64_t key0 = (int64_t)layer * c->m;
   const int64_t spb = c->slots_per_buf;
   const int64_t buf0 = cur * spb, cache0 = 2 * spb;
-  if (stored && c->pref_ticket[cur]) {  // this layer's prediction, read during the previous one
-    s = store_wait(c->kv_store, c->pref_ticket[cur]);
-    c->pref_ticket[cur] = 0;
-    if (s != CKV_OK) return s;
+  ckv_ctx::Ahead& mine = c->ahead[layer % ckv_ctx::kAhead];
+  if (stored) {  // this layer's prediction: read (or queued) during earlier layers
+    if (mine.layer != layer) {
+      mine.layer = -1;
+      mine.chunks.clear();
+      mine.keys.clear();
+    }
+    if (mine.ticket) {
+      s = store_wait(c->kv_store, mine.ticket);
+      mine.ticket = 0;
+      if (s != CKV_OK) return s;
+    }
+    c->pred = mine.chunks;
   }
-  if (stored && !c->pref_keys[cur].empty()) {
+  if (stored && !mine.keys.empty()) {
     // the predicted chunks (read from the store, or already in the pool) move
     // to this layer's HBM slots 0..|P|-1 on the prefetch stream, beside this
     // layer's scoring; this buffer's copy lists were last read two layers ago
-    const std::vector<int64_t>& pk = c->pref_keys[cur];
+    const std::vector<int64_t>& pk = mine.keys;
     const int64_t np = (int64_t)pk.size();
     c->xsrc.resize((size_t)np);
     c->xdst.resize((size_t)np);
@@ -813,9 +849,11 @@ ckv_status ckv_reprefill_layer(ckv_ctx* c, int32_t layer, const ckv_layer_io* io
         if (!keep(x)) pool_release(c, x);
     for (int64_t u = 0; u < k; ++u)
       if (!keep(key0 + c->sel_host[u])) pool_release(c, key0 + c->sel_host[u]);
-    for (int64_t x : c->pref_keys[cur])
+    for (int64_t x : mine.keys)
       if (!keep(x)) pool_release(c, x);
-    c->pref_keys[cur].clear();
+    mine.layer = -1;
+    mine.chunks.clear();
+    mine.keys.clear();
   }
 
   // the next layer's prediction (P_{l+1} = S_l) less the chunks it will find in
@@ -830,8 +868,9 @@ ckv_status ckv_reprefill_layer(ckv_ctx* c, int32_t layer, const ckv_layer_io* io
       if (next_cached && c->slot_of[nkey0 + j] >= 0) continue;
       c->pred.push_back(j);
     }
-    for (int32_t j : c->pred)
-      stv.bytes_prefetch += 2 * chunk_len(d, j) * d->n_kv_heads * d->head_dim * eb;
+    if (!stored)  // the storage tier counts what it queues, below
+      for (int32_t j : c->pred)
+        stv.bytes_prefetch += 2 * chunk_len(d, j) * d->n_kv_heads * d->head_dim * eb;
   }
   const int64_t np = (int64_t)c->pred.size();
 
@@ -840,22 +879,44 @@ ckv_status ckv_reprefill_layer(ckv_ctx* c, int32_t layer, const ckv_layer_io* io
     // layer's demand reads and runs on while this layer attends and the next
     // one scores
     if (has_next) {
-      c->pref_keys[nxt].clear();
-      c->io_keys.clear();
-      c->io_dst.clear();
-      for (int64_t u = 0; u < np; ++u) {
-        const int64_t x = nkey0 + c->pred[u];
-        c->pref_keys[nxt].push_back(x);
-        if (c->pool_of[x] >= 0) continue;
-        if (pool_take(c, x) < 0) CKV_FAIL(CKV_ESTATE, "chunk pool exhausted (internal)");
-        c->io_keys.push_back(x);
-        c->io_dst.push_back(c->pool + (int64_t)c->pool_of[x] * c->slot_bytes);
+      // layers last_ahead..: inside a Period with a SubPeriod of sp layers,
+      // every layer up to sp - 1 ahead (their set is this one); otherwise the
+      // next layer only (speculative across a Period boundary)
+      int64_t last_ahead = layer + 1;
+      if (c->period > 1 && c->subperiod > 1) {
+        const int64_t period_end = first + c->period - 1;
+        last_ahead = std::max<int64_t>(last_ahead, std::min<int64_t>(layer + c->subperiod - 1, period_end));
       }
-      if (!c->io_keys.empty()) {
-        s = store_submit(c->kv_store, c->io_keys.data(), (int64_t)c->io_keys.size(), c->io_dst.data(),
-                         &c->pref_ticket[nxt]);
-        if (s != CKV_OK) return s;
-        stv.bytes_storage += (int64_t)c->io_keys.size() * c->slot_bytes;
+      last_ahead = std::min<int64_t>(last_ahead, c->store_layers - 1);
+      for (int64_t t = layer + 1; t <= last_ahead; ++t) {
+        ckv_ctx::Ahead& a = c->ahead[t % ckv_ctx::kAhead];
+        if (a.layer == t) continue;  // queued by an earlier layer of the Period
+        if (a.layer >= 0) CKV_FAIL(CKV_ESTATE, "prediction ring overrun (internal)");
+        a.layer = (int32_t)t;
+        a.chunks.clear();
+        a.keys.clear();
+        c->io_keys.clear();
+        c->io_dst.clear();
+        const int64_t tkey0 = t * c->m;
+        const bool t_cached = cached && t < c->cache_layers;
+        for (int64_t u = 0; u < k; ++u) {
+          const int32_t j = c->sel_host[u];
+          const int64_t x = tkey0 + j;
+          if (t_cached && c->slot_of[x] >= 0) continue;
+          a.chunks.push_back(j);
+          a.keys.push_back(x);
+          stv.bytes_prefetch += 2 * chunk_len(d, j) * d->n_kv_heads * d->head_dim * eb;
+          if (c->pool_of[x] >= 0) continue;
+          if (pool_take(c, x) < 0) CKV_FAIL(CKV_ESTATE, "chunk pool exhausted (internal)");
+          c->io_keys.push_back(x);
+          c->io_dst.push_back(c->pool + (int64_t)c->pool_of[x] * c->slot_bytes);
+        }
+        if (!c->io_keys.empty()) {
+          s = store_submit(c->kv_store, c->io_keys.data(), (int64_t)c->io_keys.size(), c->io_dst.data(),
+                           &a.ticket);
+          if (s != CKV_OK) return s;
+          stv.bytes_storage += (int64_t)c->io_keys.size() * c->slot_bytes;
+        }
       }
     }
     if ((s = demand_and_attention()) != CKV_OK) return s;

@@ -318,3 +318,79 @@ def test_attach_store_refusals(tmp_path):
     ctx.close()
     cache.close()
     good.close()
+
+
+@pytest.mark.parametrize("with_cache", [False, True])
+def test_layer_store_subperiod(tmp_path, with_cache):
+    """Periods of 4 layers with a SubPeriod of 3: a Period's layers queue the
+    storage reads of the next two layers of the Period.  Outputs and sets equal
+    the pinned-store path's bit for bit; without a cache the hit/miss counts
+    and, over a request, the prefetched and file-read bytes equal those of one
+    layer ahead."""
+    import paper_2601_13631_amd as ckv
+    w = synth.WORKLOADS["c5_qwen32b_128k_host"].scaled(n_prefix=4096, n_suffix=24, n_layers=8)
+    L, m = w.n_layers, w.n_chunks
+    layers = [synth.layer_tensors(w, l) for l in range(L)]
+    stores = [_store(w, t) for t in layers]
+    path = str(tmp_path / "kv.bin")
+    with open(path, "wb") as f:
+        for t in layers:
+            synth.chunk_major(t["k_prefix"], t["v_prefix"], w.chunk_size).tofile(f)
+    span = 2 * w.chunk_size * w.n_kv_heads * w.head_dim * w.elem_bytes
+    store = ckv.Store(path, L * m, span, 4)
+    base = [{kk: dev(v) for kk, v in t.items()} for t in layers]
+    ctxs = [ckv.Context(dims_of(w), w.keep_ratio, ckv.CTX_HOST_PREFIX) for _ in range(3)]
+    k = ctxs[0].k
+    caches = []
+    for i, c in enumerate(ctxs):
+        c.set_period(4)
+        if with_cache:
+            caches.append(ckv.Cache(L * m, (L * k) // 2, L * k))
+            c.attach_cache(caches[-1])
+        if i > 0:
+            c.set_subperiod(3 if i == 2 else 1)
+            c.attach_store(store)
+    with pytest.raises(ckv.CkvError) as e:  # the SubPeriod sizes the pool: set it first
+        ctxs[2].set_subperiod(2)
+    assert e.value.status == ckv.ESTATE
+    for r in range(2):
+        for c in ctxs:
+            c.reset()
+        tot = [dict(bytes_prefetch=0, bytes_storage=0) for _ in ctxs]
+        for l in range(L):
+            print(f"subperiod cache {with_cache} request {r} layer {l}", flush=True)
+            q = dev(synth.request_queries(w, l, r))
+            outs, sels, sts = [], [], []
+            for i, c in enumerate(ctxs):
+                sel = torch.empty(k, dtype=torch.int32, device=DEV)
+                out = torch.empty_like(q)
+                kv = dict(kv_host=stores[l], kv_host_next=stores[l + 1] if l + 1 < L else None) \
+                    if i == 0 else {}
+                sts.append(c.reprefill_layer(l, q, base[l]["k_suffix"], base[l]["v_suffix"],
+                                             base[l]["k_prefix"], out, sel_idx=sel, **kv))
+                outs.append(out)
+                sels.append(sel)
+            torch.cuda.synchronize()
+            for i in (1, 2):
+                assert torch.equal(sels[0], sels[i])
+                assert torch.equal(outs[0].view(torch.int16), outs[i].view(torch.int16))
+            for i, st in enumerate(sts):
+                for f in tot[i]:
+                    tot[i][f] += st[f]
+            if not with_cache:
+                for f in ("hits", "misses", "wasted", "bytes_demand", "bytes_gathered"):
+                    assert sts[2][f] == sts[1][f] == sts[0][f], (f, sts)
+        if not with_cache:
+            assert tot[2] == tot[1], tot
+            assert tot[1]["bytes_prefetch"] == tot[0]["bytes_prefetch"]
+    for c in ctxs:
+        c.reset()
+    for c in ctxs[1:]:
+        c.attach_store(None)
+    for c in ctxs:
+        if with_cache:
+            c.attach_cache(None)
+        c.close()
+    for cache in caches:
+        cache.close()
+    store.close()
