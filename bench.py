@@ -147,7 +147,8 @@ def host_store_run(args, w, ckv, synth, np, torch, host, layers, dims, k) -> dic
             h.view(torch.uint8).numpy().tofile(f)
         f.flush()
         os.fsync(f.fileno())
-    res = {"file_gib": round(L * m * span / 2**30, 2), "direct": True, "io_threads": args.io_threads}
+    res = {"file_gib": round(L * m * span / 2**30, 2), "direct": True, "io_threads": args.io_threads,
+           "period": args.host_period, "subperiod": args.host_subperiod}
     store = ckv.Store(path, L * m, span, args.io_threads, ckv.STORE_DIRECT)
     buf = torch.empty(m * span, dtype=torch.uint8).pin_memory()
     keys = np.arange(m, dtype=np.int64) + (L - 1) * m
@@ -160,6 +161,7 @@ def host_store_run(args, w, ckv, synth, np, torch, host, layers, dims, k) -> dic
         ctx = ckv.Context(dims, w.keep_ratio, ckv.CTX_HOST_PREFIX)
         if args.host_period > 1:
             ctx.set_period(args.host_period)
+        ctx.set_subperiod(args.host_subperiod)
         cache = None
         if policy is not None:
             cache = ckv.Cache(L * m, int(args.host_cache_frac * L * k), L * k, policy)
@@ -414,6 +416,8 @@ def main() -> int:
                     help="host-resident workloads: also run the layers from a file written in this "
                          "directory, read by the storage tier (O_DIRECT)")
     ap.add_argument("--io-threads", type=int, default=16, help="storage tier I/O threads")
+    ap.add_argument("--host-subperiod", type=int, default=1,
+                    help="storage tier: reads up to this many - 1 layers ahead inside a Period")
     ap.add_argument("--io-sweep", action="store_true",
                     help="also report block-store read amplification on the 64K-token workload "
                          "at chunk sizes 8, 16, 32 and 64")
