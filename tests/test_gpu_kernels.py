@@ -34,6 +34,9 @@ SCORE_CASES = [
     W(20000, 2, 8, 8, 128, 32, seed=3),  # long prefix, large key ranges
     W(1024, 32, 4, 1, 64, 16, dtype="f32", seed=0, alpha=2.0),  # fp32 path
     W(600, 7, 3, 3, 64, 16, dtype="f32", sm_scale=0.31),
+    W(5, 1, 2, 1, 64, 4),                # one query, prefix shorter than one subtile
+    W(31, 1, 4, 2, 128, 32),             # a single partial chunk (m = 1)
+    W(64, 1, 1, 1, 128, 64),             # exactly one stage and one chunk, G = 1
 ]
 
 
@@ -149,6 +152,9 @@ ATTN_CASES = [
     (W2(4096, 256, 28, 4, 128, 32), "tenth"),  # suffix 256: long causal part
     (W2(1024, 32, 4, 1, 64, 16, dtype="f32"), "quarter"),
     (W2(500, 6, 3, 1, 64, 4, dtype="f32", sm_scale=0.2), "half"),
+    (W2(5, 1, 2, 1, 64, 4), "all"),            # one query, both chunks, the last one partial
+    (W2(31, 1, 4, 2, 128, 32), "all"),         # a single partial chunk
+    (W2(33, 2, 2, 2, 64, 32), "half"),         # keeps only the one-row last chunk
 ]
 
 

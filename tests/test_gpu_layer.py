@@ -22,6 +22,7 @@ HBM_CASES = [
     (small("c3_qwen7b_32k", n_prefix=4096, n_suffix=40, n_layers=2), 0),
     (small("c3_qwen7b_32k", n_prefix=4096, n_suffix=40, n_layers=2), 2),  # materialised gather
     (small("c4_qwen14b_64k_c8", n_prefix=3000, n_suffix=20, n_layers=2), 0),
+    (small("c3_qwen7b_32k", n_prefix=45, n_suffix=1, n_layers=2), 0),  # m = 2, one query
 ]
 
 
