@@ -77,13 +77,17 @@ def _host_store(w, tensors):
     return stores
 
 
-@pytest.mark.parametrize("scenario", ["drift", "repeat", "disjoint"])
+@pytest.mark.parametrize("scenario", ["drift", "repeat", "disjoint", "tiny"])
 def test_layer_host_resident_prefetch(scenario):
     """Host-resident prefix: outputs equal the HBM path's oracle, and the
     hit/miss/byte counts equal the oracle's set algebra with the previous
-    layer's selection as the prediction."""
+    layer's selection as the prediction.  "tiny": two chunks (the last one
+    partial, kept), one query."""
     import paper_2601_13631_amd as ckv
-    w = small("c5_qwen32b_128k_host", n_prefix=4096, n_suffix=24, n_layers=4)
+    if scenario == "tiny":
+        w = small("c5_qwen32b_128k_host", n_prefix=45, n_suffix=1, n_layers=3)
+    else:
+        w = small("c5_qwen32b_128k_host", n_prefix=4096, n_suffix=24, n_layers=4)
     hs = synth.heavy_sets(w)
     if scenario == "repeat":      # identical layers: perfect prediction after layer 0
         layers = [synth.layer_tensors(w, 0, hs[0])] * w.n_layers
