@@ -165,6 +165,7 @@ def test_attach_cache_refusals():
 
 @pytest.mark.parametrize("period,with_cache,direct,n_prefix", [
     (1, False, False, 4096), (1, True, True, 4096), (2, True, False, 4096),
+    (1, True, False, 45),     # two chunks per layer, the last one partial; one kept
     (1, True, True, 32768)])  # the last: 1,024 chunks of 128 KiB per layer, a 512 MiB file
 def test_layer_store(tmp_path, period, with_cache, direct, n_prefix):
     """Chunks read from a file by the storage tier's I/O threads into the pinned
