@@ -26,10 +26,10 @@ def _store(w, t):
     return h.pin_memory()
 
 
-@pytest.mark.parametrize("period", [1, 2])
-def test_layer_cache_requests(period):
+@pytest.mark.parametrize("period,n_prefix", [(1, 4096), (2, 4096), (1, 45)])  # 45: two chunks
+def test_layer_cache_requests(period, n_prefix):
     import paper_2601_13631_amd as ckv
-    w = synth.WORKLOADS["c5_qwen32b_128k_host"].scaled(n_prefix=4096, n_suffix=24, n_layers=4)
+    w = synth.WORKLOADS["c5_qwen32b_128k_host"].scaled(n_prefix=n_prefix, n_suffix=24, n_layers=4)
     L, m = w.n_layers, w.n_chunks
     layers = [synth.layer_tensors(w, l) for l in range(L)]
     stores = [_store(w, t) for t in layers]
