@@ -6,23 +6,25 @@ selection, contiguous-span attention over the kept chunks plus the causal
 suffix) through ``ckv_reprefill_layer``.  Steps cycle over the workload's layers,
 each with its own seeded synthetic Q/K/V resident in HBM before timing starts.
 
-Prints one JSON line.  ``roofline`` describes the scoring kernel (the dominant
-kernel): its algorithmic flops per launch (2*S*Hq*n*d) over its average
-duration, taken from HIP events inside the timed region: the kernel is
-launched on the layer's stream with two events as its own start and stop
-timestamps (two events per step; the context records no others there).  ``roofline.traffic`` is the kernel's HBM bytes per launch from
-the committed rocprofv3 counter summary (FETCH_SIZE and WRITE_SIZE, each scaled
-by what the counter reads for a plain copy of known size); it is null when the
-kernel's sources no longer match the hash recorded with those counters.
-``cpu_baseline`` times the oracle (plain C, fp64) on a bounded sample of the
-same workload on this host's cores.  ``detail`` holds an untimed diagnostic
-pass after the timed region: per-stage times from events between every stage,
-the step time with no events at all, and the average time per layer when
+Prints one JSON line.  Untimed diagnostic passes run first (they also bring
+the GPU to its working clock): per-stage times from events between every
+stage, the step time with no events, and the average time per layer when
 layers share their set over Periods of 8 layers (Def. 4.2: one layer in eight
 scores and selects) -- context only; the headline metric selects per layer.
-It also holds the kept sets' reads against a store of 64-token blocks (the
-comparison systems' granularity, Sec. 3) and the attention-guided cache's hit
-rates and host cost over a stream of requests on the same prefix (Sec. 4.5).
+Then W warm-up steps and the K timed steps, with no events at all: ``value``
+and ``ms_per_step``.  Then the same K steps again with the scoring kernel
+(the dominant kernel) launched on the layer's stream with two HIP events as
+its own start and stop timestamps: ``roofline`` is its algorithmic flops per
+launch (2*S*Hq*n*d) over their average interval.  ``roofline.traffic`` is the
+kernel's HBM bytes per launch from the committed rocprofv3 counter summary
+(FETCH_SIZE and WRITE_SIZE, each scaled by what the counter reads for a plain
+copy of known size); it is null when the kernel's sources no longer match the
+hash recorded with those counters.  ``cpu_baseline`` times the oracle (plain
+C, fp64) on a bounded sample of the same workload on this host's cores, and
+on one thread.  ``detail`` also holds the kept sets' reads against a store of
+64-token blocks (the comparison systems' granularity, Sec. 3) and the
+attention-guided cache's hit rates and host cost over a stream of requests on
+the same prefix (Sec. 4.5).
 """
 from __future__ import annotations
 
@@ -41,6 +43,18 @@ PERIOD = 8                  # layers per Period in the Period diagnostic (the pa
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_F32_TFLOPS = 157.3     # MI355X fp32 (matrix and vector)
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+
+
+def cpu_model() -> str:
+    """The host CPU's model name (as lscpu reports it, from /proc/cpuinfo)."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
 
 
 def log(msg: str) -> None:
@@ -93,7 +107,7 @@ def host_cache_requests(args, w, ckv, synth, np, torch, layers, stores, dims, k)
     res = {"requests": R, "layers": L, "gpu_slots": gpu_slots,
            "slot_bytes": 2 * w.chunk_size * w.n_kv_heads * w.head_dim * w.elem_bytes}
     for name, policy in (("none", None), ("attention", ckv.CACHE_ATTENTION), ("lfu", ckv.CACHE_LFU)):
-        ctx = ckv.Context(dims, w.keep_ratio, ckv.CTX_HOST_PREFIX)
+        ctx = ckv.Context(dims, w.n_layers, w.keep_ratio, ckv.CTX_HOST_PREFIX)
         cache = None
         if policy is not None:
             cache = ckv.Cache(L * m, gpu_slots, L * k, policy)
@@ -158,7 +172,7 @@ def host_store_run(args, w, ckv, synth, np, torch, host, layers, dims, k) -> dic
     res["raw_read_gbs"] = round(m * span / dt / 1e9, 2)
     out = torch.empty_like(layers[0]["q"])
     for name, policy in (("none", None), ("attention", ckv.CACHE_ATTENTION)):
-        ctx = ckv.Context(dims, w.keep_ratio, ckv.CTX_HOST_PREFIX)
+        ctx = ckv.Context(dims, w.n_layers, w.keep_ratio, ckv.CTX_HOST_PREFIX)
         if args.host_period > 1:
             ctx.set_period(args.host_period)
         ctx.set_subperiod(args.host_subperiod)
@@ -225,7 +239,7 @@ def host_resident(args, w, ckv, synth, np, torch) -> int:
     del host
     dims = ckv.make_dims(w.n_prefix, w.n_suffix, w.n_q_heads, w.n_kv_heads, w.head_dim,
                          w.chunk_size, ckv.DTYPE_BF16)
-    ctx = ckv.Context(dims, w.keep_ratio, ckv.CTX_HOST_PREFIX)
+    ctx = ckv.Context(dims, w.n_layers, w.keep_ratio, ckv.CTX_HOST_PREFIX)
     if args.host_period > 1:
         ctx.set_period(args.host_period)
     k = ctx.k
@@ -294,6 +308,16 @@ def host_resident(args, w, ckv, synth, np, torch) -> int:
     if store_detail is not None:
         line["detail"]["storage_tier"] = store_detail
     print(json.dumps(line), flush=True)
+    # every library object is closed above; the pinned stores and device
+    # tensors are released here too, with the device idle, rather than by
+    # interpreter and runtime teardown at exit
+    del stores, layers, outs
+    import gc
+    gc.collect()
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    if hasattr(torch._C, "_host_emptyCache"):
+        torch._C._host_emptyCache()
     return 0
 
 
@@ -307,7 +331,7 @@ def io_sweep(args, ckv, synth, np, torch, dev) -> dict:
         w = synth.WORKLOADS[name]
         dims = ckv.make_dims(w.n_prefix, w.n_suffix, w.n_q_heads, w.n_kv_heads, w.head_dim,
                              w.chunk_size, ckv.DTYPE_BF16)
-        ctx = ckv.Context(dims, w.keep_ratio, 0)
+        ctx = ckv.Context(dims, w.n_layers, w.keep_ratio, 0)
         hs = synth.heavy_sets(w)
         tot = {"tokens_selected": 0, "runs": 0, "blocks": 0, "tokens_block": 0}
         for l in range(args.io_layers):
@@ -338,7 +362,7 @@ def tiers_detail(args, w, ckv, synth, np, torch, layers, dims, dev) -> dict:
     64-token block store (Sec. 4.2; Sec. 3), and the attention-guided cache
     (Sec. 4.5) against its frequency-only foil over that request stream."""
     L, m, n, c = w.n_layers, w.n_chunks, w.n_prefix, w.chunk_size
-    ctx = ckv.Context(dims, w.keep_ratio, 0)
+    ctx = ckv.Context(dims, w.n_layers, w.keep_ratio, 0)
     k = ctx.k
     out = torch.empty_like(layers[0]["q"])
     sels, scores = [], []
@@ -457,8 +481,6 @@ def main() -> int:
     dims = ckv.make_dims(w.n_prefix, w.n_suffix, w.n_q_heads, w.n_kv_heads, w.head_dim,
                          w.chunk_size, ckv.DTYPE_F32 if w.dtype == "f32" else ckv.DTYPE_BF16)
     mat = ckv.CTX_MATERIALIZE if args.materialize else 0
-    ctx = ckv.Context(dims, w.keep_ratio, ckv.CTX_SCORE_TIMING | mat)
-    k = ctx.k
     outs = [torch.empty_like(l["q"]) for l in layers]
     stream = torch.cuda.current_stream()
 
@@ -467,30 +489,22 @@ def main() -> int:
         c.reprefill_layer(i % L, l["q"], l["k_suffix"], l["v_suffix"], l["k_prefix"], outs[i % L],
                           k_prefix=l["k_prefix"], v_prefix=l["v_prefix"], stream=stream)
 
-    log(f"warmup {args.warmup} steps")
-    for i in range(args.warmup):
-        step(ctx, i)
-    torch.cuda.synchronize()
-    ctx.reset()  # score times restart with the timed region
-    log(f"timing {args.steps} steps")
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for i in range(args.steps):
-        step(ctx, i)
-    torch.cuda.synchronize()
-    elapsed = time.perf_counter() - t0
-    score_ms, n_timed = ctx.stage_times()
-    ctx.close()
-    assert n_timed == args.steps, (n_timed, args.steps)
-    ms_per_step = elapsed * 1e3 / args.steps
-    value = w.n_prefix * args.steps / elapsed
-    score_s = score_ms["score"] / n_timed * 1e-3
-    log(f"{ms_per_step * 1e3:.1f} us/step; score kernel {score_s * 1e6:.1f} us")
+    def timed(c, n: int) -> float:
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for i in range(n):
+            step(c, i)
+        torch.cuda.synchronize()
+        return time.perf_counter() - t0
 
-    # untimed diagnostics: every stage bracketed by events, then no events at all
-    n_diag = min(args.steps, 4 * L)
-    diag = ckv.Context(dims, w.keep_ratio, ckv.CTX_STAGE_TIMING | mat)
-    for i in range(min(args.warmup, L)):
+    # untimed diagnostics first (they also bring the GPU to its working clock
+    # before anything is timed): every stage bracketed by events, then the
+    # step with no events at all, then layers sharing their set over Periods of
+    # 8 layers (Def. 4.2, the paper's setting: one layer in eight scores and
+    # selects, the others attend over its set)
+    n_diag = max(4 * L, 112)
+    diag = ckv.Context(dims, w.n_layers, w.keep_ratio, ckv.CTX_STAGE_TIMING | mat)
+    for i in range(L):
         step(diag, i)
     torch.cuda.synchronize()
     diag.reset()
@@ -499,31 +513,46 @@ def main() -> int:
     stage_ms, n_st = diag.stage_times()
     diag.close()
     per_layer = {s_: stage_ms[s_] / n_st for s_ in stage_ms}
-    plain = ckv.Context(dims, w.keep_ratio, mat)
-    for i in range(min(args.warmup, L)):
+    plain = ckv.Context(dims, w.n_layers, w.keep_ratio, mat)
+    for i in range(L):
         step(plain, i)
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    for i in range(n_diag):
-        step(plain, i)
-    torch.cuda.synchronize()
-    plain_us = (time.perf_counter() - t1) * 1e6 / n_diag
-    # Periods of 8 layers (Def. 4.2, the paper's setting): one layer in eight
-    # scores and selects, the others attend over its set
+    plain_us = timed(plain, n_diag) * 1e6 / n_diag
     plain.reset()
     plain.set_period(PERIOD)
-    for i in range(min(args.warmup, L)):
+    for i in range(L):
         step(plain, i)
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    for i in range(n_diag):
-        step(plain, i)
-    torch.cuda.synchronize()
-    period_us = (time.perf_counter() - t1) * 1e6 / n_diag
+    period_us = timed(plain, n_diag) * 1e6 / n_diag
     plain.close()
     log("diagnostic stages (us): " + ", ".join(f"{s_} {v * 1e3:.1f}" for s_, v in per_layer.items()) +
         f"; step without events {plain_us:.1f} us; with Periods of {PERIOD} layers "
         f"{period_us:.1f} us per layer")
+
+    # the headline: W warm-up steps, then K timed steps with no events at all
+    ctx = ckv.Context(dims, w.n_layers, w.keep_ratio, mat)
+    k = ctx.k
+    log(f"warmup {args.warmup} steps")
+    for i in range(args.warmup):
+        step(ctx, i)
+    log(f"timing {args.steps} steps")
+    elapsed = timed(ctx, args.steps)
+    ctx.close()
+    ms_per_step = elapsed * 1e3 / args.steps
+    value = w.n_prefix * args.steps / elapsed
+    # the same K steps again with the scoring kernel's own launch bracketed by
+    # two HIP events (its start and stop timestamps, on the layer's stream):
+    # the kernel's average duration for the roofline
+    sctx = ckv.Context(dims, w.n_layers, w.keep_ratio, ckv.CTX_SCORE_TIMING | mat)
+    for i in range(args.warmup):
+        step(sctx, i)
+    torch.cuda.synchronize()
+    sctx.reset()  # score times restart with the timed pass
+    scored_elapsed = timed(sctx, args.steps)
+    score_ms, n_timed = sctx.stage_times()
+    sctx.close()
+    assert n_timed == args.steps, (n_timed, args.steps)
+    score_s = score_ms["score"] / n_timed * 1e-3
+    log(f"{ms_per_step * 1e3:.1f} us/step; score kernel {score_s * 1e6:.1f} us "
+        f"(pass with its events: {scored_elapsed * 1e6 / args.steps:.1f} us/step)")
 
     # scoring: algorithmic flops per launch / average launch duration
     score_flops = 2.0 * w.n_suffix * w.n_q_heads * w.n_prefix * w.head_dim
@@ -547,6 +576,7 @@ def main() -> int:
         "stage_us_per_layer": {s_: round(v * 1e3, 2) for s_, v in per_layer.items()},
         "stage_events_note": "diagnostic pass with events between all stages; each event adds a gap",
         "us_per_step_without_events": round(plain_us, 2),
+        "us_per_step_scored_pass": round(scored_elapsed * 1e6 / args.steps, 2),
         "stack_ms_all_layers": round(ms_per_step * L, 4),
         f"period{PERIOD}_us_per_layer_without_events": round(period_us, 2),
         f"period{PERIOD}_prefix_tokens_per_s": round(w.n_prefix / (period_us * 1e-6), 1),
@@ -572,11 +602,27 @@ def main() -> int:
             oracle.reprefill_layer(s, w.keep_ratio, h["q"], h["k_prefix"], h["v_prefix"],
                                    h["k_suffix"], h["v_suffix"], threads=threads)
         cpu_s = time.perf_counter() - t0
+        # one thread: the first layer with its first S/8 queries (the oracle's
+        # work is linear in the number of queries: every query scores all n
+        # prefix keys and attends over the kept chunks plus its causal suffix)
+        S1 = max(1, w.n_suffix // 8)
+        s1 = oracle.Shape(w.n_prefix, S1, w.n_q_heads, w.n_kv_heads, w.head_dim, w.chunk_size,
+                          s.dtype)
+        h = host[0]
+        t0 = time.perf_counter()
+        oracle.reprefill_layer(s1, w.keep_ratio, h["q"][:S1], h["k_prefix"], h["v_prefix"],
+                               h["k_suffix"][:S1], h["v_suffix"][:S1], threads=1)
+        one_s = time.perf_counter() - t0
         cpu = {"value": round(w.n_prefix * n_cpu / cpu_s, 1), "unit": "tokens/s", "cores": threads,
                "kind": "oracle",
                "sample": f"{n_cpu} full layer(s) of {w.name} (token importance, Eq. 1 pooling, "
-                         f"top-k, sparse attention), fp64, {cpu_s:.1f}s"}
-        log(f"oracle {cpu_s:.1f}s")
+                         f"top-k, sparse attention), fp64, {cpu_s:.1f}s",
+               "cpu_model": cpu_model(),
+               "one_thread": {"sample": f"layer 0 with its first {S1} of {w.n_suffix} queries, "
+                                        f"1 thread, {one_s:.2f}s",
+                              "est_s_per_layer": round(one_s * w.n_suffix / S1, 1),
+                              "est_tokens_per_s": round(w.n_prefix * S1 / (one_s * w.n_suffix), 1)}}
+        log(f"oracle {cpu_s:.1f}s on {threads} threads; one thread {one_s:.1f}s for {S1} queries")
 
     line = {
         "metric": METRIC, "value": round(value, 1), "unit": "tokens/s", "n_gpus": 1,

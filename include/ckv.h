@@ -204,16 +204,20 @@ typedef struct ckv_store ckv_store; /* storage tier, see ckv_store_open */
 #define CKV_STAGE_ATTN 4      /* attention (and split combine)                     */
 #define CKV_N_STAGES 5
 
-/* Creates a context for layers of shape *dims at keep ratio keep_ratio.
- * Allocates the workspace (and, with CKV_CTX_HOST_PREFIX, two HBM slot
- * buffers of 2k chunks each plus pinned index staging) on the current
- * device.  *out receives the context. */
-ckv_status ckv_ctx_create(const ckv_dims* dims, double keep_ratio, int32_t flags, ckv_ctx** out);
+/* Creates a context for layers 0 .. n_layers-1 of shape *dims at keep ratio
+ * keep_ratio.  Allocates the workspace (and, with CKV_CTX_HOST_PREFIX, a ring
+ * of HBM slot buffers of 2k chunks each plus pinned index staging) on the
+ * current device.  *out receives the context.  CKV_EINVAL for n_layers < 1 or
+ * keep_ratio outside (0, 1]. */
+ckv_status ckv_ctx_create(const ckv_dims* dims, int32_t n_layers, double keep_ratio, int32_t flags,
+                          ckv_ctx** out);
 /* Waits for the context's streams, then frees everything the context owns. */
 ckv_status ckv_ctx_destroy(ckv_ctx* ctx);
-/* Forgets the previous layer's selection: the next layer runs without a
- * prediction (as the first layer of a request); also clears stage times and
- * the set held for the current Period. */
+/* Starts a request over: forgets the previous layer's selection and every
+ * prediction (the next layer, which may be any layer, runs as the first of a
+ * request), the set held for the current Period, the stage times, an armed
+ * copy-error injection, and the failed state a layer error leaves.  Waits for
+ * the context's copy streams. */
 ckv_status ckv_ctx_reset(ckv_ctx* ctx);
 
 /* Periods -- Def. 4.2 (Sec. 4.3): consecutive layers p*i .. p*i+p-1 form a
@@ -226,7 +230,14 @@ ckv_status ckv_ctx_reset(ckv_ctx* ctx);
  * io->chunk_scores untouched, and needs no host synchronisation even with a
  * host-resident prefix (its prefetch prediction, the previous layer's set,
  * is then exact).  period = 1 (the default) selects at every layer.
- * Forgets any set held.  CKV_EINVAL if period < 1. */
+ * With a host-resident prefix whose per-layer stores are registered
+ * (ckv_ctx_set_host_layers), no store attached and 1 < p <= 16, a Period's
+ * first layer also queues the copies of every later layer of its Period
+ * (intra-period prefetch, Sec. 4.3.2) as soon as its set is known; the HBM
+ * ring then holds p + 1 buffers of 2k chunk slots.  Then the Period must be
+ * set at the start of a request (CKV_ESTATE otherwise; it synchronizes the
+ * device when the ring changes).  Forgets any set held.  CKV_EINVAL if
+ * period < 1. */
 ckv_status ckv_ctx_set_period(ckv_ctx* ctx, int32_t period);
 
 /* Attention-guided cache on the layer step -- Sec. 4.5 (with the cache of
@@ -288,17 +299,44 @@ ckv_status ckv_ctx_attach_cache(ckv_ctx* ctx, ckv_cache* cache);
  * layer's attention before it reuses pool slots. */
 ckv_status ckv_ctx_attach_store(ckv_ctx* ctx, ckv_store* store);
 
-/* Intra-period prefetch depth -- Sec. 4.3.2 (with Def. 4.2's Periods) and the
- * SubPeriod size of the evaluation setup.  With a store attached and a Period
- * of p > 1 layers, a layer queues the storage reads of every later layer of
- * its Period up to subperiod - 1 layers ahead as soon as its set is known
- * (the set is the Period's, so these predictions are exact); a layer's
- * computation still waits only for its own chunks.  subperiod = 1 (the
- * default) reads one layer ahead.  The pinned-host-memory path always copies
- * one layer ahead.  1 <= subperiod <= 16 (CKV_EINVAL); must be set before the
- * store is attached (CKV_ESTATE), since it sizes the chunk pool (subperiod * k
- * more slots). */
+/* SubPeriod -- the SubPeriod size of the evaluation setup with Sec. 4.3.2's
+ * intra-period prefetch (and Def. 4.2's Periods).
+ *   - Pinned-host prefix with intra-period prefetch (see ckv_ctx_set_period):
+ *     the attention of a Period's first layer starts only once the chunks of
+ *     the Period's first `subperiod` layers (its own included) are in HBM:
+ *     the gate that decides how many layers' KV must be loaded before the
+ *     Period's computation begins.  subperiod = 1 gates nothing beyond each
+ *     layer's own chunks.
+ *   - Storage tier (a store attached) with a Period of p > 1 layers: a layer
+ *     queues the storage reads of every later layer of its Period up to
+ *     subperiod - 1 layers ahead as soon as its set is known (the set is the
+ *     Period's, so these predictions are exact); a layer's computation waits
+ *     only for its own chunks.  subperiod = 1 reads one layer ahead.
+ * 1 <= subperiod <= 16 (CKV_EINVAL); must be set before the store is attached
+ * (CKV_ESTATE), since it sizes the chunk pool (subperiod * k more slots).
+ * Gating only orders work: results do not depend on it. */
 ckv_status ckv_ctx_set_subperiod(ckv_ctx* ctx, int32_t subperiod);
+
+/* Registers the pinned host stores of every layer (kv_host[l] for layer l, in
+ * ckv_layer_io.kv_host's layout; n == n_layers) with a host-resident context,
+ * or unregisters them (kv_host NULL).  Layers may then pass io->kv_host and
+ * io->kv_host_next as NULL (the registered stores are used; if io->kv_host is
+ * given it is used for the layer's own chunks), and a Period's first layer
+ * can queue the copies of the whole Period (intra-period prefetch, see
+ * ckv_ctx_set_period).  The stores must stay valid and unchanged while
+ * registered.  At the start of a request only (CKV_ESTATE); CKV_EINVAL for a
+ * count that is not n_layers or a store that is not pinned host memory
+ * (nothing changes then).  Ignored while a store is attached. */
+ckv_status ckv_ctx_set_host_layers(ckv_ctx* ctx, const void* const* kv_host, int32_t n);
+
+/* Test hook for failure handling: the next run of `layer` on this
+ * host-resident context fails where it would enqueue its host-to-HBM demand
+ * copies, as if that copy had failed: ckv_reprefill_layer returns CKV_EHIP
+ * (after its scoring and selection were enqueued, none of its copies or its
+ * attention), and the context refuses layers until ckv_ctx_reset.  layer = -1
+ * disarms; a reset disarms too.  CKV_EINVAL for an HBM-resident context or a
+ * layer outside [-1, n_layers). */
+ckv_status ckv_ctx_inject_copy_error(ckv_ctx* ctx, int32_t layer);
 
 typedef struct ckv_layer_io {
   const void* q;         /* device [S][Hq][d]                                        */
@@ -310,14 +348,29 @@ typedef struct ckv_layer_io {
   const void* kv_host;   /* pinned host (hipHostMalloc; pageable memory is refused),
                             chunk-major: chunk j of this layer at byte offset
                             j * 2*c*Hkv*d*elem, K span then V span; rows past n of
-                            the last chunk are padding (host-resident prefix)       */
+                            the last chunk are padding (host-resident prefix); may
+                            be NULL when the stores are registered
+                            (ckv_ctx_set_host_layers)                               */
   const void* kv_host_next; /* the next layer's kv_host, prefetched during this layer
                                with this layer's selection as the prediction; NULL
-                               for the last layer                                    */
+                               for the last layer (or no prefetch); ignored when the
+                               stores are registered                                 */
   void* out;             /* device [S][Hq][d] (written)                              */
   double* chunk_scores;  /* device double[m] (written), or NULL                      */
   int32_t* sel_idx;      /* device int32[k] (written), or NULL                       */
   void* stream;          /* hipStream_t for the layer's compute                      */
+  const int32_t* pred_idx; /* host int32[n_pred], strictly ascending chunk indices: this
+                              layer's predicted set (Sec. 4.3.2: the chunks expected
+                              to be selected, e.g. the previous Period's or layer's
+                              set), copied to HBM beside this layer's scoring; it
+                              replaces the context's own prediction.  NULL: the
+                              context's own (the previous layer's set, when the
+                              previous call ran layer - 1 with a next store).
+                              Host-resident prefix only (ignored, but validated,
+                              for an HBM-resident one); not with a store attached
+                              (CKV_EUNSUPPORTED)                                     */
+  int64_t n_pred;        /* entries of pred_idx, 0 <= n_pred <= k (0: an empty
+                              prediction, every kept chunk fetched on demand)        */
 } ckv_layer_io;
 
 typedef struct ckv_layer_stats {
@@ -347,13 +400,17 @@ typedef struct ckv_layer_stats {
  * recorded on each layer's compute stream between its kernel launches. */
 ckv_status ckv_ctx_stage_times(ckv_ctx* ctx, double* ms, int64_t* n_layers);
 
-/* Runs layer `layer` (0-based; layer 0, or the first layer after
- * ckv_ctx_reset, has no prediction).  HBM-resident prefix: returns without a
- * host synchronization.  Host-resident prefix: synchronizes once on the
- * selection (the only device->host dependency of the step), enqueues the
- * demand copies of the missed chunks, the attention over the HBM slots and
- * the prefetch of the next layer's chunks; counts in *stats (may be NULL) are
- * exact.  With a host-resident prefix, layers must be run in order. */
+/* Runs layer `layer` (0 <= layer < n_layers; the first layer after creation
+ * or ckv_ctx_reset may be any layer and has no prediction unless io gives
+ * one).  HBM-resident prefix: returns without a host synchronization.
+ * Host-resident prefix: synchronizes once on the selection (the only
+ * device->host dependency of the step), enqueues the demand copies of the
+ * missed chunks, the attention over the HBM slots and the prefetch of the
+ * next layer's chunks; counts in *stats (may be NULL) are exact; after the
+ * first layer of a request, layers must run in order (layer + 1, else
+ * CKV_ESTATE).  If the call fails after it has enqueued work (a HIP error,
+ * an injected copy error), the context refuses further layers with
+ * CKV_ESTATE until ckv_ctx_reset, after which it is fully usable. */
 ckv_status ckv_reprefill_layer(ckv_ctx* ctx, int32_t layer, const ckv_layer_io* io,
                                ckv_layer_stats* stats);
 

@@ -53,7 +53,7 @@ class LayerIO(ctypes.Structure):
     """``ckv_layer_io``."""
     _fields_ = [(f, ctypes.c_void_p) for f in (
         "q", "k_suffix", "v_suffix", "k_probe", "k_prefix", "v_prefix", "kv_host", "kv_host_next",
-        "out", "chunk_scores", "sel_idx", "stream")]
+        "out", "chunk_scores", "sel_idx", "stream", "pred_idx")] + [("n_pred", ctypes.c_int64)]
 
 
 class LayerStats(ctypes.Structure):
@@ -92,7 +92,10 @@ _SIG = {
     "ckv_attn_workspace_bytes": ([_DP, ctypes.c_int64], ctypes.c_size_t),
     "ckv_sparse_prefill_attn": ([_DP, _P, _P, _P, _P, ctypes.c_int64, _P, _P, _P, _P,
                                  ctypes.c_size_t, _P], ctypes.c_int32),
-    "ckv_ctx_create": ([_DP, ctypes.c_double, ctypes.c_int32, ctypes.POINTER(_P)], ctypes.c_int32),
+    "ckv_ctx_create": ([_DP, ctypes.c_int32, ctypes.c_double, ctypes.c_int32, ctypes.POINTER(_P)],
+                       ctypes.c_int32),
+    "ckv_ctx_set_host_layers": ([_P, ctypes.POINTER(_P), ctypes.c_int32], ctypes.c_int32),
+    "ckv_ctx_inject_copy_error": ([_P, ctypes.c_int32], ctypes.c_int32),
     "ckv_ctx_destroy": ([_P], ctypes.c_int32),
     "ckv_ctx_reset": ([_P], ctypes.c_int32),
     "ckv_ctx_set_period": ([_P, ctypes.c_int32], ctypes.c_int32),
@@ -125,6 +128,11 @@ for _name, (_args, _res) in _SIG.items():
     _f.restype = _res
 
 EXPORTED = tuple(_SIG)
+
+# a valid host address for an empty caller prediction (n_pred = 0 with a
+# non-NULL pred_idx); nothing is read from it
+_EMPTY_PRED = (ctypes.c_int32 * 1)()
+_EMPTY_PRED_ADDR = ctypes.addressof(_EMPTY_PRED)
 
 
 class CkvError(RuntimeError):
@@ -218,19 +226,30 @@ def sparse_prefill_attn(dims: Dims, q, k_sel, v_sel, sel_idx, k: int, k_suffix, 
 class Context:
     """``ckv_ctx``: owns workspace, streams, events and (host-resident prefix) HBM slots."""
 
-    def __init__(self, dims: Dims, keep_ratio: float, flags: int = 0):
+    def __init__(self, dims: Dims, n_layers: int, keep_ratio: float, flags: int = 0):
         self.dims = dims
         self._h = ctypes.c_void_p()
-        _check(_lib.ckv_ctx_create(ctypes.byref(dims), keep_ratio, flags, ctypes.byref(self._h)),
-               "ckv_ctx_create")
+        _check(_lib.ckv_ctx_create(ctypes.byref(dims), n_layers, keep_ratio, flags,
+                                   ctypes.byref(self._h)), "ckv_ctx_create")
+        self.n_layers = n_layers
         self.k = num_keep(dims.n_chunks, keep_ratio)
 
     def reprefill_layer(self, layer: int, q, k_suffix, v_suffix, k_probe, out, k_prefix=None,
                         v_prefix=None, kv_host=None, kv_host_next=None, chunk_scores=None,
-                        sel_idx=None, stream=None) -> dict:
+                        sel_idx=None, stream=None, pred_idx=None) -> dict:
+        """``pred_idx``: this layer's predicted chunks (ascending; a host numpy
+        array or sequence, possibly empty), or None for the context's own."""
+        pred = None
+        if pred_idx is not None:
+            import numpy as np
+            pred = np.ascontiguousarray(pred_idx, np.int32)
+            if pred.size == 0:
+                pred = np.zeros(1, np.int32)[:0]
         io = LayerIO(_ptr(q), _ptr(k_suffix), _ptr(v_suffix), _ptr(k_probe), _ptr(k_prefix),
                      _ptr(v_prefix), _ptr(kv_host), _ptr(kv_host_next), _ptr(out),
-                     _ptr(chunk_scores), _ptr(sel_idx), _stream(stream))
+                     _ptr(chunk_scores), _ptr(sel_idx), _stream(stream),
+                     None if pred is None else (pred.ctypes.data or _EMPTY_PRED_ADDR),
+                     0 if pred is None else pred.size)
         st = LayerStats()
         _check(_lib.ckv_reprefill_layer(self._h, layer, ctypes.byref(io), ctypes.byref(st)),
                "ckv_reprefill_layer")
@@ -256,6 +275,20 @@ class Context:
         self._cache = cache  # the context must not outlive the cache it uses
         _check(_lib.ckv_ctx_attach_cache(self._h, cache._h if cache is not None else None),
                "ckv_ctx_attach_cache")
+
+    def set_host_layers(self, stores) -> None:
+        """Registers the pinned host store of every layer (a list of n_layers
+        pinned tensors), or unregisters them (None)."""
+        self._host_layers = stores  # kept alive while registered
+        if stores is None:
+            _check(_lib.ckv_ctx_set_host_layers(self._h, None, 0), "ckv_ctx_set_host_layers")
+            return
+        arr = (_P * len(stores))(*[_ptr(t) for t in stores])
+        _check(_lib.ckv_ctx_set_host_layers(self._h, arr, len(stores)), "ckv_ctx_set_host_layers")
+
+    def inject_copy_error(self, layer: int) -> None:
+        """Test hook: the next run of ``layer`` fails at its demand copies (-1 disarms)."""
+        _check(_lib.ckv_ctx_inject_copy_error(self._h, layer), "ckv_ctx_inject_copy_error")
 
     def set_subperiod(self, subperiod: int) -> None:
         """Storage reads up to subperiod - 1 layers ahead inside a Period."""

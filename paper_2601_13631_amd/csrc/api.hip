@@ -150,7 +150,7 @@ ckv_status ckv_sparse_prefill_attn(const ckv_dims* dims, const void* q, const vo
   const size_t need = make_attn_plan(dims, k).bytes;
   CKV_REQUIRE(need == 0 || (ws && ws_bytes >= need), "workspace too small: %zu < %zu", ws_bytes, need);
   ChunkSource src{k_sel, v_sel, (int64_t)dims->chunk_size * dims->n_kv_heads * dims->head_dim,
-                  nullptr, 0};
+                  nullptr, 0, k};
   return launch_attn(dims, q, src, sel_idx, k, k_suffix, v_suffix, out, ws, ws_bytes,
                      (hipStream_t)stream);
 }

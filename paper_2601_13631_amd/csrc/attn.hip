@@ -688,9 +688,9 @@ ckv_status launch_attn(const ckv_dims* d, const void* q, const ChunkSource& src,
     const int64_t hd = (int64_t)d->n_kv_heads * d->head_dim;
     if (src.chunk_stride % hd != 0) CKV_FAIL(CKV_EINVAL, "chunk stride is not a whole number of rows");
     const int64_t rps = src.chunk_stride / hd;
-    // largest source row a key can name: every slot index is below max(m, 2k)
-    const int64_t slots = std::max<int64_t>(ceil_div(d->n_prefix, d->chunk_size), 2 * k);
-    if (slots * rps >= (int64_t(1) << 31)) CKV_FAIL(CKV_EUNSUPPORTED, "chunk source too large");
+    // largest source row a key can name: every slot index is below n_slots
+    if (src.n_slots < 0 || src.n_slots * rps >= (int64_t(1) << 31))
+      CKV_FAIL(CKV_EUNSUPPORTED, "chunk source too large");
     a.rows_per_slot = (int)rps;
   }
   a.sel = sel;

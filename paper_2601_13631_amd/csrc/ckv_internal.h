@@ -117,6 +117,7 @@ struct ChunkSource {
   int64_t chunk_stride;     // elements between consecutive chunk slots
   const int32_t* chunk_off; // optional per-chunk slot table (device)
   int32_t direct;           // 1: off(u) = sel[u]; 0: off(u) = u (unless chunk_off)
+  int64_t n_slots;          // slots the source holds (every off(u) is below it)
 };
 
 // Copies whole chunk spans of span_bytes each (16-byte multiple): span chunks[i]

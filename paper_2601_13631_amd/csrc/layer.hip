@@ -10,18 +10,25 @@
 // on the device and, for a host-resident prefix, on the host), with no
 // scoring, no selection and no host synchronisation.
 //
-// Host-resident prefix (Sec. 4.3.2): the K/V store
-// of every layer lives in pinned host memory, chunk-major (chunk j of a layer
-// is one span: K rows then V rows).  Two HBM slot buffers alternate between
-// layers.  While layer l computes, the chunks that layer l selected are copied
-// for layer l+1 into the other buffer on a prefetch stream (the prediction
-// P_{l+1} = S_l).  When layer l+1 has selected S_{l+1}, only the difference
-// S_{l+1} \ P_{l+1} is fetched on a demand stream into the free slots behind
-// the prefetched ones, and the attention reads every kept chunk through a
-// chunk -> slot table.  Copies move whole chunk spans, by a kernel that reads
-// the pinned store over the host link (one launch per list of chunks instead
-// of one DMA copy per run of consecutive chunks).  The selection is the
-// step's only device -> host dependency.
+// Host-resident prefix (Sec. 4.3.2): the K/V store of every layer lives in
+// pinned host memory, chunk-major (chunk j of a layer is one span: K rows then
+// V rows).  HBM holds a ring of transient slot buffers, layer l using buffer
+// l % nbuf.  Chunks predicted for a layer are copied into its buffer ahead of
+// time on a prefetch stream (the prediction P_{l+1} = S_l, or a set the caller
+// gives); when the layer has selected S_l only the difference S_l \ P_l is
+// fetched on a demand stream into the free slots behind the predicted ones,
+// and the attention reads every kept chunk through a chunk -> slot table.
+// With Periods and the per-layer stores registered (ckv_ctx_set_host_layers),
+// a Period's first layer queues the copies of every later layer of its Period
+// as soon as its set is known (intra-period prefetch; the ring then holds
+// p + 1 buffers), and its attention waits until the first `subperiod` layers
+// of the Period are in HBM (SubPeriod gating).  Copies move whole chunk spans,
+// by a kernel that reads the pinned store over the host link.  The selection
+// is the step's only device -> host dependency.
+//
+// Pinned staging lists (slot tables, chunk lists) are rewritten only after
+// the copy that last read them has run: every staging copy records a guard
+// event that the host waits on before the next rewrite.
 
 #include <cstring>
 #include <new>
@@ -31,8 +38,36 @@
 
 using namespace ckv;
 
+namespace {
+
+constexpr int kMaxBuf = 17;  // Periods of up to 16 layers, plus the next Period's first layer
+
+// One transient slot buffer: slots_per_buf chunk slots of the arena and the
+// staging of the layer that uses it.
+struct SlotBuf {
+  void* slots = nullptr;
+  // device lists and their pinned staging: chunk -> arena slot table [k],
+  // demand chunks [k], prefetch chunks [k], cache fills [2k] (source slots,
+  // then target slots)
+  int32_t *tab_dev = nullptr, *tab_host = nullptr;
+  int32_t *dem_dev = nullptr, *dem_host = nullptr;
+  int32_t *pref_dev = nullptr, *pref_host = nullptr;
+  int32_t *fill_dev = nullptr, *fill_host = nullptr;
+  hipEvent_t ev_pref = nullptr;  // the copies into this buffer's predicted slots have landed
+  hipEvent_t ev_attn = nullptr;  // the last layer reading this buffer (attention, fills) is done
+  // staging guards: recorded after the staging copies of tab/dem (demand
+  // stream), pref (prefetch stream) and fill (compute stream)
+  hipEvent_t ev_gd = nullptr, ev_gp = nullptr, ev_gf = nullptr;
+  bool pref_pending = false, attn_rec = false, gd = false, gp = false, gf = false;
+  int32_t pred_layer = -1;      // layer whose predicted chunks sit in slots 0..|pred|-1
+  std::vector<int32_t> pred;    // those chunks, ascending
+};
+
+}  // namespace
+
 struct ckv_ctx {
   ckv_dims dims;
+  int32_t n_layers;
   double keep_ratio;
   int32_t flags;
   int64_t m, k;
@@ -44,30 +79,26 @@ struct ckv_ctx {
   // host-resident prefix
   int64_t slot_bytes = 0;  // one chunk: K span + V span
   int64_t slots_per_buf = 0;
-  // one arena of chunk slots: two transient buffers of slots_per_buf slots
-  // (slots[0], slots[1]) then cache_slots slots holding the chunks of an
-  // attached cache's GPU tier; slot tables index the whole arena
+  // one arena of chunk slots: nbuf transient buffers of slots_per_buf slots,
+  // then cache_slots slots holding the chunks of an attached cache's GPU tier;
+  // slot tables index the whole arena
+  int nbuf = 2;
   void* arena = nullptr;
-  void* slots[2] = {nullptr, nullptr};
-  int32_t* slot_tab_dev[2] = {nullptr, nullptr};
-  int32_t* sel_host = nullptr;      // pinned [k]
-  int32_t* slot_tab_host[2] = {nullptr, nullptr};  // pinned [k]
-  // chunk lists of the copy kernels: misses (demand) and the prediction
-  // (prefetch) of each slot buffer, staged in pinned memory, read on the device
-  int32_t* dem_host[2] = {nullptr, nullptr};
-  int32_t* pref_host[2] = {nullptr, nullptr};
-  int32_t* dem_dev[2] = {nullptr, nullptr};
-  int32_t* pref_dev[2] = {nullptr, nullptr};
+  SlotBuf buf[kMaxBuf];
+  int32_t* stage_host = nullptr;  // pinned staging of every buffer (5k ints each)
+  int32_t* stage_dev = nullptr;
+  int32_t* sel_host = nullptr;    // pinned [k]
   hipStream_t demand = nullptr, prefetch = nullptr;
-  hipEvent_t ev_sel = nullptr, ev_dem = nullptr, ev_pref[2] = {nullptr, nullptr},
-             ev_attn[2] = {nullptr, nullptr};
-  bool pref_pending[2] = {false, false}, attn_recorded[2] = {false, false};
-  std::vector<int32_t> pred;  // prediction for the next layer (ascending), in slots 0..|pred|-1
-  int32_t next_layer = 0;
+  hipEvent_t ev_sel = nullptr, ev_dem = nullptr;
+  std::vector<const void*> host_layers;  // device views of the registered per-layer stores
+  int32_t prev_layer = -1;  // last layer run since creation or reset (-1: none)
+  bool broken = false;      // a layer failed after enqueueing work: reset before the next
+  int32_t inject_layer = -1;  // test hook: the demand copy of this layer fails
   // Periods: layers period_first .. period_first+period-1 attend over the set
   // selected at period_first (device copy at off_pset, host copy pset_host)
   int32_t period = 1;
   int32_t period_first = -1;  // -1: no set held
+  int32_t subperiod = 1;
   size_t off_pset = 0;
   std::vector<int32_t> pset_host;
   std::vector<double> pset_A;  // the Period set's chunk scores (attached cache only)
@@ -78,10 +109,7 @@ struct ckv_ctx {
   std::vector<int32_t> free_slots;  // cache slots holding nothing
   std::vector<int64_t> keys, evicted;
   std::vector<double> key_scores;
-  double* scores_host = nullptr;                    // pinned [m]
-  int32_t* fill_host[2] = {nullptr, nullptr};       // pinned [2k]: source slots, then target slots
-  int32_t* fill_dev[2] = {nullptr, nullptr};
-  bool pref_recorded[2] = {false, false};
+  double* scores_host = nullptr;    // pinned [m]
   // storage tier: chunks come from a file into a pinned chunk pool, then to
   // HBM.  A chunk in an attached cache's GPU or CPU tier keeps its pool slot
   // (the pool is the CPU tier of Sec. 4.5, inclusive of the GPU tier); every
@@ -110,7 +138,6 @@ struct ckv_ctx {
     std::vector<int64_t> keys;
   };
   Ahead ahead[kAhead];
-  int32_t subperiod = 1;
   std::vector<int64_t> io_keys, dropped;
   std::vector<char*> io_dst;
   std::vector<int32_t> xsrc, xdst;
@@ -122,6 +149,15 @@ struct ckv_ctx {
 };
 
 namespace {
+
+// Waits for the copy that last read a pinned staging list before it is rewritten.
+ckv_status guard(hipEvent_t e, bool& recorded) {
+  if (recorded) {
+    CKV_HIP(hipEventSynchronize(e));
+    recorded = false;
+  }
+  return CKV_OK;
+}
 
 // Waits for store reads into the pool that are still in flight.
 void drain_store_reads(ckv_ctx* c) {
@@ -170,18 +206,41 @@ void pool_release(ckv_ctx* c, int64_t key) {
 }
 
 // Copies count chunks from pool slots src[] to arena slots dst[] on stream st,
-// with the lists staged through this buffer's pinned and device arrays.
+// with the lists staged through this buffer's pinned and device arrays; the
+// staging guard of that stream is recorded after the list copy.
 ckv_status pool_copy(ckv_ctx* c, int b, int which, const int32_t* src, const int32_t* dst,
                      int64_t count, hipStream_t st) {
   if (count == 0) return CKV_OK;
+  SlotBuf& B = c->buf[b];
+  ckv_status s = which == 0 ? guard(B.ev_gp, B.gp) : guard(B.ev_gd, B.gd);
+  if (s != CKV_OK) return s;
   const int64_t spb = c->slots_per_buf;
   int32_t* h = c->xfer_host[b][which];
   std::memcpy(h, src, (size_t)count * sizeof(int32_t));
   std::memcpy(h + spb, dst, (size_t)count * sizeof(int32_t));
   CKV_HIP(hipMemcpyAsync(c->xfer_dev[b][which], h, (size_t)(2 * spb) * sizeof(int32_t),
                          hipMemcpyHostToDevice, st));
+  if (which == 0) {
+    CKV_HIP(hipEventRecord(B.ev_gp, st));
+    B.gp = true;
+  } else {
+    CKV_HIP(hipEventRecord(B.ev_gd, st));
+    B.gd = true;
+  }
   return launch_copy_slots(c->pool_dev, c->xfer_dev[b][which], c->arena,
                            c->xfer_dev[b][which] + spb, count, c->slot_bytes, st);
+}
+
+void free_buffers(ckv_ctx* c) {
+  for (SlotBuf& B : c->buf) {
+    for (hipEvent_t e : {B.ev_pref, B.ev_attn, B.ev_gd, B.ev_gp, B.ev_gf})
+      if (e) (void)hipEventDestroy(e);
+    B = SlotBuf();
+  }
+  (void)hipHostFree(c->stage_host);
+  (void)hipFree(c->stage_dev);
+  c->stage_host = nullptr;
+  c->stage_dev = nullptr;
 }
 
 ckv_status free_ctx(ckv_ctx* c) {
@@ -191,18 +250,7 @@ ckv_status free_ctx(ckv_ctx* c) {
   if (c->demand) (void)hipStreamSynchronize(c->demand);
   if (c->prefetch) (void)hipStreamSynchronize(c->prefetch);
   (void)hipFree(c->ws);
-  for (int i = 0; i < 2; ++i) {
-    (void)hipFree(c->slot_tab_dev[i]);
-    (void)hipFree(c->fill_dev[i]);
-    (void)hipHostFree(c->fill_host[i]);
-    (void)hipHostFree(c->slot_tab_host[i]);
-    (void)hipFree(c->dem_dev[i]);
-    (void)hipFree(c->pref_dev[i]);
-    (void)hipHostFree(c->dem_host[i]);
-    (void)hipHostFree(c->pref_host[i]);
-    if (c->ev_pref[i]) (void)hipEventDestroy(c->ev_pref[i]);
-    if (c->ev_attn[i]) (void)hipEventDestroy(c->ev_attn[i]);
-  }
+  free_buffers(c);
   (void)hipFree(c->arena);
   free_pool(c);
   (void)hipHostFree(c->sel_host);
@@ -228,6 +276,88 @@ ckv_status free_ctx(ckv_ctx* c) {
     }                                                                                    \
   } while (0)
 
+// Staging of every slot buffer: one pinned and one device block of kMaxBuf *
+// 5k ints, carved per buffer, and the buffers' events.
+ckv_status alloc_buffers(ckv_ctx* c) {
+  const size_t per = (size_t)(5 * c->k);
+  const size_t bytes = per * kMaxBuf * sizeof(int32_t);
+  hipError_t e = hipHostMalloc((void**)&c->stage_host, bytes, hipHostMallocDefault);
+  if (e == hipSuccess) e = hipMalloc((void**)&c->stage_dev, bytes);
+  for (int b = 0; b < kMaxBuf && e == hipSuccess; ++b) {
+    SlotBuf& B = c->buf[b];
+    int32_t* h = c->stage_host + b * per;
+    int32_t* d = c->stage_dev + b * per;
+    B.tab_host = h;
+    B.tab_dev = d;
+    B.dem_host = h + c->k;
+    B.dem_dev = d + c->k;
+    B.pref_host = h + 2 * c->k;
+    B.pref_dev = d + 2 * c->k;
+    B.fill_host = h + 3 * c->k;
+    B.fill_dev = d + 3 * c->k;
+    for (hipEvent_t* ev : {&B.ev_pref, &B.ev_attn, &B.ev_gd, &B.ev_gp, &B.ev_gf})
+      if (e == hipSuccess) e = hipEventCreateWithFlags(ev, hipEventDisableTiming);
+  }
+  if (e != hipSuccess)
+    CKV_FAIL(e == hipErrorOutOfMemory ? CKV_ENOMEM : CKV_EHIP, "slot buffer staging: %s",
+             hipGetErrorString(e));
+  return CKV_OK;
+}
+
+// (Re)allocates the slot arena for nbuf transient buffers and G cache slots;
+// with keep_cache, the bytes of the current G cache slots move to the new
+// arena (the chunks of an attached cache's GPU tier stay in HBM).  The device
+// must be idle (nothing in flight may read the old arena).
+ckv_status alloc_arena(ckv_ctx* c, int nbuf, int64_t G, bool keep_cache = false) {
+  const size_t bytes = (size_t)((nbuf * c->slots_per_buf + G) * c->slot_bytes);
+  void* arena = nullptr;
+  hipError_t e = hipMalloc(&arena, bytes);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    CKV_FAIL(e == hipErrorOutOfMemory ? CKV_ENOMEM : CKV_EHIP,
+             "hipMalloc of %zu bytes of chunk slots failed: %s", bytes, hipGetErrorString(e));
+  }
+  if (keep_cache && c->arena && G > 0 && G == c->cache_slots) {
+    e = hipMemcpy(static_cast<char*>(arena) + nbuf * c->slots_per_buf * c->slot_bytes,
+                  static_cast<char*>(c->arena) + c->nbuf * c->slots_per_buf * c->slot_bytes,
+                  (size_t)(G * c->slot_bytes), hipMemcpyDeviceToDevice);
+    if (e != hipSuccess) {
+      (void)hipFree(arena);
+      CKV_FAIL(CKV_EHIP, "moving the cache slots to the new arena failed: %s", hipGetErrorString(e));
+    }
+  }
+  CKV_HIP(hipFree(c->arena));
+  c->arena = arena;
+  c->nbuf = nbuf;
+  for (int b = 0; b < kMaxBuf; ++b) {
+    SlotBuf& B = c->buf[b];
+    B.slots = b < nbuf ? static_cast<char*>(arena) + b * c->slots_per_buf * c->slot_bytes : nullptr;
+    B.pred_layer = -1;
+    B.pred.clear();
+    B.pref_pending = false;
+    B.attn_rec = false;
+  }
+  return CKV_OK;
+}
+
+// Ring size the current settings call for: a Period's layers plus the next
+// Period's first layer when intra-period prefetch is possible (pinned stores
+// registered, no storage tier, 1 < p < kMaxBuf), else two buffers.
+int wanted_buffers(const ckv_ctx* c) {
+  if (!(c->flags & CKV_CTX_HOST_PREFIX) || c->kv_store || c->host_layers.empty()) return 2;
+  if (c->period <= 1 || c->period + 1 > kMaxBuf) return 2;
+  return c->period + 1;
+}
+
+bool period_wide(const ckv_ctx* c) { return c->nbuf > 2; }
+
+ckv_status resize_ring(ckv_ctx* c) {
+  const int nb = wanted_buffers(c);
+  if (nb == c->nbuf) return CKV_OK;
+  CKV_HIP(hipDeviceSynchronize());
+  return alloc_arena(c, nb, c->cache_slots, true);
+}
+
 bool all_stages(const ckv_ctx* c) { return c->flags & CKV_CTX_STAGE_TIMING; }
 
 // Adds the stage times of the oldest unaccounted layer to the totals.
@@ -248,11 +378,65 @@ int64_t chunk_len(const ckv_dims* d, int64_t j) {
   return std::min<int64_t>(d->chunk_size, d->n_prefix - j * d->chunk_size);
 }
 
+int64_t chunk_bytes(const ckv_ctx* c, int64_t j) {
+  const ckv_dims* d = &c->dims;
+  return 2 * chunk_len(d, j) * d->n_kv_heads * d->head_dim * elem_bytes(d->dtype);
+}
+
+// Queues, on the prefetch stream, the copy of `chunks` (ascending) of layer
+// t's pinned store into slots 0.. of buffer b, after the layer that last read
+// the buffer and after this layer's demand copies; the buffer then predicts
+// layer t.  Returns the bytes queued.
+ckv_status queue_prefetch(ckv_ctx* c, int b, int32_t t, const void* store,
+                          const std::vector<int32_t>& chunks, bool after_demand, int64_t* bytes) {
+  SlotBuf& B = c->buf[b];
+  if (B.attn_rec) CKV_HIP(hipStreamWaitEvent(c->prefetch, B.ev_attn, 0));
+  if (after_demand) CKV_HIP(hipStreamWaitEvent(c->prefetch, c->ev_dem, 0));
+  const int64_t n = (int64_t)chunks.size();
+  if (n > 0) {
+    ckv_status s = guard(B.ev_gp, B.gp);
+    if (s != CKV_OK) return s;
+    std::memcpy(B.pref_host, chunks.data(), (size_t)n * sizeof(int32_t));
+    CKV_HIP(hipMemcpyAsync(B.pref_dev, B.pref_host, (size_t)n * sizeof(int32_t),
+                           hipMemcpyHostToDevice, c->prefetch));
+    CKV_HIP(hipEventRecord(B.ev_gp, c->prefetch));
+    B.gp = true;
+    s = launch_copy_spans(store, B.pref_dev, n, 0, B.slots, c->slot_bytes, c->prefetch);
+    if (s != CKV_OK) return s;
+  }
+  CKV_HIP(hipEventRecord(B.ev_pref, c->prefetch));
+  B.pref_pending = true;
+  B.pred = chunks;
+  B.pred_layer = t;
+  for (int32_t j : chunks) *bytes += chunk_bytes(c, j);
+  return CKV_OK;
+}
+
+// The chunks of `set` that layer t does not find in the attached cache's HBM slots.
+void uncached(const ckv_ctx* c, int32_t t, const int32_t* set, int64_t n, std::vector<int32_t>& out) {
+  out.clear();
+  const bool t_cached = c->cache && t < c->cache_layers;
+  const int64_t key0 = (int64_t)t * c->m;
+  for (int64_t u = 0; u < n; ++u)
+    if (!(t_cached && c->slot_of[key0 + set[u]] >= 0)) out.push_back(set[u]);
+}
+
+struct LayerArgs {
+  int32_t layer;
+  const ckv_layer_io* io;
+  const void* store;       // this layer's pinned store as the device reads it
+  const void* store_next;  // the next layer's, or nullptr
+  bool explicit_pred;
+};
+
+ckv_status run_layer(ckv_ctx* c, const LayerArgs& la, ckv_layer_stats* stats);
+
 }  // namespace
 
 extern "C" {
 
-ckv_status ckv_ctx_create(const ckv_dims* dims, double keep_ratio, int32_t flags, ckv_ctx** out) {
+ckv_status ckv_ctx_create(const ckv_dims* dims, int32_t n_layers, double keep_ratio, int32_t flags,
+                          ckv_ctx** out) {
   clear_error();
   if (!out) CKV_FAIL(CKV_EINVAL, "out is NULL");
   *out = nullptr;
@@ -260,6 +444,7 @@ ckv_status ckv_ctx_create(const ckv_dims* dims, double keep_ratio, int32_t flags
     ckv_status s = check_dims(dims);
     if (s != CKV_OK) return s;
   }
+  if (n_layers < 1) CKV_FAIL(CKV_EINVAL, "n_layers must be >= 1 (got %d)", n_layers);
   if (!(keep_ratio > 0.0 && keep_ratio <= 1.0)) CKV_FAIL(CKV_EINVAL, "keep_ratio must be in (0, 1]");
   if (flags & ~(CKV_CTX_HOST_PREFIX | CKV_CTX_MATERIALIZE | CKV_CTX_STAGE_TIMING |
                 CKV_CTX_SCORE_TIMING))
@@ -267,6 +452,7 @@ ckv_status ckv_ctx_create(const ckv_dims* dims, double keep_ratio, int32_t flags
   ckv_ctx* c = new (std::nothrow) ckv_ctx();
   if (!c) CKV_FAIL(CKV_ENOMEM, "host allocation failed");
   c->dims = *dims;
+  c->n_layers = n_layers;
   c->keep_ratio = keep_ratio;
   c->flags = flags;
   c->m = ckv_num_chunks(dims->n_prefix, dims->chunk_size);
@@ -303,23 +489,11 @@ ckv_status ckv_ctx_create(const ckv_dims* dims, double keep_ratio, int32_t flags
   if (flags & CKV_CTX_HOST_PREFIX) {
     c->slot_bytes = 2 * span;
     c->slots_per_buf = 2 * c->k;  // prefetched chunks plus room for a full miss set
-    CKV_HIP_ALLOC(hipMalloc(&c->arena, (size_t)(2 * c->slots_per_buf * c->slot_bytes)));
-    for (int i = 0; i < 2; ++i) {
-      c->slots[i] = static_cast<char*>(c->arena) + i * c->slots_per_buf * c->slot_bytes;
-      CKV_HIP_ALLOC(hipMalloc((void**)&c->fill_dev[i], (size_t)(2 * c->k) * sizeof(int32_t)));
-      CKV_HIP_ALLOC(hipHostMalloc((void**)&c->fill_host[i], (size_t)(2 * c->k) * sizeof(int32_t),
-                                  hipHostMallocDefault));
-      CKV_HIP_ALLOC(hipMalloc((void**)&c->slot_tab_dev[i], (size_t)c->k * sizeof(int32_t)));
-      CKV_HIP_ALLOC(hipHostMalloc((void**)&c->slot_tab_host[i], (size_t)c->k * sizeof(int32_t),
-                                  hipHostMallocDefault));
-      CKV_HIP_ALLOC(hipMalloc((void**)&c->dem_dev[i], (size_t)c->k * sizeof(int32_t)));
-      CKV_HIP_ALLOC(hipMalloc((void**)&c->pref_dev[i], (size_t)c->k * sizeof(int32_t)));
-      CKV_HIP_ALLOC(hipHostMalloc((void**)&c->dem_host[i], (size_t)c->k * sizeof(int32_t),
-                                  hipHostMallocDefault));
-      CKV_HIP_ALLOC(hipHostMalloc((void**)&c->pref_host[i], (size_t)c->k * sizeof(int32_t),
-                                  hipHostMallocDefault));
-      CKV_HIP_ALLOC(hipEventCreateWithFlags(&c->ev_pref[i], hipEventDisableTiming));
-      CKV_HIP_ALLOC(hipEventCreateWithFlags(&c->ev_attn[i], hipEventDisableTiming));
+    ckv_status s = alloc_buffers(c);
+    if (s == CKV_OK) s = alloc_arena(c, 2, 0);
+    if (s != CKV_OK) {
+      free_ctx(c);
+      return s;
     }
     CKV_HIP_ALLOC(hipHostMalloc((void**)&c->sel_host, (size_t)c->k * sizeof(int32_t),
                                 hipHostMallocDefault));
@@ -357,8 +531,55 @@ ckv_status ckv_ctx_set_period(ckv_ctx* ctx, int32_t period) {
   clear_error();
   if (!ctx) CKV_FAIL(CKV_EINVAL, "ctx is NULL");
   if (period < 1) CKV_FAIL(CKV_EINVAL, "period must be >= 1 (got %d)", period);
+  const int old = ctx->period;
   ctx->period = period;
+  if (wanted_buffers(ctx) != ctx->nbuf) {
+    if (ctx->prev_layer >= 0) {
+      ctx->period = old;
+      CKV_FAIL(CKV_ESTATE, "with registered host stores, set the Period at the start of a request");
+    }
+    ckv_status s = resize_ring(ctx);
+    if (s != CKV_OK) {
+      ctx->period = old;
+      return s;
+    }
+  }
   ctx->period_first = -1;
+  return CKV_OK;
+}
+
+ckv_status ckv_ctx_set_host_layers(ckv_ctx* ctx, const void* const* kv_host, int32_t n) {
+  clear_error();
+  if (!ctx) CKV_FAIL(CKV_EINVAL, "ctx is NULL");
+  if (!(ctx->flags & CKV_CTX_HOST_PREFIX))
+    CKV_FAIL(CKV_EINVAL, "host stores need a context with a host-resident prefix");
+  if (ctx->prev_layer >= 0)
+    CKV_FAIL(CKV_ESTATE, "register host stores at the start of a request (before its first layer)");
+  std::vector<const void*> views;
+  if (kv_host) {
+    if (n != ctx->n_layers)
+      CKV_FAIL(CKV_EINVAL, "%d host stores for a context of %d layers", n, ctx->n_layers);
+    views.resize((size_t)n);
+    for (int32_t l = 0; l < n; ++l) {
+      views[l] = kv_host[l] ? device_view(kv_host[l]) : nullptr;
+      if (!views[l])
+        CKV_FAIL(CKV_EINVAL, "host store of layer %d is not pinned host memory (hipHostMalloc)", l);
+    }
+  }
+  std::swap(ctx->host_layers, views);
+  ckv_status s = resize_ring(ctx);
+  if (s != CKV_OK) std::swap(ctx->host_layers, views);
+  return s;
+}
+
+ckv_status ckv_ctx_inject_copy_error(ckv_ctx* ctx, int32_t layer) {
+  clear_error();
+  if (!ctx) CKV_FAIL(CKV_EINVAL, "ctx is NULL");
+  if (!(ctx->flags & CKV_CTX_HOST_PREFIX))
+    CKV_FAIL(CKV_EINVAL, "copy errors are injected on a host-resident prefix only");
+  if (layer < -1 || layer >= ctx->n_layers)
+    CKV_FAIL(CKV_EINVAL, "layer must be -1 or in [0, %d)", ctx->n_layers);
+  ctx->inject_layer = layer;
   return CKV_OK;
 }
 
@@ -367,8 +588,8 @@ ckv_status ckv_ctx_attach_cache(ckv_ctx* ctx, ckv_cache* cache) {
   if (!ctx) CKV_FAIL(CKV_EINVAL, "ctx is NULL");
   if (!(ctx->flags & CKV_CTX_HOST_PREFIX))
     CKV_FAIL(CKV_EINVAL, "a cache needs a context with a host-resident prefix");
-  if (ctx->next_layer != 0)
-    CKV_FAIL(CKV_ESTATE, "attach a cache at the start of a request (before layer 0 or after a reset)");
+  if (ctx->prev_layer >= 0)
+    CKV_FAIL(CKV_ESTATE, "attach a cache at the start of a request (before its first layer or after a reset)");
   if (ctx->kv_store)
     CKV_FAIL(CKV_ESTATE, "attach the cache before the store (the store's chunk pool holds its tiers)");
   int64_t G = 0;
@@ -379,23 +600,13 @@ ckv_status ckv_ctx_attach_cache(ckv_ctx* ctx, ckv_cache* cache) {
     if (cache_gpu_size(cache) != 0)
       CKV_FAIL(CKV_ESTATE, "the cache's GPU tier must be empty when it is attached");
     G = std::min(cache_gpu_slots(cache), cache_keys(cache));
-    if (2 * ctx->slots_per_buf + G > INT32_MAX)
+    if (kMaxBuf * ctx->slots_per_buf + G > INT32_MAX)
       CKV_FAIL(CKV_EUNSUPPORTED, "too many cache slots (%lld)", (long long)G);
   }
   // the arena is replaced with nothing in flight that could still read it
   CKV_HIP(hipDeviceSynchronize());
-  const size_t bytes = (size_t)((2 * ctx->slots_per_buf + G) * ctx->slot_bytes);
-  void* arena = nullptr;
-  hipError_t e = hipMalloc(&arena, bytes);
-  if (e != hipSuccess) {
-    (void)hipGetLastError();
-    CKV_FAIL(e == hipErrorOutOfMemory ? CKV_ENOMEM : CKV_EHIP, "hipMalloc of %zu bytes of cache slots failed: %s",
-             bytes, hipGetErrorString(e));
-  }
-  CKV_HIP(hipFree(ctx->arena));
-  ctx->arena = arena;
-  for (int i = 0; i < 2; ++i)
-    ctx->slots[i] = static_cast<char*>(arena) + i * ctx->slots_per_buf * ctx->slot_bytes;
+  ckv_status s = alloc_arena(ctx, ctx->nbuf, G);
+  if (s != CKV_OK) return s;
   if (ctx->cache) cache_log_gpu_evictions(ctx->cache, false);
   ctx->cache = cache;
   ctx->cache_slots = G;
@@ -423,8 +634,8 @@ ckv_status ckv_ctx_attach_store(ckv_ctx* ctx, ckv_store* store) {
   if (!ctx) CKV_FAIL(CKV_EINVAL, "ctx is NULL");
   if (!(ctx->flags & CKV_CTX_HOST_PREFIX))
     CKV_FAIL(CKV_EINVAL, "a store needs a context with a host-resident prefix");
-  if (ctx->next_layer != 0)
-    CKV_FAIL(CKV_ESTATE, "attach a store at the start of a request (before layer 0 or after a reset)");
+  if (ctx->prev_layer >= 0)
+    CKV_FAIL(CKV_ESTATE, "attach a store at the start of a request (before its first layer or after a reset)");
   if (store) {
     if (store_span_bytes(store) != ctx->slot_bytes)
       CKV_FAIL(CKV_EINVAL, "store spans of %lld bytes, chunks of %lld", (long long)store_span_bytes(store),
@@ -440,7 +651,7 @@ ckv_status ckv_ctx_attach_store(ckv_ctx* ctx, ckv_store* store) {
   free_pool(ctx);
   ctx->kv_store = nullptr;
   ctx->store_layers = 0;
-  if (!store) return CKV_OK;
+  if (!store) return resize_ring(ctx);
   // room for the cache's tiers, plus the transient chunks of two layers in
   // flight and of the layer whose slots wait for release
   const int64_t keys = store_keys(store), k = ctx->k;
@@ -469,13 +680,14 @@ ckv_status ckv_ctx_attach_store(ckv_ctx* ctx, ckv_store* store) {
   for (int64_t i = n - 1; i >= 0; --i) ctx->pool_free.push_back((int32_t)i);
   ctx->kv_store = store;
   ctx->store_layers = keys / ctx->m;
-  return CKV_OK;
+  return resize_ring(ctx);  // the storage tier runs on two buffers
 }
 
 ckv_status ckv_ctx_reset(ckv_ctx* ctx) {
   clear_error();
   if (!ctx) CKV_FAIL(CKV_EINVAL, "ctx is NULL");
   if (ctx->prefetch) CKV_HIP(hipStreamSynchronize(ctx->prefetch));
+  if (ctx->demand) CKV_HIP(hipStreamSynchronize(ctx->demand));
   drain_store_reads(ctx);
   if (ctx->kv_store) {
     // predictions read for a layer that will not run: release their slots
@@ -489,10 +701,15 @@ ckv_status ckv_ctx_reset(ckv_ctx* ctx) {
       a.keys.clear();
     }
   }
-  ctx->pred.clear();
-  ctx->pref_pending[0] = ctx->pref_pending[1] = false;
-  ctx->next_layer = 0;
+  for (SlotBuf& B : ctx->buf) {
+    B.pred_layer = -1;
+    B.pred.clear();
+    B.pref_pending = false;
+  }
+  ctx->prev_layer = -1;
   ctx->period_first = -1;
+  ctx->broken = false;
+  ctx->inject_layer = -1;
   while (ctx->t_done < ctx->t_issued) {
     ckv_status s = harvest_one(ctx);
     if (s != CKV_OK) return s;
@@ -506,50 +723,86 @@ ckv_status ckv_reprefill_layer(ckv_ctx* c, int32_t layer, const ckv_layer_io* io
                                ckv_layer_stats* stats) {
   clear_error();
   if (!c || !io) CKV_FAIL(CKV_EINVAL, "NULL ctx or io");
-  const ckv_dims* d = &c->dims;
+  if (c->broken)
+    CKV_FAIL(CKV_ESTATE, "an earlier layer failed after enqueueing work: reset the context first");
   const bool host = c->flags & CKV_CTX_HOST_PREFIX;
-  const void* store = nullptr;       // kv_host as the device reads it
-  const void* store_next = nullptr;  // kv_host_next as the device reads it
+  if (layer < 0 || layer >= c->n_layers)
+    CKV_FAIL(CKV_EINVAL, "layer must be in [0, %d) (got %d)", c->n_layers, layer);
   if (!io->q || !io->k_suffix || !io->v_suffix || !io->k_probe || !io->out)
     CKV_FAIL(CKV_EINVAL, "NULL tensor in io");
   if (!aligned16(io->q) || !aligned16(io->k_suffix) || !aligned16(io->v_suffix) ||
       !aligned16(io->k_probe) || !aligned16(io->out))
     CKV_FAIL(CKV_EINVAL, "tensors must be 16-byte aligned");
+  LayerArgs la{layer, io, nullptr, nullptr, io->pred_idx != nullptr};
+  if (la.explicit_pred) {
+    if (io->n_pred < 0 || io->n_pred > c->k)
+      CKV_FAIL(CKV_EINVAL, "n_pred must be in [0, k = %lld] (got %lld)", (long long)c->k,
+               (long long)io->n_pred);
+    for (int64_t u = 0; u < io->n_pred; ++u) {
+      const int32_t j = io->pred_idx[u];
+      if (j < 0 || j >= c->m || (u > 0 && j <= io->pred_idx[u - 1]))
+        CKV_FAIL(CKV_EINVAL, "pred_idx must be strictly ascending chunk indices in [0, %lld)",
+                 (long long)c->m);
+    }
+  }
   const bool stored = host && c->kv_store;  // chunks come from the storage tier
-  if (stored) {
-    if (layer != c->next_layer)
+  if (host) {
+    if (c->prev_layer >= 0 && layer != c->prev_layer + 1)
       CKV_FAIL(CKV_ESTATE, "host-resident layers must run in order (expected %d, got %d)",
-               c->next_layer, layer);
+               c->prev_layer + 1, layer);
+  }
+  if (stored) {
     if (layer >= c->store_layers)
       CKV_FAIL(CKV_EINVAL, "layer %d is not in the attached store (%lld layers)", layer,
                (long long)c->store_layers);
+    if (la.explicit_pred)
+      CKV_FAIL(CKV_EUNSUPPORTED, "a caller prediction with an attached store is not supported");
   } else if (host) {
-    if (!io->kv_host) CKV_FAIL(CKV_EINVAL, "host-resident prefix needs kv_host");
-    if (layer != c->next_layer)
-      CKV_FAIL(CKV_ESTATE, "host-resident layers must run in order (expected %d, got %d)",
-               c->next_layer, layer);
     // the copy kernels read the stores through the device's mapping of them
-    store = device_view(io->kv_host);
-    if (!store) CKV_FAIL(CKV_EINVAL, "kv_host must be pinned host memory (hipHostMalloc)");
-    if (io->kv_host_next) {
-      store_next = device_view(io->kv_host_next);
-      if (!store_next) CKV_FAIL(CKV_EINVAL, "kv_host_next must be pinned host memory (hipHostMalloc)");
+    if (io->kv_host) {
+      la.store = device_view(io->kv_host);
+      if (!la.store) CKV_FAIL(CKV_EINVAL, "kv_host must be pinned host memory (hipHostMalloc)");
+    } else if (!c->host_layers.empty()) {
+      la.store = c->host_layers[layer];
+    } else {
+      CKV_FAIL(CKV_EINVAL, "host-resident prefix needs kv_host (or registered host stores)");
+    }
+    if (!c->host_layers.empty()) {
+      la.store_next = layer + 1 < c->n_layers ? c->host_layers[layer + 1] : nullptr;
+    } else if (io->kv_host_next && layer + 1 < c->n_layers) {
+      la.store_next = device_view(io->kv_host_next);
+      if (!la.store_next) CKV_FAIL(CKV_EINVAL, "kv_host_next must be pinned host memory (hipHostMalloc)");
     }
   } else {
     if (!io->k_prefix || !io->v_prefix) CKV_FAIL(CKV_EINVAL, "HBM-resident prefix needs k/v_prefix");
     if (!aligned16(io->k_prefix) || !aligned16(io->v_prefix))
       CKV_FAIL(CKV_EINVAL, "tensors must be 16-byte aligned");
   }
-  if (layer < 0) CKV_FAIL(CKV_EINVAL, "layer must be >= 0 (got %d)", layer);
   if (host && c->cache && layer >= c->cache_layers)
     CKV_FAIL(CKV_EINVAL, "layer %d has no keys in the attached cache (%lld layers)", layer,
              (long long)c->cache_layers);
   // a layer past the first of its Period reuses the set selected there
   const int32_t first = layer - layer % c->period;
-  const bool reuse = first != layer;
-  if (reuse && c->period_first != first)
+  if (first != layer && c->period_first != first)
     CKV_FAIL(CKV_ESTATE, "layer %d reuses the set of layer %d, the first of its Period, which has not run",
              layer, first);
+  const ckv_status s = run_layer(c, la, stats);
+  if (s != CKV_OK) c->broken = true;
+  return s;
+}
+
+}  // extern "C"
+
+namespace {
+
+ckv_status run_layer(ckv_ctx* c, const LayerArgs& la, ckv_layer_stats* stats) {
+  const ckv_layer_io* io = la.io;
+  const int32_t layer = la.layer;
+  const ckv_dims* d = &c->dims;
+  const bool host = c->flags & CKV_CTX_HOST_PREFIX;
+  const bool stored = host && c->kv_store;
+  const int32_t first = layer - layer % c->period;
+  const bool reuse = first != layer;
   hipStream_t st = (hipStream_t)io->stream;
   char* ws = static_cast<char*>(c->ws);
   double* scores = io->chunk_scores ? io->chunk_scores : reinterpret_cast<double*>(ws + c->off_scores);
@@ -559,12 +812,25 @@ ckv_status ckv_reprefill_layer(ckv_ctx* c, int32_t layer, const ckv_layer_io* io
   const int64_t k = c->k;
   const int eb = elem_bytes(d->dtype);
   const int64_t span_elems = (int64_t)d->chunk_size * d->n_kv_heads * d->head_dim;
+  ckv_layer_stats stv{};
+  stv.k = k;
+  ckv_status s = CKV_OK;
+
+  // a caller prediction for this pinned-host layer: its copy goes out first,
+  // beside this layer's scoring
+  const int cur = host ? layer % c->nbuf : 0;
+  if (host && !stored && la.explicit_pred) {
+    std::vector<int32_t> P;
+    uncached(c, layer, io->pred_idx, io->n_pred, P);
+    s = queue_prefetch(c, cur, layer, la.store, P, false, &stv.bytes_prefetch);
+    if (s != CKV_OK) return s;
+  }
 
   hipEvent_t* tev = nullptr;
   // a reused layer has no scoring kernel to time alone
   if ((c->flags & CKV_CTX_STAGE_TIMING) || ((c->flags & CKV_CTX_SCORE_TIMING) && !reuse)) {
     if (c->t_issued - c->t_done >= ckv_ctx::kRing) {  // reuse the oldest set: account it first
-      ckv_status s = harvest_one(c);
+      s = harvest_one(c);
       if (s != CKV_OK) return s;
     }
     tev = c->tev[c->t_issued % ckv_ctx::kRing];
@@ -577,7 +843,6 @@ ckv_status ckv_reprefill_layer(ckv_ctx* c, int32_t layer, const ckv_layer_io* io
     return CKV_OK;
   };
 
-  ckv_status s = CKV_OK;
   if (!reuse) {
     const bool bracket = tev && !all_stages(c) && d->dtype == CKV_DTYPE_BF16;
     s = launch_score(d, io->q, io->k_probe, scores, ws, c->ws_score, st, tev ? tev[1] : nullptr,
@@ -600,16 +865,14 @@ ckv_status ckv_reprefill_layer(ckv_ctx* c, int32_t layer, const ckv_layer_io* io
     if ((s = mark(3)) != CKV_OK) return s;
   }
 
-  ckv_layer_stats stv{};
-  stv.k = k;
   if (!host) {
-    ChunkSource src{io->k_prefix, io->v_prefix, span_elems, nullptr, 1};
+    ChunkSource src{io->k_prefix, io->v_prefix, span_elems, nullptr, 1, c->m};
     if (c->flags & CKV_CTX_MATERIALIZE) {
       void* ksel = ws + c->off_ksel;
       void* vsel = ws + c->off_vsel;
       s = launch_gather(d, io->k_prefix, io->v_prefix, sel, k, ksel, vsel, st);
       if (s != CKV_OK) return s;
-      src = ChunkSource{ksel, vsel, span_elems, nullptr, 0};
+      src = ChunkSource{ksel, vsel, span_elems, nullptr, 0, k};
     }
     if ((s = mark(4)) != CKV_OK) return s;
     s = launch_attn(d, io->q, src, sel, k, io->k_suffix, io->v_suffix, io->out, ws + c->off_attn,
@@ -620,17 +883,19 @@ ckv_status ckv_reprefill_layer(ckv_ctx* c, int32_t layer, const ckv_layer_io* io
     // K+V bytes of k full chunks (the set stays on the device, so a short last
     // chunk, if kept, is counted at full length)
     stv.bytes_gathered = 2 * k * span_elems * eb;
+    c->prev_layer = layer;
     if (stats) *stats = stv;
     return CKV_OK;
   }
 
   // ---- host-resident prefix ------------------------------------------------
-  const int cur = layer & 1, nxt = cur ^ 1;
+  SlotBuf& B = c->buf[cur];
   const bool cached = c->cache != nullptr;
   const int64_t key0 = (int64_t)layer * c->m;
   const int64_t spb = c->slots_per_buf;
-  const int64_t buf0 = cur * spb, cache0 = 2 * spb;
+  const int64_t buf0 = cur * spb, cache0 = c->nbuf * spb;
   ckv_ctx::Ahead& mine = c->ahead[layer % ckv_ctx::kAhead];
+  std::vector<int32_t> P;  // this layer's predicted chunks, in slots 0..|P|-1 of its buffer
   if (stored) {  // this layer's prediction: read (or queued) during earlier layers
     if (mine.layer != layer) {
       mine.layer = -1;
@@ -642,40 +907,37 @@ ckv_status ckv_reprefill_layer(ckv_ctx* c, int32_t layer, const ckv_layer_io* io
       mine.ticket = 0;
       if (s != CKV_OK) return s;
     }
-    c->pred = mine.chunks;
-  }
-  if (stored && !mine.keys.empty()) {
-    // the predicted chunks (read from the store, or already in the pool) move
-    // to this layer's HBM slots 0..|P|-1 on the prefetch stream, beside this
-    // layer's scoring; this buffer's copy lists were last read two layers ago
-    const std::vector<int64_t>& pk = mine.keys;
-    const int64_t np = (int64_t)pk.size();
-    c->xsrc.resize((size_t)np);
-    c->xdst.resize((size_t)np);
-    for (int64_t i = 0; i < np; ++i) {
-      c->xsrc[i] = c->pool_of[pk[i]];
-      c->xdst[i] = (int32_t)(buf0 + i);
-      if (c->xsrc[i] < 0) CKV_FAIL(CKV_ESTATE, "predicted chunk not in the pool (internal)");
+    // a predicted chunk whose pool slot was released since it was listed (the
+    // cache sent it out of memory at an intervening layer) is fetched on
+    // demand like any miss
+    c->xsrc.clear();
+    c->xdst.clear();
+    for (size_t i = 0; i < mine.chunks.size(); ++i) {
+      const int32_t sl = c->pool_of[mine.keys[i]];
+      if (sl < 0) continue;
+      c->xsrc.push_back(sl);
+      c->xdst.push_back((int32_t)(buf0 + P.size()));
+      P.push_back(mine.chunks[i]);
     }
-    if (c->attn_recorded[cur]) {
-      CKV_HIP(hipEventSynchronize(c->ev_attn[cur]));
-      CKV_HIP(hipStreamWaitEvent(c->prefetch, c->ev_attn[cur], 0));
+    if (!P.empty()) {
+      // the predicted chunks move to this layer's HBM slots 0..|P|-1 on the
+      // prefetch stream, beside this layer's scoring
+      if (B.attn_rec) CKV_HIP(hipStreamWaitEvent(c->prefetch, B.ev_attn, 0));
+      CKV_HIP(hipStreamWaitEvent(c->prefetch, c->ev_dem, 0));
+      s = pool_copy(c, cur, 0, c->xsrc.data(), c->xdst.data(), (int64_t)P.size(), c->prefetch);
+      if (s != CKV_OK) return s;
+      CKV_HIP(hipEventRecord(B.ev_pref, c->prefetch));
+      B.pref_pending = true;
     }
-    CKV_HIP(hipStreamWaitEvent(c->prefetch, c->ev_dem, 0));
-    s = pool_copy(c, cur, 0, c->xsrc.data(), c->xdst.data(), np, c->prefetch);
-    if (s != CKV_OK) return s;
-    CKV_HIP(hipEventRecord(c->ev_pref[cur], c->prefetch));
-    c->pref_pending[cur] = true;
-    c->pref_recorded[cur] = true;
+  } else if (B.pred_layer == layer) {
+    P = B.pred;
   }
   if (reuse) {  // the Period's set is already on the host: no synchronisation
-    if (cached || stored) {
-      // the host staging written below was last read by the copies of two
-      // layers ago (and the prefetch list, or the store's staging buffer, by
-      // the previous layer's); their contents differ from layer to layer
-      if (c->attn_recorded[cur]) CKV_HIP(hipEventSynchronize(c->ev_attn[cur]));
-      if (c->pref_recorded[nxt]) CKV_HIP(hipEventSynchronize(c->ev_pref[nxt]));
-      if (stored && c->attn_recorded[nxt]) CKV_HIP(hipEventSynchronize(c->ev_attn[nxt]));
+    if (stored) {
+      // pool slots released by the previous layer are reused below: its copies
+      // out of them must have finished
+      const SlotBuf& Bn = c->buf[(layer + c->nbuf - 1) % c->nbuf];
+      if (Bn.attn_rec) CKV_HIP(hipEventSynchronize(Bn.ev_attn));
     }
     std::memcpy(c->sel_host, c->pset_host.data(), (size_t)k * sizeof(int32_t));
   } else {
@@ -701,16 +963,16 @@ ckv_status ckv_reprefill_layer(ckv_ctx* c, int32_t layer, const ckv_layer_io* io
   // slot table, in arena slots: chunks held in the cache's HBM slots are read
   // there; predicted chunks sit in this layer's buffer at slots 0..|P|-1 (in P
   // order), misses follow
-  const std::vector<int32_t>& P = c->pred;
+  if ((s = guard(B.ev_gd, B.gd)) != CKV_OK) return s;
   std::vector<int32_t> miss;
   miss.reserve((size_t)k);
-  int32_t* tab = c->slot_tab_host[cur];
+  int32_t* tab = B.tab_host;
   size_t pi = 0;
   int64_t hits = 0;
   for (int64_t u = 0; u < k; ++u) {
     const int32_t j = c->sel_host[u];
-    const int64_t chunk_bytes = 2 * chunk_len(d, j) * d->n_kv_heads * d->head_dim * eb;
-    stv.bytes_gathered += chunk_bytes;
+    const int64_t cb = chunk_bytes(c, j);
+    stv.bytes_gathered += cb;
     if (cached && c->slot_of[key0 + j] >= 0) {
       tab[u] = (int32_t)(cache0 + c->slot_of[key0 + j]);
       ++stv.cache_hits;
@@ -723,24 +985,23 @@ ckv_status ckv_reprefill_layer(ckv_ctx* c, int32_t layer, const ckv_layer_io* io
     } else {
       tab[u] = (int32_t)(buf0 + P.size() + miss.size());
       miss.push_back(j);
-      stv.bytes_demand += chunk_bytes;
+      stv.bytes_demand += cb;
     }
   }
   stv.hits = hits;
   stv.misses = (int64_t)miss.size();
   stv.wasted = (int64_t)P.size() - hits;
-  // misses follow the predicted chunks in this layer's buffer (c->pred is
-  // replaced by the next layer's prediction below)
   const int64_t n_pred = (int64_t)P.size();
 
   // storage tier: the pool slots the misses move from; those not in the pool
   // get free slots and are read from the file below
   c->io_keys.clear();  // this layer's demand reads (none without misses)
   c->io_dst.clear();
+  std::vector<int32_t> msrc, mdst;
   if (stored && !miss.empty()) {
     const size_t nm = miss.size();
-    c->xsrc.resize(nm);
-    c->xdst.resize(nm);
+    msrc.resize(nm);
+    mdst.resize(nm);
     for (size_t i = 0; i < nm; ++i) {
       const int64_t x = key0 + miss[i];
       if (c->pool_of[x] < 0) {
@@ -748,8 +1009,8 @@ ckv_status ckv_reprefill_layer(ckv_ctx* c, int32_t layer, const ckv_layer_io* io
         c->io_keys.push_back(x);
         c->io_dst.push_back(c->pool + (int64_t)c->pool_of[x] * c->slot_bytes);
       }
-      c->xsrc[i] = c->pool_of[x];
-      c->xdst[i] = (int32_t)(buf0 + n_pred + i);
+      msrc[i] = c->pool_of[x];
+      mdst[i] = (int32_t)(buf0 + n_pred + i);
     }
   }
   // the storage tier's demand reads start now; the layer waits for them below
@@ -761,6 +1022,26 @@ ckv_status ckv_reprefill_layer(ckv_ctx* c, int32_t layer, const ckv_layer_io* io
     stv.bytes_storage += (int64_t)c->io_keys.size() * c->slot_bytes;
   }
 
+  // The layer's own set is known: the rest of a Period is predicted exactly.
+  // With intra-period prefetch the first layer of a Period queues the copies of
+  // every later layer of the Period (behind its own demand copies) before its
+  // attention goes out, so that the SubPeriod gate can wait for them.
+  const bool pw = period_wide(c) && !reuse && c->period > 1;
+  int32_t gate_layer = -1;
+  auto period_prefetch = [&]() -> ckv_status {
+    if (!pw) return CKV_OK;
+    const int32_t last = std::min<int32_t>(first + c->period - 1, c->n_layers - 1);
+    std::vector<int32_t> Pt;
+    for (int32_t t = layer + 1; t <= last; ++t) {
+      uncached(c, t, c->sel_host, k, Pt);
+      ckv_status r = queue_prefetch(c, t % c->nbuf, t, c->host_layers[t], Pt, true,
+                                    &stv.bytes_prefetch);
+      if (r != CKV_OK) return r;
+    }
+    if (c->subperiod > 1) gate_layer = std::min<int32_t>(layer + c->subperiod - 1, last);
+    return CKV_OK;
+  };
+
   // demand copies into this layer's buffer (after the attention that last used
   // it; from the pool once its reads have landed), then the attention.  The
   // small index copies go first, so they never queue behind span copies.
@@ -769,27 +1050,41 @@ ckv_status ckv_reprefill_layer(ckv_ctx* c, int32_t layer, const ckv_layer_io* io
       ckv_status w = store_wait(c->kv_store, dem_ticket);
       if (w != CKV_OK) return w;
     }
-    if (c->attn_recorded[cur]) CKV_HIP(hipStreamWaitEvent(c->demand, c->ev_attn[cur], 0));
-    CKV_HIP(hipMemcpyAsync(c->slot_tab_dev[cur], tab, (size_t)k * sizeof(int32_t),
-                           hipMemcpyHostToDevice, c->demand));
+    if (c->inject_layer == layer) {  // test hook: the copy enqueue fails here
+      c->inject_layer = -1;
+      CKV_FAIL(CKV_EHIP, "injected host-to-HBM copy failure at layer %d", layer);
+    }
+    if (B.attn_rec) CKV_HIP(hipStreamWaitEvent(c->demand, B.ev_attn, 0));
+    CKV_HIP(hipMemcpyAsync(B.tab_dev, tab, (size_t)k * sizeof(int32_t), hipMemcpyHostToDevice,
+                           c->demand));
     ckv_status r = CKV_OK;
     if (!miss.empty() && stored) {
-      r = pool_copy(c, cur, 1, c->xsrc.data(), c->xdst.data(), (int64_t)miss.size(), c->demand);
+      r = pool_copy(c, cur, 1, msrc.data(), mdst.data(), (int64_t)miss.size(), c->demand);
     } else if (!miss.empty()) {
-      std::memcpy(c->dem_host[cur], miss.data(), miss.size() * sizeof(int32_t));
-      CKV_HIP(hipMemcpyAsync(c->dem_dev[cur], c->dem_host[cur], miss.size() * sizeof(int32_t),
+      std::memcpy(B.dem_host, miss.data(), miss.size() * sizeof(int32_t));
+      CKV_HIP(hipMemcpyAsync(B.dem_dev, B.dem_host, miss.size() * sizeof(int32_t),
                              hipMemcpyHostToDevice, c->demand));
-      r = launch_copy_spans(store, c->dem_dev[cur], (int64_t)miss.size(), n_pred, c->slots[cur],
+      CKV_HIP(hipEventRecord(B.ev_gd, c->demand));
+      B.gd = true;
+      r = launch_copy_spans(la.store, B.dem_dev, (int64_t)miss.size(), n_pred, B.slots,
                             c->slot_bytes, c->demand);
+    } else {
+      CKV_HIP(hipEventRecord(B.ev_gd, c->demand));
+      B.gd = true;
     }
     if (r != CKV_OK) return r;
     CKV_HIP(hipEventRecord(c->ev_dem, c->demand));
+    if ((r = period_prefetch()) != CKV_OK) return r;
     CKV_HIP(hipStreamWaitEvent(st, c->ev_dem, 0));
-    if (c->pref_pending[cur]) CKV_HIP(hipStreamWaitEvent(st, c->ev_pref[cur], 0));
-    c->pref_pending[cur] = false;
+    if (B.pref_pending) CKV_HIP(hipStreamWaitEvent(st, B.ev_pref, 0));
+    B.pref_pending = false;
+    if (gate_layer > layer) {  // SubPeriod gate: the Period's first layers are in HBM
+      SlotBuf& Bg = c->buf[gate_layer % c->nbuf];
+      CKV_HIP(hipStreamWaitEvent(st, Bg.ev_pref, 0));
+    }
     if ((r = mark(4)) != CKV_OK) return r;
     ChunkSource src{c->arena, static_cast<char*>(c->arena) + span_elems * eb, 2 * span_elems,
-                    c->slot_tab_dev[cur], 0};
+                    B.tab_dev, 0, c->nbuf * spb + c->cache_slots};
     r = launch_attn(d, io->q, src, sel, k, io->k_suffix, io->v_suffix, io->out, ws + c->off_attn,
                     c->ws_attn, st);
     if (r != CKV_OK) return r;
@@ -807,6 +1102,7 @@ ckv_status ckv_reprefill_layer(ckv_ctx* c, int32_t layer, const ckv_layer_io* io
   // go on the stream after the attention that reads both.
   int64_t nf = 0;
   if (cached) {
+    if ((s = guard(B.ev_gf, B.gf)) != CKV_OK) return s;
     c->keys.resize((size_t)k);
     c->key_scores.resize((size_t)k);
     for (int64_t u = 0; u < k; ++u) {
@@ -826,7 +1122,7 @@ ckv_status ckv_reprefill_layer(ckv_ctx* c, int32_t layer, const ckv_layer_io* io
         c->free_slots.push_back(c->slot_of[x]);
         c->slot_of[x] = -1;
       }
-    int32_t* fill = c->fill_host[cur];
+    int32_t* fill = B.fill_host;
     for (int64_t u = 0; u < k; ++u) {
       const int64_t x = c->keys[u];
       if (cache_tier(c->cache, x) != CKV_TIER_GPU || c->slot_of[x] >= 0) continue;
@@ -856,104 +1152,85 @@ ckv_status ckv_reprefill_layer(ckv_ctx* c, int32_t layer, const ckv_layer_io* io
     mine.keys.clear();
   }
 
-  // the next layer's prediction (P_{l+1} = S_l) less the chunks it will find in
-  // the cache's HBM slots
-  c->pred.clear();
-  const bool has_next = stored ? layer + 1 < c->store_layers : io->kv_host_next != nullptr;
-  const int64_t nkey0 = (int64_t)(layer + 1) * c->m;
-  if (has_next) {
-    const bool next_cached = cached && layer + 1 < c->cache_layers;
-    for (int64_t u = 0; u < k; ++u) {
-      const int32_t j = c->sel_host[u];
-      if (next_cached && c->slot_of[nkey0 + j] >= 0) continue;
-      c->pred.push_back(j);
-    }
-    if (!stored)  // the storage tier counts what it queues, below
-      for (int32_t j : c->pred)
-        stv.bytes_prefetch += 2 * chunk_len(d, j) * d->n_kv_heads * d->head_dim * eb;
-  }
-  const int64_t np = (int64_t)c->pred.size();
-
-  if (stored) {
-    // the next layer's prediction joins the I/O threads' queue behind this
+  const bool has_next = stored ? layer + 1 < c->store_layers : la.store_next != nullptr;
+  if (stored && has_next) {
+    // the next layer's prediction (P_{l+1} = S_l, less the chunks it will find
+    // in the cache's HBM slots) joins the I/O threads' queue behind this
     // layer's demand reads and runs on while this layer attends and the next
-    // one scores
-    if (has_next) {
-      // layers last_ahead..: inside a Period with a SubPeriod of sp layers,
-      // every layer up to sp - 1 ahead (their set is this one); otherwise the
-      // next layer only (speculative across a Period boundary)
-      int64_t last_ahead = layer + 1;
-      if (c->period > 1 && c->subperiod > 1) {
-        const int64_t period_end = first + c->period - 1;
-        last_ahead = std::max<int64_t>(last_ahead, std::min<int64_t>(layer + c->subperiod - 1, period_end));
+    // one scores.  Layers last_ahead..: inside a Period with a SubPeriod of sp
+    // layers, every layer up to sp - 1 ahead (their set is this one);
+    // otherwise the next layer only (speculative across a Period boundary)
+    int64_t last_ahead = layer + 1;
+    if (c->period > 1 && c->subperiod > 1) {
+      const int64_t period_end = first + c->period - 1;
+      last_ahead = std::max<int64_t>(last_ahead, std::min<int64_t>(layer + c->subperiod - 1, period_end));
+    }
+    last_ahead = std::min<int64_t>(last_ahead, c->store_layers - 1);
+    for (int64_t t = layer + 1; t <= last_ahead; ++t) {
+      ckv_ctx::Ahead& a = c->ahead[t % ckv_ctx::kAhead];
+      if (a.layer == t) continue;  // queued by an earlier layer of the Period
+      if (a.layer >= 0) CKV_FAIL(CKV_ESTATE, "prediction ring overrun (internal)");
+      a.layer = (int32_t)t;
+      a.chunks.clear();
+      a.keys.clear();
+      c->io_keys.clear();
+      c->io_dst.clear();
+      const int64_t tkey0 = t * c->m;
+      const bool t_cached = cached && t < c->cache_layers;
+      for (int64_t u = 0; u < k; ++u) {
+        const int32_t j = c->sel_host[u];
+        const int64_t x = tkey0 + j;
+        if (t_cached && c->slot_of[x] >= 0) continue;
+        a.chunks.push_back(j);
+        a.keys.push_back(x);
+        stv.bytes_prefetch += chunk_bytes(c, j);
+        if (c->pool_of[x] >= 0) continue;
+        if (pool_take(c, x) < 0) CKV_FAIL(CKV_ESTATE, "chunk pool exhausted (internal)");
+        c->io_keys.push_back(x);
+        c->io_dst.push_back(c->pool + (int64_t)c->pool_of[x] * c->slot_bytes);
       }
-      last_ahead = std::min<int64_t>(last_ahead, c->store_layers - 1);
-      for (int64_t t = layer + 1; t <= last_ahead; ++t) {
-        ckv_ctx::Ahead& a = c->ahead[t % ckv_ctx::kAhead];
-        if (a.layer == t) continue;  // queued by an earlier layer of the Period
-        if (a.layer >= 0) CKV_FAIL(CKV_ESTATE, "prediction ring overrun (internal)");
-        a.layer = (int32_t)t;
-        a.chunks.clear();
-        a.keys.clear();
-        c->io_keys.clear();
-        c->io_dst.clear();
-        const int64_t tkey0 = t * c->m;
-        const bool t_cached = cached && t < c->cache_layers;
-        for (int64_t u = 0; u < k; ++u) {
-          const int32_t j = c->sel_host[u];
-          const int64_t x = tkey0 + j;
-          if (t_cached && c->slot_of[x] >= 0) continue;
-          a.chunks.push_back(j);
-          a.keys.push_back(x);
-          stv.bytes_prefetch += 2 * chunk_len(d, j) * d->n_kv_heads * d->head_dim * eb;
-          if (c->pool_of[x] >= 0) continue;
-          if (pool_take(c, x) < 0) CKV_FAIL(CKV_ESTATE, "chunk pool exhausted (internal)");
-          c->io_keys.push_back(x);
-          c->io_dst.push_back(c->pool + (int64_t)c->pool_of[x] * c->slot_bytes);
-        }
-        if (!c->io_keys.empty()) {
-          s = store_submit(c->kv_store, c->io_keys.data(), (int64_t)c->io_keys.size(), c->io_dst.data(),
-                           &a.ticket);
-          if (s != CKV_OK) return s;
-          stv.bytes_storage += (int64_t)c->io_keys.size() * c->slot_bytes;
-        }
+      if (!c->io_keys.empty()) {
+        s = store_submit(c->kv_store, c->io_keys.data(), (int64_t)c->io_keys.size(), c->io_dst.data(),
+                         &a.ticket);
+        if (s != CKV_OK) return s;
+        stv.bytes_storage += (int64_t)c->io_keys.size() * c->slot_bytes;
       }
     }
-    if ((s = demand_and_attention()) != CKV_OK) return s;
   }
+  if (stored && (s = demand_and_attention()) != CKV_OK) return s;
 
   if (nf > 0) {  // chunks entering the GPU tier, after the attention that read their slots
-    CKV_HIP(hipMemcpyAsync(c->fill_dev[cur], c->fill_host[cur], (size_t)(2 * k) * sizeof(int32_t),
+    CKV_HIP(hipMemcpyAsync(B.fill_dev, B.fill_host, (size_t)(2 * k) * sizeof(int32_t),
                            hipMemcpyHostToDevice, st));
-    s = launch_copy_slots(c->arena, c->fill_dev[cur], c->arena, c->fill_dev[cur] + k, nf,
-                          c->slot_bytes, st);
+    CKV_HIP(hipEventRecord(B.ev_gf, st));
+    B.gf = true;
+    s = launch_copy_slots(c->arena, B.fill_dev, c->arena, B.fill_dev + k, nf, c->slot_bytes, st);
     if (s != CKV_OK) return s;
     stv.bytes_cache_fill = nf * c->slot_bytes;
   }
   // after the cache fills too: they read this layer's buffer
-  CKV_HIP(hipEventRecord(c->ev_attn[cur], st));
-  c->attn_recorded[cur] = true;
+  CKV_HIP(hipEventRecord(B.ev_attn, st));
+  B.attn_rec = true;
+  B.pred_layer = -1;  // consumed
+  B.pred.clear();
 
-  if (has_next && !stored) {  // the next layer's copy, over the host link on the side stream
-    if (c->attn_recorded[nxt]) CKV_HIP(hipStreamWaitEvent(c->prefetch, c->ev_attn[nxt], 0));
-    // after this layer's demand copies: those are on the critical path and get
-    // the host link to themselves
-    CKV_HIP(hipStreamWaitEvent(c->prefetch, c->ev_dem, 0));
-    if (np > 0) {
-      std::memcpy(c->pref_host[nxt], c->pred.data(), (size_t)np * sizeof(int32_t));
-      CKV_HIP(hipMemcpyAsync(c->pref_dev[nxt], c->pref_host[nxt], (size_t)np * sizeof(int32_t),
-                             hipMemcpyHostToDevice, c->prefetch));
-      s = launch_copy_spans(store_next, c->pref_dev[nxt], np, 0, c->slots[nxt], c->slot_bytes,
-                            c->prefetch);
+  // the next layer's copy over the host link on the side stream, unless the
+  // Period's prefetch has already queued it: P_{l+1} = S_l less the chunks the
+  // next layer will find in the cache's HBM slots (after this layer's cache
+  // decisions)
+  if (!stored && has_next) {
+    const int32_t t = layer + 1;
+    const int bn = t % c->nbuf;
+    if (c->buf[bn].pred_layer != t) {
+      std::vector<int32_t> Pn;
+      uncached(c, t, c->sel_host, k, Pn);
+      s = queue_prefetch(c, bn, t, la.store_next, Pn, true, &stv.bytes_prefetch);
       if (s != CKV_OK) return s;
     }
-    CKV_HIP(hipEventRecord(c->ev_pref[nxt], c->prefetch));
-    c->pref_pending[nxt] = true;
-    c->pref_recorded[nxt] = true;
   }
-  c->next_layer = layer + 1;
+  c->prev_layer = layer;
   if (stats) *stats = stv;
   return CKV_OK;
 }
 
-}  // extern "C"
+}  // namespace

@@ -71,24 +71,47 @@ def rel_err(a: np.ndarray, ref: np.ndarray) -> float:
     return float(np.max(np.abs(a - ref) / np.maximum(np.abs(ref), max(floor, 1e-300))))
 
 
-def check_set(A_ref: np.ndarray, sel_gpu: np.ndarray, k: int, err: float) -> bool:
-    """Certified comparison of a top-k set (returns True when certified).
+# Relative score error allowed on the seeded workloads.  The arithmetic bounds
+# a chunk score's error by ~2e-6 (fp32 logits, exp2 and per-chunk partials
+# over at most one chunk, every cross-row sum in fp64); what the seeded
+# workloads achieve is 2e-9 .. 6e-9, so they are held to 1e-7 and a loss of
+# accuracy shows.  The worst-case bound is kept for inputs built to sit at
+# the edge of fp32's range (the forced exact-recompute cases).
+# The small shapes of the unit tests sum a chunk's score over few rows and
+# tokens (20 rows of 4-token chunks in the smallest), so per-term rounding
+# (fp32 exp2 within ~2 ulp, fp32 logits) does not average out: they are held
+# to 4e-7, about three fp32 ulps of one term.
+SCORE_RTOL = 1e-7
+SCORE_RTOL_UNIT = 4e-7
+SCORE_RTOL_BOUND = 2e-6
+
+
+def check_set(A_ref: np.ndarray, sel_gpu: np.ndarray, k: int, err: float, require: bool = True) -> dict:
+    """Certified comparison of a top-k set.
 
     With e the measured relative score error: if A_ref(k) (1-e) > A_ref(k+1) (1+e)
     the set is certified and must equal the oracle's exactly; otherwise every
     chunk in the symmetric difference must have its oracle score inside the
-    uncertainty band [A_ref(k+1)(1-e), A_ref(k)(1+e)]."""
+    uncertainty band [A_ref(k+1)(1-e), A_ref(k)(1+e)].  With require=True an
+    uncertified set fails the test (with its gap/error ratio).  Returns
+    {"certified", "gap_over_err", "equal"}."""
     sel_ref = oracle.select_topk(A_ref, k)
     order = np.lexsort((np.arange(A_ref.size), -A_ref))
     kth = A_ref[order[k - 1]]
     nxt = A_ref[order[k]] if k < A_ref.size else -np.inf
     e = max(err, 1e-15)
-    certified = kth * (1 - e) > nxt * (1 + e)
+    certified = bool(kth * (1 - e) > nxt * (1 + e))
+    gap = float((kth - nxt) / kth) if np.isfinite(nxt) and kth > 0 else float("inf")
+    ratio = gap / e
+    equal = bool(np.array_equal(np.sort(sel_gpu), sel_ref))
     if certified:
-        assert np.array_equal(np.sort(sel_gpu), sel_ref), "certified set differs"
-        return True
-    diff = set(sel_gpu.tolist()) ^ set(sel_ref.tolist())
-    lo, hi = nxt * (1 - e) * (1 - 1e-12), kth * (1 + e) * (1 + 1e-12)
-    for j in diff:
-        assert lo <= A_ref[j] <= hi, f"chunk {j} outside the near-tie band"
-    return False
+        assert equal, "certified set differs"
+    else:
+        diff = set(sel_gpu.tolist()) ^ set(sel_ref.tolist())
+        lo, hi = nxt * (1 - e) * (1 - 1e-12), kth * (1 + e) * (1 + 1e-12)
+        for j in diff:
+            assert lo <= A_ref[j] <= hi, f"chunk {j} outside the near-tie band"
+        print(f"  uncertified set: boundary gap / score error = {ratio:.3g} (sets equal: {equal})",
+              flush=True)
+        assert not require, f"uncertified set (gap/error ratio {ratio:.3g}, sets equal: {equal})"
+    return {"certified": certified, "gap_over_err": ratio, "equal": equal}

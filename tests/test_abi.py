@@ -86,10 +86,14 @@ def test_validation_before_launch(ckv):
     assert L.ckv_sparse_prefill_attn(ctypes.byref(good), P, P, P, P, -1, P, P, P, None, 0, None) == ckv.EINVAL
     assert L.ckv_sparse_prefill_attn(ctypes.byref(good), P, None, P, P, 3, P, P, P, None, 0, None) == ckv.EINVAL
     h = ctypes.c_void_p()
-    assert L.ckv_ctx_create(ctypes.byref(good), 0.0, 0, ctypes.byref(h)) == ckv.EINVAL
-    assert L.ckv_ctx_create(ctypes.byref(good), 0.5, 0x80, ctypes.byref(h)) == ckv.EINVAL
-    assert L.ckv_ctx_create(ctypes.byref(bad_hd), 0.5, 0, ctypes.byref(h)) == ckv.EUNSUPPORTED
+    assert L.ckv_ctx_create(ctypes.byref(good), 4, 0.0, 0, ctypes.byref(h)) == ckv.EINVAL
+    assert L.ckv_ctx_create(ctypes.byref(good), 4, 0.5, 0x80, ctypes.byref(h)) == ckv.EINVAL
+    assert L.ckv_ctx_create(ctypes.byref(good), 0, 0.5, 0, ctypes.byref(h)) == ckv.EINVAL
+    assert "n_layers" in ckv.last_error()
+    assert L.ckv_ctx_create(ctypes.byref(bad_hd), 4, 0.5, 0, ctypes.byref(h)) == ckv.EUNSUPPORTED
     assert not h.value
+    assert L.ckv_ctx_set_host_layers(None, None, 0) == ckv.EINVAL
+    assert L.ckv_ctx_inject_copy_error(None, 0) == ckv.EINVAL
     assert L.ckv_reprefill_layer(None, 0, None, None) == ckv.EINVAL
     assert L.ckv_ctx_destroy(None) == ckv.OK
 

@@ -35,8 +35,8 @@ def test_layer_cache_requests(period, n_prefix):
     stores = [_store(w, t) for t in layers]
     base = [{kk: dev(v) for kk, v in t.items()} for t in layers]
     s = oshape(w)
-    ctx = ckv.Context(dims_of(w), w.keep_ratio, ckv.CTX_HOST_PREFIX)
-    plain = ckv.Context(dims_of(w), w.keep_ratio, ckv.CTX_HOST_PREFIX)
+    ctx = ckv.Context(dims_of(w), w.n_layers, w.keep_ratio, ckv.CTX_HOST_PREFIX)
+    plain = ckv.Context(dims_of(w), w.n_layers, w.keep_ratio, ckv.CTX_HOST_PREFIX)
     ctx.set_period(period)
     plain.set_period(period)
     k = ctx.k
@@ -127,13 +127,13 @@ def test_attach_cache_refusals():
     t = synth.layer_tensors(w, 0)
     tt = {kk: dev(v) for kk, v in t.items()}
     store = _store(w, t)
-    hbm = ckv.Context(dims_of(w), w.keep_ratio, 0)
+    hbm = ckv.Context(dims_of(w), w.n_layers, w.keep_ratio, 0)
     cache = ckv.Cache(2 * m, 8, 8)
     with pytest.raises(ckv.CkvError) as e:  # needs a host-resident prefix
         hbm.attach_cache(cache)
     assert e.value.status == ckv.EINVAL
     hbm.close()
-    ctx = ckv.Context(dims_of(w), w.keep_ratio, ckv.CTX_HOST_PREFIX)
+    ctx = ckv.Context(dims_of(w), w.n_layers, w.keep_ratio, ckv.CTX_HOST_PREFIX)
     odd = ckv.Cache(2 * m + 1, 8, 8)
     with pytest.raises(ckv.CkvError) as e:  # keys not a whole number of layers
         ctx.attach_cache(odd)
@@ -190,7 +190,7 @@ def test_layer_store(tmp_path, period, with_cache, direct, n_prefix):
     except ckv.CkvError:
         pytest.skip("this filesystem refuses O_DIRECT")
     base = [{kk: dev(v) for kk, v in t.items()} for t in layers]
-    ctxs = [ckv.Context(dims_of(w), w.keep_ratio, ckv.CTX_HOST_PREFIX) for _ in range(2)]
+    ctxs = [ckv.Context(dims_of(w), w.n_layers, w.keep_ratio, ckv.CTX_HOST_PREFIX) for _ in range(2)]
     k = ctxs[0].k
     gpu_slots, cpu_slots = (L * k) // 2, L * k
     caches = []
@@ -287,13 +287,13 @@ def test_attach_store_refusals(tmp_path):
         cm.tofile(f)  # two layers' worth of spans
     tt = {kk: dev(v) for kk, v in t.items()}
     out = torch.empty_like(tt["q"])
-    hbm = ckv.Context(dims_of(w), w.keep_ratio, 0)
+    hbm = ckv.Context(dims_of(w), w.n_layers, w.keep_ratio, 0)
     good = ckv.Store(path, 2 * m, span, 2)
     with pytest.raises(ckv.CkvError) as e:  # needs a host-resident prefix
         hbm.attach_store(good)
     assert e.value.status == ckv.EINVAL
     hbm.close()
-    ctx = ckv.Context(dims_of(w), w.keep_ratio, ckv.CTX_HOST_PREFIX)
+    ctx = ckv.Context(dims_of(w), 4, w.keep_ratio, ckv.CTX_HOST_PREFIX)  # layers past the store's
     for bad in (ckv.Store(path, 2 * m, span // 2, 2),      # spans are not chunks
                 ckv.Store(path, 2 * m - 1, span, 2)):     # not a whole number of layers
         with pytest.raises(ckv.CkvError) as e:
@@ -321,7 +321,7 @@ def test_attach_store_refusals(tmp_path):
     good.close()
 
 
-@pytest.mark.parametrize("with_cache", [False, True])
+@pytest.mark.parametrize("with_cache", [False, True, "small"])
 def test_layer_store_subperiod(tmp_path, with_cache):
     """Periods of 4 layers with a SubPeriod of 3: a Period's layers queue the
     storage reads of the next two layers of the Period.  Outputs and sets equal
@@ -340,12 +340,18 @@ def test_layer_store_subperiod(tmp_path, with_cache):
     span = 2 * w.chunk_size * w.n_kv_heads * w.head_dim * w.elem_bytes
     store = ckv.Store(path, L * m, span, 4)
     base = [{kk: dev(v) for kk, v in t.items()} for t in layers]
-    ctxs = [ckv.Context(dims_of(w), w.keep_ratio, ckv.CTX_HOST_PREFIX) for _ in range(3)]
+    ctxs = [ckv.Context(dims_of(w), w.n_layers, w.keep_ratio, ckv.CTX_HOST_PREFIX) for _ in range(3)]
     k = ctxs[0].k
     caches = []
     for i, c in enumerate(ctxs):
         c.set_period(4)
-        if with_cache:
+        if with_cache == "small":
+            # tiers of about one layer's chunks: the cascade sends chunks of
+            # later layers, listed by read-ahead entries while in the CPU
+            # tier, out of memory before their layer runs
+            caches.append(ckv.Cache(L * m, k // 2, k))
+            c.attach_cache(caches[-1])
+        elif with_cache:
             caches.append(ckv.Cache(L * m, (L * k) // 2, L * k))
             c.attach_cache(caches[-1])
         if i > 0:

@@ -15,11 +15,10 @@ import torch
 
 import oracle
 import synth
-from gpu_common import DEV, check_set, dev, dims_of, oshape, rel_err, to_f64
+from gpu_common import DEV, SCORE_RTOL, check_set, dev, dims_of, oshape, rel_err, to_f64
 
 pytestmark = pytest.mark.gpu
 
-SCORE_RTOL = 2e-6
 ATTN_ATOL = 2e-2
 N_SAMPLE = 96
 
@@ -35,7 +34,7 @@ def _rows(w, seed=7):
 
 def _run(w, layer, t, flags=0, kv_host=None):
     import paper_2601_13631_amd as ckv
-    ctx = ckv.Context(dims_of(w), w.keep_ratio, flags)
+    ctx = ckv.Context(dims_of(w), w.n_layers, w.keep_ratio, flags)
     k = ctx.k
     tt = {kk: dev(v) for kk, v in t.items()}
     A = torch.empty(w.n_chunks, dtype=torch.float64, device=DEV)

@@ -1,9 +1,12 @@
 """GPU parity of each kernel against the oracle, called through the C ABI.
 
 Bars: chunk indices bit-exact (certified sets; select itself on identical
-scores always exact); gather byte-exact; chunk scores within rtol 2e-6 (bound
-derived from fp32 logits/exp2 with fp64 cross-row sums); attention max-abs
-2e-2 for bf16 and 1e-5 for fp32 against the oracle run with the GPU's own set.
+scores always exact); gather byte-exact; chunk scores within rtol 4e-7 on these
+small seeded shapes (1e-7 at the workloads' full sizes, where a chunk's score
+sums thousands of terms; 2e-6, the bound derived from fp32 logits/exp2 with
+fp64 cross-row sums, only for inputs built at the edge of fp32's range); attention
+max-abs 2e-2 for bf16 and 1e-5 for fp32 against the oracle run with the GPU's
+own set.
 """
 import numpy as np
 import pytest
@@ -11,12 +14,11 @@ import torch
 
 import oracle
 import synth
-from gpu_common import (DEV, check_set, dev, dims_of, gpu_scores, gpu_select, host_bits, oshape,
-                        rel_err, to_f64, workspace)
+from gpu_common import (DEV, SCORE_RTOL_UNIT as SCORE_RTOL, SCORE_RTOL_BOUND, check_set, dev, dims_of, gpu_scores,
+                        gpu_select, host_bits, oshape, rel_err, to_f64, workspace)
 
 pytestmark = pytest.mark.gpu
 
-SCORE_RTOL = 2e-6
 
 
 def W(n, S, Hq, Hkv, d, c, keep=0.2, dtype="bf16", seed=1, alpha=1.5, sm_scale=0.0):
@@ -84,7 +86,7 @@ def test_scores_exact_fallback_on_overflow(dtype):
     s = oshape(w)
     A_ref = oracle.chunk_scores(s, oracle.token_importance(s, t["q"], t["k_prefix"]))
     assert np.isfinite(A).all()
-    assert rel_err(A, A_ref) <= SCORE_RTOL
+    assert rel_err(A, A_ref) <= SCORE_RTOL_BOUND
     assert int(np.argmax(A)) == 100 // c
 
 
@@ -202,3 +204,26 @@ def test_attention_matches_oracle(w, how):
     tol = 1e-5 if w.dtype == "f32" else 2e-2
     print(f"  max abs err {err:.3e} (tol {tol})", flush=True)
     assert err <= tol
+
+
+def test_attention_deterministic():
+    """Attention run twice (with split-K and its combine) is bitwise equal."""
+    import paper_2601_13631_amd as ckv
+    w = W2(4096, 256, 28, 4, 128, 32)
+    t = synth.layer_tensors(w, 0)
+    sel = _sel_for(w, "tenth", np.random.default_rng(5))
+    k = sel.size
+    d = dims_of(w)
+    tt = {kk: dev(v) for kk, v in t.items()}
+    sel_d = torch.from_numpy(sel).to(DEV)
+    kd = torch.empty((k * w.chunk_size, w.n_kv_heads, w.head_dim), dtype=torch.bfloat16, device=DEV)
+    vd = torch.empty_like(kd)
+    ckv.gather_chunks(d, tt["k_prefix"], tt["v_prefix"], sel_d, k, kd, vd)
+    ws = workspace(ckv.attn_workspace_bytes(d, k))
+    outs = []
+    for _ in range(2):
+        out = torch.empty_like(tt["q"])
+        ckv.sparse_prefill_attn(d, tt["q"], kd, vd, sel_d, k, tt["k_suffix"], tt["v_suffix"], out, ws)
+        outs.append(out)
+    torch.cuda.synchronize()
+    assert torch.equal(outs[0].view(torch.int16), outs[1].view(torch.int16))
