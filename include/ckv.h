@@ -415,6 +415,35 @@ ckv_status ckv_reprefill_layer(ckv_ctx* ctx, int32_t layer, const ckv_layer_io* 
                                ckv_layer_stats* stats);
 
 /* ---------------------------------------------------------------------------
+ * The layer step without allocation -- for callers that cannot allocate
+ * device memory: code under HIP graph capture, tight serving loops, harnesses
+ * that forbid hipMalloc.  One HBM-resident layer (score -> select ->
+ * attention over the kept chunks' spans read in place) like ckv_reprefill_layer
+ * on an HBM-resident context, with the same kernels and bit-identical results,
+ * but with no context: its scratch is a fixed device array of
+ * CKV_NOALLOC_SCRATCH_BYTES inside the library (each device the library runs
+ * on holds its own copy until the process ends; its address is looked up on a
+ * device's first call).  The call allocates nothing and needs no initial
+ * scratch contents.  Scratch needed: max(ckv_score_workspace_bytes,
+ * ckv_attn_workspace_bytes(k)) rounded up to 256 bytes, plus m doubles (256-
+ * byte rounded) when chunk_scores is NULL and k int32 when sel_idx is NULL;
+ * a shape needing more is refused with CKV_EINVAL before anything is
+ * enqueued (the 32K-token 7B-shaped layer needs ~32 MB).  Every call on a
+ * device uses that device's one array: calls that overlap in time on one
+ * device (several streams or threads) race and must be serialized by the
+ * caller.
+ *   q, k_prefix, v_prefix, k_suffix, v_suffix, out: as ckv_reprefill_layer
+ *   chunk_scores  device double[m] (written), or NULL
+ *   sel_idx       device int32[k] (written, ascending), or NULL
+ * k = ckv_num_keep(ceil(n/c), keep_ratio); asynchronous on `stream`.
+ * ------------------------------------------------------------------------- */
+#define CKV_NOALLOC_SCRATCH_BYTES (64u << 20)
+ckv_status ckv_reprefill_layer_noalloc(const ckv_dims* dims, double keep_ratio, const void* q,
+                                       const void* k_prefix, const void* v_prefix,
+                                       const void* k_suffix, const void* v_suffix, void* out,
+                                       double* chunk_scores, int32_t* sel_idx, void* stream);
+
+/* ---------------------------------------------------------------------------
  * Read accounting -- Sec. 4.2 (a ContiguousChunk store reads exactly the
  * selected chunks) against Sec. 3, Motivation 1 (a store of fixed coarse
  * blocks reads every block that holds a needed token: read amplification).

@@ -110,6 +110,8 @@ _SIG = {
                             ctypes.c_int32),
     "ckv_reprefill_layer": ([_P, ctypes.c_int32, ctypes.POINTER(LayerIO),
                              ctypes.POINTER(LayerStats)], ctypes.c_int32),
+    "ckv_reprefill_layer_noalloc": ([_DP, ctypes.c_double, _P, _P, _P, _P, _P, _P, _P, _P, _P],
+                                    ctypes.c_int32),
     "ckv_io_account": ([ctypes.c_int64, ctypes.c_int32, _P, ctypes.c_int64, ctypes.c_int32,
                         ctypes.POINTER(IoCounts)], ctypes.c_int32),
     "ckv_cache_create": ([ctypes.c_int64, ctypes.c_int64, ctypes.c_int64, ctypes.c_int32,
@@ -221,6 +223,20 @@ def sparse_prefill_attn(dims: Dims, q, k_sel, v_sel, sel_idx, k: int, k_suffix, 
                                         _ptr(sel_idx), k, _ptr(k_suffix), _ptr(v_suffix), _ptr(out),
                                         _ptr(ws), nbytes, _stream(stream)),
            "ckv_sparse_prefill_attn")
+
+
+NOALLOC_SCRATCH_BYTES = 64 << 20
+
+
+def reprefill_layer_noalloc(dims: Dims, keep_ratio: float, q, k_prefix, v_prefix, k_suffix, v_suffix,
+                            out, chunk_scores=None, sel_idx=None, stream=None) -> None:
+    """``ckv_reprefill_layer_noalloc``: one HBM-resident layer step that allocates
+    nothing (scratch in the library's fixed device array)."""
+    _check(_lib.ckv_reprefill_layer_noalloc(ctypes.byref(dims), keep_ratio, _ptr(q), _ptr(k_prefix),
+                                            _ptr(v_prefix), _ptr(k_suffix), _ptr(v_suffix),
+                                            _ptr(out), _ptr(chunk_scores), _ptr(sel_idx),
+                                            _stream(stream)),
+           "ckv_reprefill_layer_noalloc")
 
 
 class Context:

@@ -15,7 +15,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libckv.so")
 SOURCES = ["api.hip", "score.hip", "select.hip", "gather.hip", "attn.hip", "layer.hip",
-           "io_account.hip", "cache.hip", "store.hip"]
+           "io_account.hip", "cache.hip", "store.hip", "noalloc.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-Wall",
