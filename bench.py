@@ -106,7 +106,8 @@ def host_cache_requests(args, w, ckv, synth, np, torch, layers, stores, dims, k)
     out = torch.empty_like(layers[0]["q"])
     res = {"requests": R, "layers": L, "gpu_slots": gpu_slots,
            "slot_bytes": 2 * w.chunk_size * w.n_kv_heads * w.head_dim * w.elem_bytes}
-    for name, policy in (("none", None), ("attention", ckv.CACHE_ATTENTION), ("lfu", ckv.CACHE_LFU)):
+    for name, policy in (("none", None), ("attention", ckv.CACHE_ATTENTION),
+                         ("attention_f_loads", ckv.CACHE_LOADS), ("lfu", ckv.CACHE_LFU)):
         ctx = ckv.Context(dims, w.n_layers, w.keep_ratio, ckv.CTX_HOST_PREFIX)
         cache = None
         if policy is not None:
@@ -214,6 +215,51 @@ def host_store_run(args, w, ckv, synth, np, torch, host, layers, dims, k) -> dic
     return res
 
 
+def period_sweep(args, w, ckv, torch, layers, stores, outs, dims, stream) -> dict:
+    """Periods of --host-period layers with every layer's pinned store
+    registered: a Period's first layer queues the copies of the whole Period
+    (intra-period prefetch, Sec. 4.3.2) and its attention waits until the
+    Period's first sp layers are in HBM (the SubPeriod gate), for sp in
+    1, 2, 4, ... up to the Period.  Per sp: time per layer (host link
+    included) over --host-reps passes, and the same without registration
+    (one layer ahead) as the reference."""
+    L = len(layers)
+    res = {"period": args.host_period, "layers": L, "passes": max(1, args.host_reps)}
+
+    def run(ctx):
+        def one_pass():
+            ctx.reset()
+            for l in range(L):
+                t = layers[l]
+                ctx.reprefill_layer(l, t["q"], t["k_suffix"], t["v_suffix"], t["k_prefix"], outs[l],
+                                    kv_host=stores[l],
+                                    kv_host_next=stores[l + 1] if l + 1 < L else None, stream=stream)
+        one_pass()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(res["passes"]):
+            one_pass()
+        torch.cuda.synchronize()
+        return (time.perf_counter() - t0) * 1e6 / (res["passes"] * L)
+
+    ctx = ckv.Context(dims, w.n_layers, w.keep_ratio, ckv.CTX_HOST_PREFIX)
+    ctx.set_period(args.host_period)
+    res["one_layer_ahead_us_per_layer"] = round(run(ctx), 1)
+    ctx.close()
+    sp = 1
+    while sp <= args.host_period:
+        ctx = ckv.Context(dims, w.n_layers, w.keep_ratio, ckv.CTX_HOST_PREFIX)
+        ctx.set_host_layers(stores[:L] + [stores[-1]] * (w.n_layers - L))
+        ctx.set_period(args.host_period)
+        ctx.set_subperiod(sp)
+        res[f"sp{sp}_us_per_layer"] = round(run(ctx), 1)
+        ctx.close()
+        sp *= 2
+    log("intra-period prefetch, Period " + str(args.host_period) + ": " +
+        ", ".join(f"{k} {v}" for k, v in res.items() if k.endswith("per_layer")))
+    return res
+
+
 def host_resident(args, w, ckv, synth, np, torch) -> int:
     """Host-resident prefix (K/V of every layer in pinned host memory, a probe
     copy of K in HBM for scoring): per-layer steps in order, each fetching only
@@ -275,6 +321,8 @@ def host_resident(args, w, ckv, synth, np, torch) -> int:
     hits = sum(s_["hits"] for s_ in stats)
     later = [s_ for i, s_ in enumerate(stats) if i % L]
     log(f"{us:.1f} us per layer including the host link; {link / elapsed / 1e9:.1f} GB/s over it")
+    sweep_detail = period_sweep(args, w, ckv, torch, layers, stores, outs, dims, stream) \
+        if args.host_period > 1 and args.host_sweep else None
     cache_detail = host_cache_requests(args, w, ckv, synth, np, torch, layers, stores, dims, k) \
         if args.host_requests > 0 else None
     store_detail = host_store_run(args, w, ckv, synth, np, torch, stores, layers, dims, k) \
@@ -303,6 +351,8 @@ def host_resident(args, w, ckv, synth, np, torch) -> int:
             "hits_per_layer": round(hits / n, 1),
         },
     }
+    if sweep_detail is not None:
+        line["detail"]["intra_period_prefetch"] = sweep_detail
     if cache_detail is not None:
         line["detail"]["cache_requests"] = cache_detail
     if store_detail is not None:
@@ -394,7 +444,10 @@ def tiers_detail(args, w, ckv, synth, np, torch, layers, dims, dev) -> dict:
     gpu_slots, cpu_slots = L * k // 2, L * k
     cache = {"requests": args.requests, "keys": "layer*m+chunk", "gpu_slots": gpu_slots,
              "cpu_slots": cpu_slots}
-    for name, policy in (("attention", ckv.CACHE_ATTENTION), ("lfu", ckv.CACHE_LFU)):
+    # F counting uses (the library's reading), F counting loads into GPU or CPU
+    # memory (the paper's wording read literally), and the frequency-only foil
+    for name, policy in (("attention", ckv.CACHE_ATTENTION), ("attention_f_loads", ckv.CACHE_LOADS),
+                         ("lfu", ckv.CACHE_LFU)):
         cm = ckv.Cache(L * m, gpu_slots, cpu_slots, policy)
         first = None
         t0 = time.perf_counter()
@@ -440,6 +493,9 @@ def main() -> int:
                     help="host-resident workloads: also run the layers from a file written in this "
                          "directory, read by the storage tier (O_DIRECT)")
     ap.add_argument("--io-threads", type=int, default=16, help="storage tier I/O threads")
+    ap.add_argument("--host-sweep", action="store_true",
+                    help="host-resident workloads with --host-period p > 1: also time intra-period "
+                         "prefetch with the SubPeriod gate at 1, 2, 4, ... p layers")
     ap.add_argument("--host-subperiod", type=int, default=1,
                     help="storage tier: reads up to this many - 1 layers ahead inside a Period")
     ap.add_argument("--io-sweep", action="store_true",

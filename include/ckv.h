@@ -509,8 +509,11 @@ ckv_status ckv_store_read(ckv_store* store, const int64_t* keys, int64_t count, 
  * also after eviction (the in-memory score table):
  *   I  cumulative importance: the sum of the attention scores A_j (Eq. 1) of
  *      the requests that used the chunk,
- *   F  access frequency: the number of requests that used it,
- *   S  cache score I * F (CKV_CACHE_ATTENTION), or F alone
+ *   F  access frequency: the number of requests that used it, or, with
+ *      CKV_CACHE_LOADS (the paper's wording read literally), the number of
+ *      times it was loaded into GPU or CPU memory: its uses that found it
+ *      outside the GPU tier,
+ *   S  cache score I * F (CKV_CACHE_ATTENTION, CKV_CACHE_LOADS), or F alone
  *      (CKV_CACHE_LFU, the frequency-only policy of the ablation).
  * Two tiers of gpu_slots and cpu_slots entries are kept as min-heaps on
  * (S, time of latest access): the weakest entry is the one with the lowest S,
@@ -532,6 +535,7 @@ ckv_status ckv_store_read(ckv_store* store, const int64_t* keys, int64_t count, 
 /* (ckv_cache is declared beside ckv_ctx above) */
 #define CKV_CACHE_ATTENTION 0
 #define CKV_CACHE_LFU 1
+#define CKV_CACHE_LOADS 2
 #define CKV_TIER_NONE 0
 #define CKV_TIER_CPU 1
 #define CKV_TIER_GPU 2
@@ -544,8 +548,8 @@ typedef struct ckv_cache_counts {
   int64_t dropped;  /* chunks that left memory or were not kept after a load */
 } ckv_cache_counts;
 
-/* n_keys >= 1, gpu_slots >= 0, cpu_slots >= 0, policy CKV_CACHE_ATTENTION or
- * CKV_CACHE_LFU.  Host allocation of O(n_keys + slots); CKV_ENOMEM on failure. */
+/* n_keys >= 1, gpu_slots >= 0, cpu_slots >= 0, policy CKV_CACHE_ATTENTION,
+ * CKV_CACHE_LFU or CKV_CACHE_LOADS.  Host allocation of O(n_keys + slots); CKV_ENOMEM on failure. */
 ckv_status ckv_cache_create(int64_t n_keys, int64_t gpu_slots, int64_t cpu_slots, int32_t policy,
                             ckv_cache** out);
 ckv_status ckv_cache_destroy(ckv_cache* cache);

@@ -302,7 +302,7 @@ def io_account(n: int, c: int, sel, block_tokens: int) -> dict:
     return {f: int(getattr(out, f)) for f, _ in _IoCounts._fields_}
 
 
-CACHE_ATTENTION, CACHE_LFU = 0, 1
+CACHE_ATTENTION, CACHE_LFU, CACHE_LOADS = 0, 1, 2
 TIER_NONE, TIER_CPU, TIER_GPU = 0, 1, 2
 
 

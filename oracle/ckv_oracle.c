@@ -552,7 +552,7 @@ struct ckvo_cache {
   int64_t n_keys, gpu_slots, cpu_slots;
   int policy;
   double* I;      /* cumulative importance: sum of A over the key's accesses */
-  int64_t* F;     /* accesses */
+  int64_t* F;     /* accesses (CKVO_CACHE_LOADS: loads into GPU or CPU memory) */
   int64_t* last;  /* time of the key's latest access (0: never) */
   int8_t* tier;
   int64_t clock;
@@ -561,7 +561,8 @@ struct ckvo_cache {
 
 ckvo_cache* ckvo_cache_create(int64_t n_keys, int64_t gpu_slots, int64_t cpu_slots, int policy) {
   if (n_keys < 1 || gpu_slots < 0 || cpu_slots < 0) return NULL;
-  if (policy != CKVO_CACHE_ATTENTION && policy != CKVO_CACHE_LFU) return NULL;
+  if (policy != CKVO_CACHE_ATTENTION && policy != CKVO_CACHE_LFU && policy != CKVO_CACHE_LOADS)
+    return NULL;
   ckvo_cache* c = (ckvo_cache*)calloc(1, sizeof *c);
   if (!c) return NULL;
   c->n_keys = n_keys;
@@ -674,7 +675,9 @@ int ckvo_cache_access(ckvo_cache* c, const int64_t* keys, const double* A, int64
     else if (was == CKVO_TIER_CPU) c->counts.hits_cpu++;
     else c->counts.misses++;
     c->I[x] += A[u];
-    c->F[x] += 1;
+    /* F: every use; or, read literally, every load into GPU or CPU memory
+     * (a use of a chunk already in the GPU tier loads nothing) */
+    if (c->policy != CKVO_CACHE_LOADS || was != CKVO_TIER_GPU) c->F[x] += 1;
     c->last[x] = ++c->clock;
     c->tier[x] = CKVO_TIER_NONE;
     admit_gpu(c, x);

@@ -123,14 +123,17 @@ int ckvo_io_account(int64_t n, int32_t c, const int32_t* sel, int64_t k, int32_t
  * of its accesses), F (number of accesses) and the time of its latest access,
  * for evicted keys too (the in-memory score table).  Two tiers of gpu_slots and
  * cpu_slots entries hold keys by cache score S = I*F (policy ATTENTION) or S = F
- * (policy LFU, the ablation's frequency-only foil).  Readings where the paper
- * is silent: F counts accesses; an accessed key goes to the GPU tier when there
+ * (policy LFU, the ablation's frequency-only foil).  Policy LOADS is S = I*F
+ * with F read literally as the number of times the chunk was loaded into GPU
+ * or CPU memory: a use of a key already in the GPU tier adds to I but not to
+ * F.  Readings where the paper is silent: F counts accesses (ATTENTION, LFU);
+ * an accessed key goes to the GPU tier when there
  * is room or it outranks the GPU tier's weakest entry, which is then demoted to
  * the CPU tier by the same rule, else the key goes to the CPU tier by that
  * rule; whatever the CPU tier does not take leaves memory; ranking is by S,
  * then by latest access (older leaves first).  This oracle finds the weakest
  * entry by scanning every key. */
-enum { CKVO_CACHE_ATTENTION = 0, CKVO_CACHE_LFU = 1 };
+enum { CKVO_CACHE_ATTENTION = 0, CKVO_CACHE_LFU = 1, CKVO_CACHE_LOADS = 2 };
 enum { CKVO_TIER_NONE = 0, CKVO_TIER_CPU = 1, CKVO_TIER_GPU = 2 };
 typedef struct {
   int64_t hits_gpu, hits_cpu, misses; /* where each accessed key was found        */

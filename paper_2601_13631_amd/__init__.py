@@ -21,7 +21,7 @@ LIB_PATH = os.path.join(_HERE, "libckv.so")
 OK, EINVAL, EUNSUPPORTED, EHIP, ENOMEM, ESTATE = range(6)
 DTYPE_F32, DTYPE_BF16 = 0, 1
 CTX_HOST_PREFIX, CTX_MATERIALIZE, CTX_STAGE_TIMING, CTX_SCORE_TIMING = 0x1, 0x2, 0x4, 0x8
-CACHE_ATTENTION, CACHE_LFU = 0, 1
+CACHE_ATTENTION, CACHE_LFU, CACHE_LOADS = 0, 1, 2
 STORE_DIRECT = 0x1
 TIER_NONE, TIER_CPU, TIER_GPU = 0, 1, 2
 STAGES = ("score", "finalize", "select", "move", "attn")

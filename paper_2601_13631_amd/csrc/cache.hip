@@ -1,7 +1,9 @@
 // cache.hip -- attention-guided cache management (Sec. 4.5, Eq. 2), host code.
 // Per key: I (sum of the attention scores of the requests that used it), F (that
-// number of requests), the time of its latest use, and S = I*F (or F alone for
-// the frequency-only policy).  The GPU and CPU tiers are indexed binary
+// number of requests; with CKV_CACHE_LOADS the number of those uses that loaded
+// the chunk into GPU or CPU memory, i.e. found it outside the GPU tier), the
+// time of its latest use, and S = I*F (or F alone for the frequency-only
+// policy).  The GPU and CPU tiers are indexed binary
 // min-heaps on (S, latest use), so the weakest entry is at the root and any
 // entry can be taken out when its key is used again.  A key's S changes only
 // when it is used, and it is out of its heap at that moment, so the heaps stay
@@ -153,7 +155,7 @@ ckv_status ckv_cache_create(int64_t n_keys, int64_t gpu_slots, int64_t cpu_slots
   *out = nullptr;
   if (n_keys < 1 || gpu_slots < 0 || cpu_slots < 0)
     CKV_FAIL(CKV_EINVAL, "n_keys must be >= 1 and slot counts >= 0");
-  if (policy != CKV_CACHE_ATTENTION && policy != CKV_CACHE_LFU)
+  if (policy != CKV_CACHE_ATTENTION && policy != CKV_CACHE_LFU && policy != CKV_CACHE_LOADS)
     CKV_FAIL(CKV_EINVAL, "unknown cache policy %d", policy);
   ckv_cache* c = new (std::nothrow) ckv_cache;
   if (!c) CKV_FAIL(CKV_ENOMEM, "cache allocation failed");
@@ -213,7 +215,7 @@ ckv_status ckv_cache_access(ckv_cache* cache, const int64_t* keys, const double*
     else c.counts.misses++;
     if (was != CKV_TIER_NONE) heap_erase(c, was, x);
     c.I[x] += scores[u];
-    c.F[x] += 1;
+    if (c.policy != CKV_CACHE_LOADS || was != CKV_TIER_GPU) c.F[x] += 1;  // a use, or a load
     c.last[x] = ++c.clock;
     c.S[x] = c.policy == CKV_CACHE_LFU ? (double)c.F[x] : c.I[x] * (double)c.F[x];
     place(c, x);

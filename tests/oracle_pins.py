@@ -434,6 +434,27 @@ def pin_cache_hand_trace():
     w, n = c.access([3], [0.5])  # key 3 (F=2) displaces key 4 (F=1) to the CPU tier
     assert list(w) == [T1] and list(c.state()[2]) == [T0, T0, T2, T2, T1, T0]
     c.close()
+    # F read as loads into GPU or CPU memory: the same three requests place
+    # every key as with F counting uses (each use loaded its chunk); then key 2,
+    # used from the GPU tier, gains I but no F (S = .5 * 2 = 1 against 1.5 when
+    # uses count), so when key 1 (CPU tier, S = 1 * 2 = 2) returns, it is key 2
+    # that goes down -- with F counting uses, key 3 (S 1.5, older) goes down
+    for policy, F_end, tier_end in (
+            (oracle.CACHE_LOADS, [0, 2, 2, 2, 1, 0], [T0, T2, T1, T2, T0, T0]),
+            (oracle.CACHE_ATTENTION, [0, 2, 3, 2, 1, 0], [T0, T2, T2, T1, T0, T0])):
+        c = oracle.Cache(6, 2, 1, policy)
+        c.access([1, 2, 3], [0.5, 0.125, 0.25])
+        c.access([2, 4], [0.125, 0.375])
+        w, n = c.access([3], [0.5])
+        assert list(c.state()[2]) == [T0, T1, T2, T2, T0, T0]
+        w, n = c.access([2], [0.25])
+        assert list(w) == [T2]
+        w, n = c.access([1], [0.5])
+        I, F, tier = c.state()
+        assert list(w) == [T1] and list(F) == F_end and list(tier) == tier_end
+        assert list(I) == [0, 1.0, 0.5, 0.75, 0.375, 0]
+        assert n == dict(hits_gpu=1, hits_cpu=2, misses=5, demoted=4, dropped=2)
+        c.close()
 
 
 def pin_cache_tiers_are_top_ranks():
@@ -442,7 +463,7 @@ def pin_cache_tiers_are_top_ranks():
     CPU tier equal to the next cpu_slots; checked after every request of random
     streams by sorting every accessed key."""
     rng = np.random.default_rng(3)
-    for policy in (oracle.CACHE_ATTENTION, oracle.CACHE_LFU):
+    for policy in (oracle.CACHE_ATTENTION, oracle.CACHE_LFU, oracle.CACHE_LOADS):
         for n_keys, g, cpu in ((40, 5, 7), (200, 16, 0), (64, 0, 10), (30, 40, 40)):
             c = oracle.Cache(n_keys, g, cpu, policy)
             one = oracle.Cache(n_keys, g, cpu, policy)  # fed one key per call
@@ -462,9 +483,10 @@ def pin_cache_tiers_are_top_ranks():
                     w1, tot1 = one.access(keys[u:u + 1], A[u:u + 1])
                     assert w1[0] == before == w[u]
                 assert tot1 == tot
-                for x, a in zip(keys, A):
+                for x, a, where in zip(keys, A, w):
                     I[x] += a
-                    F[x] += 1
+                    if policy != oracle.CACHE_LOADS or where != oracle.TIER_GPU:
+                        F[x] += 1
                     clock += 1
                     last[x] = clock
                 S = F.astype(np.float64) if policy == oracle.CACHE_LFU else I * F

@@ -63,7 +63,7 @@ def _stream(rng, n_keys, n_req, max_len, zipf=1.3):
         yield keys, A
 
 
-@pytest.mark.parametrize("policy", [ckv.CACHE_ATTENTION, ckv.CACHE_LFU])
+@pytest.mark.parametrize("policy", [ckv.CACHE_ATTENTION, ckv.CACHE_LFU, ckv.CACHE_LOADS])
 @pytest.mark.parametrize("n_keys,gpu,cpu", [(50, 4, 6), (300, 32, 64), (120, 0, 20), (80, 12, 0),
                                             (40, 100, 100), (1, 1, 0), (2000, 64, 256)])
 def test_cache_matches_oracle(policy, n_keys, gpu, cpu):
@@ -93,7 +93,7 @@ def test_cache_layer_chunk_stream():
     L, m, k = 28, 1024, 103
     hot = [np.sort(rng.choice(m, size=51, replace=False)) for _ in range(L)]
     caches = [(ckv.Cache(L * m, 2048, 4096, p), oracle.Cache(L * m, 2048, 4096, p))
-              for p in (ckv.CACHE_ATTENTION, ckv.CACHE_LFU)]
+              for p in (ckv.CACHE_ATTENTION, ckv.CACHE_LFU, ckv.CACHE_LOADS)]
     for r in range(8):
         for layer in range(L):
             rest = rng.choice(np.setdiff1d(np.arange(m), hot[layer]), size=k - 51, replace=False)

@@ -54,6 +54,10 @@ MUTANTS = {
     "cache_cpu_never_evicts": ("  if (y >= 0 && leaves_before(c, y, x)) {\n    c->tier[y] = CKVO_TIER_NONE;\n    c->counts.dropped++;",
                                "  if (0) {\n    c->tier[y] = CKVO_TIER_NONE;\n    c->counts.dropped++;"),
     "cache_frequency_not_counted": ("c->F[x] += 1;", ";"),
+    "cache_loads_counts_gpu_uses": ("if (c->policy != CKVO_CACHE_LOADS || was != CKVO_TIER_GPU) c->F[x] += 1;",
+                                    "c->F[x] += 1;"),
+    "cache_loads_skips_cpu_loads": ("if (c->policy != CKVO_CACHE_LOADS || was != CKVO_TIER_GPU) c->F[x] += 1;",
+                                    "if (c->policy != CKVO_CACHE_LOADS || was == CKVO_TIER_NONE) c->F[x] += 1;"),
 }
 
 
