@@ -38,6 +38,42 @@ typedef __attribute__((ext_vector_type(4))) float f32x4;
 typedef __attribute__((ext_vector_type(4))) short s16x4;
 typedef __attribute__((ext_vector_type(4))) uint32_t u32x4;
 
+// ---- cross-lane moves without LDS ----------------------------------------------
+// DPP inside a row of 16 lanes, and the gfx950 permlane swaps across rows.  A
+// swap hands each lane its own value and its partner's (lane ^ 16 or ^ 32) in
+// some order, which is all a symmetric reduction (min, max) needs.
+template <int CTRL>
+__device__ __forceinline__ uint32_t dpp32(uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, CTRL, 0xF, 0xF, true);
+}
+constexpr int kDppQuadXor1 = 0xB1, kDppQuadXor2 = 0x4E, kDppRowHalfMirror = 0x141,
+              kDppRowMirror = 0x140;
+constexpr int kDppRowShr1 = 0x111, kDppRowShr2 = 0x112, kDppRowShr4 = 0x114, kDppRowShr8 = 0x118;
+
+__device__ __forceinline__ uint64_t join64(uint32_t h, uint32_t l) { return ((uint64_t)h << 32) | l; }
+
+template <int CTRL>
+__device__ __forceinline__ uint64_t dpp64(uint64_t v) {
+  return join64(dpp32<CTRL>((uint32_t)(v >> 32)), dpp32<CTRL>((uint32_t)v));
+}
+
+// (own, partner) of a 64-bit value for partner lane ^ 16 (WIDTH 16) or ^ 32.
+template <int WIDTH>
+__device__ __forceinline__ void swap_pair64(uint64_t v, uint64_t& a, uint64_t& b) {
+  const uint32_t l = (uint32_t)v, h = (uint32_t)(v >> 32);
+  if constexpr (WIDTH == 16) {
+    const auto rl = __builtin_amdgcn_permlane16_swap(l, l, false, false);
+    const auto rh = __builtin_amdgcn_permlane16_swap(h, h, false, false);
+    a = join64(rh[0], rl[0]);
+    b = join64(rh[1], rl[1]);
+  } else {
+    const auto rl = __builtin_amdgcn_permlane32_swap(l, l, false, false);
+    const auto rh = __builtin_amdgcn_permlane32_swap(h, h, false, false);
+    a = join64(rh[0], rl[0]);
+    b = join64(rh[1], rl[1]);
+  }
+}
+
 // ---- shape checks ------------------------------------------------------------
 inline int elem_bytes(int dtype) { return dtype == CKV_DTYPE_F32 ? 4 : 2; }
 

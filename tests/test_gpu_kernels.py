@@ -90,7 +90,8 @@ def test_scores_exact_fallback_on_overflow(dtype):
     assert int(np.argmax(A)) == 100 // c
 
 
-SELECT_CASES = [1, 2, 7, 64, 512, 1000, 4096, 8192, 16384, 20000, 70000]
+SELECT_CASES = [1, 2, 7, 64, 512, 1000, 1024, 1025, 2048, 3000, 4096, 4097, 8192, 16384, 20000,
+                70000]
 
 
 @pytest.mark.parametrize("m", SELECT_CASES)
