@@ -498,17 +498,19 @@ __global__ __launch_bounds__(256) void combine_kernel(const uint16_t* __restrict
   float M = -INFINITY, Lsum = 0.f;
   float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
   for (int s0 = 0; s0 < n_splits; s0 += kCombineBatch) {
+    // unconditional loads (a split past the last re-reads the last one and is
+    // then ignored), so the whole batch is in flight together
     float2 ml[kCombineBatch];
     uint4 raw[kCombineBatch];
 #pragma unroll
     for (int i = 0; i < kCombineBatch; ++i) {
-      if (s0 + i < n_splits) {
-        ml[i] = ml_part[(s0 + i) * rows + grow];
-        raw[i] = *reinterpret_cast<const uint4*>(o_part + ((s0 + i) * rows + grow) * D + c8);
-      } else {
-        ml[i] = make_float2(0.f, 0.f);
-      }
+      const int64_t sp = min(s0 + i, n_splits - 1);
+      ml[i] = ml_part[sp * rows + grow];
+      raw[i] = *reinterpret_cast<const uint4*>(o_part + (sp * rows + grow) * D + c8);
     }
+#pragma unroll
+    for (int i = 0; i < kCombineBatch; ++i)
+      if (s0 + i >= n_splits) ml[i] = make_float2(0.f, 0.f);
 #pragma unroll
     for (int i = 0; i < kCombineBatch; ++i) {
       if (!(ml[i].y > 0.f)) continue;  // absent, or the split saw no key of this row
