@@ -12,10 +12,13 @@ stage, the step time with no events, and the average time per layer when
 layers share their set over Periods of 8 layers (Def. 4.2: one layer in eight
 scores and selects) -- context only; the headline metric selects per layer.
 Then W warm-up steps and the K timed steps, with no events at all: ``value``
-and ``ms_per_step``.  Then the same K steps again with the scoring kernel
-(the dominant kernel) launched on the layer's stream with two HIP events as
-its own start and stop timestamps: ``roofline`` is its algorithmic flops per
-launch (2*S*Hq*n*d) over their average interval.  ``roofline.traffic`` is the
+and ``ms_per_step``.  Then the same K steps again on a context that times the
+scoring kernel (the dominant kernel) by the kernel's own timestamps (from its
+first workgroup's start to its last workgroup's end, 100 MHz realtime
+counter), with nothing added between the launches: ``roofline`` is its
+algorithmic flops per launch (2*S*Hq*n*d) over the average span, and
+``roofline.event_avg_us`` the kernel's average time between the HIP events of
+the diagnostic pass (which include its dispatch).  ``roofline.traffic`` is the
 kernel's HBM bytes per launch from the committed rocprofv3 counter summary
 (FETCH_SIZE and WRITE_SIZE, each scaled by what the counter reads for a plain
 copy of known size); it is null when the kernel's sources no longer match the
@@ -594,9 +597,9 @@ def main() -> int:
     ctx.close()
     ms_per_step = elapsed * 1e3 / args.steps
     value = w.n_prefix * args.steps / elapsed
-    # the same K steps again with the scoring kernel's own launch bracketed by
-    # two HIP events (its start and stop timestamps, on the layer's stream):
-    # the kernel's average duration for the roofline
+    # the same K steps again with the scoring kernel timed by its own
+    # timestamps (first workgroup start to last workgroup end): the kernel's
+    # average duration for the roofline
     sctx = ckv.Context(dims, w.n_layers, w.keep_ratio, ckv.CTX_SCORE_TIMING | mat)
     for i in range(args.warmup):
         step(sctx, i)
@@ -608,7 +611,8 @@ def main() -> int:
     assert n_timed == args.steps, (n_timed, args.steps)
     score_s = score_ms["score"] / n_timed * 1e-3
     log(f"{ms_per_step * 1e3:.1f} us/step; score kernel {score_s * 1e6:.1f} us "
-        f"(pass with its events: {scored_elapsed * 1e6 / args.steps:.1f} us/step)")
+        f"(timed pass: {scored_elapsed * 1e6 / args.steps:.1f} us/step; between events "
+        f"{per_layer['score'] * 1e3:.1f} us)")
 
     # scoring: algorithmic flops per launch / average launch duration
     score_flops = 2.0 * w.n_suffix * w.n_q_heads * w.n_prefix * w.head_dim
@@ -619,7 +623,9 @@ def main() -> int:
                 "peak": PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_F32_TFLOPS, "unit": "TFLOP/s",
                 "frac": round(achieved / (PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_F32_TFLOPS), 4),
                 "traffic": round(traffic) if traffic else None, "traffic_source": traffic_src,
-                "flops_per_launch": score_flops, "avg_launch_us": round(score_s * 1e6, 2)}
+                "flops_per_launch": score_flops, "avg_launch_us": round(score_s * 1e6, 2),
+                "timing": "kernel's own timestamps, first workgroup start to last workgroup end",
+                "event_avg_us": round(per_layer["score"] * 1e3, 2)}
     # attention and kept-chunk bytes, as context
     T = k * w.chunk_size
     attn_flops = 4.0 * w.head_dim * w.n_q_heads * (w.n_suffix * T + w.n_suffix * (w.n_suffix + 1) / 2)

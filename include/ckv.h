@@ -189,10 +189,12 @@ typedef struct ckv_store ckv_store; /* storage tier, see ckv_store_open */
                                        attention instead of reading spans in place */
 #define CKV_CTX_STAGE_TIMING 0x4    /* record HIP events between the stages of every
                                        layer (see ckv_ctx_stage_times) */
-#define CKV_CTX_SCORE_TIMING 0x8    /* time only the chunk-scoring main kernel: two
-                                       events per layer instead of six (bf16: the
-                                       kernel's own launch start and stop timestamps,
-                                       so the interval is its execution alone);
+#define CKV_CTX_SCORE_TIMING 0x8    /* time only the chunk-scoring main kernel and
+                                       nothing else (bf16: from its first workgroup's
+                                       start to its last workgroup's end, stamped by
+                                       the kernel from the 100 MHz realtime counter,
+                                       so no event sits between the launches; fp32:
+                                       two events per layer);
                                        ckv_ctx_stage_times then reports the score stage
                                        and zero for the others */
 
@@ -395,9 +397,11 @@ typedef struct ckv_layer_stats {
  * every layer run since the context was created or last reset, and that
  * number of layers in *n_layers.  Requires CKV_CTX_STAGE_TIMING or
  * CKV_CTX_SCORE_TIMING (then only ms[CKV_STAGE_SCORE] is filled, and only
- * layers that ran scoring are counted); waits for the events of the layers
- * not yet accounted.  Stage times come from events
- * recorded on each layer's compute stream between its kernel launches. */
+ * layers that ran scoring are counted); waits for the layers not yet
+ * accounted (with CKV_CTX_SCORE_TIMING on bf16, for the whole device).  Stage
+ * times come from events recorded on each layer's compute stream between its
+ * kernel launches, or, for the bf16 scoring kernel alone, from the kernel's
+ * own timestamps. */
 ckv_status ckv_ctx_stage_times(ckv_ctx* ctx, double* ms, int64_t* n_layers);
 
 /* Runs layer `layer` (0 <= layer < n_layers; the first layer after creation

@@ -131,13 +131,14 @@ struct ScorePlan {
   size_t off_part, off_mc, off_z, off_flags, bytes;
 };
 ScorePlan make_score_plan(const ckv_dims* d);
-// Optional timing events of the main kernel: with both, the kernel is
-// launched with them as its own start and stop timestamps (the interval is
-// the kernel's execution alone); with only main_stop, that event is recorded
-// between the main kernel and the fold.
+// Optional timing of the main kernel: main_stop is recorded between the main
+// kernel and the fold; main_span (bf16 only; score_span_words(d) words)
+// receives every workgroup's start and end, in ticks of the 100 MHz realtime
+// counter (the kernel's span is the earliest start to the latest end).
+int64_t score_span_words(const ckv_dims* d);
 ckv_status launch_score(const ckv_dims* d, const void* q, const void* k, double* scores,
                         void* ws, size_t ws_bytes, hipStream_t st,
-                        hipEvent_t main_stop = nullptr, hipEvent_t main_start = nullptr);
+                        hipEvent_t main_stop = nullptr, unsigned long long* main_span = nullptr);
 
 size_t select_ws_bytes(int64_t m);
 ckv_status launch_select(const double* scores, int64_t m, int64_t k, int32_t* sel, void* ws,

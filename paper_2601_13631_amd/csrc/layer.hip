@@ -146,6 +146,12 @@ struct ckv_ctx {
   hipEvent_t tev[kRing][CKV_N_STAGES + 1] = {};
   int64_t t_issued = 0, t_done = 0;
   double t_ms[CKV_N_STAGES] = {};
+  // scoring-kernel timing (bf16): per scored layer, every workgroup's start
+  // and end from the realtime counter (span_words per layer), in a device ring
+  static constexpr int kSpanRing = 1024;
+  unsigned long long* tspan = nullptr;  // [kSpanRing][span_words]
+  int64_t span_words = 0;
+  bool span_mode = false;
 };
 
 namespace {
@@ -258,6 +264,7 @@ ckv_status free_ctx(ckv_ctx* c) {
   for (auto& set : c->tev)
     for (auto& e : set)
       if (e) (void)hipEventDestroy(e);
+  (void)hipFree(c->tspan);
   if (c->ev_sel) (void)hipEventDestroy(c->ev_sel);
   if (c->ev_dem) (void)hipEventDestroy(c->ev_dem);
   if (c->demand) (void)hipStreamDestroy(c->demand);
@@ -371,6 +378,40 @@ ckv_status harvest_one(ckv_ctx* c) {
     c->t_ms[s] += ms;
   }
   ++c->t_done;
+  return CKV_OK;
+}
+
+// Ticks of the realtime counter the scoring kernel's spans are measured in.
+constexpr double kRealtimeTickMs = 1e-5;  // 100 MHz
+
+// Adds the span (earliest workgroup start to latest end) of every scored
+// layer not yet accounted; waits for the device.
+ckv_status harvest_spans(ckv_ctx* c) {
+  if (c->t_done == c->t_issued) return CKV_OK;
+  CKV_HIP(hipDeviceSynchronize());
+  const int64_t wpl = c->span_words;
+  std::vector<unsigned long long> h((size_t)(wpl * ckv_ctx::kSpanRing));
+  CKV_HIP(hipMemcpy(h.data(), c->tspan, h.size() * sizeof(unsigned long long),
+                    hipMemcpyDeviceToHost));
+  for (int64_t i = c->t_done; i < c->t_issued; ++i) {
+    const unsigned long long* t = h.data() + (i % ckv_ctx::kSpanRing) * wpl;
+    unsigned long long t0 = ~0ull, t1 = 0;
+    for (int64_t w = 0; w < wpl; w += 2) {
+      t0 = std::min(t0, t[w]);
+      t1 = std::max(t1, t[w + 1]);
+    }
+    if (t1 > t0) c->t_ms[CKV_STAGE_SCORE] += (double)(t1 - t0) * kRealtimeTickMs;
+  }
+  c->t_done = c->t_issued;
+  return CKV_OK;
+}
+
+ckv_status harvest_all(ckv_ctx* c) {
+  if (c->span_mode) return harvest_spans(c);
+  while (c->t_done < c->t_issued) {
+    ckv_status s = harvest_one(c);
+    if (s != CKV_OK) return s;
+  }
   return CKV_OK;
 }
 
@@ -504,9 +545,16 @@ ckv_status ckv_ctx_create(const ckv_dims* dims, int32_t n_layers, double keep_ra
     CKV_HIP_ALLOC(hipEventCreateWithFlags(&c->ev_sel, hipEventDisableTiming));
     CKV_HIP_ALLOC(hipEventCreateWithFlags(&c->ev_dem, hipEventDisableTiming));
   }
-  if (flags & (CKV_CTX_STAGE_TIMING | CKV_CTX_SCORE_TIMING))
+  c->span_mode = (flags & CKV_CTX_SCORE_TIMING) && !(flags & CKV_CTX_STAGE_TIMING) &&
+                 dims->dtype == CKV_DTYPE_BF16;
+  if (c->span_mode) {
+    c->span_words = score_span_words(dims);
+    CKV_HIP_ALLOC(hipMalloc((void**)&c->tspan, (size_t)(c->span_words * ckv_ctx::kSpanRing) *
+                                                   sizeof(unsigned long long)));
+  } else if (flags & (CKV_CTX_STAGE_TIMING | CKV_CTX_SCORE_TIMING)) {
     for (auto& set : c->tev)
       for (auto& e : set) CKV_HIP_ALLOC(hipEventCreate(&e));
+  }
   *out = c;
   return CKV_OK;
 }
@@ -516,8 +564,8 @@ ckv_status ckv_ctx_stage_times(ckv_ctx* ctx, double* ms, int64_t* n_layers) {
   if (!ctx || !ms || !n_layers) CKV_FAIL(CKV_EINVAL, "NULL argument");
   if (!(ctx->flags & (CKV_CTX_STAGE_TIMING | CKV_CTX_SCORE_TIMING)))
     CKV_FAIL(CKV_ESTATE, "context created without CKV_CTX_STAGE_TIMING or CKV_CTX_SCORE_TIMING");
-  while (ctx->t_done < ctx->t_issued) {
-    ckv_status s = harvest_one(ctx);
+  {
+    ckv_status s = harvest_all(ctx);
     if (s != CKV_OK) return s;
   }
   for (int s = 0; s < CKV_N_STAGES; ++s) ms[s] = ctx->t_ms[s];
@@ -710,8 +758,8 @@ ckv_status ckv_ctx_reset(ckv_ctx* ctx) {
   ctx->period_first = -1;
   ctx->broken = false;
   ctx->inject_layer = -1;
-  while (ctx->t_done < ctx->t_issued) {
-    ckv_status s = harvest_one(ctx);
+  {
+    ckv_status s = harvest_all(ctx);
     if (s != CKV_OK) return s;
   }
   for (double& x : ctx->t_ms) x = 0.0;
@@ -827,16 +875,23 @@ ckv_status run_layer(ckv_ctx* c, const LayerArgs& la, ckv_layer_stats* stats) {
   }
 
   hipEvent_t* tev = nullptr;
+  unsigned long long* span = nullptr;
   // a reused layer has no scoring kernel to time alone
-  if ((c->flags & CKV_CTX_STAGE_TIMING) || ((c->flags & CKV_CTX_SCORE_TIMING) && !reuse)) {
+  if (c->span_mode) {
+    if (!reuse) {
+      if (c->t_issued - c->t_done >= ckv_ctx::kSpanRing) {  // ring full: account it first
+        s = harvest_spans(c);
+        if (s != CKV_OK) return s;
+      }
+      span = c->tspan + c->span_words * (c->t_issued % ckv_ctx::kSpanRing);
+    }
+  } else if ((c->flags & CKV_CTX_STAGE_TIMING) || ((c->flags & CKV_CTX_SCORE_TIMING) && !reuse)) {
     if (c->t_issued - c->t_done >= ckv_ctx::kRing) {  // reuse the oldest set: account it first
       s = harvest_one(c);
       if (s != CKV_OK) return s;
     }
     tev = c->tev[c->t_issued % ckv_ctx::kRing];
-    // every stage: the set starts here; the scoring kernel alone: its own
-    // launch brackets it (bf16), else the set starts here too
-    if (all_stages(c) || d->dtype != CKV_DTYPE_BF16) CKV_HIP(hipEventRecord(tev[0], st));
+    CKV_HIP(hipEventRecord(tev[0], st));  // the set starts here
   }
   auto mark = [&](int i) -> ckv_status {
     if (tev && all_stages(c)) CKV_HIP(hipEventRecord(tev[i], st));
@@ -844,10 +899,10 @@ ckv_status run_layer(ckv_ctx* c, const LayerArgs& la, ckv_layer_stats* stats) {
   };
 
   if (!reuse) {
-    const bool bracket = tev && !all_stages(c) && d->dtype == CKV_DTYPE_BF16;
     s = launch_score(d, io->q, io->k_probe, scores, ws, c->ws_score, st, tev ? tev[1] : nullptr,
-                     bracket ? tev[0] : nullptr);
+                     span);
     if (s != CKV_OK) return s;
+    if (span) ++c->t_issued;
     if ((s = mark(2)) != CKV_OK) return s;
     s = launch_select(scores, c->m, k, sel, nullptr, 0, st);
     if (s != CKV_OK) return s;

@@ -28,8 +28,6 @@
 //
 // All sums have a fixed order: results are bitwise reproducible run to run.
 
-#include <hip/hip_ext.h>
-
 #include <cfloat>
 
 #include "ckv_internal.h"
@@ -98,6 +96,7 @@ struct ScoreArgs {
   float c1;            // sm_scale * log2(e)
   ScoreWork w;
   uint32_t nwg, nwg_padded;  // Hkv*RB*NS workgroups (the flags are indexed by workgroup)
+  unsigned long long* tstamp;  // optional [nwg][2]: each workgroup's start and end (realtime clock)
 };
 
 constexpr int kStage = 64;  // keys per LDS stage: two 32-key subtiles
@@ -712,6 +711,9 @@ __global__ __launch_bounds__(kWaves * 64, 2) void score_bf16_kernel(ScoreArgs a)
   __shared__ __attribute__((aligned(16))) uint16_t lds[2 * kStage * SubtileLds<D>::kRow];
   const uint32_t w = xcd_remap(blockIdx.x, a.nwg_padded);
   if (w >= a.nwg) return;
+  // timing mode: each workgroup's start and end from the 100 MHz realtime
+  // counter, one 16-byte store per workgroup
+  const unsigned long long t_start = a.tstamp ? __builtin_amdgcn_s_memrealtime() : 0;
   const Segment sg = segment_of(a.w, a.n, (int)w);
   const int g = sg.rbh / a.w.RB, row0 = (sg.rbh % a.w.RB) * kBlockRows;
   bf16x8 qf[2][D / 16];  // loaded by run_segment_fast
@@ -720,6 +722,13 @@ __global__ __launch_bounds__(kWaves * 64, 2) void score_bf16_kernel(ScoreArgs a)
   const int any_of = __syncthreads_or(of ? 1 : 0);
   if (threadIdx.x == 0) a.flags[sg.rbh * a.w.NS + sg.s] = any_of;
   store_stats(a, sg.rbh, sg.s, st);
+  if (a.tstamp) {
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      const unsigned long long t_end = __builtin_amdgcn_s_memrealtime();
+      *reinterpret_cast<ulonglong2*>(a.tstamp + 2 * w) = make_ulonglong2(t_start, t_end);
+    }
+  }
 }
 
 // Fold pass, one workgroup per row block: redoes exactly (against its own
@@ -1038,8 +1047,14 @@ ScorePlan make_score_plan(const ckv_dims* d) {
   return p;
 }
 
+int64_t score_span_words(const ckv_dims* d) {
+  const ScorePlan p = make_score_plan(d);
+  return 2 * (int64_t)d->n_kv_heads * p.w.RB * p.w.NS;
+}
+
 ckv_status launch_score(const ckv_dims* d, const void* q, const void* k, double* scores, void* ws,
-                        size_t ws_bytes, hipStream_t st, hipEvent_t main_stop, hipEvent_t main_start) {
+                        size_t ws_bytes, hipStream_t st, hipEvent_t main_stop,
+                        unsigned long long* main_span) {
   const ScorePlan p = make_score_plan(d);
   if (p.bytes == 0) CKV_FAIL(CKV_EUNSUPPORTED, "shape too large for the scoring decomposition");
   if (ws_bytes < p.bytes) CKV_FAIL(CKV_EINVAL, "score workspace too small: %zu < %zu", ws_bytes, p.bytes);
@@ -1064,17 +1079,13 @@ ckv_status launch_score(const ckv_dims* d, const void* q, const void* k, double*
     a.R = p.rows; a.c = d->chunk_size; a.c1 = c1; a.w = p.w;
     a.nwg = nwg;
     a.nwg_padded = (uint32_t)align_up(nwg, 8);
+    a.tstamp = main_span;
     dim3 grid(a.nwg_padded), block(kWaves * 64);
     const dim3 fold_grid((unsigned)(d->n_kv_heads * p.w.RB));
 #define CKV_SCORE_LAUNCH(DD, MM)                                                           \
   do {                                                                                     \
-    if (main_start && main_stop) {                                                         \
-      hipExtLaunchKernelGGL((score_bf16_kernel<DD, MM>), grid, block, 0, st, main_start,   \
-                            main_stop, 0, a);                                              \
-    } else {                                                                               \
-      hipLaunchKernelGGL((score_bf16_kernel<DD, MM>), grid, block, 0, st, a);              \
-      if (main_stop) CKV_HIP(hipEventRecord(main_stop, st));                              \
-    }                                                                                      \
+    hipLaunchKernelGGL((score_bf16_kernel<DD, MM>), grid, block, 0, st, a);                \
+    if (main_stop) CKV_HIP(hipEventRecord(main_stop, st));                                \
     hipLaunchKernelGGL((score_fold_kernel<DD, MM>), fold_grid, block, 0, st, a);           \
   } while (0)
     if (d->head_dim == 128) {
@@ -1112,10 +1123,8 @@ ckv_status launch_score(const ckv_dims* d, const void* q, const void* k, double*
       case kC32: hipLaunchKernelGGL((score_f32_kernel<64, kC32>), grid, block, 0, st, a); break;
       default: hipLaunchKernelGGL((score_f32_kernel<64, kC32x>), grid, block, 0, st, a); break;
     }
-    if (main_stop) {
-      if (main_start) CKV_FAIL(CKV_EUNSUPPORTED, "kernel-bracketing timing is for the bf16 path");
-      CKV_HIP(hipEventRecord(main_stop, st));
-    }
+    if (main_span) CKV_FAIL(CKV_EUNSUPPORTED, "in-kernel timing is for the bf16 path");
+    if (main_stop) CKV_HIP(hipEventRecord(main_stop, st));
     hipLaunchKernelGGL(score_fold_f32_kernel, dim3((unsigned)(d->n_kv_heads * p.w.RB)),
                        dim3(kWaveRows), 0, st, mc, z, p.w);
   }
