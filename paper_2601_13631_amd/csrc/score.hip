@@ -948,6 +948,9 @@ __global__ __launch_bounds__(64) void score_f32_kernel(ScoreArgsF32 a) {
 // in order (16-byte partial loads, 32-byte weight loads), then a fixed tree
 // over LDS reduces the 256 sums.
 constexpr int kReduceThreads = 256;
+constexpr int kReduceWide = 4;       // chunks per workgroup of the many-chunk reduction
+constexpr int kReduceUnroll = 4;     // (head, row group) pairs per step
+constexpr int64_t kReduceWideChunks = 4096;  // chunk count from which it is used
 
 __global__ __launch_bounds__(kReduceThreads) void chunk_reduce_kernel(
     const float* __restrict__ part, const double* __restrict__ w, double* __restrict__ A,
@@ -990,6 +993,101 @@ __global__ __launch_bounds__(kReduceThreads) void chunk_reduce_kernel(
 #pragma unroll
     for (int off = 32; off >= 1; off >>= 1) s += __shfl_xor(s, off);
     if (tid == 0) A[j] = s;
+  }
+}
+
+// The same reduction for many chunks: NJ consecutive chunks per workgroup,
+// which share each weight load while they lie in one segment (SAME), and a
+// flat walk over (head, 4-row group) pairs, UNR pairs per step with all their
+// loads issued before any is used (indices clamped, so no load waits on a
+// predicate).  Each chunk's sum takes its terms in a fixed order (thread i:
+// pairs i, i + 256, ...), then a fixed tree over LDS.
+template <int NJ, int UNR, bool SAME>
+__device__ __forceinline__ void reduce_flat_sums(const float* __restrict__ part,
+                                                 const double* __restrict__ w, const ScoreWork& wk,
+                                                 int Hkv, int R, int64_t m_pad, int log2_rpb,
+                                                 const int64_t (&jc)[NJ], const int (&seg)[NJ],
+                                                 double (&s)[NJ]) {
+  constexpr int NW = SAME ? 1 : NJ;  // weight sets per pair
+  const int nq = (R + 3) / 4;        // 4-row groups per head
+  const int total = Hkv * nq;
+  for (int base = threadIdx.x; base < total; base += UNR * kReduceThreads) {
+    f32x4 pv[UNR][NJ];
+    double wv[UNR][NW][4];
+    int rr[UNR];
+#pragma unroll
+    for (int u = 0; u < UNR; ++u) {
+      const int idx = min(base + u * kReduceThreads, total - 1);
+      const int g = idx / nq, r = 4 * (idx - g * nq);
+      rr[u] = r;
+      const float* p = part + (int64_t)g * m_pad * wk.ldp + r;
+#pragma unroll
+      for (int q = 0; q < NJ; ++q) pv[u][q] = *reinterpret_cast<const f32x4*>(p + jc[q] * wk.ldp);
+      const int rbh = g * wk.RB + (r >> log2_rpb);
+      const double* wb = w + (int64_t)rbh * wk.NS * wk.rpb + (r & (wk.rpb - 1));
+#pragma unroll
+      for (int q = 0; q < NW; ++q) {
+        const double* wr = wb + (int64_t)seg[q] * wk.rpb;
+        const double2 w01 = *reinterpret_cast<const double2*>(wr);
+        const double2 w23 = *reinterpret_cast<const double2*>(wr + 2);
+        wv[u][q][0] = w01.x; wv[u][q][1] = w01.y; wv[u][q][2] = w23.x; wv[u][q][3] = w23.y;
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < UNR; ++u) {
+      if (base + u * kReduceThreads >= total) break;
+      const int r = rr[u];
+#pragma unroll
+      for (int q = 0; q < NJ; ++q)
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          if (r + e < R) s[q] += (double)pv[u][q][e] * wv[u][SAME ? 0 : q][e];
+    }
+  }
+}
+
+template <int NJ, int UNR>
+__global__ __launch_bounds__(kReduceThreads) void chunk_reduce_flat_kernel(
+    const float* __restrict__ part, const double* __restrict__ w, double* __restrict__ A,
+    ScoreWork wk, int Hkv, int R, int64_t m, int64_t m_pad, int c, int log2_rpb) {
+  __shared__ double red[NJ][kReduceThreads];
+  const int64_t j0 = (int64_t)blockIdx.x * NJ;
+  const int tid = threadIdx.x;
+  int64_t jc[NJ];
+  int seg[NJ];
+  bool same = true;
+#pragma unroll
+  for (int q = 0; q < NJ; ++q) {
+    jc[q] = j0 + q < m ? j0 + q : m - 1;
+    seg[q] = wk.seg_of_unit((int)(jc[q] * c / wk.UK));
+    same = same && seg[q] == seg[0];
+  }
+  double s[NJ];
+#pragma unroll
+  for (int q = 0; q < NJ; ++q) s[q] = 0.0;
+  if (same)  // uniform
+    reduce_flat_sums<NJ, UNR, true>(part, w, wk, Hkv, R, m_pad, log2_rpb, jc, seg, s);
+  else  // a workgroup across a segment boundary: one pair per step (the order is the same)
+    reduce_flat_sums<NJ, 1, false>(part, w, wk, Hkv, R, m_pad, log2_rpb, jc, seg, s);
+#pragma unroll
+  for (int q = 0; q < NJ; ++q) red[q][tid] = s[q];
+  __syncthreads();
+#pragma unroll
+  for (int width = kReduceThreads / 2; width >= 64; width >>= 1) {
+    if (tid < width) {
+#pragma unroll
+      for (int q = 0; q < NJ; ++q) red[q][tid] += red[q][tid + width];
+    }
+    __syncthreads();
+  }
+  if (tid < 64) {
+#pragma unroll
+    for (int q = 0; q < NJ; ++q) {
+      double x = red[q][tid];
+#pragma unroll
+      for (int off = 32; off >= 1; off >>= 1) x += __shfl_xor(x, off);
+      if (tid == 0 && j0 + q < m) A[j0 + q] = x;
+    }
   }
 }
 
@@ -1130,8 +1228,17 @@ ckv_status launch_score(const ckv_dims* d, const void* q, const void* k, double*
   }
   CKV_HIP(hipGetLastError());
   const int log2_rpb = p.w.rpb == 256 ? 8 : 6;
-  hipLaunchKernelGGL(chunk_reduce_kernel, dim3((unsigned)p.m), dim3(kReduceThreads), 0, st, part,
-                     z, scores, p.w, d->n_kv_heads, p.rows, m_pad, d->chunk_size, log2_rpb);
+  // one chunk per workgroup while the chunks are few (the reduction is bound
+  // by load latency); with many chunks (the partials then run to hundreds of
+  // MB) kReduceWide chunks per workgroup share each weight load
+  if (p.m < kReduceWideChunks)
+    hipLaunchKernelGGL(chunk_reduce_kernel, dim3((unsigned)p.m), dim3(kReduceThreads), 0, st, part,
+                       z, scores, p.w, d->n_kv_heads, p.rows, m_pad, d->chunk_size, log2_rpb);
+  else
+    hipLaunchKernelGGL((chunk_reduce_flat_kernel<kReduceWide, kReduceUnroll>),
+                       dim3((unsigned)ceil_div(p.m, kReduceWide)), dim3(kReduceThreads), 0, st,
+                       part, z, scores, p.w, d->n_kv_heads, p.rows, p.m, m_pad, d->chunk_size,
+                       log2_rpb);
   CKV_HIP(hipGetLastError());
   return CKV_OK;
 }

@@ -39,6 +39,11 @@ SCORE_CASES = [
     W(5, 1, 2, 1, 64, 4),                # one query, prefix shorter than one subtile
     W(31, 1, 4, 2, 128, 32),             # a single partial chunk (m = 1)
     W(64, 1, 1, 1, 128, 64),             # exactly one stage and one chunk, G = 1
+    # 4,096 chunks or more: the reduction's many-chunk kernel, with a ragged
+    # row count (6 and 15 rows), a chunk count that is not a multiple of its
+    # chunks per workgroup, and (c = 32) workgroups across segment boundaries
+    W(131099, 3, 2, 1, 64, 32, seed=5),
+    W(16411, 5, 3, 1, 128, 4, seed=6),
 ]
 
 
@@ -108,11 +113,26 @@ def test_select_exchange_exact(m):
             assert np.array_equal(sel, ref), (m, k)
 
 
+SPECIAL = np.array([np.nan, -0.0, 0.0, -np.inf, np.inf, 1.0, np.nan, -1.0, 5e-324, -5e-324])
+
+
 def test_select_special_values():
-    A = np.array([np.nan, -0.0, 0.0, -np.inf, np.inf, 1.0, np.nan, -1.0, 5e-324, -5e-324])
+    A = SPECIAL
     for k in range(1, len(A) + 1):
         sel = gpu_select(torch.from_numpy(A).to(DEV), k).cpu().numpy()
         assert np.array_equal(sel, oracle.select_topk(A, k)), k
+
+
+# the register paths with 2 and 4 scores per thread and the LDS-histogram path
+@pytest.mark.parametrize("m", [1500, 4000, 9000, 20000])
+def test_select_special_values_large(m):
+    rng = np.random.default_rng(m + 1)
+    A = rng.normal(0, 1, m) * np.exp(rng.normal(0, 30, m))  # both signs, wide exponents
+    pos = rng.choice(m, 40 * len(SPECIAL), replace=False)
+    A[pos] = np.tile(SPECIAL, 40)
+    for k in sorted({1, 45, 80, 81, m // 3, m - 50, m}):
+        sel = gpu_select(torch.from_numpy(A).to(DEV), k).cpu().numpy()
+        assert np.array_equal(sel, oracle.select_topk(A, k)), (m, k)
 
 
 @pytest.mark.parametrize("c,d,n", [(4, 128, 37), (16, 64, 1000), (32, 128, 1000), (64, 128, 3000)])
