@@ -1,7 +1,7 @@
 // select.hip -- standalone top-k ContiguousChunk selection (Sec. 4.4).
 //
 // Up to kSmallKeys scores: one workgroup of 1024 threads holds every key in
-// registers (E = 1, 2 or 4 consecutive scores per thread) and runs the
+// registers (E = 1, 2, 4 or 8 consecutive scores per thread) and runs the
 // register-resident radix select of select_regs.h.  Larger m: one 256-thread
 // workgroup runs select_topk_block (select_block.h) with the keys cached in
 // LDS when m <= kLdsKeys.  Both produce the same set under the same total
@@ -14,7 +14,7 @@ namespace {
 
 constexpr int64_t kLdsKeys = 16384;  // 128 KiB of keys
 constexpr int kSmallThreads = 1024;
-constexpr int64_t kSmallKeys = 4 * kSmallThreads;
+constexpr int64_t kSmallKeys = 8 * kSmallThreads;
 
 template <int THREADS>
 __global__ __launch_bounds__(THREADS) void select_kernel(const double* __restrict__ scores,
@@ -49,8 +49,10 @@ ckv_status launch_select(const double* scores, int64_t m, int64_t k, int32_t* se
       launch_small<1>(scores, (int)m, (int)k, sel, st);
     else if (m <= 2 * kSmallThreads)
       launch_small<2>(scores, (int)m, (int)k, sel, st);
-    else
+    else if (m <= 4 * kSmallThreads)
       launch_small<4>(scores, (int)m, (int)k, sel, st);
+    else
+      launch_small<8>(scores, (int)m, (int)k, sel, st);
     CKV_HIP(hipGetLastError());
     return CKV_OK;
   }

@@ -5,7 +5,8 @@
 // Keeps the k largest of m fp64 chunk scores under the total order (score
 // descending, index ascending) and writes their indices in ascending order.
 // A radix select on order-preserving 64-bit keys (select_block.h's order_key)
-// with 4-bit digits whose counts come from wave ballots (no LDS atomics: the
+// with 4-bit digits whose counts come from wave ballots, or for 4 or more keys
+// per thread from packed per-lane counters summed by DPP (no LDS atomics: the
 // chunk scores of a layer share their high bits, so per-bin atomics would all
 // collide): the first digit ends at the highest bit where the smallest and
 // largest key differ, every later one is the next 4 bits down; the search ends
@@ -51,6 +52,52 @@ __device__ __forceinline__ void wave_minmax(uint64_t& lo, uint64_t& hi) {
   lo = la;
   hi = ha;
   minmax_with(lo, hi, lb, hb);
+}
+
+// x + (x of lane l ^ 16) and x + (x of lane l ^ 32): the swaps hand each lane
+// its own value and its partner's, in some order, and the sum is symmetric.
+__device__ __forceinline__ uint32_t pair_sum16(uint32_t x) {
+  const auto r = __builtin_amdgcn_permlane16_swap(x, x, false, false);
+  return r[0] + r[1];
+}
+__device__ __forceinline__ uint32_t pair_sum32(uint32_t x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(x, x, false, false);
+  return r[0] + r[1];
+}
+
+// The wave's count of keys per digit value 0..15 (digit 16: not a candidate),
+// for E >= 4 keys per lane, without ballots: each lane counts its digits in
+// 4-bit fields of one 64-bit word (E <= 15), the fields are spread to bytes
+// and summed over each row of 16 lanes by DPP (at most 16 * E <= 255), then
+// widened to 16-bit fields and summed over the four rows by the permlane
+// swaps.  Lane 15 returns digit pair (2i, 2i + 1) in cnt[i] (low, high half).
+template <int E>
+__device__ __forceinline__ void wave_digit_counts(const int (&cd)[E], uint32_t (&cnt)[8]) {
+  static_assert(E <= 15, "4-bit per-lane fields");
+  uint64_t acc = 0;
+#pragma unroll
+  for (int e = 0; e < E; ++e) acc += cd[e] < 16 ? 1ull << (4 * cd[e]) : 0ull;
+  const uint32_t lo = (uint32_t)acc, hi = (uint32_t)(acc >> 32);
+  // byte j of by[q]: digit 8 * (q / 2) + 2 * j + (q % 2)
+  uint32_t by[4] = {lo & 0x0F0F0F0Fu, (lo >> 4) & 0x0F0F0F0Fu, hi & 0x0F0F0F0Fu,
+                    (hi >> 4) & 0x0F0F0F0Fu};
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {  // inclusive sums along the row: lane 15 holds the row's
+    by[q] += dpp32<kDppRowShr1>(by[q]);
+    by[q] += dpp32<kDppRowShr2>(by[q]);
+    by[q] += dpp32<kDppRowShr4>(by[q]);
+    by[q] += dpp32<kDppRowShr8>(by[q]);
+  }
+  // 16-bit fields: cnt[i] = (digit 2i, digit 2i + 1); by[q] byte j is digit
+  // 8 * (q / 2) + 2 * j + (q % 2), so digit pair i = 4 * (q / 2) + j comes from
+  // byte j of by[2 * (q / 2)] (even digit) and of by[2 * (q / 2) + 1] (odd)
+#pragma unroll
+  for (int h = 0; h < 2; ++h)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const uint32_t ev = (by[2 * h] >> (8 * j)) & 0xFFu, od = (by[2 * h + 1] >> (8 * j)) & 0xFFu;
+      cnt[4 * h + j] = pair_sum32(pair_sum16(ev | (od << 16)));
+    }
 }
 
 // Called by all THREADS threads; m <= E * THREADS, 1 <= k <= m.  Thread t
@@ -103,15 +150,26 @@ __device__ __forceinline__ void select_topk_regs(const double* __restrict__ scor
 #pragma unroll
       for (int e = 0; e < E; ++e)
         cd[e] = valid[e] && (x[e] & mask) == prefix ? (int)((x[e] >> shift) & 15) : 16;
-      int mine = 0;
+      if constexpr (E >= 4) {  // vector counts (ballots would need 16 * E scalar masks)
+        uint32_t cnt[8];
+        wave_digit_counts<E>(cd, cnt);
+        if (lane == 15)
 #pragma unroll
-      for (int b = 0; b < 16; ++b) {
-        int c = 0;
+          for (int i = 0; i < 8; ++i) {
+            sh.whist[wave][2 * i] = cnt[i] & 0xFFFFu;
+            sh.whist[wave][2 * i + 1] = cnt[i] >> 16;
+          }
+      } else {
+        int mine = 0;
 #pragma unroll
-        for (int e = 0; e < E; ++e) c += __popcll(__ballot(cd[e] == b));
-        if (lane == b) mine = c;
+        for (int b = 0; b < 16; ++b) {
+          int c = 0;
+#pragma unroll
+          for (int e = 0; e < E; ++e) c += __popcll(__ballot(cd[e] == b));
+          if (lane == b) mine = c;
+        }
+        if (lane < 16) sh.whist[wave][lane] = (uint32_t)mine;
       }
-      if (lane < 16) sh.whist[wave][lane] = (uint32_t)mine;
       __syncthreads();
       if (wave == 0) {
         // lane i < 16 takes digit 15 - i; inclusive scan over i gives the
