@@ -600,24 +600,28 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(AttnArgsF32 a) {
     for (int e = 0; e < D; ++e) o[e] = fmaf(p, vr[e], o[e] * alpha);
     m = mn;
   }
-  // butterfly merge of (m, l, o) across the wave
+  // merge of the 64 lanes' (m, l, o) through LDS: the wave's maximum
+  // reference, each lane's scale, then lane e sums element e over the lanes
+  __shared__ float so[64][D + 1];  // padded: lane j's row starts one bank later
+  __shared__ float sa[64];
 #pragma unroll
-  for (int off = 1; off < 64; off <<= 1) {
-    const float m2 = __shfl_xor(m, off), l2 = __shfl_xor(l, off);
-    const float mn = fmaxf(m, m2);
-    const float a1 = m == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m - mn);
-    const float a2 = m2 == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m2 - mn);
-    l = l * a1 + l2 * a2;
+  for (int e = 0; e < D; ++e) so[lane][e] = o[e];
+  float M = m;
 #pragma unroll
-    for (int e = 0; e < D; ++e) o[e] = o[e] * a1 + __shfl_xor(o[e], off) * a2;
-    m = mn;
-  }
-  const float inv = 1.f / l;
+  for (int off = 1; off < 64; off <<= 1) M = fmaxf(M, __shfl_xor(M, off));
+  const float scale = m == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m - M);
+  float L = l * scale;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) L += __shfl_xor(L, off);
+  sa[lane] = scale;
+  __syncthreads();
+  const float inv = L > 0.f ? 1.f / L : 0.f;
   float* dst = a.out + rid * D;
-  // every lane holds the merged row; lane e writes element e
-#pragma unroll
-  for (int e = 0; e < D; ++e)
-    if (e % 64 == lane) dst[e] = o[e] * inv;
+  for (int e = lane; e < D; e += 64) {
+    float acc = 0.f;
+    for (int j = 0; j < 64; ++j) acc = fmaf(so[j][e], sa[j], acc);
+    dst[e] = acc * inv;
+  }
 }
 
 }  // namespace

@@ -1119,9 +1119,10 @@ ScorePlan make_score_plan(const ckv_dims* d) {
   const int64_t H_RB = (int64_t)d->n_kv_heads * w.RB;
   // A fixed grid target (two 256-thread workgroups per CU of a 256-CU MI355X
   // for bf16) keeps the decomposition, and so every rounding, independent of
-  // the device the library runs on.  Segments keep at least 8 stages.
+  // the device the library runs on.  Segments keep at least 8 stages of the
+  // pipelined bf16 kernel, or 64 keys of the one-wave fp32 kernel.
   const int64_t target = f32 ? 1024 : 512;
-  const int64_t min_units = std::max<int64_t>(1, 512 / UK);
+  const int64_t min_units = std::max<int64_t>(1, (f32 ? 64 : 512) / UK);
   int64_t NS = std::max<int64_t>(1, target / H_RB);
   NS = std::min<int64_t>(NS, std::max<int64_t>(1, U / min_units));
   // bytes == 0 marks an unsupported shape
