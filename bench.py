@@ -624,7 +624,8 @@ def main() -> int:
                 "frac": round(achieved / (PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_F32_TFLOPS), 4),
                 "traffic": round(traffic) if traffic else None, "traffic_source": traffic_src,
                 "flops_per_launch": score_flops, "avg_launch_us": round(score_s * 1e6, 2),
-                "timing": "kernel's own timestamps, first workgroup start to last workgroup end",
+                "timing": ("kernel's own timestamps, first workgroup start to last workgroup end"
+                           if w.dtype == "bf16" else "HIP events around the kernel"),
                 "event_avg_us": round(per_layer["score"] * 1e3, 2)}
     # attention and kept-chunk bytes, as context
     T = k * w.chunk_size
