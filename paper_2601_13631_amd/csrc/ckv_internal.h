@@ -141,8 +141,9 @@ ckv_status launch_score(const ckv_dims* d, const void* q, const void* k, double*
                         hipEvent_t main_stop = nullptr, unsigned long long* main_span = nullptr);
 
 size_t select_ws_bytes(int64_t m);
+// sel_copy (optional, device): a second array that receives the same k indices.
 ckv_status launch_select(const double* scores, int64_t m, int64_t k, int32_t* sel, void* ws,
-                         size_t ws_bytes, hipStream_t st);
+                         size_t ws_bytes, hipStream_t st, int32_t* sel_copy = nullptr);
 
 // Chunk addressing for gather/attention: chunk u's K rows start at
 // k_base + off(u) * chunk_stride elements (V likewise from v_base), where

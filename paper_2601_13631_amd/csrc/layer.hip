@@ -904,13 +904,11 @@ ckv_status run_layer(ckv_ctx* c, const LayerArgs& la, ckv_layer_stats* stats) {
     if (s != CKV_OK) return s;
     if (span) ++c->t_issued;
     if ((s = mark(2)) != CKV_OK) return s;
-    s = launch_select(scores, c->m, k, sel, nullptr, 0, st);
+    // with Periods the selection also keeps the set for the rest of the Period
+    s = launch_select(scores, c->m, k, sel, nullptr, 0, st, c->period > 1 ? pset : nullptr);
     if (s != CKV_OK) return s;
     if ((s = mark(3)) != CKV_OK) return s;
-    if (c->period > 1) {  // keep the set for the rest of the Period
-      CKV_HIP(hipMemcpyAsync(pset, sel, (size_t)k * sizeof(int32_t), hipMemcpyDeviceToDevice, st));
-      c->period_first = layer;
-    }
+    if (c->period > 1) c->period_first = layer;
   } else {
     if ((s = mark(1)) != CKV_OK) return s;
     if ((s = mark(2)) != CKV_OK) return s;

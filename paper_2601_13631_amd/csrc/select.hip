@@ -27,15 +27,18 @@ __global__ __launch_bounds__(THREADS) void select_kernel(const double* __restric
 
 template <int E>
 __global__ __launch_bounds__(kSmallThreads) void select_small_kernel(
-    const double* __restrict__ scores, int m, int k, int32_t* __restrict__ sel) {
+    const double* __restrict__ scores, int m, int k, int32_t* __restrict__ sel,
+    int32_t* __restrict__ sel_copy) {
   __shared__ RegSelShared<kSmallThreads> sh;
-  select_topk_regs<kSmallThreads, E>(scores, m, k, sh, sel, nullptr);
+  select_topk_regs<kSmallThreads, E>(scores, m, k, sh, sel, sel_copy);
 }
 
 // One workgroup with the keys in registers: select_small_kernel<E>.
 template <int E>
-void launch_small(const double* scores, int m, int k, int32_t* sel, hipStream_t st) {
-  hipLaunchKernelGGL(select_small_kernel<E>, dim3(1), dim3(kSmallThreads), 0, st, scores, m, k, sel);
+void launch_small(const double* scores, int m, int k, int32_t* sel, int32_t* sel_copy,
+                  hipStream_t st) {
+  hipLaunchKernelGGL(select_small_kernel<E>, dim3(1), dim3(kSmallThreads), 0, st, scores, m, k, sel,
+                     sel_copy);
 }
 
 }  // namespace
@@ -43,16 +46,16 @@ void launch_small(const double* scores, int m, int k, int32_t* sel, hipStream_t 
 size_t select_ws_bytes(int64_t) { return 0; }
 
 ckv_status launch_select(const double* scores, int64_t m, int64_t k, int32_t* sel, void*, size_t,
-                         hipStream_t st) {
-  if (m <= kSmallKeys) {
+                         hipStream_t st, int32_t* sel_copy) {
+  if (m <= kSmallKeys) {  // the kernel writes both arrays
     if (m <= kSmallThreads)
-      launch_small<1>(scores, (int)m, (int)k, sel, st);
+      launch_small<1>(scores, (int)m, (int)k, sel, sel_copy, st);
     else if (m <= 2 * kSmallThreads)
-      launch_small<2>(scores, (int)m, (int)k, sel, st);
+      launch_small<2>(scores, (int)m, (int)k, sel, sel_copy, st);
     else if (m <= 4 * kSmallThreads)
-      launch_small<4>(scores, (int)m, (int)k, sel, st);
+      launch_small<4>(scores, (int)m, (int)k, sel, sel_copy, st);
     else
-      launch_small<8>(scores, (int)m, (int)k, sel, st);
+      launch_small<8>(scores, (int)m, (int)k, sel, sel_copy, st);
     CKV_HIP(hipGetLastError());
     return CKV_OK;
   }
@@ -66,6 +69,8 @@ ckv_status launch_select(const double* scores, int64_t m, int64_t k, int32_t* se
   hipLaunchKernelGGL(select_kernel<256>, dim3(1), dim3(256), shmem, st, scores, m, k, sel,
                      use_cache);
   CKV_HIP(hipGetLastError());
+  if (sel_copy)
+    CKV_HIP(hipMemcpyAsync(sel_copy, sel, (size_t)k * sizeof(int32_t), hipMemcpyDeviceToDevice, st));
   return CKV_OK;
 }
 
