@@ -1119,12 +1119,18 @@ ScorePlan make_score_plan(const ckv_dims* d) {
   const int64_t H_RB = (int64_t)d->n_kv_heads * w.RB;
   // A fixed grid target (two 256-thread workgroups per CU of a 256-CU MI355X
   // for bf16) keeps the decomposition, and so every rounding, independent of
-  // the device the library runs on.  Segments keep at least 8 stages of the
-  // pipelined bf16 kernel, or 64 keys of the one-wave fp32 kernel.
+  // the device the library runs on.  Segments of the pipelined bf16 kernel
+  // keep at least 4 stages while the fold still holds a row's segments in
+  // registers (kFoldBatch), else at least 8; the one-wave fp32 kernel's keep
+  // 64 keys.
   const int64_t target = f32 ? 1024 : 512;
-  const int64_t min_units = std::max<int64_t>(1, (f32 ? 64 : 512) / UK);
-  int64_t NS = std::max<int64_t>(1, target / H_RB);
-  NS = std::min<int64_t>(NS, std::max<int64_t>(1, U / min_units));
+  const int64_t NS_max = std::max<int64_t>(1, target / H_RB);
+  auto segments = [&](int64_t min_keys) {
+    const int64_t min_units = std::max<int64_t>(1, min_keys / UK);
+    return std::min<int64_t>(NS_max, std::max<int64_t>(1, U / min_units));
+  };
+  int64_t NS = segments(f32 ? 64 : 256);
+  if (!f32 && NS > kFoldBatch) NS = segments(512);
   // bytes == 0 marks an unsupported shape
   if (UK > INT32_MAX || U > INT32_MAX || H_RB * NS >= (int64_t(1) << 31)) return p;
   w.UK = (int32_t)UK;
