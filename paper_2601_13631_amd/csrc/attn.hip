@@ -37,7 +37,8 @@ constexpr int kTile = 64;                       // keys per LDS stage
 constexpr int kSub = 32;                        // keys per MFMA product
 constexpr int kMaxSliceKeys = 1024;             // keys per workgroup slice (8 KiB of key tables)
 constexpr float kLazy = 8.f;                    // headroom of the lazy softmax reference (log2 units)
-// Key tables: for every key of a slice, the row of its K/V source and its
+// Key tables: for every key of a slice, the row of its K/V source (as a byte
+// offset from the source's base when all of them fit in 32 bits) and its
 // visibility threshold -- a query t sees the key iff t >= thr.  thr = -1 marks
 // a row of the prefix source (seen by every query); a suffix token p has
 // thr = p (causal) and a row of the suffix source; a padding key has
@@ -98,7 +99,15 @@ struct AttnArgs {
   int S, Hq, Hkv, G, R, n_splits, tiles_per_split, n_row_blocks;
   float c1;
   uint32_t nblocks, nblocks_padded;
+  uint32_t row_bytes;      // Hkv * D * 2: bytes between consecutive rows of a source
+  int off32;               // every row of both sources lies below 4 GiB from its base
+  uint32_t pre_bytes, suf_bytes;  // bytes of the prefix and suffix sources (capped at 2^32 - 1)
 };
+
+// Buffer resource over `bytes` bytes from p (raw loads; offsets past the end read 0).
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t raw_rsrc(const void* p, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes, 0x00020000);
+}
 
 // Table entries of compact key position pos, in two steps so that a workgroup
 // can issue all its index loads before using any: key_chunk_loads fetches
@@ -151,7 +160,8 @@ struct TileRegs {
 };
 
 // The table entries of this thread's keys of one stage (read one stage ahead,
-// so the row loads never wait on LDS).
+// so the row loads never wait on LDS): the row's byte offset from its source's
+// base (AttnArgs::off32) or the row itself, and the threshold.
 template <int D>
 struct TileKeys {
   int row[TileRegs<D>::kPer], thr[TileRegs<D>::kPer];
@@ -167,14 +177,37 @@ __device__ __forceinline__ void tile_keys(const int* rows, const int* thrs, Tile
   }
 }
 
+// Stage kinds (bits 1-2 of a stage's flags): every key from the prefix source,
+// every key from the suffix source (padding keys read suffix row 0), or both.
+constexpr int kStagePrefix = 1, kStageSuffix = 2;
+
+// A stage from one source (the common case) addresses its pieces as 32-bit
+// byte offsets from that source's base, which stays in scalar registers; a
+// stage across the prefix/suffix boundary selects a 64-bit base per piece.
 template <int D>
-__device__ __forceinline__ void tile_load(const AttnArgs& a, int g, const TileKeys<D>& tk,
+__device__ __forceinline__ void tile_load(const AttnArgs& a, int g, int kind, const TileKeys<D>& tk,
                                           TileRegs<D>& r) {
-  const uint32_t hd = (uint32_t)(a.Hkv * D);
-  const uint64_t col = (uint64_t)(g * D + (threadIdx.x % TileRegs<D>::kSegs) * 8);
+  const int seg8 = (threadIdx.x % TileRegs<D>::kSegs) * 8;
+  if (a.off32 && kind != (kStagePrefix | kStageSuffix)) {  // uniform
+    const bool pre = kind == kStagePrefix;
+    const uint32_t bytes = pre ? a.pre_bytes : a.suf_bytes;
+    const __amdgpu_buffer_rsrc_t kr = raw_rsrc(pre ? a.kbase : a.ks, bytes);
+    const __amdgpu_buffer_rsrc_t vr = raw_rsrc(pre ? a.vbase : a.vs, bytes);
+    const uint32_t col = (uint32_t)(g * D + seg8) * 2u;
+#pragma unroll
+    for (int p = 0; p < TileRegs<D>::kPer; ++p) {
+      const uint32_t off = (uint32_t)tk.row[p] + col;  // the table holds byte offsets
+      r.k[p] = __builtin_amdgcn_raw_buffer_load_b128(kr, off, 0, 0);
+      r.v[p] = __builtin_amdgcn_raw_buffer_load_b128(vr, off, 0, 0);
+    }
+    return;
+  }
+  const uint64_t col = (uint64_t)(g * D + seg8);
 #pragma unroll
   for (int p = 0; p < TileRegs<D>::kPer; ++p) {
-    const uint64_t e = (uint64_t)(uint32_t)tk.row[p] * hd + col;
+    // element offset of the piece: from the table's byte offset, or its row
+    const uint64_t e = a.off32 ? (uint64_t)((uint32_t)tk.row[p] >> 1) + col
+                               : (uint64_t)(uint32_t)tk.row[p] * (uint32_t)(a.Hkv * D) + col;
     const bool pre = tk.thr[p] == kPrefix;
     r.k[p] = *reinterpret_cast<const u32x4*>((pre ? a.kbase : a.ks) + e);
     r.v[p] = *reinterpret_cast<const u32x4*>((pre ? a.vbase : a.vs) + e);
@@ -317,12 +350,13 @@ template <int D>
 __global__ __launch_bounds__(kWaves * 64, 2) void attn_kernel(AttnArgs a) {
   __shared__ __attribute__((aligned(16))) uint16_t lk[2][kTile * KLds<D>::kRow];
   __shared__ __attribute__((aligned(16))) uint16_t lv[2][kTile * D];
-  // key tables of the slice (rows, thresholds), then one need-mask flag per
-  // stage (dynamic: tiles_per_split * (2 * kTile + 1) ints)
+  // key tables of the slice (rows, thresholds), then one flags word per stage:
+  // bit 0 a key some row of the block must not see, bits 1-2 the stage's kind
+  // (dynamic: tiles_per_split * (2 * kTile + 1) ints)
   extern __shared__ int slice_lds[];
   int* rows = slice_lds;
   int* thrs = slice_lds + a.tiles_per_split * kTile;
-  int* need_mask = slice_lds + 2 * a.tiles_per_split * kTile;
+  int* stage_flags = slice_lds + 2 * a.tiles_per_split * kTile;
 
   // logical order (g, split, row block): blocks reading the same K/V tiles are
   // adjacent, hence on the same XCD and its L2
@@ -377,12 +411,16 @@ __global__ __launch_bounds__(kWaves * 64, 2) void attn_kernel(AttnArgs a) {
     const int pos = (tile0 + st) * kTile + lane;
     int krow = 0, kthr = kNever;
     if (pos < np_block) key_entry(a, pos, jv[it], sv[it], krow, kthr);
-    rows[st * kTile + lane] = krow;
+    // the row's byte offset from its source's base when every one fits in 32 bits
+    rows[st * kTile + lane] = a.off32 ? (int)((uint32_t)krow * a.row_bytes) : krow;
     thrs[st * kTile + lane] = kthr;
-    const uint64_t bad = __ballot(kthr > first_t);
-    if (lane == 0) need_mask[st] = bad != 0;
+    const uint64_t bad = __ballot(kthr > first_t), pre = __ballot(kthr == kPrefix);
+    if (lane == 0)
+      stage_flags[st] = (bad != 0 ? 1 : 0) | (pre != 0 ? kStagePrefix << 1 : 0) |
+                        (pre != ~0ull ? kStageSuffix << 1 : 0);
   }
   __syncthreads();
+  auto stage_kind = [&](int st) { return __builtin_amdgcn_readfirstlane(stage_flags[st] >> 1); };
 
   // per-lane LDS element offsets of the operand reads (the same for every stage)
   const int kbase_off = kappa(lane & 31) * KLds<D>::kRow + 8 * half;
@@ -411,7 +449,7 @@ __global__ __launch_bounds__(kWaves * 64, 2) void attn_kernel(AttnArgs a) {
   TileKeys<D> tk;
   if (nt > 0) {
     tile_keys<D>(rows, thrs, tk);
-    tile_load<D>(a, g, tk, regs);
+    tile_load<D>(a, g, stage_kind(0), tk, regs);
     if (nt > 1) tile_keys<D>(rows + kTile, thrs + kTile, tk);
     tile_store<D>(regs, lk[0], lv[0]);
     __syncthreads();
@@ -422,11 +460,11 @@ __global__ __launch_bounds__(kWaves * 64, 2) void attn_kernel(AttnArgs a) {
     // the next stage's K/V rows load during this stage; the table entries of
     // the stage after it are read now, for the next iteration
     if (has_next) {
-      tile_load<D>(a, g, tk, regs);
+      tile_load<D>(a, g, stage_kind(st + 1), tk, regs);
       if (st + 2 < nt) tile_keys<D>(rows + (st + 2) * kTile, thrs + (st + 2) * kTile, tk);
     }
     f32x16 s[2];
-    stage_softmax<D>(a, lk[cur], thrs + st * kTile, need_mask[st], t, kbase_off, qf, rs, s);
+    stage_softmax<D>(a, lk[cur], thrs + st * kTile, stage_flags[st] & 1, t, kbase_off, qf, rs, s);
     stage_pv<D>(lv[cur], voff, s, rs);
     if (has_next) {
       tile_store<D>(regs, lk[cur ^ 1], lv[cur ^ 1]);
@@ -698,6 +736,13 @@ ckv_status launch_attn(const ckv_dims* d, const void* q, const ChunkSource& src,
     if (src.n_slots < 0 || src.n_slots * rps >= (int64_t(1) << 31))
       CKV_FAIL(CKV_EUNSUPPORTED, "chunk source too large");
     a.rows_per_slot = (int)rps;
+    // 32-bit byte offsets reach every row of both sources
+    const int64_t rb = hd * (int64_t)sizeof(uint16_t);
+    a.row_bytes = (uint32_t)rb;
+    const int64_t pre = src.n_slots * rps * rb, suf = (int64_t)d->n_suffix * rb;
+    a.off32 = pre <= (int64_t(1) << 32) && suf <= (int64_t(1) << 32);
+    a.pre_bytes = (uint32_t)std::min<int64_t>(pre, UINT32_MAX);
+    a.suf_bytes = (uint32_t)std::min<int64_t>(suf, UINT32_MAX);
   }
   a.sel = sel;
   a.kc = (int)(k * d->chunk_size);
