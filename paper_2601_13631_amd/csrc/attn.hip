@@ -101,7 +101,7 @@ struct AttnArgs {
   uint32_t nblocks, nblocks_padded;
   uint32_t row_bytes;      // Hkv * D * 2: bytes between consecutive rows of a source
   int off32;               // every row of both sources lies below 4 GiB from its base
-  uint32_t pre_bytes, suf_bytes;  // bytes of the prefix and suffix sources (capped at 2^32 - 1)
+  uint32_t pre_bytes, suf_bytes;  // bytes of the prefix and suffix sources (when off32)
 };
 
 // Buffer resource over `bytes` bytes from p (raw loads; offsets past the end read 0).
@@ -739,8 +739,9 @@ ckv_status launch_attn(const ckv_dims* d, const void* q, const ChunkSource& src,
     // 32-bit byte offsets reach every row of both sources
     const int64_t rb = hd * (int64_t)sizeof(uint16_t);
     a.row_bytes = (uint32_t)rb;
+    // (strictly below 4 GiB, so each source's byte count is a buffer size)
     const int64_t pre = src.n_slots * rps * rb, suf = (int64_t)d->n_suffix * rb;
-    a.off32 = pre <= (int64_t(1) << 32) && suf <= (int64_t(1) << 32);
+    a.off32 = pre < (int64_t(1) << 32) && suf < (int64_t(1) << 32);
     a.pre_bytes = (uint32_t)std::min<int64_t>(pre, UINT32_MAX);
     a.suf_bytes = (uint32_t)std::min<int64_t>(suf, UINT32_MAX);
   }
