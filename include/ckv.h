@@ -174,6 +174,15 @@ ckv_status ckv_sparse_prefill_attn(const ckv_dims* dims, const void* q, const vo
                                    const void* k_suffix, const void* v_suffix, void* out,
                                    void* ws, size_t ws_bytes, void* stream);
 
+/* Test hook for the attention's K/V addressing.  A source whose rows all lie
+ * below 4 GiB from its base is read through 32-bit byte offsets; a larger one
+ * through a 64-bit address per row.  force_wide = 1 makes every later launch
+ * in the process (standalone or in a layer step) take the 64-bit form, so that
+ * tests can run it on small inputs; the two forms read the same bytes and give
+ * bit-identical results.  0 restores the default.  Process-wide, thread-safe;
+ * launches already enqueued are not affected. */
+ckv_status ckv_debug_attn_wide_addressing(int32_t force_wide);
+
 /* ---------------------------------------------------------------------------
  * Layer step -- one Re-Prefill layer: score -> select -> move chunks ->
  * attention, with the context owning streams, events, workspace and (for a

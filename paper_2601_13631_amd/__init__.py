@@ -90,6 +90,7 @@ _SIG = {
                                ctypes.c_int32),
     "ckv_gather_chunks": ([_DP, _P, _P, _P, ctypes.c_int64, _P, _P, _P], ctypes.c_int32),
     "ckv_attn_workspace_bytes": ([_DP, ctypes.c_int64], ctypes.c_size_t),
+    "ckv_debug_attn_wide_addressing": ([ctypes.c_int32], ctypes.c_int32),
     "ckv_sparse_prefill_attn": ([_DP, _P, _P, _P, _P, ctypes.c_int64, _P, _P, _P, _P,
                                  ctypes.c_size_t, _P], ctypes.c_int32),
     "ckv_ctx_create": ([_DP, ctypes.c_int32, ctypes.c_double, ctypes.c_int32, ctypes.POINTER(_P)],
@@ -214,6 +215,13 @@ def gather_chunks(dims: Dims, k_src, v_src, sel_idx, k: int, k_sel, v_sel, strea
 
 def attn_workspace_bytes(dims: Dims, k: int) -> int:
     return int(_lib.ckv_attn_workspace_bytes(ctypes.byref(dims), k))
+
+
+def debug_attn_wide_addressing(force_wide: bool) -> None:
+    """Test hook: every later attention launch reads K/V through 64-bit row
+    addresses (the form sources past 4 GiB take) instead of 32-bit offsets."""
+    _check(_lib.ckv_debug_attn_wide_addressing(1 if force_wide else 0),
+           "ckv_debug_attn_wide_addressing")
 
 
 def sparse_prefill_attn(dims: Dims, q, k_sel, v_sel, sel_idx, k: int, k_suffix, v_suffix, out,

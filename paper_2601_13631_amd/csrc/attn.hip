@@ -25,10 +25,14 @@
 // type and range) plus (reference, l) in fp32; a combine kernel merges them in
 // split order (deterministic).
 
+#include <atomic>
+
 #include "ckv_internal.h"
 
 namespace ckv {
 namespace {
+
+std::atomic<int> g_force_wide{0};  // ckv_debug_attn_wide_addressing
 
 constexpr int kWaves = 4;
 constexpr int kWaveRows = 32;
@@ -741,7 +745,8 @@ ckv_status launch_attn(const ckv_dims* d, const void* q, const ChunkSource& src,
     a.row_bytes = (uint32_t)rb;
     // (strictly below 4 GiB, so each source's byte count is a buffer size)
     const int64_t pre = src.n_slots * rps * rb, suf = (int64_t)d->n_suffix * rb;
-    a.off32 = pre < (int64_t(1) << 32) && suf < (int64_t(1) << 32);
+    a.off32 = pre < (int64_t(1) << 32) && suf < (int64_t(1) << 32) &&
+              g_force_wide.load(std::memory_order_relaxed) == 0;
     a.pre_bytes = (uint32_t)std::min<int64_t>(pre, UINT32_MAX);
     a.suf_bytes = (uint32_t)std::min<int64_t>(suf, UINT32_MAX);
   }
@@ -785,3 +790,10 @@ ckv_status launch_attn(const ckv_dims* d, const void* q, const ChunkSource& src,
 }
 
 }  // namespace ckv
+
+extern "C" ckv_status ckv_debug_attn_wide_addressing(int32_t force_wide) {
+  ckv::clear_error();
+  if (force_wide != 0 && force_wide != 1) CKV_FAIL(CKV_EINVAL, "force_wide must be 0 or 1");
+  ckv::g_force_wide.store(force_wide, std::memory_order_relaxed);
+  return CKV_OK;
+}

@@ -248,3 +248,54 @@ def test_attention_deterministic():
         outs.append(out)
     torch.cuda.synchronize()
     assert torch.equal(outs[0].view(torch.int16), outs[1].view(torch.int16))
+
+
+@pytest.mark.parametrize("w,how", [(W2(2048, 40, 28, 4, 128, 32), "tenth"), (W2(1000, 9, 6, 2, 64, 16), "third"),
+                                   (W2(512, 17, 8, 1, 128, 8), "none")],
+                         ids=lambda x: x.name if hasattr(x, "name") else x)
+def test_attention_wide_addressing(w, how):
+    """The 64-bit row addressing that sources past 4 GiB take, forced on small
+    inputs: the standalone attention over the compact copy and the layer step
+    reading the kept spans in place give bit-identical outputs either way."""
+    import paper_2601_13631_amd as ckv
+    print(f"case {w.name} {how}", flush=True)
+    t = synth.layer_tensors(w, 0)
+    sel = _sel_for(w, how, np.random.default_rng(13))
+    k = sel.size
+    d = dims_of(w)
+    tt = {kk: dev(v) for kk, v in t.items()}
+    sel_d = torch.from_numpy(sel).to(DEV) if k else torch.zeros(1, dtype=torch.int32, device=DEV)
+    if k:
+        kd = torch.empty((k * w.chunk_size, w.n_kv_heads, w.head_dim), dtype=torch.bfloat16, device=DEV)
+        vd = torch.empty_like(kd)
+        ckv.gather_chunks(d, tt["k_prefix"], tt["v_prefix"], sel_d, k, kd, vd)
+    else:
+        kd = vd = None
+    ws = workspace(ckv.attn_workspace_bytes(d, k))
+
+    def run_both():
+        out = torch.empty_like(tt["q"])
+        ckv.sparse_prefill_attn(d, tt["q"], kd, vd, sel_d if k else None, k, tt["k_suffix"],
+                                tt["v_suffix"], out, ws)
+        ctx = ckv.Context(d, 1, w.keep_ratio)
+        A = torch.empty(w.n_chunks, dtype=torch.float64, device=DEV)
+        lsel = torch.empty(ctx.k, dtype=torch.int32, device=DEV)
+        lout = torch.empty_like(tt["q"])
+        ctx.reprefill_layer(0, tt["q"], tt["k_suffix"], tt["v_suffix"], tt["k_prefix"], lout,
+                            k_prefix=tt["k_prefix"], v_prefix=tt["v_prefix"], chunk_scores=A,
+                            sel_idx=lsel)
+        torch.cuda.synchronize()
+        ctx.close()
+        return out, lout
+
+    narrow = run_both()
+    ckv.debug_attn_wide_addressing(True)
+    try:
+        wide = run_both()
+    finally:
+        ckv.debug_attn_wide_addressing(False)
+    for a, b in zip(narrow, wide):
+        assert torch.equal(a.view(torch.int16), b.view(torch.int16))
+    ref = oracle.sparse_attn(oshape(w), t["q"], t["k_prefix"], t["v_prefix"], sel, t["k_suffix"],
+                             t["v_suffix"])
+    assert float(np.abs(to_f64(wide[0]) - ref).max()) <= 2e-2
