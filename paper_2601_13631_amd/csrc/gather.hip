@@ -33,16 +33,20 @@ __global__ __launch_bounds__(kThreads) void gather_kernel(const uint8_t* __restr
   const uint8_t* s = src + first * row_bytes;
   uint8_t* d = dst + u * slot_bytes;
   const int64_t base = ((int64_t)blockIdx.x * kThreads * kUnroll + threadIdx.x) * 16;
+  // every load unconditional, at an offset clamped into the valid bytes (a
+  // load behind its own predicate would wait for the one before it); pieces
+  // past the valid bytes are zeroed afterwards
+  const int64_t last = valid > 0 ? valid - 16 : 0;
   u32x4 v[kUnroll];
 #pragma unroll
   for (int p = 0; p < kUnroll; ++p) {
     const int64_t off = base + (int64_t)p * kThreads * 16;
-    v[p] = u32x4{0u, 0u, 0u, 0u};
-    if (off < valid) v[p] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(s + off));
+    v[p] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(s + min(off, last)));
   }
 #pragma unroll
   for (int p = 0; p < kUnroll; ++p) {
     const int64_t off = base + (int64_t)p * kThreads * 16;
+    if (off >= valid) v[p] = u32x4{0u, 0u, 0u, 0u};
     if (off < slot_bytes) *reinterpret_cast<u32x4*>(d + off) = v[p];
   }
 }
@@ -71,6 +75,9 @@ __global__ __launch_bounds__(kThreads) void copy_spans_kernel(const uint8_t* __r
     const uint8_t* s = src + (int64_t)chunks[i] * span_bytes;
     uint8_t* d = dst + (dst_slots ? (int64_t)dst_slots[i] : slot0 + i) * span_bytes;
     const int64_t base = piece * kPiece + (int64_t)threadIdx.x * 16;
+    // the loads stay behind their predicates, one in flight per thread: with
+    // all four issued at once the host-resident 128K-token layer measured
+    // 2.83 ms against 2.64 ms (the copy runs beside the attention)
     u32x4 v[kUnroll];
 #pragma unroll
     for (int p = 0; p < kUnroll; ++p) {
