@@ -5,10 +5,11 @@
 // Keeps the k largest of m fp64 chunk scores under the total order (score
 // descending, index ascending) and writes their indices in ascending order.
 // A radix select on order-preserving 64-bit keys (select_block.h's order_key)
-// with 4-bit digits whose counts come from wave ballots, or for 4 or more keys
-// per thread from packed per-lane counters summed by DPP (no LDS atomics: the
-// chunk scores of a layer share their high bits, so per-bin atomics would all
-// collide): the first digit ends at the highest bit where the smallest and
+// with 4-bit digits whose counts come from packed per-lane counters summed by
+// DPP and the permlane swaps (no ballots: 16 masks per key in scalar registers
+// queue every wave on the CU's scalar unit; no LDS atomics: the chunk scores
+// of a layer share their high bits, so per-bin atomics would all collide):
+// the first digit ends at the highest bit where the smallest and
 // largest key differ, every later one is the next 4 bits down; the search ends
 // when the chosen digit holds exactly the keys still needed or the last bit
 // is fixed (then the lowest indices win).  The ordered compaction counts with
@@ -66,7 +67,7 @@ __device__ __forceinline__ uint32_t pair_sum32(uint32_t x) {
 }
 
 // The wave's count of keys per digit value 0..15 (digit 16: not a candidate),
-// for E >= 4 keys per lane, without ballots: each lane counts its digits in
+// for E keys per lane: each lane counts its digits in
 // 4-bit fields of one 64-bit word (E <= 15), the fields are spread to bytes
 // and summed over each row of 16 lanes by DPP (at most 16 * E <= 255), then
 // widened to 16-bit fields and summed over the four rows by the permlane
@@ -100,13 +101,14 @@ __device__ __forceinline__ void wave_digit_counts(const int (&cd)[E], uint32_t (
     }
 }
 
-// Called by all THREADS threads; m <= E * THREADS, 1 <= k <= m.  Thread t
+// Called by all THREADS threads; m <= E * THREADS, 1 <= k <= m, 4 <= E <= 15.  Thread t
 // holds scores t*E .. t*E+E-1.  The k indices go to out0[0..k) and, when
 // out1 is not null, to out1 too (each thread writes its own kept indices).
 template <int THREADS, int E>
 __device__ __forceinline__ void select_topk_regs(const double* __restrict__ scores, int m, int k,
                                                  RegSelShared<THREADS>& sh, int32_t* out0,
                                                  int32_t* out1) {
+  static_assert(E >= 4 && E <= 15, "keys per thread");
   constexpr int kWaves = THREADS / 64;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int i0 = tid * E;
@@ -150,7 +152,7 @@ __device__ __forceinline__ void select_topk_regs(const double* __restrict__ scor
 #pragma unroll
       for (int e = 0; e < E; ++e)
         cd[e] = valid[e] && (x[e] & mask) == prefix ? (int)((x[e] >> shift) & 15) : 16;
-      if constexpr (E >= 4) {  // vector counts (ballots would need 16 * E scalar masks)
+      {
         uint32_t cnt[8];
         wave_digit_counts<E>(cd, cnt);
         if (lane == 15)
@@ -159,16 +161,6 @@ __device__ __forceinline__ void select_topk_regs(const double* __restrict__ scor
             sh.whist[wave][2 * i] = cnt[i] & 0xFFFFu;
             sh.whist[wave][2 * i + 1] = cnt[i] >> 16;
           }
-      } else {
-        int mine = 0;
-#pragma unroll
-        for (int b = 0; b < 16; ++b) {
-          int c = 0;
-#pragma unroll
-          for (int e = 0; e < E; ++e) c += __popcll(__ballot(cd[e] == b));
-          if (lane == b) mine = c;
-        }
-        if (lane < 16) sh.whist[wave][lane] = (uint32_t)mine;
       }
       __syncthreads();
       if (wave == 0) {

@@ -123,8 +123,9 @@ def test_select_special_values():
         assert np.array_equal(sel, oracle.select_topk(A, k)), k
 
 
-# the register paths with 2, 4 and 8 scores per thread and the LDS-histogram path
-@pytest.mark.parametrize("m", [1500, 4000, 6000, 9000, 20000])
+# every selection path: 256 threads with 4 and with 8 keys each, 512 and 1024
+# threads with 8, and the LDS-histogram kernel
+@pytest.mark.parametrize("m", [1000, 1500, 4000, 6000, 9000, 20000])
 def test_select_special_values_large(m):
     rng = np.random.default_rng(m + 1)
     A = rng.normal(0, 1, m) * np.exp(rng.normal(0, 30, m))  # both signs, wide exponents
