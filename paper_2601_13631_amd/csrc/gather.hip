@@ -55,8 +55,10 @@ __global__ __launch_bounds__(kThreads) void gather_kernel(const uint8_t* __restr
 // all 16 KiB pieces of all listed spans (grid-stride), so the copy keeps
 // thousands of 16-byte loads in flight over the host link -- one launch per
 // list instead of one DMA copy per run of chunks -- while occupying only a
-// few wave slots per CU, next to the compute kernels it overlaps.
-constexpr int kCopyBlocks = 32;
+// few wave slots, next to the compute kernels it overlaps: 8 workgroups with
+// every thread's four loads in flight at once (32 with one load at a time, or
+// 16 with four, measured slower on the host-resident 128K-token layer).
+constexpr int kCopyBlocks = 8;
 // HBM-to-HBM slot moves (cache fills) run on the compute stream: a wider grid
 constexpr int kSlotCopyBlocks = 256;
 
@@ -75,15 +77,13 @@ __global__ __launch_bounds__(kThreads) void copy_spans_kernel(const uint8_t* __r
     const uint8_t* s = src + (int64_t)chunks[i] * span_bytes;
     uint8_t* d = dst + (dst_slots ? (int64_t)dst_slots[i] : slot0 + i) * span_bytes;
     const int64_t base = piece * kPiece + (int64_t)threadIdx.x * 16;
-    // the loads stay behind their predicates, one in flight per thread: with
-    // all four issued at once the host-resident 128K-token layer measured
-    // 2.83 ms against 2.64 ms (the copy runs beside the attention)
+    // unconditional loads at offsets clamped into the span (see gather_kernel)
     u32x4 v[kUnroll];
 #pragma unroll
     for (int p = 0; p < kUnroll; ++p) {
       const int64_t off = base + (int64_t)p * kThreads * 16;
-      if (off < span_bytes)
-        v[p] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(s + off));
+      v[p] = __builtin_nontemporal_load(
+          reinterpret_cast<const u32x4*>(s + min(off, span_bytes - 16)));
     }
 #pragma unroll
     for (int p = 0; p < kUnroll; ++p) {
