@@ -86,6 +86,46 @@ SCORE_RTOL_UNIT = 4e-7
 SCORE_RTOL_BOUND = 2e-6
 
 
+# Attention: a per-element bound from the arithmetic, not a blanket
+# tolerance.  With u = 2^-8 (bf16's unit roundoff, round to nearest even) and
+# a the same row's attention over |V| (the same softmax weights, so a >= |o|),
+# the GPU's bf16 output differs from the fp64 oracle by at most
+#   u |o|   the output's rounding to bf16;
+#   u a     the numerators rounded to bf16 for the P V product (the
+#           denominator sums them unrounded);
+#   u a     each split's normalised partial stored in bf16 (the combine
+#           weights sum to one);
+# plus the fp32 effects -- logits accumulated over head_dim, O over a split's
+# keys, the denominators and combine weights -- which stay below 2^-11 a.
+# The fp32 path is held to 1e-5 absolute.
+BF16_U = 2.0 ** -8
+ATTN_ATOL_F32 = 1e-5
+
+
+def _abs_vals(a: np.ndarray) -> np.ndarray:
+    """|x| elementwise: bf16 bit patterns lose their sign bit, fp32 takes abs."""
+    return a & np.uint16(0x7FFF) if a.dtype == np.uint16 else np.abs(a)
+
+
+def attn_check(s: oracle.Shape, t: dict, sel: np.ndarray, got: np.ndarray, ref: np.ndarray,
+               attn=None) -> tuple:
+    """Checks the GPU's attention `got` against the oracle's `ref` (computed with
+    attention function `attn`, default oracle.sparse_attn, over the kept set
+    `sel` and the inputs `t`) element by element.  Returns (largest absolute
+    error, largest error / bound)."""
+    err = np.abs(got - ref)
+    if s.dtype == oracle.F32:
+        bound = ATTN_ATOL_F32
+    else:
+        attn = attn or oracle.sparse_attn
+        a = attn(s, t["q"], t["k_prefix"], _abs_vals(t["v_prefix"]), sel, t["k_suffix"],
+                 _abs_vals(t["v_suffix"]))
+        bound = BF16_U * np.abs(ref) + (2 * BF16_U + 2.0 ** -11) * a + 1e-6
+    ratio = float(np.max(err / bound))
+    assert ratio <= 1.0, f"attention error {float(err.max()):.3e} exceeds its bound ({ratio:.3g} x)"
+    return float(err.max()), ratio
+
+
 def check_set(A_ref: np.ndarray, sel_gpu: np.ndarray, k: int, err: float, require: bool = True) -> dict:
     """Certified comparison of a top-k set.
 

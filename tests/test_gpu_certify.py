@@ -15,7 +15,8 @@ Per layer, against the oracle's matrix-product form (``oracle/blas.py``, fp64):
   more than the measured score error) and then equal to the oracle's bit for
   bit -- an uncertified layer fails the test, with its gap/error ratio;
 - the oracle's selection from the GPU's own scores equals the GPU's set;
-- every output row within max-abs 2e-2 (bf16) / 1e-5 (fp32) of the oracle's
+- every output element within its bound (gpu_common.attn_check: derived from
+  the bf16 roundings of the kernels; 1e-5 absolute for fp32) of the oracle's
   attention over the GPU's set;
 - on the host path, hits/misses/wasted and prefetched/demand bytes equal the
   oracle's set algebra for the prediction used.
@@ -34,7 +35,7 @@ import torch
 import oracle
 import oracle.blas as blas
 import synth
-from gpu_common import DEV, SCORE_RTOL, check_set, dev, dims_of, oshape, rel_err, to_f64
+from gpu_common import DEV, SCORE_RTOL, attn_check, check_set, dev, dims_of, oshape, rel_err, to_f64
 
 pytestmark = pytest.mark.gpu
 
@@ -54,9 +55,10 @@ class Record:
     def __init__(self, w, path):
         self.r = {"config": w.name, "path": path, "layers": [], "certified": 0, "total": 0,
                   "sets_equal": 0, "max_score_rel_err": 0.0, "max_attn_abs_err": 0.0,
+                  "max_attn_err_over_bound": 0.0,
                   "attn_rows_checked": 0, "min_gap_over_err": float("inf")}
 
-    def add(self, layer, err, cs, aerr, rows):
+    def add(self, layer, err, cs, aerr, ratio, rows):
         r = self.r
         r["layers"].append(layer)
         r["total"] += 1
@@ -64,6 +66,7 @@ class Record:
         r["sets_equal"] += int(cs["equal"])
         r["max_score_rel_err"] = max(r["max_score_rel_err"], err)
         r["max_attn_abs_err"] = max(r["max_attn_abs_err"], aerr)
+        r["max_attn_err_over_bound"] = max(r["max_attn_err_over_bound"], ratio)
         r["attn_rows_checked"] += rows
         r["min_gap_over_err"] = min(r["min_gap_over_err"], cs["gap_over_err"])
 
@@ -91,12 +94,11 @@ def _check(w, t, A, sel, out, k, rec, layer):
     ref = blas.sparse_attn(s, t["q"], t["k_prefix"], t["v_prefix"], sel, t["k_suffix"], t["v_suffix"])
     got = to_f64(out).reshape(ref.shape)
     aerr = float(np.abs(got - ref).max())
-    tol = 1e-5 if w.dtype == "f32" else 2e-2
     print(f"  layer {layer}: score rel err {err:.2e}, gap/err {cs['gap_over_err']:.3g}, "
-          f"attention max abs {aerr:.2e} over {got.shape[0] * got.shape[1]} rows "
-          f"(oracle {time.time() - t0:.1f}s)", flush=True)
-    assert aerr <= tol, (layer, aerr)
-    rec.add(layer, err, cs, aerr, got.shape[0] * got.shape[1])
+          f"attention max abs {aerr:.2e} over {got.shape[0] * got.shape[1]} rows", flush=True)
+    _, ratio = attn_check(s, t, sel, got, ref, attn=blas.sparse_attn)
+    print(f"    {ratio:.2f} of the attention bound (oracle {time.time() - t0:.1f}s)", flush=True)
+    rec.add(layer, err, cs, aerr, ratio, got.shape[0] * got.shape[1])
     if w.heavy == "planted3":  # the planted chunks are always kept
         assert set(synth.heavy_sets(w)[layer].tolist()) <= set(sel.tolist())
 

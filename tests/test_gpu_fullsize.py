@@ -15,11 +15,10 @@ import torch
 
 import oracle
 import synth
-from gpu_common import DEV, SCORE_RTOL, check_set, dev, dims_of, oshape, rel_err, to_f64
+from gpu_common import DEV, SCORE_RTOL, attn_check, check_set, dev, dims_of, oshape, rel_err, to_f64
 
 pytestmark = pytest.mark.gpu
 
-ATTN_ATOL = 2e-2
 N_SAMPLE = 96
 
 
@@ -70,7 +69,7 @@ def _check_layer(w, t, A, sel, out, k):
     got = to_f64(out).reshape(-1, w.head_dim)[rows]
     aerr = float(np.abs(got - ref).max())
     print(f"  attention max abs err {aerr:.3e} over {rows.size} rows", flush=True)
-    assert aerr <= (1e-5 if w.dtype == "f32" else ATTN_ATOL)
+    attn_check(s, t, sel, got, ref, attn=lambda *a: oracle.sparse_attn(*a, row_ids=rows))
 
 
 FULL = ["c1_f32_1k", "c2_qwen05b_8k", "c3_qwen7b_32k", "c4_qwen14b_64k_c8", "c4_qwen14b_64k_c16",
