@@ -97,8 +97,10 @@ SCORE_RTOL_BOUND = 2e-6
 #           weights sum to one);
 # plus the fp32 effects -- logits accumulated over head_dim, O over a split's
 # keys, the denominators and combine weights -- which stay below 2^-11 a.
-# The fp32 path is held to 1e-5 absolute.
+# Each element is held to the smaller of that bound and the stated max-abs
+# tolerance of 2e-2; the fp32 path is held to 1e-5 absolute.
 BF16_U = 2.0 ** -8
+ATTN_ATOL_BF16 = 2e-2
 ATTN_ATOL_F32 = 1e-5
 
 
@@ -120,7 +122,8 @@ def attn_check(s: oracle.Shape, t: dict, sel: np.ndarray, got: np.ndarray, ref: 
         attn = attn or oracle.sparse_attn
         a = attn(s, t["q"], t["k_prefix"], _abs_vals(t["v_prefix"]), sel, t["k_suffix"],
                  _abs_vals(t["v_suffix"]))
-        bound = BF16_U * np.abs(ref) + (2 * BF16_U + 2.0 ** -11) * a + 1e-6
+        bound = np.minimum(BF16_U * np.abs(ref) + (2 * BF16_U + 2.0 ** -11) * a + 1e-6,
+                           ATTN_ATOL_BF16)
     ratio = float(np.max(err / bound))
     assert ratio <= 1.0, f"attention error {float(err.max()):.3e} exceeds its bound ({ratio:.3g} x)"
     return float(err.max()), ratio
