@@ -62,7 +62,8 @@ constexpr int kCopyBlocks = 8;
 // HBM-to-HBM slot moves (cache fills) run on the compute stream: a wider grid
 constexpr int kSlotCopyBlocks = 256;
 
-// dst_slots == nullptr: span i goes to slot slot0 + i
+// dst_slots == nullptr: span i goes to slot slot0 + i.  span_bytes is a
+// positive multiple of 16 (checked by the launchers).
 __global__ __launch_bounds__(kThreads) void copy_spans_kernel(const uint8_t* __restrict__ src,
                                                               const int32_t* __restrict__ chunks,
                                                               int64_t count, int64_t slot0,
@@ -97,7 +98,8 @@ __global__ __launch_bounds__(kThreads) void copy_spans_kernel(const uint8_t* __r
 
 ckv_status launch_copy_spans(const void* src, const int32_t* chunks, int64_t count, int64_t slot0,
                              void* dst, int64_t span_bytes, hipStream_t st) {
-  if (span_bytes % 16 != 0) CKV_FAIL(CKV_EINVAL, "span bytes must be a multiple of 16");
+  if (span_bytes <= 0 || span_bytes % 16 != 0)
+    CKV_FAIL(CKV_EINVAL, "span bytes must be a positive multiple of 16");
   if (count == 0) return CKV_OK;
   const int64_t pieces = count * ceil_div(span_bytes, (int64_t)kThreads * kUnroll * 16);
   const unsigned grid = (unsigned)std::min<int64_t>(pieces, kCopyBlocks);
@@ -111,7 +113,8 @@ ckv_status launch_copy_spans(const void* src, const int32_t* chunks, int64_t cou
 ckv_status launch_copy_slots(const void* src, const int32_t* src_slots, void* dst,
                              const int32_t* dst_slots, int64_t count, int64_t span_bytes,
                              hipStream_t st) {
-  if (span_bytes % 16 != 0) CKV_FAIL(CKV_EINVAL, "span bytes must be a multiple of 16");
+  if (span_bytes <= 0 || span_bytes % 16 != 0)
+    CKV_FAIL(CKV_EINVAL, "span bytes must be a positive multiple of 16");
   if (count == 0) return CKV_OK;
   const int64_t pieces = count * ceil_div(span_bytes, (int64_t)kThreads * kUnroll * 16);
   const unsigned grid = (unsigned)std::min<int64_t>(pieces, kSlotCopyBlocks);
