@@ -101,6 +101,8 @@ struct AttnArgs {
   uint16_t* o_part;        // [splits][Hkv][R][D]: O / l, bf16
   float2* ml_part;         // [splits][Hkv][R]: (reference, sum)
   int S, Hq, Hkv, G, R, n_splits, tiles_per_split, n_row_blocks;
+  int partial;             // write split partials for a combine (else the output itself)
+  int with_suffix;         // the keys end with the causal suffix (else prefix chunks only)
   float c1;
   uint32_t nblocks, nblocks_padded;
   uint32_t row_bytes;      // Hkv * D * 2: bytes between consecutive rows of a source
@@ -380,7 +382,7 @@ __global__ __launch_bounds__(kWaves * 64, 2) void attn_kernel(AttnArgs a) {
   // suffix key up to its own position
   const int first_t = (rb * kBlockRows) / a.G;
   const int last_row = min(a.R - 1, rb * kBlockRows + kBlockRows - 1);
-  const int np_block = a.kc + last_row / a.G + 1;
+  const int np_block = a.kc + (a.with_suffix ? last_row / a.G + 1 : 0);
   const int ntiles = (np_block + kTile - 1) / kTile;
   const int tile0 = split * a.tiles_per_split;
   const int nt = max(0, min(ntiles, tile0 + a.tiles_per_split) - tile0);
@@ -507,7 +509,7 @@ __global__ __launch_bounds__(kWaves * 64, 2) void attn_kernel(AttnArgs a) {
       const uint4 v = *reinterpret_cast<const uint4*>(tile + rr * kRow + seg * 8);
       if (orow < a.R) {
         uint16_t* dst;
-        if (a.n_splits == 1)
+        if (!a.partial)
           dst = a.out + ((int64_t)(orow / a.G) * a.Hq + (int64_t)g * a.G + orow % a.G) * D;
         else
           dst = a.o_part + (((int64_t)split * a.Hkv + g) * a.R + orow) * D;
@@ -516,7 +518,7 @@ __global__ __launch_bounds__(kWaves * 64, 2) void attn_kernel(AttnArgs a) {
     }
   }
   // the reference the numerators were taken against (0 while no key was seen)
-  if (a.n_splits > 1 && row_ok && half == 0)
+  if (a.partial && row_ok && half == 0)
     a.ml_part[((int64_t)split * a.Hkv + g) * a.R + row] =
         make_float2(rs.m_run == -INFINITY ? 0.f : rs.m_run, rs.l_run);
 }
@@ -668,7 +670,7 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(AttnArgsF32 a) {
 
 }  // namespace
 
-AttnPlan make_attn_plan(const ckv_dims* d, int64_t k) {
+AttnPlan make_attn_plan(const ckv_dims* d, int64_t k, bool with_suffix) {
   AttnPlan p{};
   const int G = d->n_q_heads / d->n_kv_heads;
   p.rows = G * d->n_suffix;
@@ -676,7 +678,7 @@ AttnPlan make_attn_plan(const ckv_dims* d, int64_t k) {
     p.n_splits = 1;
     return p;
   }
-  const int64_t np = k * d->chunk_size + d->n_suffix;
+  const int64_t np = k * d->chunk_size + (with_suffix ? d->n_suffix : 0);
   const int64_t ntiles = ceil_div(np, kTile);
   const int64_t base = (int64_t)d->n_kv_heads * ceil_div(p.rows, kBlockRows);
   // at most ~2 workgroups per CU, keeping >= 4 stages per split and no more
@@ -699,34 +701,13 @@ AttnPlan make_attn_plan(const ckv_dims* d, int64_t k) {
   return p;
 }
 
-ckv_status launch_attn(const ckv_dims* d, const void* q, const ChunkSource& src, const int32_t* sel,
-                       int64_t k, const void* k_suffix, const void* v_suffix, void* out, void* ws,
-                       size_t ws_bytes, hipStream_t st) {
-  if (d->dtype == CKV_DTYPE_F32) {
-    AttnArgsF32 a;
-    a.q = static_cast<const float*>(q);
-    a.kbase = static_cast<const float*>(src.k_base);
-    a.vbase = static_cast<const float*>(src.v_base);
-    a.chunk_stride = src.chunk_stride;
-    a.chunk_off = src.chunk_off;
-    a.direct = src.direct;
-    a.sel = sel;
-    a.kc = k * d->chunk_size;
-    a.n = d->n_prefix;
-    a.c = d->chunk_size;
-    a.ks = static_cast<const float*>(k_suffix);
-    a.vs = static_cast<const float*>(v_suffix);
-    a.out = static_cast<float*>(out);
-    a.S = d->n_suffix; a.Hq = d->n_q_heads; a.Hkv = d->n_kv_heads;
-    a.G = d->n_q_heads / d->n_kv_heads;
-    a.c1 = resolve_scale(d) * 1.4426950408889634f;
-    hipLaunchKernelGGL(attn_f32_kernel<64>, dim3((unsigned)((int64_t)a.S * a.Hq)), dim3(64), 0, st, a);
-    CKV_HIP(hipGetLastError());
-    return CKV_OK;
-  }
-  const AttnPlan p = make_attn_plan(d, k);
-  if (ws_bytes < p.bytes) CKV_FAIL(CKV_EINVAL, "attention workspace too small: %zu < %zu", ws_bytes, p.bytes);
-  AttnArgs a;
+namespace {
+
+// Arguments of one bf16 attention launch over the kept chunks sel[0..k) of
+// src (and the suffix when with_suffix) in n_splits key splits.
+ckv_status attn_args(const ckv_dims* d, const void* q, const ChunkSource& src, const int32_t* sel,
+                     int64_t k, const void* k_suffix, const void* v_suffix, bool with_suffix,
+                     int32_t n_splits, AttnArgs& a) {
   a.q = static_cast<const uint16_t*>(q);
   a.kbase = static_cast<const uint16_t*>(src.k_base);
   a.vbase = static_cast<const uint16_t*>(src.v_base);
@@ -758,35 +739,139 @@ ckv_status launch_attn(const ckv_dims* d, const void* q, const ChunkSource& src,
   a.log2c = (d->chunk_size & (d->chunk_size - 1)) == 0 ? __builtin_ctz(d->chunk_size) : -1;
   a.ks = static_cast<const uint16_t*>(k_suffix);
   a.vs = static_cast<const uint16_t*>(v_suffix);
-  a.out = static_cast<uint16_t*>(out);
-  a.o_part = p.n_splits > 1 ? reinterpret_cast<uint16_t*>(static_cast<char*>(ws) + p.off_o) : nullptr;
-  a.ml_part = p.n_splits > 1 ? reinterpret_cast<float2*>(static_cast<char*>(ws) + p.off_ml) : nullptr;
   a.S = d->n_suffix; a.Hq = d->n_q_heads; a.Hkv = d->n_kv_heads;
-  a.G = d->n_q_heads / d->n_kv_heads; a.R = p.rows;
-  a.n_splits = p.n_splits;
-  const int64_t ntiles = ceil_div(a.kc + a.S, kTile);
-  a.tiles_per_split = (int)ceil_div(ntiles, p.n_splits);  // <= kMaxSliceKeys / kTile
-  a.n_row_blocks = (int)ceil_div(p.rows, kBlockRows);
+  a.G = d->n_q_heads / d->n_kv_heads; a.R = a.G * d->n_suffix;
+  a.n_splits = n_splits;
+  a.with_suffix = with_suffix ? 1 : 0;
+  const int64_t ntiles = ceil_div(a.kc + (with_suffix ? a.S : 0), kTile);
+  a.tiles_per_split = (int)ceil_div(ntiles, n_splits);  // <= kMaxSliceKeys / kTile
+  a.n_row_blocks = (int)ceil_div(a.R, kBlockRows);
   a.c1 = resolve_scale(d) * 1.4426950408889634f;
   a.nblocks = (uint32_t)((int64_t)a.Hkv * a.n_row_blocks * a.n_splits);
   a.nblocks_padded = (uint32_t)align_up(a.nblocks, 8);
+  return CKV_OK;
+}
+
+ckv_status launch_attn_kernel(const ckv_dims* d, const AttnArgs& a, hipStream_t st) {
   const size_t slice_bytes = (size_t)a.tiles_per_split * (2 * kTile + 1) * sizeof(int);
   if (d->head_dim == 128)
     hipLaunchKernelGGL(attn_kernel<128>, dim3(a.nblocks_padded), dim3(kWaves * 64), slice_bytes, st, a);
   else
     hipLaunchKernelGGL(attn_kernel<64>, dim3(a.nblocks_padded), dim3(kWaves * 64), slice_bytes, st, a);
   CKV_HIP(hipGetLastError());
-  if (p.n_splits > 1) {
-    const int64_t work = (int64_t)a.Hkv * a.R * (d->head_dim / 8);
-    if (d->head_dim == 128)
-      hipLaunchKernelGGL(combine_kernel<128>, dim3((unsigned)ceil_div(work, 256)), dim3(256), 0, st,
-                         a.o_part, a.ml_part, a.out, a.n_splits, a.Hkv, a.R, a.G, a.Hq);
-    else
-      hipLaunchKernelGGL(combine_kernel<64>, dim3((unsigned)ceil_div(work, 256)), dim3(256), 0, st,
-                         a.o_part, a.ml_part, a.out, a.n_splits, a.Hkv, a.R, a.G, a.Hq);
-    CKV_HIP(hipGetLastError());
-  }
   return CKV_OK;
+}
+
+ckv_status launch_combine(const ckv_dims* d, const uint16_t* o_part, const float2* ml_part,
+                          int32_t n_splits, void* out, hipStream_t st) {
+  const int G = d->n_q_heads / d->n_kv_heads, R = G * d->n_suffix;
+  const int64_t work = (int64_t)d->n_kv_heads * R * (d->head_dim / 8);
+  uint16_t* o = static_cast<uint16_t*>(out);
+  if (d->head_dim == 128)
+    hipLaunchKernelGGL(combine_kernel<128>, dim3((unsigned)ceil_div(work, 256)), dim3(256), 0, st,
+                       o_part, ml_part, o, n_splits, d->n_kv_heads, R, G, d->n_q_heads);
+  else
+    hipLaunchKernelGGL(combine_kernel<64>, dim3((unsigned)ceil_div(work, 256)), dim3(256), 0, st,
+                       o_part, ml_part, o, n_splits, d->n_kv_heads, R, G, d->n_q_heads);
+  CKV_HIP(hipGetLastError());
+  return CKV_OK;
+}
+
+// Split partials of a two-part launch: splits [0, max_splits) of o_part
+// ([split][Hkv][R][D] bf16) then of ml_part ([split][Hkv][R] float2).
+size_t part_o_bytes(const ckv_dims* d, int64_t max_splits) {
+  const int G = d->n_q_heads / d->n_kv_heads;
+  return align_up((size_t)max_splits * d->n_kv_heads * G * d->n_suffix * d->head_dim *
+                      sizeof(uint16_t), 256);
+}
+
+}  // namespace
+
+ckv_status launch_attn(const ckv_dims* d, const void* q, const ChunkSource& src, const int32_t* sel,
+                       int64_t k, const void* k_suffix, const void* v_suffix, void* out, void* ws,
+                       size_t ws_bytes, hipStream_t st) {
+  if (d->dtype == CKV_DTYPE_F32) {
+    AttnArgsF32 a;
+    a.q = static_cast<const float*>(q);
+    a.kbase = static_cast<const float*>(src.k_base);
+    a.vbase = static_cast<const float*>(src.v_base);
+    a.chunk_stride = src.chunk_stride;
+    a.chunk_off = src.chunk_off;
+    a.direct = src.direct;
+    a.sel = sel;
+    a.kc = k * d->chunk_size;
+    a.n = d->n_prefix;
+    a.c = d->chunk_size;
+    a.ks = static_cast<const float*>(k_suffix);
+    a.vs = static_cast<const float*>(v_suffix);
+    a.out = static_cast<float*>(out);
+    a.S = d->n_suffix; a.Hq = d->n_q_heads; a.Hkv = d->n_kv_heads;
+    a.G = d->n_q_heads / d->n_kv_heads;
+    a.c1 = resolve_scale(d) * 1.4426950408889634f;
+    hipLaunchKernelGGL(attn_f32_kernel<64>, dim3((unsigned)((int64_t)a.S * a.Hq)), dim3(64), 0, st, a);
+    CKV_HIP(hipGetLastError());
+    return CKV_OK;
+  }
+  const AttnPlan p = make_attn_plan(d, k);
+  if (ws_bytes < p.bytes) CKV_FAIL(CKV_EINVAL, "attention workspace too small: %zu < %zu", ws_bytes, p.bytes);
+  AttnArgs a;
+  ckv_status s = attn_args(d, q, src, sel, k, k_suffix, v_suffix, true, p.n_splits, a);
+  if (s != CKV_OK) return s;
+  a.out = static_cast<uint16_t*>(out);
+  a.partial = p.n_splits > 1 ? 1 : 0;
+  a.o_part = a.partial ? reinterpret_cast<uint16_t*>(static_cast<char*>(ws) + p.off_o) : nullptr;
+  a.ml_part = a.partial ? reinterpret_cast<float2*>(static_cast<char*>(ws) + p.off_ml) : nullptr;
+  if ((s = launch_attn_kernel(d, a, st)) != CKV_OK) return s;
+  if (a.partial) return launch_combine(d, a.o_part, a.ml_part, a.n_splits, out, st);
+  return CKV_OK;
+}
+
+int64_t attn_two_part_splits(const ckv_dims* d, int64_t k) {
+  int64_t most = 0;
+  for (int64_t ka = 0; ka <= k; ++ka)
+    most = std::max<int64_t>(most, make_attn_plan(d, ka, true).n_splits +
+                                       (ka < k ? make_attn_plan(d, k - ka, false).n_splits : 0));
+  return most;
+}
+
+size_t attn_two_part_bytes(const ckv_dims* d, int64_t max_splits) {
+  const int G = d->n_q_heads / d->n_kv_heads;
+  return align_up(part_o_bytes(d, max_splits) +
+                      (size_t)max_splits * d->n_kv_heads * G * d->n_suffix * sizeof(float2),
+                  256);
+}
+
+ckv_status launch_attn_part(const ckv_dims* d, const void* q, const ChunkSource& src,
+                            const int32_t* sel, int64_t k, const void* k_suffix,
+                            const void* v_suffix, bool with_suffix, void* ws, int64_t max_splits,
+                            int32_t split_base, int32_t* n_splits, hipStream_t st) {
+  if (d->dtype != CKV_DTYPE_BF16) CKV_FAIL(CKV_EUNSUPPORTED, "two-part attention is bf16 only");
+  const AttnPlan p = make_attn_plan(d, k, with_suffix);
+  if (split_base < 0 || split_base + (int64_t)p.n_splits > max_splits)
+    CKV_FAIL(CKV_EINVAL, "attention splits %d + %d exceed the workspace's %lld", split_base,
+             p.n_splits, (long long)max_splits);
+  AttnArgs a;
+  ckv_status s = attn_args(d, q, src, sel, k, k_suffix, v_suffix, with_suffix, p.n_splits, a);
+  if (s != CKV_OK) return s;
+  const size_t rows = (size_t)d->n_kv_heads * a.R;
+  a.out = nullptr;
+  a.partial = 1;
+  a.o_part = static_cast<uint16_t*>(ws) + (size_t)split_base * rows * d->head_dim;
+  a.ml_part = reinterpret_cast<float2*>(static_cast<char*>(ws) + part_o_bytes(d, max_splits)) +
+              (size_t)split_base * rows;
+  *n_splits = p.n_splits;
+  return launch_attn_kernel(d, a, st);
+}
+
+ckv_status launch_attn_combine(const ckv_dims* d, const void* ws, int64_t max_splits,
+                               int32_t n_splits, void* out, hipStream_t st) {
+  if (n_splits < 1 || n_splits > max_splits)
+    CKV_FAIL(CKV_EINVAL, "combine of %d splits (workspace holds %lld)", n_splits,
+             (long long)max_splits);
+  return launch_combine(d, static_cast<const uint16_t*>(ws),
+                        reinterpret_cast<const float2*>(static_cast<const char*>(ws) +
+                                                        part_o_bytes(d, max_splits)),
+                        n_splits, out, st);
 }
 
 }  // namespace ckv

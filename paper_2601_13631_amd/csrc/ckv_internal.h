@@ -175,9 +175,26 @@ struct AttnPlan {
   int32_t n_splits;  // key splits (1: no combine)
   size_t off_o, off_ml, bytes;
 };
-AttnPlan make_attn_plan(const ckv_dims* d, int64_t k);
+// Keys: the k kept chunks, then (with_suffix) the causal suffix.
+AttnPlan make_attn_plan(const ckv_dims* d, int64_t k, bool with_suffix = true);
 ckv_status launch_attn(const ckv_dims* d, const void* q, const ChunkSource& src,
                        const int32_t* sel, int64_t k, const void* k_suffix, const void* v_suffix,
                        void* out, void* ws, size_t ws_bytes, hipStream_t st);
+// Attention in two parts over one kept set (bf16): each part is a launch over
+// some of the kept chunks (the first part with the suffix) that writes its
+// split partials at split_base.. of a shared workspace, and one combine merges
+// the n_splits partials of both parts in split order.  The parts may wait on
+// different events: a host-resident layer attends over the chunks already in
+// HBM while the rest are still being copied.  attn_two_part_splits is the
+// most splits any division of k chunks into two parts takes;
+// attn_two_part_bytes the workspace for that many.
+int64_t attn_two_part_splits(const ckv_dims* d, int64_t k);
+size_t attn_two_part_bytes(const ckv_dims* d, int64_t max_splits);
+ckv_status launch_attn_part(const ckv_dims* d, const void* q, const ChunkSource& src,
+                            const int32_t* sel, int64_t k, const void* k_suffix,
+                            const void* v_suffix, bool with_suffix, void* ws, int64_t max_splits,
+                            int32_t split_base, int32_t* n_splits, hipStream_t st);
+ckv_status launch_attn_combine(const ckv_dims* d, const void* ws, int64_t max_splits,
+                               int32_t n_splits, void* out, hipStream_t st);
 
 }  // namespace ckv

@@ -90,6 +90,11 @@ struct ckv_ctx {
   int32_t* sel_host = nullptr;    // pinned [k]
   hipStream_t demand = nullptr, prefetch = nullptr;
   hipEvent_t ev_sel = nullptr, ev_dem = nullptr;
+  hipEvent_t ev_tab = nullptr;  // the attention lists of the layer are on the device
+  // host-resident bf16 layers attend in two parts (chunks already in HBM and
+  // the suffix, then the chunks copied on demand): the most splits they take
+  int64_t attn_splits = 0;
+  std::vector<int32_t> slot_sorted;  // arena slot of each kept chunk, ascending chunk order
   std::vector<const void*> host_layers;  // device views of the registered per-layer stores
   int32_t prev_layer = -1;  // last layer run since creation or reset (-1: none)
   bool broken = false;      // a layer failed after enqueueing work: reset before the next
@@ -267,6 +272,7 @@ ckv_status free_ctx(ckv_ctx* c) {
   (void)hipFree(c->tspan);
   if (c->ev_sel) (void)hipEventDestroy(c->ev_sel);
   if (c->ev_dem) (void)hipEventDestroy(c->ev_dem);
+  if (c->ev_tab) (void)hipEventDestroy(c->ev_tab);
   if (c->demand) (void)hipStreamDestroy(c->demand);
   if (c->prefetch) (void)hipStreamDestroy(c->prefetch);
   delete c;
@@ -508,6 +514,10 @@ ckv_status ckv_ctx_create(const ckv_dims* dims, int32_t n_layers, double keep_ra
     CKV_FAIL(CKV_EUNSUPPORTED, "shape too large for the scoring decomposition");
   }
   c->ws_attn = make_attn_plan(dims, c->k).bytes;
+  if ((flags & CKV_CTX_HOST_PREFIX) && dims->dtype == CKV_DTYPE_BF16) {
+    c->attn_splits = attn_two_part_splits(dims, c->k);
+    c->ws_attn = std::max(c->ws_attn, attn_two_part_bytes(dims, c->attn_splits));
+  }
   // scoring and attention scratch are used one after the other on one stream,
   // so both start at the front of the workspace
   c->off_attn = 0;
@@ -544,6 +554,7 @@ ckv_status ckv_ctx_create(const ckv_dims* dims, int32_t n_layers, double keep_ra
     CKV_HIP_ALLOC(hipStreamCreateWithFlags(&c->prefetch, hipStreamNonBlocking));
     CKV_HIP_ALLOC(hipEventCreateWithFlags(&c->ev_sel, hipEventDisableTiming));
     CKV_HIP_ALLOC(hipEventCreateWithFlags(&c->ev_dem, hipEventDisableTiming));
+    CKV_HIP_ALLOC(hipEventCreateWithFlags(&c->ev_tab, hipEventDisableTiming));
   }
   c->span_mode = (flags & CKV_CTX_SCORE_TIMING) && !(flags & CKV_CTX_STAGE_TIMING) &&
                  dims->dtype == CKV_DTYPE_BF16;
@@ -1013,13 +1024,15 @@ ckv_status run_layer(ckv_ctx* c, const LayerArgs& la, ckv_layer_stats* stats) {
     c->pool_quarantine.clear();
   }
 
-  // slot table, in arena slots: chunks held in the cache's HBM slots are read
-  // there; predicted chunks sit in this layer's buffer at slots 0..|P|-1 (in P
-  // order), misses follow
+  // slot of each kept chunk, in arena slots: chunks held in the cache's HBM
+  // slots are read there; predicted chunks sit in this layer's buffer at slots
+  // 0..|P|-1 (in P order), misses follow
   if ((s = guard(B.ev_gd, B.gd)) != CKV_OK) return s;
   std::vector<int32_t> miss;
   miss.reserve((size_t)k);
-  int32_t* tab = B.tab_host;
+  std::vector<int32_t>& tab = c->slot_sorted;
+  tab.resize((size_t)k);
+  std::vector<char> late((size_t)k, 0);  // fetched on demand by this layer
   size_t pi = 0;
   int64_t hits = 0;
   for (int64_t u = 0; u < k; ++u) {
@@ -1037,6 +1050,7 @@ ckv_status run_layer(ckv_ctx* c, const LayerArgs& la, ckv_layer_stats* stats) {
       ++hits;
     } else {
       tab[u] = (int32_t)(buf0 + P.size() + miss.size());
+      late[u] = 1;
       miss.push_back(j);
       stv.bytes_demand += cb;
     }
@@ -1045,6 +1059,21 @@ ckv_status run_layer(ckv_ctx* c, const LayerArgs& la, ckv_layer_stats* stats) {
   stv.misses = (int64_t)miss.size();
   stv.wasted = (int64_t)P.size() - hits;
   const int64_t n_pred = (int64_t)P.size();
+  // the attention's lists (pinned staging, one copy to the device): chunk
+  // indices and slots of the kept chunks already in HBM, then of the misses,
+  // each part in ascending chunk order.  The misses' indices are also the
+  // demand copy's list.
+  const int64_t n_early = k - (int64_t)miss.size();
+  {
+    int32_t* tabp = B.tab_host;
+    int32_t* selp = B.dem_host;  // = tab_host + k (one staging block)
+    int64_t e = 0, x = n_early;
+    for (int64_t u = 0; u < k; ++u) {
+      const int64_t at = late[u] ? x++ : e++;
+      tabp[at] = tab[u];
+      selp[at] = c->sel_host[u];
+    }
+  }
 
   // storage tier: the pool slots the misses move from; those not in the pool
   // get free slots and are read from the file below
@@ -1108,27 +1137,26 @@ ckv_status run_layer(ckv_ctx* c, const LayerArgs& la, ckv_layer_stats* stats) {
       CKV_FAIL(CKV_EHIP, "injected host-to-HBM copy failure at layer %d", layer);
     }
     if (B.attn_rec) CKV_HIP(hipStreamWaitEvent(c->demand, B.ev_attn, 0));
-    CKV_HIP(hipMemcpyAsync(B.tab_dev, tab, (size_t)k * sizeof(int32_t), hipMemcpyHostToDevice,
-                           c->demand));
+    // slots then chunk indices: adjacent on the host and on the device
+    CKV_HIP(hipMemcpyAsync(B.tab_dev, B.tab_host, (size_t)(2 * k) * sizeof(int32_t),
+                           hipMemcpyHostToDevice, c->demand));
+    CKV_HIP(hipEventRecord(c->ev_tab, c->demand));
     ckv_status r = CKV_OK;
     if (!miss.empty() && stored) {
+      // its staging guard, recorded after its own list copy, covers the lists above
       r = pool_copy(c, cur, 1, msrc.data(), mdst.data(), (int64_t)miss.size(), c->demand);
-    } else if (!miss.empty()) {
-      std::memcpy(B.dem_host, miss.data(), miss.size() * sizeof(int32_t));
-      CKV_HIP(hipMemcpyAsync(B.dem_dev, B.dem_host, miss.size() * sizeof(int32_t),
-                             hipMemcpyHostToDevice, c->demand));
-      CKV_HIP(hipEventRecord(B.ev_gd, c->demand));
-      B.gd = true;
-      r = launch_copy_spans(la.store, B.dem_dev, (int64_t)miss.size(), n_pred, B.slots,
-                            c->slot_bytes, c->demand);
     } else {
       CKV_HIP(hipEventRecord(B.ev_gd, c->demand));
       B.gd = true;
+      if (!miss.empty())
+        r = launch_copy_spans(la.store, B.dem_dev + n_early, (int64_t)miss.size(), n_pred, B.slots,
+                              c->slot_bytes, c->demand);
     }
     if (r != CKV_OK) return r;
     CKV_HIP(hipEventRecord(c->ev_dem, c->demand));
     if ((r = period_prefetch()) != CKV_OK) return r;
-    CKV_HIP(hipStreamWaitEvent(st, c->ev_dem, 0));
+    const bool two_part = c->attn_splits > 0;
+    CKV_HIP(hipStreamWaitEvent(st, two_part ? c->ev_tab : c->ev_dem, 0));
     if (B.pref_pending) CKV_HIP(hipStreamWaitEvent(st, B.ev_pref, 0));
     B.pref_pending = false;
     if (gate_layer > layer) {  // SubPeriod gate: the Period's first layers are in HBM
@@ -1138,8 +1166,27 @@ ckv_status run_layer(ckv_ctx* c, const LayerArgs& la, ckv_layer_stats* stats) {
     if ((r = mark(4)) != CKV_OK) return r;
     ChunkSource src{c->arena, static_cast<char*>(c->arena) + span_elems * eb, 2 * span_elems,
                     B.tab_dev, 0, c->nbuf * spb + c->cache_slots};
-    r = launch_attn(d, io->q, src, sel, k, io->k_suffix, io->v_suffix, io->out, ws + c->off_attn,
-                    c->ws_attn, st);
+    if (two_part) {
+      // the chunks already in HBM and the suffix while the misses are copied,
+      // then the misses, then one merge of both parts' splits
+      void* aw = ws + c->off_attn;
+      int32_t s1 = 0, s2 = 0;
+      r = launch_attn_part(d, io->q, src, B.dem_dev, n_early, io->k_suffix, io->v_suffix, true, aw,
+                           c->attn_splits, 0, &s1, st);
+      if (r != CKV_OK) return r;
+      CKV_HIP(hipStreamWaitEvent(st, c->ev_dem, 0));
+      if (n_early < k) {
+        ChunkSource late = src;
+        late.chunk_off = B.tab_dev + n_early;
+        r = launch_attn_part(d, io->q, late, B.dem_dev + n_early, k - n_early, io->k_suffix,
+                             io->v_suffix, false, aw, c->attn_splits, s1, &s2, st);
+        if (r != CKV_OK) return r;
+      }
+      r = launch_attn_combine(d, aw, c->attn_splits, s1 + s2, io->out, st);
+    } else {
+      r = launch_attn(d, io->q, src, B.dem_dev, k, io->k_suffix, io->v_suffix, io->out,
+                      ws + c->off_attn, c->ws_attn, st);
+    }
     if (r != CKV_OK) return r;
     if ((r = mark(5)) != CKV_OK) return r;
     if (tev) ++c->t_issued;

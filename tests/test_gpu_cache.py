@@ -1,8 +1,12 @@
 """The attention-guided cache (Sec. 4.5) on the host-resident layer step.
 
 Three requests on one prefix run layer by layer through a context with a
-cache attached and through one without.  Outputs and kept sets must agree bit
-for bit (the cache only changes where the chunk bytes come from); the
+cache attached and through one without.  Kept sets and chunk scores must
+agree bit for bit (the cache only changes where the chunk bytes come from),
+and both outputs must lie within their bound of the oracle's attention: a
+host-resident layer attends first over the chunks already in HBM (cache slots
+and prefetched chunks) and then over the chunks copied on demand, so the
+cache changes how the keys are grouped and with it the roundings.  The
 chunks read from HBM cache slots, the host-link counts and the cache fills
 must equal what the oracle cache, fed the same chunk scores, predicts; the
 final tiers and scores must equal the oracle cache's.
@@ -73,7 +77,6 @@ def test_layer_cache_requests(period, n_prefix):
             torch.cuda.synchronize()
             sel = sels[0].cpu().numpy().astype(np.int64)
             assert np.array_equal(sel, sels[1].cpu().numpy())
-            assert torch.equal(outs[0].view(torch.int16), outs[1].view(torch.int16))
             if first == l:
                 A_first = As[0].cpu().numpy()
                 assert np.array_equal(A_first.view(np.int64), As[1].cpu().numpy().view(np.int64))
@@ -103,7 +106,8 @@ def test_layer_cache_requests(period, n_prefix):
             t = dict(layers[l], q=synth.request_queries(w, l, r))
             out_ref = oracle.sparse_attn(s, t["q"], t["k_prefix"], t["v_prefix"],
                                          sel.astype(np.int32), t["k_suffix"], t["v_suffix"])
-            attn_check(s, t, sel.astype(np.int32), to_f64(outs[0]).reshape(out_ref.shape), out_ref)
+            for o in outs:
+                attn_check(s, t, sel.astype(np.int32), to_f64(o).reshape(out_ref.shape), out_ref)
             total_cache_hits += st["cache_hits"]
             print(f"  cache hits {st['cache_hits']} prefetch hits {st['hits']} "
                   f"misses {st['misses']} fills {fills}", flush=True)
@@ -325,10 +329,13 @@ def test_attach_store_refusals(tmp_path):
 @pytest.mark.parametrize("with_cache", [False, True, "small"])
 def test_layer_store_subperiod(tmp_path, with_cache):
     """Periods of 4 layers with a SubPeriod of 3: a Period's layers queue the
-    storage reads of the next two layers of the Period.  Outputs and sets equal
-    the pinned-store path's bit for bit; without a cache the hit/miss counts
-    and, over a request, the prefetched and file-read bytes equal those of one
-    layer ahead."""
+    storage reads of the next two layers of the Period.  Sets equal the
+    pinned-store path's; without a cache so do the outputs, bit for bit (the
+    same chunks are in HBM when each layer attends), the hit/miss counts and,
+    over a request, the prefetched and file-read bytes of one layer ahead.
+    With a cache the read-ahead is listed against an earlier cache state, so
+    which chunks a layer finds in HBM may differ: every output is checked
+    against the oracle's attention instead."""
     import paper_2601_13631_amd as ckv
     w = synth.WORKLOADS["c5_qwen32b_128k_host"].scaled(n_prefix=4096, n_suffix=24, n_layers=8)
     L, m = w.n_layers, w.n_chunks
@@ -381,7 +388,15 @@ def test_layer_store_subperiod(tmp_path, with_cache):
             torch.cuda.synchronize()
             for i in (1, 2):
                 assert torch.equal(sels[0], sels[i])
-                assert torch.equal(outs[0].view(torch.int16), outs[i].view(torch.int16))
+                if not with_cache:
+                    assert torch.equal(outs[0].view(torch.int16), outs[i].view(torch.int16))
+            if with_cache:
+                t = dict(layers[l], q=synth.request_queries(w, l, r))
+                sel0 = sels[0].cpu().numpy()
+                out_ref = oracle.sparse_attn(oshape(w), t["q"], t["k_prefix"], t["v_prefix"],
+                                             sel0, t["k_suffix"], t["v_suffix"])
+                for o in outs:
+                    attn_check(oshape(w), t, sel0, to_f64(o).reshape(out_ref.shape), out_ref)
             for i, st in enumerate(sts):
                 for f in tot[i]:
                     tot[i][f] += st[f]

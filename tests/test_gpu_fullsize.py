@@ -106,14 +106,17 @@ def test_full_size_128k_shard_hbm_and_host_paths():
     A, sel, out, st, k = _run(w, layer, t)
     _check_layer(w, t, A, sel, out, k)
     # the same layer with its K/V store in pinned host memory (chunk-major):
-    # identical kernels over identical data give bitwise identical results
+    # identical scoring and selection give bitwise identical scores and set; the
+    # attention runs in two parts there (the chunks already in HBM -- none on a
+    # first layer -- with the suffix, then the chunks copied on demand), so its
+    # output is checked against the oracle on its own
     import paper_2601_13631_amd as ckv
     cm = synth.chunk_major(t["k_prefix"], t["v_prefix"], w.chunk_size)
     store = torch.from_numpy(cm.reshape(-1)).view(torch.bfloat16).pin_memory()
     A2, sel2, out2, st2, _ = _run(w, 0, t, flags=ckv.CTX_HOST_PREFIX, kv_host=store)
     assert np.array_equal(A.view(np.uint64), A2.view(np.uint64))
     assert np.array_equal(sel, sel2)
-    assert torch.equal(out.view(torch.int16), out2.view(torch.int16))
+    _check_layer(w, t, A2, sel2, out2, k)
     # a first layer has no prediction: every kept chunk is fetched on demand
     acc = oracle.layer_accounting(oshape(w), sel2, np.zeros(0, np.int32))
     assert st2["hits"] == 0 and st2["misses"] == k

