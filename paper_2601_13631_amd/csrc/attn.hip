@@ -826,11 +826,23 @@ ckv_status launch_attn(const ckv_dims* d, const void* q, const ChunkSource& src,
   return CKV_OK;
 }
 
-int64_t attn_two_part_splits(const ckv_dims* d, int64_t k) {
+int64_t attn_late_part_begin(int64_t n_late, int parts, int i) {
+  return n_late * i / parts;
+}
+
+int64_t attn_two_part_splits(const ckv_dims* d, int64_t k, int max_late_parts) {
   int64_t most = 0;
-  for (int64_t ka = 0; ka <= k; ++ka)
-    most = std::max<int64_t>(most, make_attn_plan(d, ka, true).n_splits +
-                                       (ka < k ? make_attn_plan(d, k - ka, false).n_splits : 0));
+  for (int64_t ka = 0; ka <= k; ++ka) {
+    const int64_t nl = k - ka;
+    for (int parts = 1; parts <= max_late_parts; ++parts) {
+      int64_t n = make_attn_plan(d, ka, true).n_splits;
+      for (int i = 0; i < parts; ++i) {
+        const int64_t cnt = attn_late_part_begin(nl, parts, i + 1) - attn_late_part_begin(nl, parts, i);
+        if (cnt > 0) n += make_attn_plan(d, cnt, false).n_splits;
+      }
+      most = std::max(most, n);
+    }
+  }
   return most;
 }
 

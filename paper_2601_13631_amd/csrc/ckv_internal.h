@@ -180,15 +180,19 @@ AttnPlan make_attn_plan(const ckv_dims* d, int64_t k, bool with_suffix = true);
 ckv_status launch_attn(const ckv_dims* d, const void* q, const ChunkSource& src,
                        const int32_t* sel, int64_t k, const void* k_suffix, const void* v_suffix,
                        void* out, void* ws, size_t ws_bytes, hipStream_t st);
-// Attention in two parts over one kept set (bf16): each part is a launch over
+// Attention in parts over one kept set (bf16): each part is a launch over
 // some of the kept chunks (the first part with the suffix) that writes its
 // split partials at split_base.. of a shared workspace, and one combine merges
-// the n_splits partials of both parts in split order.  The parts may wait on
+// the n_splits partials of all parts in split order.  The parts may wait on
 // different events: a host-resident layer attends over the chunks already in
-// HBM while the rest are still being copied.  attn_two_part_splits is the
-// most splits any division of k chunks into two parts takes;
-// attn_two_part_bytes the workspace for that many.
-int64_t attn_two_part_splits(const ckv_dims* d, int64_t k);
+// HBM while the rest (the late chunks) are still being copied, and over each
+// share of the late chunks once its copy has landed.  The n_late late chunks
+// go in `parts` consecutive shares, share i beginning at
+// attn_late_part_begin(n_late, parts, i).  attn_two_part_splits is the most
+// splits any division of k chunks into a first part and 1..max_late_parts
+// late shares takes; attn_two_part_bytes the workspace for that many.
+int64_t attn_late_part_begin(int64_t n_late, int parts, int i);
+int64_t attn_two_part_splits(const ckv_dims* d, int64_t k, int max_late_parts);
 size_t attn_two_part_bytes(const ckv_dims* d, int64_t max_splits);
 ckv_status launch_attn_part(const ckv_dims* d, const void* q, const ChunkSource& src,
                             const int32_t* sel, int64_t k, const void* k_suffix,

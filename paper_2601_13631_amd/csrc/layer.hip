@@ -91,8 +91,13 @@ struct ckv_ctx {
   hipStream_t demand = nullptr, prefetch = nullptr;
   hipEvent_t ev_sel = nullptr, ev_dem = nullptr;
   hipEvent_t ev_tab = nullptr;  // the attention lists of the layer are on the device
-  // host-resident bf16 layers attend in two parts (chunks already in HBM and
-  // the suffix, then the chunks copied on demand): the most splits they take
+  // host-resident bf16 layers attend in parts: the chunks already in HBM with
+  // the suffix, then each of up to kLateParts shares of the chunks copied on
+  // demand once its copy has landed (ev_late[i]; the storage tier's one copy
+  // out of its pool lands every share).  attn_splits: the most splits the
+  // parts take
+  static constexpr int kLateParts = 4;
+  hipEvent_t ev_late[kLateParts] = {};
   int64_t attn_splits = 0;
   std::vector<int32_t> slot_sorted;  // arena slot of each kept chunk, ascending chunk order
   std::vector<const void*> host_layers;  // device views of the registered per-layer stores
@@ -273,6 +278,8 @@ ckv_status free_ctx(ckv_ctx* c) {
   if (c->ev_sel) (void)hipEventDestroy(c->ev_sel);
   if (c->ev_dem) (void)hipEventDestroy(c->ev_dem);
   if (c->ev_tab) (void)hipEventDestroy(c->ev_tab);
+  for (hipEvent_t e : c->ev_late)
+    if (e) (void)hipEventDestroy(e);
   if (c->demand) (void)hipStreamDestroy(c->demand);
   if (c->prefetch) (void)hipStreamDestroy(c->prefetch);
   delete c;
@@ -515,7 +522,7 @@ ckv_status ckv_ctx_create(const ckv_dims* dims, int32_t n_layers, double keep_ra
   }
   c->ws_attn = make_attn_plan(dims, c->k).bytes;
   if ((flags & CKV_CTX_HOST_PREFIX) && dims->dtype == CKV_DTYPE_BF16) {
-    c->attn_splits = attn_two_part_splits(dims, c->k);
+    c->attn_splits = attn_two_part_splits(dims, c->k, ckv_ctx::kLateParts);
     c->ws_attn = std::max(c->ws_attn, attn_two_part_bytes(dims, c->attn_splits));
   }
   // scoring and attention scratch are used one after the other on one stream,
@@ -555,6 +562,7 @@ ckv_status ckv_ctx_create(const ckv_dims* dims, int32_t n_layers, double keep_ra
     CKV_HIP_ALLOC(hipEventCreateWithFlags(&c->ev_sel, hipEventDisableTiming));
     CKV_HIP_ALLOC(hipEventCreateWithFlags(&c->ev_dem, hipEventDisableTiming));
     CKV_HIP_ALLOC(hipEventCreateWithFlags(&c->ev_tab, hipEventDisableTiming));
+    for (hipEvent_t& e : c->ev_late) CKV_HIP_ALLOC(hipEventCreateWithFlags(&e, hipEventDisableTiming));
   }
   c->span_mode = (flags & CKV_CTX_SCORE_TIMING) && !(flags & CKV_CTX_STAGE_TIMING) &&
                  dims->dtype == CKV_DTYPE_BF16;
@@ -1142,17 +1150,27 @@ ckv_status run_layer(ckv_ctx* c, const LayerArgs& la, ckv_layer_stats* stats) {
                            hipMemcpyHostToDevice, c->demand));
     CKV_HIP(hipEventRecord(c->ev_tab, c->demand));
     ckv_status r = CKV_OK;
-    if (!miss.empty() && stored) {
+    const int64_t nm = (int64_t)miss.size();
+    // shares of the misses, each copied and then attended over on its own (from
+    // the storage tier's pool one copy lands every share; the shares, and so
+    // the roundings, stay those of the pinned-store path)
+    const int parts = nm == 0 ? 0 : (int)std::min<int64_t>(ckv_ctx::kLateParts, nm);
+    if (nm > 0 && stored) {
       // its staging guard, recorded after its own list copy, covers the lists above
-      r = pool_copy(c, cur, 1, msrc.data(), mdst.data(), (int64_t)miss.size(), c->demand);
+      r = pool_copy(c, cur, 1, msrc.data(), mdst.data(), nm, c->demand);
+      if (r != CKV_OK) return r;
+      for (int i = 0; i < parts; ++i) CKV_HIP(hipEventRecord(c->ev_late[i], c->demand));
     } else {
       CKV_HIP(hipEventRecord(B.ev_gd, c->demand));
       B.gd = true;
-      if (!miss.empty())
-        r = launch_copy_spans(la.store, B.dem_dev + n_early, (int64_t)miss.size(), n_pred, B.slots,
+      for (int i = 0; i < parts; ++i) {
+        const int64_t b0 = attn_late_part_begin(nm, parts, i), b1 = attn_late_part_begin(nm, parts, i + 1);
+        r = launch_copy_spans(la.store, B.dem_dev + n_early + b0, b1 - b0, n_pred + b0, B.slots,
                               c->slot_bytes, c->demand);
+        if (r != CKV_OK) return r;
+        CKV_HIP(hipEventRecord(c->ev_late[i], c->demand));
+      }
     }
-    if (r != CKV_OK) return r;
     CKV_HIP(hipEventRecord(c->ev_dem, c->demand));
     if ((r = period_prefetch()) != CKV_OK) return r;
     const bool two_part = c->attn_splits > 0;
@@ -1168,21 +1186,26 @@ ckv_status run_layer(ckv_ctx* c, const LayerArgs& la, ckv_layer_stats* stats) {
                     B.tab_dev, 0, c->nbuf * spb + c->cache_slots};
     if (two_part) {
       // the chunks already in HBM and the suffix while the misses are copied,
-      // then the misses, then one merge of both parts' splits
+      // then each share of the misses once it has landed, then one merge of
+      // every part's splits
       void* aw = ws + c->off_attn;
-      int32_t s1 = 0, s2 = 0;
+      int32_t done = 0, ns = 0;
       r = launch_attn_part(d, io->q, src, B.dem_dev, n_early, io->k_suffix, io->v_suffix, true, aw,
-                           c->attn_splits, 0, &s1, st);
+                           c->attn_splits, 0, &ns, st);
       if (r != CKV_OK) return r;
-      CKV_HIP(hipStreamWaitEvent(st, c->ev_dem, 0));
-      if (n_early < k) {
+      done += ns;
+      for (int i = 0; i < parts; ++i) {
+        const int64_t b0 = attn_late_part_begin(nm, parts, i), b1 = attn_late_part_begin(nm, parts, i + 1);
+        CKV_HIP(hipStreamWaitEvent(st, c->ev_late[i], 0));
         ChunkSource late = src;
-        late.chunk_off = B.tab_dev + n_early;
-        r = launch_attn_part(d, io->q, late, B.dem_dev + n_early, k - n_early, io->k_suffix,
-                             io->v_suffix, false, aw, c->attn_splits, s1, &s2, st);
+        late.chunk_off = B.tab_dev + n_early + b0;
+        r = launch_attn_part(d, io->q, late, B.dem_dev + n_early + b0, b1 - b0, io->k_suffix,
+                             io->v_suffix, false, aw, c->attn_splits, done, &ns, st);
         if (r != CKV_OK) return r;
+        done += ns;
       }
-      r = launch_attn_combine(d, aw, c->attn_splits, s1 + s2, io->out, st);
+      CKV_HIP(hipStreamWaitEvent(st, c->ev_dem, 0));
+      r = launch_attn_combine(d, aw, c->attn_splits, done, io->out, st);
     } else {
       r = launch_attn(d, io->q, src, B.dem_dev, k, io->k_suffix, io->v_suffix, io->out,
                       ws + c->off_attn, c->ws_attn, st);
