@@ -777,7 +777,7 @@ ckv_status launch_combine(const ckv_dims* d, const uint16_t* o_part, const float
   return CKV_OK;
 }
 
-// Split partials of a two-part launch: splits [0, max_splits) of o_part
+// Split partials of a parted attention: splits [0, max_splits) of o_part
 // ([split][Hkv][R][D] bf16) then of ml_part ([split][Hkv][R] float2).
 size_t part_o_bytes(const ckv_dims* d, int64_t max_splits) {
   const int G = d->n_q_heads / d->n_kv_heads;
@@ -830,7 +830,7 @@ int64_t attn_late_part_begin(int64_t n_late, int parts, int i) {
   return n_late * i / parts;
 }
 
-int64_t attn_two_part_splits(const ckv_dims* d, int64_t k, int max_late_parts) {
+int64_t attn_parted_splits(const ckv_dims* d, int64_t k, int max_late_parts) {
   int64_t most = 0;
   for (int64_t ka = 0; ka <= k; ++ka) {
     const int64_t nl = k - ka;
@@ -846,7 +846,7 @@ int64_t attn_two_part_splits(const ckv_dims* d, int64_t k, int max_late_parts) {
   return most;
 }
 
-size_t attn_two_part_bytes(const ckv_dims* d, int64_t max_splits) {
+size_t attn_parted_bytes(const ckv_dims* d, int64_t max_splits) {
   const int G = d->n_q_heads / d->n_kv_heads;
   return align_up(part_o_bytes(d, max_splits) +
                       (size_t)max_splits * d->n_kv_heads * G * d->n_suffix * sizeof(float2),
@@ -857,7 +857,7 @@ ckv_status launch_attn_part(const ckv_dims* d, const void* q, const ChunkSource&
                             const int32_t* sel, int64_t k, const void* k_suffix,
                             const void* v_suffix, bool with_suffix, void* ws, int64_t max_splits,
                             int32_t split_base, int32_t* n_splits, hipStream_t st) {
-  if (d->dtype != CKV_DTYPE_BF16) CKV_FAIL(CKV_EUNSUPPORTED, "two-part attention is bf16 only");
+  if (d->dtype != CKV_DTYPE_BF16) CKV_FAIL(CKV_EUNSUPPORTED, "parted attention is bf16 only");
   const AttnPlan p = make_attn_plan(d, k, with_suffix);
   if (split_base < 0 || split_base + (int64_t)p.n_splits > max_splits)
     CKV_FAIL(CKV_EINVAL, "attention splits %d + %d exceed the workspace's %lld", split_base,

@@ -188,12 +188,12 @@ ckv_status launch_attn(const ckv_dims* d, const void* q, const ChunkSource& src,
 // HBM while the rest (the late chunks) are still being copied, and over each
 // share of the late chunks once its copy has landed.  The n_late late chunks
 // go in `parts` consecutive shares, share i beginning at
-// attn_late_part_begin(n_late, parts, i).  attn_two_part_splits is the most
+// attn_late_part_begin(n_late, parts, i).  attn_parted_splits is the most
 // splits any division of k chunks into a first part and 1..max_late_parts
-// late shares takes; attn_two_part_bytes the workspace for that many.
+// late shares takes; attn_parted_bytes the workspace for that many.
 int64_t attn_late_part_begin(int64_t n_late, int parts, int i);
-int64_t attn_two_part_splits(const ckv_dims* d, int64_t k, int max_late_parts);
-size_t attn_two_part_bytes(const ckv_dims* d, int64_t max_splits);
+int64_t attn_parted_splits(const ckv_dims* d, int64_t k, int max_late_parts);
+size_t attn_parted_bytes(const ckv_dims* d, int64_t max_splits);
 ckv_status launch_attn_part(const ckv_dims* d, const void* q, const ChunkSource& src,
                             const int32_t* sel, int64_t k, const void* k_suffix,
                             const void* v_suffix, bool with_suffix, void* ws, int64_t max_splits,

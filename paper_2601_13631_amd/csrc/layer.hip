@@ -17,7 +17,9 @@
 // time on a prefetch stream (the prediction P_{l+1} = S_l, or a set the caller
 // gives); when the layer has selected S_l only the difference S_l \ P_l is
 // fetched on a demand stream into the free slots behind the predicted ones,
-// and the attention reads every kept chunk through a chunk -> slot table.
+// and the attention reads every kept chunk through a chunk -> slot table: it
+// attends over the chunks already in HBM while the misses are copied, and
+// over each share of the misses once that share's copy has landed (bf16).
 // With Periods and the per-layer stores registered (ckv_ctx_set_host_layers),
 // a Period's first layer queues the copies of every later layer of its Period
 // as soon as its set is known (intra-period prefetch; the ring then holds
@@ -522,8 +524,8 @@ ckv_status ckv_ctx_create(const ckv_dims* dims, int32_t n_layers, double keep_ra
   }
   c->ws_attn = make_attn_plan(dims, c->k).bytes;
   if ((flags & CKV_CTX_HOST_PREFIX) && dims->dtype == CKV_DTYPE_BF16) {
-    c->attn_splits = attn_two_part_splits(dims, c->k, ckv_ctx::kLateParts);
-    c->ws_attn = std::max(c->ws_attn, attn_two_part_bytes(dims, c->attn_splits));
+    c->attn_splits = attn_parted_splits(dims, c->k, ckv_ctx::kLateParts);
+    c->ws_attn = std::max(c->ws_attn, attn_parted_bytes(dims, c->attn_splits));
   }
   // scoring and attention scratch are used one after the other on one stream,
   // so both start at the front of the workspace
@@ -1173,8 +1175,8 @@ ckv_status run_layer(ckv_ctx* c, const LayerArgs& la, ckv_layer_stats* stats) {
     }
     CKV_HIP(hipEventRecord(c->ev_dem, c->demand));
     if ((r = period_prefetch()) != CKV_OK) return r;
-    const bool two_part = c->attn_splits > 0;
-    CKV_HIP(hipStreamWaitEvent(st, two_part ? c->ev_tab : c->ev_dem, 0));
+    const bool parted = c->attn_splits > 0;
+    CKV_HIP(hipStreamWaitEvent(st, parted ? c->ev_tab : c->ev_dem, 0));
     if (B.pref_pending) CKV_HIP(hipStreamWaitEvent(st, B.ev_pref, 0));
     B.pref_pending = false;
     if (gate_layer > layer) {  // SubPeriod gate: the Period's first layers are in HBM
@@ -1184,7 +1186,7 @@ ckv_status run_layer(ckv_ctx* c, const LayerArgs& la, ckv_layer_stats* stats) {
     if ((r = mark(4)) != CKV_OK) return r;
     ChunkSource src{c->arena, static_cast<char*>(c->arena) + span_elems * eb, 2 * span_elems,
                     B.tab_dev, 0, c->nbuf * spb + c->cache_slots};
-    if (two_part) {
+    if (parted) {
       // the chunks already in HBM and the suffix while the misses are copied,
       // then each share of the misses once it has landed, then one merge of
       // every part's splits
