@@ -679,7 +679,7 @@ AttnPlan make_attn_plan(const ckv_dims* d, int64_t k, bool with_suffix) {
     return p;
   }
   const int64_t np = k * d->chunk_size + (with_suffix ? d->n_suffix : 0);
-  const int64_t ntiles = ceil_div(np, kTile);
+  const int64_t ntiles = std::max<int64_t>(1, ceil_div(np, kTile));  // no keys: one empty split
   const int64_t base = (int64_t)d->n_kv_heads * ceil_div(p.rows, kBlockRows);
   // at most ~2 workgroups per CU, keeping >= 4 stages per split and no more
   // keys per split than the workgroup's code table holds; then the fewest
@@ -826,22 +826,35 @@ ckv_status launch_attn(const ckv_dims* d, const void* q, const ChunkSource& src,
   return CKV_OK;
 }
 
+// Every share holds one chunk plus a part of the rest that shrinks
+// geometrically, share j weighing kShareA^j kShareB^(parts-1-j), so that the
+// last share -- whose attention is all that follows the last copy -- is the
+// smallest and no share is empty (integer arithmetic: the same shares on every
+// host).  1 <= parts <= n_late.
+constexpr int64_t kShareA = 1, kShareB = 2;
+
 int64_t attn_late_part_begin(int64_t n_late, int parts, int i) {
-  return n_late * i / parts;
+  int64_t cum = 0, total = 0;
+  for (int j = 0; j < parts; ++j) {
+    int64_t w = 1;
+    for (int e = 0; e < j; ++e) w *= kShareA;
+    for (int e = 0; e < parts - 1 - j; ++e) w *= kShareB;
+    if (j < i) cum += w;
+    total += w;
+  }
+  return i + (n_late - parts) * cum / total;
 }
 
 int64_t attn_parted_splits(const ckv_dims* d, int64_t k, int max_late_parts) {
   int64_t most = 0;
   for (int64_t ka = 0; ka <= k; ++ka) {
     const int64_t nl = k - ka;
-    for (int parts = 1; parts <= max_late_parts; ++parts) {
-      int64_t n = make_attn_plan(d, ka, true).n_splits;
-      for (int i = 0; i < parts; ++i) {
-        const int64_t cnt = attn_late_part_begin(nl, parts, i + 1) - attn_late_part_begin(nl, parts, i);
-        if (cnt > 0) n += make_attn_plan(d, cnt, false).n_splits;
-      }
-      most = std::max(most, n);
-    }
+    const int parts = (int)std::min<int64_t>(max_late_parts, nl);
+    int64_t n = make_attn_plan(d, ka, true).n_splits;
+    for (int i = 0; i < parts; ++i)
+      n += make_attn_plan(d, attn_late_part_begin(nl, parts, i + 1) -
+                                 attn_late_part_begin(nl, parts, i), false).n_splits;
+    most = std::max(most, n);
   }
   return most;
 }
@@ -858,6 +871,7 @@ ckv_status launch_attn_part(const ckv_dims* d, const void* q, const ChunkSource&
                             const void* v_suffix, bool with_suffix, void* ws, int64_t max_splits,
                             int32_t split_base, int32_t* n_splits, hipStream_t st) {
   if (d->dtype != CKV_DTYPE_BF16) CKV_FAIL(CKV_EUNSUPPORTED, "parted attention is bf16 only");
+  if (k == 0 && !with_suffix) CKV_FAIL(CKV_EINVAL, "an attention part without the suffix needs chunks");
   const AttnPlan p = make_attn_plan(d, k, with_suffix);
   if (split_base < 0 || split_base + (int64_t)p.n_splits > max_splits)
     CKV_FAIL(CKV_EINVAL, "attention splits %d + %d exceed the workspace's %lld", split_base,

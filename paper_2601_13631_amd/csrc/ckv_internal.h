@@ -187,10 +187,11 @@ ckv_status launch_attn(const ckv_dims* d, const void* q, const ChunkSource& src,
 // different events: a host-resident layer attends over the chunks already in
 // HBM while the rest (the late chunks) are still being copied, and over each
 // share of the late chunks once its copy has landed.  The n_late late chunks
-// go in `parts` consecutive shares, share i beginning at
-// attn_late_part_begin(n_late, parts, i).  attn_parted_splits is the most
-// splits any division of k chunks into a first part and 1..max_late_parts
-// late shares takes; attn_parted_bytes the workspace for that many.
+// go in parts = min(max_late_parts, n_late) consecutive non-empty shares,
+// share i beginning at attn_late_part_begin(n_late, parts, i).
+// attn_parted_splits is the most splits any division of k chunks into a
+// first part and its late shares takes; attn_parted_bytes the workspace for
+// that many.
 int64_t attn_late_part_begin(int64_t n_late, int parts, int i);
 int64_t attn_parted_splits(const ckv_dims* d, int64_t k, int max_late_parts);
 size_t attn_parted_bytes(const ckv_dims* d, int64_t max_splits);

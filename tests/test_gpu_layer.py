@@ -245,7 +245,8 @@ def _run_host(ctx, w, t, store, layer, pred=None, nxt=None):
     return A, sel, out, st
 
 
-@pytest.mark.parametrize("how", ["empty", "perfect", "complement", "partial"])
+@pytest.mark.parametrize("how", ["empty", "perfect", "complement", "partial", "four_misses",
+                                 "five_misses"])
 def test_layer_caller_prediction(how):
     """A caller-given prediction (ckv_layer_io.pred_idx, Sec. 4.3.2's set from a
     previous Period or layer) replaces the context's own: its chunks are copied
@@ -271,7 +272,10 @@ def test_layer_caller_prediction(how):
     rng = np.random.default_rng(3)
     pred = {"empty": np.zeros(0, np.int32), "perfect": sel0,
             "complement": rest[:k],
-            "partial": np.sort(np.concatenate([sel0[: k // 2], rng.choice(rest, k - k // 2, replace=False)]))
+            "partial": np.sort(np.concatenate([sel0[: k // 2], rng.choice(rest, k - k // 2, replace=False)])),
+            # few misses: as many shares of the demand copy as misses, or fewer
+            "four_misses": np.delete(sel0, [0, 3, 6, 9]),
+            "five_misses": np.delete(sel0, [1, 2, 5, 8, 11]),
             }[how].astype(np.int32)
     ctx.reset()
     print(f"prediction {how}: {pred.size} chunks", flush=True)
@@ -294,6 +298,8 @@ def test_layer_caller_prediction(how):
         assert st["misses"] == 0 and st["hits"] == k
     if how == "complement":
         assert st["hits"] == 0 and st["wasted"] == k
+    if how.endswith("_misses"):
+        assert st["misses"] == (4 if how == "four_misses" else 5)
     print(f"  hits {st['hits']} misses {st['misses']} wasted {st['wasted']}", flush=True)
     # refusals: not ascending, out of range, more than k
     ctx.reset()
