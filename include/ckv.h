@@ -419,7 +419,12 @@ ckv_status ckv_ctx_stage_times(ckv_ctx* ctx, double* ms, int64_t* n_layers);
  * Host-resident prefix: synchronizes once on the selection (the only
  * device->host dependency of the step), enqueues the demand copies of the
  * missed chunks, the attention over the HBM slots and the prefetch of the
- * next layer's chunks; counts in *stats (may be NULL) are exact; after the
+ * next layer's chunks.  With bf16 the attention runs in parts over the same
+ * kept set -- the chunks already in HBM (prefetched or in a cache's slots)
+ * with the suffix during the demand copies, then each share of the missed
+ * chunks once it has landed -- merged in a fixed order: the output is
+ * deterministic, but it is bit-identical to another context's only when the
+ * same chunks were already in HBM.  Counts in *stats (may be NULL) are exact; after the
  * first layer of a request, layers must run in order (layer + 1, else
  * CKV_ESTATE).  If the call fails after it has enqueued work (a HIP error,
  * an injected copy error), the context refuses further layers with
