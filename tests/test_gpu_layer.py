@@ -76,15 +76,21 @@ def _host_store(w, tensors):
     return stores
 
 
-@pytest.mark.parametrize("scenario", ["drift", "repeat", "disjoint", "tiny"])
+@pytest.mark.parametrize("scenario", ["drift", "repeat", "disjoint", "tiny", "d64", "f32"])
 def test_layer_host_resident_prefetch(scenario):
     """Host-resident prefix: outputs equal the HBM path's oracle, and the
     hit/miss/byte counts equal the oracle's set algebra with the previous
     layer's selection as the prediction.  "tiny": two chunks (the last one
-    partial, kept), one query."""
+    partial, kept), one query; "d64": head_dim 64, 7 query heads per KV head,
+    16-token chunks; "f32": the fp32 path (one attention launch after the
+    demand copy)."""
     import paper_2601_13631_amd as ckv
     if scenario == "tiny":
         w = small("c5_qwen32b_128k_host", n_prefix=45, n_suffix=1, n_layers=3)
+    elif scenario == "d64":
+        w = small("c2_qwen05b_8k", n_prefix=3000, n_suffix=20, n_layers=4)
+    elif scenario == "f32":
+        w = small("c1_f32_1k", n_prefix=1000, n_suffix=12, n_layers=3)
     else:
         w = small("c5_qwen32b_128k_host", n_prefix=4096, n_suffix=24, n_layers=4)
     hs = synth.heavy_sets(w)
