@@ -431,6 +431,35 @@ __device__ __forceinline__ void fast_stage(const ScoreArgs& a, const bf16x8 (&qf
   carry_rk = rk0 + kSub;
 }
 
+// The first full stage of a segment: its first subtile's logits are already
+// in `first` (the reference was taken from them), so only slot 1 remains --
+// the second subtile's MFMAs beside the first subtile's VALU work.
+template <int D, int MODE>
+__device__ __forceinline__ void fast_stage_first(const ScoreArgs& a, const bf16x8 (&qf)[2][D / 16],
+                                                 const uint16_t* cur, int rk0, int nkeys, float* part,
+                                                 int row, RangeState& st, f32x16 (&first)[2],
+                                                 f32x16 (&carry)[2], int& carry_rk) {
+  __builtin_amdgcn_sched_barrier(0);
+  mfma_subtile<D>(cur, kSub, qf, carry);
+  valu_subtile<MODE>(a, first, rk0, nkeys, part, row, st);
+  __builtin_amdgcn_sched_barrier(0);
+  carry_rk = rk0 + kSub;
+}
+
+// Reference from a full subtile's logits: the scaled maximum of each row's,
+// rounded up to a whole number.
+__device__ __forceinline__ void reference_of(const ScoreArgs& a, const f32x16 (&acc)[2],
+                                             RangeState& st) {
+#pragma unroll
+  for (int rt = 0; rt < 2; ++rt) {
+    float mx = acc[rt][0];
+#pragma unroll
+    for (int v = 1; v < 16; ++v) mx = fmaxf(mx, acc[rt][v]);
+    mx = fmaxf(mx, partner_f(mx));
+    st.mref[rt] = ceilf(mx * a.c1);
+  }
+}
+
 // Segment reference: the scaled maximum of each row's logits over the
 // segment's first 32 keys (already in LDS buffer 0).
 template <int D, int MODE>
@@ -479,9 +508,14 @@ __device__ __forceinline__ bool run_segment_fast(const ScoreArgs& a, int g, int6
   else
     stage_store<D, false>(r, lds);
   __syncthreads();
-  segment_reference<D, MODE>(a, qf, lds, nkeys, my_row0, st);
-  f32x16 carry[2];
+  f32x16 carry[2], first[2];
   int carry_rk = 0;
+  if (nfull > 0) {  // the first subtile's logits serve the reference and the first stage
+    mfma_subtile<D>(lds, 0, qf, first);
+    reference_of(a, first, st);
+  } else {
+    segment_reference<D, MODE>(a, qf, lds, nkeys, my_row0, st);
+  }
   for (int s = 0; s < nfull; ++s) {
     const int rk0 = s * kStage;
     const uint16_t* next = kbase + (s + 1) * stage_elems;
@@ -492,7 +526,8 @@ __device__ __forceinline__ bool run_segment_fast(const ScoreArgs& a, int g, int6
       stage_load<D>(next, nkeys - rk0 - kStage, o, r);
     const uint16_t* cur = lds + (s & 1) * kBuf;
     if (s == 0)
-      fast_stage<D, MODE, false>(a, qf, cur, rk0, nkeys, part, my_row0 + lane, st, carry, carry_rk);
+      fast_stage_first<D, MODE>(a, qf, cur, rk0, nkeys, part, my_row0 + lane, st, first, carry,
+                                carry_rk);
     else
       fast_stage<D, MODE, true>(a, qf, cur, rk0, nkeys, part, my_row0 + lane, st, carry, carry_rk);
     uint16_t* nbuf = lds + ((s + 1) & 1) * kBuf;
