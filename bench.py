@@ -16,9 +16,12 @@ and ``ms_per_step``.  Then the same K steps again on a context that times the
 scoring kernel (the dominant kernel) by the kernel's own timestamps (from its
 first workgroup's start to its last workgroup's end, 100 MHz realtime
 counter), with nothing added between the launches: ``roofline`` is its
-algorithmic flops per launch (2*S*Hq*n*d) over the average span, and
+algorithmic flops per launch (2*S*Hq*n*d) over the average span,
 ``roofline.event_avg_us`` the kernel's average time between the HIP events of
-the diagnostic pass (which include its dispatch).  ``roofline.traffic`` is the
+the diagnostic pass (which include its dispatch), and
+``roofline.trace_avg_us`` / ``frac_at_trace_avg`` the committed rocprofv3
+kernel trace's duration of the kernel (dispatch to completion) and the
+fraction of the peak at that duration.  ``roofline.traffic`` is the
 kernel's HBM bytes per launch from the committed rocprofv3 counter summary
 (FETCH_SIZE and WRITE_SIZE, each scaled by what the counter reads for a plain
 copy of known size); it is null when the kernel's sources no longer match the
@@ -93,6 +96,20 @@ def counter_traffic(workload: str):
     fetch = float(kv["fetch_size_kib_per_dispatch"]) * float(kv["fetch_scale"])
     write = float(kv["write_size_kib_per_dispatch"]) * float(kv["write_scale"])
     return (fetch + write) * 1024.0, os.path.relpath(path, ROOT)
+
+
+def trace_avg_us(workload: str, kernel: str):
+    """The kernel's average duration in the committed rocprofv3 kernel-trace
+    summary of this workload (dispatch to completion), or None."""
+    path = os.path.join(ROOT, "profiles", f"kernels_{workload}.txt")
+    if not os.path.exists(path):
+        return None, None
+    with open(path) as fh:
+        for line in fh:
+            f = line.split()
+            if len(f) == 4 and f[0] == kernel:
+                return float(f[2]), os.path.relpath(path, ROOT)
+    return None, None
 
 
 def host_cache_requests(args, w, ckv, synth, np, torch, layers, stores, dims, k) -> dict:
@@ -627,6 +644,14 @@ def main() -> int:
                 "timing": ("kernel's own timestamps, first workgroup start to last workgroup end"
                            if w.dtype == "bf16" else "HIP events around the kernel"),
                 "event_avg_us": round(per_layer["score"] * 1e3, 2)}
+    # the committed kernel trace's duration of the same kernel (dispatch to
+    # completion: it also holds the dispatch of the workgroups and the
+    # end-of-kernel drain), and the fraction of the peak at that duration
+    t_us, t_src = trace_avg_us(w.name, roofline["kernel"])
+    if t_us:
+        roofline.update({"trace_avg_us": t_us, "trace_source": t_src,
+                         "frac_at_trace_avg": round(score_flops / (t_us * 1e-6) / 1e12 /
+                                                    roofline["peak"], 4)})
     # attention and kept-chunk bytes, as context
     T = k * w.chunk_size
     attn_flops = 4.0 * w.head_dim * w.n_q_heads * (w.n_suffix * T + w.n_suffix * (w.n_suffix + 1) / 2)
