@@ -1,0 +1,102 @@
+"""Randomized parity of the layer step: seeded shapes drawn across the
+supported ranges -- head_dim 64 and 128, chunk sizes 4 to 96, 1 to 4 KV heads
+with 1 to 7 query heads each, ragged prefixes and suffixes, keep ratios from a
+single chunk to every chunk -- each run for two layers through the
+HBM-resident or the host-resident path (the second layer with the first
+one's set as its prediction) and compared with the oracle layer by layer:
+chunk scores within SCORE_RTOL_UNIT, the kept set equal to the oracle's when
+certified and inside the near-tie band otherwise, the oracle's selection from
+the GPU's own scores equal to the GPU's set, every attention element within
+its bound, and on the host path the hit/miss/byte counts equal to the
+oracle's set algebra."""
+from dataclasses import replace
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+from gpu_common import (DEV, SCORE_RTOL_UNIT, attn_check, check_set, dev, dims_of, oshape,
+                        rel_err, to_f64)
+
+pytestmark = pytest.mark.gpu
+
+N_CASES = 48
+
+
+def _case(i: int):
+    rng = np.random.default_rng(2026 + i)
+    if i % 10 == 9:  # fp32: head_dim 64, the small case's recipe
+        base = synth.WORKLOADS["c1_f32_1k"]
+        d, c = 64, 16
+        hkv, G = int(rng.choice([1, 2])), int(rng.choice([1, 2, 4]))
+    else:
+        base = synth.WORKLOADS["c2_qwen05b_8k"]
+        d = int(rng.choice([64, 128]))
+        c = int(rng.choice([4, 8, 16, 32, 64] + ([96] if d == 128 else [])))
+        hkv, G = int(rng.choice([1, 2, 4])), int(rng.choice([1, 2, 5, 7]))
+    S = int(rng.integers(1, 49))
+    n = int(rng.integers(c, 4001))
+    m = -(-n // c)
+    keep = float(rng.choice([0.5 / m, 0.1, 0.37, 1.0]))
+    w = replace(base, name=f"random{i}", n_layers=2, n_prefix=n, n_suffix=S, n_q_heads=hkv * G,
+                n_kv_heads=hkv, head_dim=d, chunk_size=c, keep_ratio=keep, seed=100 + i)
+    return w, ("host" if i % 2 else "hbm")
+
+
+def _store(w, t):
+    cm = synth.chunk_major(t["k_prefix"], t["v_prefix"], w.chunk_size)
+    h = torch.from_numpy(cm.reshape(-1))
+    if cm.dtype == np.uint16:
+        h = h.view(torch.bfloat16)
+    return h.pin_memory()
+
+
+@pytest.mark.parametrize("i", range(N_CASES))
+def test_random_layer_step(i):
+    import paper_2601_13631_amd as ckv
+    w, path = _case(i)
+    print(f"case {i} {path}: {w.dtype} n {w.n_prefix} S {w.n_suffix} Hq {w.n_q_heads} "
+          f"Hkv {w.n_kv_heads} d {w.head_dim} c {w.chunk_size} keep {w.keep_ratio:.4f}", flush=True)
+    host = path == "host"
+    s = oshape(w)
+    hs = synth.heavy_sets(w)
+    layers = [synth.layer_tensors(w, l, hs[l]) for l in range(w.n_layers)]
+    stores = [_store(w, t) for t in layers] if host else None
+    ctx = ckv.Context(dims_of(w), w.n_layers, w.keep_ratio, ckv.CTX_HOST_PREFIX if host else 0)
+    k = ctx.k
+    prev = np.zeros(0, np.int32)
+    for l, t in enumerate(layers):
+        tt = {kk: dev(v) for kk, v in t.items()}
+        A = torch.empty(w.n_chunks, dtype=torch.float64, device=DEV)
+        sel = torch.empty(k, dtype=torch.int32, device=DEV)
+        out = torch.empty_like(tt["q"])
+        if host:
+            nxt = stores[l + 1] if l + 1 < w.n_layers else None
+            st = ctx.reprefill_layer(l, tt["q"], tt["k_suffix"], tt["v_suffix"], tt["k_prefix"], out,
+                                     kv_host=stores[l], kv_host_next=nxt, chunk_scores=A,
+                                     sel_idx=sel)
+        else:
+            st = ctx.reprefill_layer(l, tt["q"], tt["k_suffix"], tt["v_suffix"], tt["k_prefix"], out,
+                                     k_prefix=tt["k_prefix"], v_prefix=tt["v_prefix"],
+                                     chunk_scores=A, sel_idx=sel)
+        torch.cuda.synchronize()
+        A, sel = A.cpu().numpy(), sel.cpu().numpy()
+        A_ref = oracle.chunk_scores(s, oracle.token_importance(s, t["q"], t["k_prefix"]))
+        err = rel_err(A, A_ref)
+        assert err <= SCORE_RTOL_UNIT, (l, err)
+        cs = check_set(A_ref, sel, k, err, require=False)
+        assert np.all(np.diff(sel) > 0)
+        assert np.array_equal(oracle.select_topk(A, k), sel)
+        ref = oracle.sparse_attn(s, t["q"], t["k_prefix"], t["v_prefix"], sel, t["k_suffix"],
+                                 t["v_suffix"])
+        aerr, ratio = attn_check(s, t, sel, to_f64(out).reshape(ref.shape), ref)
+        print(f"  layer {l}: k {k} score rel err {err:.2e} certified {cs['certified']} "
+              f"attn max abs {aerr:.2e} ({ratio:.2f} of its bound)", flush=True)
+        if host:
+            acc = oracle.layer_accounting(s, sel, prev)
+            for f in ("hits", "misses", "wasted", "bytes_demand"):
+                assert st[f] == acc[f], (l, f, st[f], acc[f])
+            prev = sel
+    ctx.close()
