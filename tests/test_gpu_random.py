@@ -4,7 +4,8 @@ with 1 to 7 query heads each, ragged prefixes and suffixes, keep ratios from a
 single chunk to every chunk -- each run for two layers through the
 HBM-resident or the host-resident path (the second layer with the first
 one's set as its prediction) and compared with the oracle layer by layer:
-chunk scores within SCORE_RTOL_UNIT, the kept set equal to the oracle's when
+chunk scores within SCORE_RTOL_UNIT (the derived SCORE_RTOL_BOUND for fp32
+inputs), the kept set equal to the oracle's when
 certified and inside the near-tie band otherwise, the oracle's selection from
 the GPU's own scores equal to the GPU's set, every attention element within
 its bound, and on the host path the hit/miss/byte counts equal to the
@@ -17,8 +18,8 @@ import torch
 
 import oracle
 import synth
-from gpu_common import (DEV, SCORE_RTOL_UNIT, attn_check, check_set, dev, dims_of, oshape,
-                        rel_err, to_f64)
+from gpu_common import (DEV, SCORE_RTOL_BOUND, SCORE_RTOL_UNIT, attn_check, check_set, dev,
+                        dims_of, oshape, rel_err, to_f64)
 
 pytestmark = pytest.mark.gpu
 
@@ -85,7 +86,11 @@ def test_random_layer_step(i):
         A, sel = A.cpu().numpy(), sel.cpu().numpy()
         A_ref = oracle.chunk_scores(s, oracle.token_importance(s, t["q"], t["k_prefix"]))
         err = rel_err(A, A_ref)
-        assert err <= SCORE_RTOL_UNIT, (l, err)
+        # fp32 inputs: unlike bf16 ones their products round in fp32, and with
+        # a handful of rows (3 in one case) that rounding does not average out
+        # (a CPU emulation of the same fp32 arithmetic lands at 4.7e-7 there):
+        # they are held to the derived bound
+        assert err <= (SCORE_RTOL_BOUND if w.dtype == "f32" else SCORE_RTOL_UNIT), (l, err)
         cs = check_set(A_ref, sel, k, err, require=False)
         assert np.all(np.diff(sel) > 0)
         assert np.array_equal(oracle.select_topk(A, k), sel)
