@@ -4,8 +4,8 @@ with 1 to 7 query heads each, ragged prefixes and suffixes, keep ratios from a
 single chunk to every chunk -- each run for two layers through the
 HBM-resident or the host-resident path (the second layer with the first
 one's set as its prediction) and compared with the oracle layer by layer:
-chunk scores within SCORE_RTOL_UNIT (the derived SCORE_RTOL_BOUND for fp32
-inputs), the kept set equal to the oracle's when
+chunk scores within the derived bound SCORE_RTOL_BOUND, the kept set equal
+to the oracle's when
 certified and inside the near-tie band otherwise, the oracle's selection from
 the GPU's own scores equal to the GPU's set, every attention element within
 its bound, and on the host path the hit/miss/byte counts equal to the
@@ -18,10 +18,18 @@ import torch
 
 import oracle
 import synth
-from gpu_common import (DEV, SCORE_RTOL_BOUND, SCORE_RTOL_UNIT, attn_check, check_set, dev,
-                        dims_of, oshape, rel_err, to_f64)
+from gpu_common import (DEV, SCORE_RTOL_BOUND, attn_check, check_set, dev, dims_of, oshape,
+                        rel_err, to_f64)
 
 pytestmark = pytest.mark.gpu
+
+# Scores are held to the derived bound, not to the 4e-7 of the fixed unit
+# shapes: the random shapes include chunks summed over 2-4 rows of 4 tokens,
+# where the rounding of each term does not average out -- an fp32 logit's
+# rounding grows with its distance from the segment's reference, and fp32
+# inputs also round their products (a 3-row fp32 case reached 5.1e-7 on the
+# GPU; a CPU emulation of the same fp32 arithmetic 4.7e-7).  A structural
+# mistake (a wrong chunk, row or weight) shows up orders of magnitude above.
 
 N_CASES = 48
 
@@ -86,11 +94,7 @@ def test_random_layer_step(i):
         A, sel = A.cpu().numpy(), sel.cpu().numpy()
         A_ref = oracle.chunk_scores(s, oracle.token_importance(s, t["q"], t["k_prefix"]))
         err = rel_err(A, A_ref)
-        # fp32 inputs: unlike bf16 ones their products round in fp32, and with
-        # a handful of rows (3 in one case) that rounding does not average out
-        # (a CPU emulation of the same fp32 arithmetic lands at 4.7e-7 there):
-        # they are held to the derived bound
-        assert err <= (SCORE_RTOL_BOUND if w.dtype == "f32" else SCORE_RTOL_UNIT), (l, err)
+        assert err <= SCORE_RTOL_BOUND, (l, err)
         cs = check_set(A_ref, sel, k, err, require=False)
         assert np.all(np.diff(sel) > 0)
         assert np.array_equal(oracle.select_topk(A, k), sel)
