@@ -722,10 +722,14 @@ ckv_status ckv_ctx_attach_store(ckv_ctx* ctx, ckv_store* store) {
   ctx->store_layers = 0;
   if (!store) return resize_ring(ctx);
   // room for the cache's tiers, plus the transient chunks of two layers in
-  // flight and of the layer whose slots wait for release
+  // flight and of the layer whose slots wait for release.  With few keys the
+  // count is capped at one slot per key plus the quarantine: a layer releases
+  // at most 3k slots (its set, its unused prediction and the chunks the
+  // cascade dropped), and a key released that way can take a second slot for
+  // the next layer's reads while its old one still waits
   const int64_t keys = store_keys(store), k = ctx->k;
   const int64_t kept = ctx->cache ? std::min(keys, cache_gpu_slots(ctx->cache) + cache_cpu_slots(ctx->cache)) : 0;
-  const int64_t n = std::min(keys, kept + (6 + ctx->subperiod) * k) + 16;
+  const int64_t n = std::min(keys + 3 * k, kept + (6 + ctx->subperiod) * k) + 16;
   const int64_t spb = ctx->slots_per_buf;
   hipError_t e = hipHostMalloc((void**)&ctx->pool, (size_t)(n * ctx->slot_bytes), hipHostMallocDefault);
   for (int b = 0; b < 2 && e == hipSuccess; ++b)
