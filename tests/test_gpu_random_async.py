@@ -1,11 +1,12 @@
-"""Randomized parity of the host-resident layer step run without any host
-synchronisation between layers: seeded shapes, a Period of 1 to 4 layers, the
-chunks coming from per-call pinned stores, from stores registered for every
-layer (the Period's copies queued at its first layer, a SubPeriod of 1 to 3)
-or from a file through the storage tier, with or without the attention-guided
-cache, two requests.  Layers inside a Period never wait on the host, so the
-host runs ahead of the GPU and rewrites staging lists and pool slots while
-earlier layers' copies and attention may still be in flight; every layer's
+"""Randomized parity of the layer step run without any host synchronisation
+between layers: seeded shapes, a Period of 1 to 4 layers, the chunks coming
+from per-call pinned stores, from stores registered for every layer (the
+Period's copies queued at its first layer, a SubPeriod of 1 to 3), from a
+file through the storage tier (each with or without the attention-guided
+cache) or from HBM (read in place or through the materialised copy), two
+requests.  Layers inside a Period never wait on the host, so the host runs
+ahead of the GPU and rewrites staging lists and pool slots while earlier
+layers' copies and attention may still be in flight; every layer's
 scores, set and output are read only after the whole request and compared
 with the oracle: scores within the derived bound at a Period's first layer,
 untouched elsewhere, every set the Period's, every output within its bound."""
@@ -22,8 +23,11 @@ from gpu_common import (DEV, SCORE_RTOL_BOUND, attn_check, check_set, dev, dims_
 
 pytestmark = pytest.mark.gpu
 
-N_CASES = 18
+N_CASES = 20
 SEED0 = 5300
+
+
+SOURCES = ("pinned", "registered", "store", "hbm", "hbm-copy")
 
 
 def _case(seed: int):
@@ -37,9 +41,9 @@ def _case(seed: int):
     m = -(-n // c)
     keep = float(rng.choice([0.5 / m, 0.1, 0.37, 1.0]))
     period = int(rng.integers(1, 5))
-    source = ("pinned", "registered", "store")[seed % 3]
-    sub = int(rng.integers(1, 4)) if source != "pinned" else 1
-    cache = bool(rng.integers(0, 2))
+    source = SOURCES[seed % len(SOURCES)]
+    sub = int(rng.integers(1, 4)) if source in ("registered", "store") else 1
+    cache = bool(rng.integers(0, 2)) and not source.startswith("hbm")
     L = int(rng.integers(4, 8))
     w = replace(base, name=f"random_async{seed}", n_layers=L, n_prefix=n, n_suffix=S,
                 n_q_heads=hkv * G, n_kv_heads=hkv, head_dim=d, chunk_size=c, keep_ratio=keep,
@@ -66,7 +70,8 @@ def test_random_async_layer_step(seed, tmp_path):
     s = oshape(w)
     hs = synth.heavy_sets(w)
     layers = [synth.layer_tensors(w, l, hs[l]) for l in range(L)]
-    ctx = ckv.Context(dims_of(w), L, w.keep_ratio, ckv.CTX_HOST_PREFIX)
+    flags = {"hbm": 0, "hbm-copy": ckv.CTX_MATERIALIZE}.get(source, ckv.CTX_HOST_PREFIX)
+    ctx = ckv.Context(dims_of(w), L, w.keep_ratio, flags)
     ctx.set_period(period)
     k = ctx.k
     stores, store, cache = None, None, None
@@ -81,7 +86,7 @@ def test_random_async_layer_step(seed, tmp_path):
         store = ckv.Store(path, L * m, 2 * w.chunk_size * w.n_kv_heads * w.head_dim * w.elem_bytes, 4, 0)
         ctx.set_subperiod(sub)
         ctx.attach_store(store)
-    else:
+    elif not source.startswith("hbm"):
         stores = [_pinned(w, t) for t in layers]
         if source == "registered":
             ctx.set_host_layers(stores)
@@ -100,6 +105,8 @@ def test_random_async_layer_step(seed, tmp_path):
             kw = {}
             if source == "pinned":
                 kw = dict(kv_host=stores[l], kv_host_next=stores[l + 1] if l + 1 < L else None)
+            elif source.startswith("hbm"):
+                kw = dict(k_prefix=base[l]["k_prefix"], v_prefix=base[l]["v_prefix"])
             ctx.reprefill_layer(l, qd[l], base[l]["k_suffix"], base[l]["v_suffix"],
                                 base[l]["k_prefix"], out, chunk_scores=A, sel_idx=sel, **kw)
         torch.cuda.synchronize()
