@@ -64,9 +64,15 @@ def _store(w, t):
 
 @pytest.mark.parametrize("i", range(N_CASES))
 def test_random_layer_step(i):
-    import paper_2601_13631_amd as ckv
     w, path = _case(i)
-    print(f"case {i} {path}: {w.dtype} n {w.n_prefix} S {w.n_suffix} Hq {w.n_q_heads} "
+    print(f"case {i}", end=" ")
+    run_layers(w, path)
+
+
+def run_layers(w, path):
+    """Runs every layer of w through the given path and checks it against the oracle."""
+    import paper_2601_13631_amd as ckv
+    print(f"{path}: {w.dtype} n {w.n_prefix} S {w.n_suffix} Hq {w.n_q_heads} "
           f"Hkv {w.n_kv_heads} d {w.head_dim} c {w.chunk_size} keep {w.keep_ratio:.4f}", flush=True)
     host = path == "host"
     s = oshape(w)
